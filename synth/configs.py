@@ -1,0 +1,79 @@
+"""The five synthetic workloads of the expert-slot-cache MoE FFN, by name.
+
+Shapes stand in for the paper's GGUF model profiles (its model-profile
+table): an "A3B"-shaped Q8_0 stack, a Q4_0 stack and a tiny one-layer case.
+Nothing here computes anything of the method; it only names sizes, seeds and
+distributions for the generator in this package.
+"""
+from dataclasses import dataclass, field, replace
+from typing import Tuple
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n_layers: int
+    hidden: int
+    n_experts: int
+    top_k: int
+    inter: int
+    qtype: str                 # "q8_0" or "q4_0"
+    weight_sigma: float        # expert weights ~ N(0, sigma) before quantisation
+    router_sigma: float        # router W_r ~ N(0, sigma), fp32 [hidden, n_experts]
+    n_tokens: int              # decode: tokens generated one at a time; prefill: chunk size
+    rho: float                 # AR(1) coefficient of the hidden-state drift; <0 means iid N(0,1)
+    budget_slots: int          # expert slots per layer
+    model_seed: int            # seed of the expert store and routers
+    hidden_seed: int           # seed of the hidden states
+    mode: str = "decode"       # "decode" (one token per layer call) or "prefill" (whole chunk per call)
+    sweep_slots: Tuple[int, ...] = field(default=())
+    sweep_rhos: Tuple[float, ...] = field(default=())
+
+    @property
+    def block_bytes(self) -> int:
+        return 34 if self.qtype == "q8_0" else 18
+
+    @property
+    def qcode(self) -> int:
+        """Block-type code used by the C interfaces (8 = Q8_0, 2 = Q4_0)."""
+        return 8 if self.qtype == "q8_0" else 2
+
+    @property
+    def matrix_bytes(self) -> int:
+        return self.inter * self.hidden // 32 * self.block_bytes
+
+    @property
+    def payload_bytes(self) -> int:
+        return 3 * self.matrix_bytes
+
+    @property
+    def store_bytes(self) -> int:
+        return self.n_layers * self.n_experts * self.payload_bytes
+
+    def hidden_stream(self, rho: float) -> int:
+        """Stream id of the hidden states for a given rho (iid when rho < 0)."""
+        return 255 if rho < 0 else int(round(10 * rho))
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+TINY = Workload("tiny", n_layers=1, hidden=256, n_experts=16, top_k=2, inter=128,
+                qtype="q8_0", weight_sigma=0.02, router_sigma=0.1, n_tokens=64, rho=0.8,
+                budget_slots=4, model_seed=1, hidden_seed=1)
+
+A3B_DECODE = Workload("a3b_decode", n_layers=48, hidden=2048, n_experts=128, top_k=8, inter=768,
+                      qtype="q8_0", weight_sigma=0.02, router_sigma=0.05, n_tokens=96, rho=0.8,
+                      budget_slots=19, model_seed=2, hidden_seed=2)
+
+A3B_SWEEP = A3B_DECODE.with_(name="a3b_sweep", hidden_seed=3, sweep_slots=(19, 45, 96),
+                             sweep_rhos=(0.3, 0.9))
+
+Q4_DECODE = Workload("q4_decode", n_layers=30, hidden=2816, n_experts=128, top_k=8, inter=1408,
+                     qtype="q4_0", weight_sigma=0.02, router_sigma=0.05, n_tokens=96, rho=0.8,
+                     budget_slots=45, model_seed=4, hidden_seed=4)
+
+A3B_PREFILL = A3B_DECODE.with_(name="a3b_prefill", n_tokens=4096, rho=-1.0, budget_slots=45,
+                               hidden_seed=5, mode="prefill")
+
+WORKLOADS = {w.name: w for w in (TINY, A3B_DECODE, A3B_SWEEP, Q4_DECODE, A3B_PREFILL)}
