@@ -1,0 +1,181 @@
+/*
+ * moecache: routed-expert MoE FFN over a bounded per-layer expert-slot cache,
+ * for AMD Instinct MI355X (gfx950).  C ABI.
+ *
+ * The method is MawForge's bounded expert materialisation (arXiv 2607.09686):
+ * the full set of routed-expert weights stays in a large backing store; each
+ * MoE layer owns a fixed number of slots for expert weight blocks; the router
+ * decides which experts a token needs; a needed expert that holds no slot is
+ * copied ("materialised") into one, and the route-to-slot metadata is updated
+ * (the paper's Native Serving Path section; the store layout follows its
+ * Split-Pack section: one block of bytes per layer and expert).
+ *
+ * Here the backing store is pinned host memory, the slots are HBM, and a
+ * layer call does, in order:
+ *   1. router logits z = x W_r, top-k by (-z, id), softmax over the chosen k;
+ *   2. LRU slot-table lookup on the host with hit / miss / eviction counters;
+ *   3. one host-to-device copy per miss into the chosen slot, on a side stream;
+ *   4. fused dequantise + SwiGLU gate/up, then down projection with the
+ *      routing-weighted combine (and optional residual add); hit experts run
+ *      while the misses are still being copied.
+ *
+ * Conventions for every function below:
+ *   - returns MOE_OK (0) or a negative MOE_E* code; moe_last_error() then
+ *     holds a message for the calling thread;
+ *   - no C++ exception crosses this boundary;
+ *   - after MOE_EHIP the handle is poisoned: every later call on it returns
+ *     MOE_ESTATE, and only moe_cache_destroy is meaningful;
+ *   - one handle must not be used from two threads at once.
+ */
+#ifndef MOECACHE_H
+#define MOECACHE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_OK 0
+#define MOE_EINVAL (-1) /* bad argument: shape, pointer, range */
+#define MOE_ENOMEM (-2) /* device or pinned-host allocation failed */
+#define MOE_EHIP (-3)   /* a HIP runtime call failed (text in moe_last_error) */
+#define MOE_ESTATE (-4) /* handle poisoned by an earlier MOE_EHIP */
+
+/* Block formats of the expert weights (GGUF-style, 32 weights per block).
+ * Q8_0: 34 bytes = fp16 scale d (little-endian) + 32 int8 q; weight d*q.
+ * Q4_0: 18 bytes = fp16 scale d + 16 bytes, byte j holding element j in its
+ *       low nibble and element j+16 in its high nibble; weight d*(n-8). */
+#define MOE_Q8_0 8
+#define MOE_Q4_0 2
+
+/* desc.flags */
+#define MOE_F_RESIDUAL 1u /* y = x + moe(x) instead of y = moe(x) */
+#define MOE_F_TRACE 2u    /* keep one moe_step_rec per routed expert per call */
+#define MOE_F_TIMING 4u   /* bracket router, FFN kernels and copies with HIP events */
+
+typedef struct moe_cache moe_cache; /* opaque, owned by the library */
+
+typedef struct {
+  int32_t n_layers;  /* MoE layers, >= 1 */
+  int32_t n_experts; /* routed experts per layer, 1..256 */
+  int32_t top_k;     /* experts per token, 1..min(n_experts, 16) */
+  int32_t hidden;    /* H, model width, multiple of 64, <= 8192 */
+  int32_t inter;     /* I, expert intermediate width, multiple of 64, <= 8192;
+                        top_k * inter <= 12288 (decode activations live in LDS) */
+  int32_t qtype;     /* MOE_Q8_0 or MOE_Q4_0 */
+  /* Expert store, caller-owned, must outlive the handle and stay unchanged.
+   * Layout: for layer l and expert e a payload of P bytes at offset
+   * (l*n_experts + e)*P, P = 3*M with M = inter*(hidden/32)*block_bytes:
+   *   [W_gate: inter rows x hidden | W_up: inter x hidden | W_down: hidden x inter]
+   * each row-major, one row per output, a row = its inputs as consecutive
+   * 32-weight blocks.  Must be pinned host memory from hipHostMalloc (e.g.
+   * moe_host_alloc); device memory is accepted too.  Pageable memory is
+   * rejected with MOE_EINVAL. */
+  const void *host_store;
+  uint64_t store_bytes; /* must equal n_layers*n_experts*P */
+  void *hip_stream;     /* caller's hipStream_t for all compute; NULL = null stream */
+  uint32_t flags;       /* MOE_F_* */
+} moe_model_desc;
+
+typedef struct {
+  uint64_t hits;               /* routed distinct experts found in a slot */
+  uint64_t misses;             /* routed distinct experts copied into a slot */
+  uint64_t evictions;          /* misses that displaced a resident expert */
+  uint64_t materialized_bytes; /* always misses * P */
+} moe_counters;
+
+/* One slot-table decision.  Within a layer call, records come in ascending
+ * expert id; step counts that layer's calls from 0 (reset by moe_cache_reset). */
+typedef struct {
+  int32_t layer, step, expert;
+  int32_t hit;     /* 1 hit, 0 miss */
+  int32_t slot;    /* slot the expert occupies after the call, 0..budget_slots-1 */
+  int32_t evicted; /* expert displaced by this miss, or -1 */
+} moe_step_rec;
+
+/* Per-kind totals of the MOE_F_TIMING events (kinds below). */
+typedef struct {
+  uint64_t launches; /* kernel launches, or copies for MOE_KIND_COPY */
+  double total_ms;   /* sum of event-bracketed durations */
+  uint64_t bytes;    /* algorithmic bytes moved by those launches / copies */
+  uint64_t flops;    /* algorithmic floating-point operations */
+} moe_kernel_stats;
+#define MOE_KIND_ROUTER 0 /* router logits + top-k kernel(s) */
+#define MOE_KIND_GATEUP 1 /* fused dequant + gate/up + SwiGLU */
+#define MOE_KIND_DOWN 2   /* dequant + down projection + weighted combine */
+#define MOE_KIND_COPY 3   /* miss materialisation copies (host to device) */
+#define MOE_KIND_COUNT 4
+
+/* Create a cache with budget_slots slots per layer (top_k <= budget_slots <=
+ * n_experts), all empty.  Allocates n_layers*budget_slots*P bytes of HBM for
+ * the slots plus small scratch, on the current HIP device.  MOE_EINVAL on a
+ * bad descriptor, MOE_ENOMEM if the slots do not fit. */
+int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache **out);
+
+/* One MoE layer call for n_tokens tokens (the Native Serving Path section's
+ * per-layer work).
+ *   x        device, [n_tokens][hidden] fp32, read only
+ *   router_w device, [hidden][n_experts] fp32 row-major (z = x W_r)
+ *   layer    0..n_layers-1
+ *   y        device, [n_tokens][hidden] fp32, written; must not overlap x
+ *   delta    host, nullable: this call's counter increments
+ * n_tokens == 1 takes the decode path (fp32 activations, GEMV kernels);
+ * n_tokens > 1 the prefill path (bf16 MFMA grouped GEMM: weights, x and the
+ * SwiGLU activations rounded to bf16, fp32 accumulation).
+ * Work is queued on desc.hip_stream; the host blocks once per call, until the
+ * routes are known.  y is ready when that stream passes this call; delta is
+ * final on return.  Routing reads x, so x must be ready on that stream. */
+int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                      int32_t layer, float *y, moe_counters *delta);
+
+/* As moe_layer_forward, also copying the routes out (host, nullable):
+ * topk_idx [n_tokens][top_k] int32 in rank order, topk_w [n_tokens][top_k] fp32. */
+int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                          int32_t layer, float *y, moe_counters *delta, int32_t *topk_idx,
+                          float *topk_w);
+
+/* Counters since creation or the last reset: one layer, or layer = -1 for the sum. */
+int moe_cache_counters(const moe_cache *c, int32_t layer, moe_counters *out);
+
+/* Move up to cap kept records (MOE_F_TRACE) into buf, oldest first; *n_out
+ * gets the number moved.  Records not moved stay for the next read. */
+int moe_cache_read_trace(moe_cache *c, moe_step_rec *buf, int64_t cap, int64_t *n_out);
+
+/* Empty every slot, zero counters, drop the trace and timing totals.
+ * Synchronises with the handle's streams first. */
+int moe_cache_reset(moe_cache *c);
+
+/* Totals of one MOE_KIND_* since creation or reset (needs MOE_F_TIMING).
+ * Synchronises with the handle's streams first. */
+int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out);
+
+/* Waits for the handle's work, frees everything the library allocated. NULL-safe. */
+void moe_cache_destroy(moe_cache *c);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *moe_last_error(void);
+
+/* Pinned (page-locked) host memory suitable as desc.host_store, via
+ * hipHostMalloc.  MOE_ENOMEM if it cannot be pinned. */
+int moe_host_alloc(uint64_t bytes, void **out);
+int moe_host_free(void *p);
+
+/* The slot table alone, with no HIP dependency (used to check it on the CPU).
+ * Same rule as inside moe_layer_forward: for one call with routed experts ids
+ * (any order, duplicates allowed), stamp the distinct ids in ascending order,
+ * count hits, then give each miss (ascending) the lowest free slot or the slot
+ * of the resident expert with the smallest stamp. */
+typedef struct moe_lru moe_lru;
+int moe_lru_create(int32_t n_experts, int32_t n_slots, uint64_t payload_bytes, int32_t layer,
+                   moe_lru **out);
+/* out: room for n records (one per distinct id is written); *n_out = records written. */
+int moe_lru_step(moe_lru *lru, const int32_t *ids, int32_t n, moe_step_rec *out, int32_t *n_out);
+int moe_lru_counters(const moe_lru *lru, moe_counters *out);
+void moe_lru_destroy(moe_lru *lru);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOECACHE_H */

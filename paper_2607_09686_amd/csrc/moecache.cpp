@@ -1,0 +1,472 @@
+// Host side of libmoecache: the C ABI declared in include/moecache.h.
+//
+// One handle = one model's expert store (pinned host memory, caller-owned),
+// per-layer HBM slot slabs, per-layer LRU slot tables, a side stream for the
+// miss copies, and small scratch buffers.  A layer call is: router kernel on
+// the caller's stream -> host waits for the routes -> LRU step -> miss copies
+// on the side stream -> FFN for hit experts on the caller's stream (overlaps
+// the copies) -> caller's stream waits for the copies -> FFN for the misses.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/moecache.h"
+#include "kernels.h"
+#include "slot_lru.h"
+
+using namespace moecache;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+struct TimedSpan {
+  int kind;
+  hipEvent_t start, stop;
+  uint64_t launches, bytes, flops;
+};
+
+}  // namespace
+
+struct moe_cache {
+  moe_model_desc d{};
+  int32_t C = 0;
+  int bb = 0;           // block bytes
+  int64_t M = 0, P = 0; // matrix bytes, payload bytes
+  hipStream_t main = nullptr, side = nullptr;
+  int device = 0;
+  bool poisoned = false;
+  const uint8_t *store = nullptr;
+
+  uint8_t *slots = nullptr;  // [L][C][P]
+  float *partial = nullptr;  // router split partials [grid][E]
+  uint32_t *counter = nullptr;
+  int32_t *topk_idx = nullptr;  // device [cap_tokens][k]
+  float *topk_w = nullptr;
+  float *zbuf = nullptr;  // prefill logits [cap_tokens][E]
+  int64_t cap_tokens = 0;
+  float *h = nullptr;  // decode SwiGLU activations [k][I]
+  int32_t *host_idx = nullptr;  // host mirrors [k] (decode)
+  float *host_w = nullptr;
+  hipEvent_t ev_route = nullptr, ev_copy = nullptr;
+
+  std::vector<SlotLru> lru;
+  std::vector<moe_step_rec> trace;
+  size_t trace_head = 0;
+  std::vector<moe_step_rec> recs;  // scratch for one call
+
+  // timing (MOE_F_TIMING)
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<TimedSpan> pending;
+  moe_kernel_stats stats[MOE_KIND_COUNT]{};
+
+  uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
+};
+
+namespace {
+
+#define HIP_TRY(c, expr)                                                                   \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) {                                                                \
+      if (c) (c)->poisoned = true;                                                         \
+      return fail(MOE_EHIP, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(e_), __FILE__, \
+                  __LINE__);                                                               \
+    }                                                                                      \
+  } while (0)
+
+hipEvent_t get_event(moe_cache *c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Fold completed timing spans into the totals.  Only called once the spans'
+// streams have been synchronised (or are known complete).
+int drain_timing(moe_cache *c) {
+  for (auto &sp : c->pending) {
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, sp.start, sp.stop));
+    auto &st = c->stats[sp.kind];
+    st.launches += sp.launches;
+    st.total_ms += ms;
+    st.bytes += sp.bytes;
+    st.flops += sp.flops;
+    c->ev_pool.push_back(sp.start);
+    c->ev_pool.push_back(sp.stop);
+  }
+  c->pending.clear();
+  return MOE_OK;
+}
+
+struct Span {
+  moe_cache *c;
+  hipStream_t s;
+  TimedSpan sp{};
+  bool on = false;
+  Span(moe_cache *c_, hipStream_t s_, int kind, uint64_t launches, uint64_t bytes, uint64_t flops)
+      : c(c_), s(s_) {
+    if (!(c->d.flags & MOE_F_TIMING)) return;
+    sp = TimedSpan{kind, get_event(c), get_event(c), launches, bytes, flops};
+    on = sp.start && sp.stop && hipEventRecord(sp.start, s) == hipSuccess;
+  }
+  void end() {
+    if (on && hipEventRecord(sp.stop, s) == hipSuccess) c->pending.push_back(sp);
+    on = false;
+  }
+};
+
+int check_desc(const moe_model_desc *d, int32_t budget) {
+  if (!d) return fail(MOE_EINVAL, "desc is NULL");
+  if (d->n_layers < 1 || d->n_experts < 1 || d->n_experts > 256)
+    return fail(MOE_EINVAL, "n_layers must be >= 1 and n_experts in [1, 256]");
+  if (d->top_k < 1 || d->top_k > d->n_experts || d->top_k > kMaxRouted)
+    return fail(MOE_EINVAL, "top_k must be in [1, min(n_experts, %d)]", kMaxRouted);
+  if (d->hidden < 64 || d->hidden % 64 || d->hidden > 8192 || d->inter < 64 || d->inter % 64 ||
+      d->inter > 8192)
+    return fail(MOE_EINVAL, "hidden and inter must be multiples of 64 in [64, 8192]");
+  if ((int64_t)d->top_k * d->inter > 12288)
+    return fail(MOE_EINVAL, "top_k * inter must be <= 12288 (decode activations are staged in LDS)");
+  if (d->qtype != MOE_Q8_0 && d->qtype != MOE_Q4_0) return fail(MOE_EINVAL, "qtype must be MOE_Q8_0 or MOE_Q4_0");
+  if (budget < d->top_k || budget > d->n_experts)
+    return fail(MOE_EINVAL, "budget_slots %d outside [top_k=%d, n_experts=%d]", budget, d->top_k,
+                d->n_experts);
+  if (!d->host_store) return fail(MOE_EINVAL, "host_store is NULL");
+  return MOE_OK;
+}
+
+void free_all(moe_cache *c) {
+  if (!c) return;
+  if (c->main || c->side) {
+    if (c->side) (void)hipStreamSynchronize(c->side);
+    (void)hipStreamSynchronize(c->main);
+  }
+  (void)hipFree(c->slots);
+  (void)hipFree(c->partial);
+  (void)hipFree(c->counter);
+  (void)hipFree(c->topk_idx);
+  (void)hipFree(c->topk_w);
+  (void)hipFree(c->zbuf);
+  (void)hipFree(c->h);
+  if (c->host_idx) (void)hipHostFree(c->host_idx);
+  if (c->host_w) (void)hipHostFree(c->host_w);
+  if (c->ev_route) (void)hipEventDestroy(c->ev_route);
+  if (c->ev_copy) (void)hipEventDestroy(c->ev_copy);
+  for (auto &sp : c->pending) {
+    (void)hipEventDestroy(sp.start);
+    (void)hipEventDestroy(sp.stop);
+  }
+  for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->side) (void)hipStreamDestroy(c->side);
+  delete c;
+}
+
+int ensure_tokens(moe_cache *c, int64_t T) {
+  if (T <= c->cap_tokens) return MOE_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  (void)hipFree(c->topk_idx);
+  (void)hipFree(c->topk_w);
+  (void)hipFree(c->zbuf);
+  c->topk_idx = nullptr;
+  c->topk_w = nullptr;
+  c->zbuf = nullptr;
+  c->cap_tokens = 0;
+  const int64_t k = c->d.top_k, E = c->d.n_experts;
+  if (hipMalloc(&c->topk_idx, T * k * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->topk_w, T * k * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->zbuf, T * E * sizeof(float)) != hipSuccess)
+    return fail(MOE_ENOMEM, "cannot allocate routing buffers for %lld tokens", (long long)T);
+  c->cap_tokens = T;
+  return MOE_OK;
+}
+
+int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer, float *y,
+                   moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  const moe_model_desc &d = c->d;
+  const int k = d.top_k;
+  if (c->d.flags & MOE_F_TIMING) {
+    int rc = drain_timing(c);  // the previous call's spans ended before its router sync
+    if (rc) return rc;
+  }
+  {
+    Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
+            2ull * d.hidden * d.n_experts);
+    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->counter,
+                                    c->topk_idx, c->topk_w, c->host_idx, c->host_w, c->main));
+    sp.end();
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
+  HIP_TRY(c, hipEventSynchronize(c->ev_route));
+
+  int32_t ids[kMaxRouted];
+  for (int i = 0; i < k; ++i) {
+    ids[i] = c->host_idx[i];
+    if (ids[i] < 0 || ids[i] >= d.n_experts) {
+      c->poisoned = true;
+      return fail(MOE_EHIP, "router produced expert id %d", ids[i]);
+    }
+  }
+  if (dbg_idx) std::memcpy(dbg_idx, ids, sizeof(int32_t) * k);
+  if (dbg_w) std::memcpy(dbg_w, c->host_w, sizeof(float) * k);
+
+  SlotLru &t = c->lru[layer];
+  const moe_counters before = t.counters();
+  c->recs.clear();
+  t.step(ids, k, c->recs);
+
+  // hit/miss per routed position, and the miss copies (ascending expert order)
+  ExpertList hits{}, misses{};
+  int n_copy = 0;
+  for (const auto &r : c->recs) n_copy += r.hit ? 0 : 1;
+  if (n_copy) {
+    Span sp(c, c->side, MOE_KIND_COPY, n_copy, (uint64_t)n_copy * c->P, 0);
+    for (const auto &r : c->recs) {
+      if (r.hit) continue;
+      const uint8_t *src = c->store + ((int64_t)layer * d.n_experts + r.expert) * c->P;
+      HIP_TRY(c, hipMemcpyAsync(c->slot_ptr(layer, r.slot), src, c->P, hipMemcpyDefault, c->side));
+    }
+    sp.end();
+    HIP_TRY(c, hipEventRecord(c->ev_copy, c->side));
+  }
+  for (int i = 0; i < k; ++i) {
+    const int32_t e = ids[i];
+    const int32_t s = t.slot_of(e);
+    bool hit = false;
+    for (const auto &r : c->recs)
+      if (r.expert == e) hit = r.hit;
+    ExpertList &L = hit ? hits : misses;
+    L.payload[L.n] = c->slot_ptr(layer, s);
+    L.pos[L.n] = i;
+    ++L.n;
+  }
+  const bool resid = d.flags & MOE_F_RESIDUAL;
+  const uint64_t gu_bytes = 2ull * c->M, dn_bytes = (uint64_t)c->M;
+  const uint64_t gu_flops = 4ull * d.hidden * d.inter, dn_flops = 2ull * d.hidden * d.inter;
+  bool wrote = false;
+  for (int pass = 0; pass < 2; ++pass) {
+    ExpertList &L = pass == 0 ? hits : misses;
+    if (!L.n) continue;
+    if (pass == 1) HIP_TRY(c, hipStreamWaitEvent(c->main, c->ev_copy, 0));
+    {
+      Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
+      HIP_TRY(c, launch_gateup(d.qtype, x, d.hidden, d.inter, L, c->h, c->main));
+      sp.end();
+    }
+    {
+      Span sp(c, c->main, MOE_KIND_DOWN, 1, L.n * dn_bytes, L.n * dn_flops);
+      int mode = wrote ? 2 : (resid ? 1 : 0);
+      HIP_TRY(c, launch_down(d.qtype, c->h, d.hidden, d.inter, L, c->topk_w, x, y, mode, c->main));
+      sp.end();
+    }
+    wrote = true;
+  }
+
+  if (d.flags & MOE_F_TRACE) c->trace.insert(c->trace.end(), c->recs.begin(), c->recs.end());
+  if (delta) {
+    const moe_counters &a = t.counters();
+    *delta = moe_counters{a.hits - before.hits, a.misses - before.misses,
+                          a.evictions - before.evictions,
+                          a.materialized_bytes - before.materialized_bytes};
+  }
+  return MOE_OK;
+}
+
+int forward_prefill(moe_cache *, const float *, int32_t, const float *, int32_t, float *,
+                    moe_counters *, int32_t *, float *);
+
+}  // namespace
+
+extern "C" {
+
+const char *moe_last_error(void) { return g_err.c_str(); }
+
+int moe_host_alloc(uint64_t bytes, void **out) {
+  if (!out || bytes == 0) return fail(MOE_EINVAL, "moe_host_alloc: bad arguments");
+  *out = nullptr;
+  if (hipHostMalloc(out, bytes, hipHostMallocDefault) != hipSuccess || !*out)
+    return fail(MOE_ENOMEM, "hipHostMalloc of %llu bytes failed", (unsigned long long)bytes);
+  return MOE_OK;
+}
+
+int moe_host_free(void *p) {
+  if (!p) return MOE_OK;
+  hipError_t e = hipHostFree(p);
+  return e == hipSuccess ? MOE_OK : fail(MOE_EHIP, "hipHostFree: %s", hipGetErrorString(e));
+}
+
+int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache **out) {
+  if (!out) return fail(MOE_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_desc(desc, budget_slots);
+  if (rc) return rc;
+  moe_cache *c = new (std::nothrow) moe_cache;
+  if (!c) return fail(MOE_ENOMEM, "out of host memory");
+  c->d = *desc;
+  c->C = budget_slots;
+  c->bb = desc->qtype == MOE_Q8_0 ? 34 : 18;
+  c->M = (int64_t)desc->inter * (desc->hidden / 32) * c->bb;
+  c->P = 3 * c->M;
+  c->store = static_cast<const uint8_t *>(desc->host_store);
+  c->main = static_cast<hipStream_t>(desc->hip_stream);
+  const uint64_t want = (uint64_t)desc->n_layers * desc->n_experts * c->P;
+  if (desc->store_bytes != want) {
+    delete c;
+    return fail(MOE_EINVAL, "store_bytes %llu != n_layers*n_experts*P = %llu",
+                (unsigned long long)desc->store_bytes, (unsigned long long)want);
+  }
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, desc->host_store) != hipSuccess ||
+      (attr.type != hipMemoryTypeHost && attr.type != hipMemoryTypeDevice)) {
+    (void)hipGetLastError();
+    delete c;
+    return fail(MOE_EINVAL, "host_store must be pinned host memory (hipHostMalloc) or device memory");
+  }
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return fail(MOE_EHIP, "no HIP device");
+  }
+  for (int32_t l = 0; l < desc->n_layers; ++l) c->lru.emplace_back(desc->n_experts, budget_slots, c->P, l);
+
+  const int64_t slot_bytes = (int64_t)desc->n_layers * budget_slots * c->P;
+  if (hipMalloc(&c->slots, slot_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    free_all(c);
+    return fail(MOE_ENOMEM, "cannot allocate %lld bytes of expert slots", (long long)slot_bytes);
+  }
+  const int grid = router_decode_grid(desc->hidden);
+  if (hipMalloc(&c->partial, (size_t)grid * desc->n_experts * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->counter, 64) != hipSuccess ||
+      hipMalloc(&c->h, (size_t)desc->top_k * desc->inter * sizeof(float)) != hipSuccess ||
+      hipHostMalloc(&c->host_idx, kMaxRouted * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
+      hipHostMalloc(&c->host_w, kMaxRouted * sizeof(float), hipHostMallocCoherent) != hipSuccess) {
+    (void)hipGetLastError();
+    free_all(c);
+    return fail(MOE_ENOMEM, "cannot allocate scratch buffers");
+  }
+  if (hipMemset(c->counter, 0, 64) != hipSuccess ||
+      hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_route, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_copy, hipEventDisableTiming) != hipSuccess) {
+    free_all(c);
+    return fail(MOE_EHIP, "HIP setup failed");
+  }
+  rc = ensure_tokens(c, 1);
+  if (rc) {
+    free_all(c);
+    return rc;
+  }
+  *out = c;
+  return MOE_OK;
+}
+
+int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                          int32_t layer, float *y, moe_counters *delta, int32_t *topk_idx,
+                          float *topk_w) {
+  if (!c) return fail(MOE_EINVAL, "handle is NULL");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  if (!x || !router_w || !y) return fail(MOE_EINVAL, "x, router_w and y must be non-NULL");
+  if (n_tokens < 1) return fail(MOE_EINVAL, "n_tokens must be >= 1");
+  if (layer < 0 || layer >= c->d.n_layers)
+    return fail(MOE_EINVAL, "layer %d outside [0, %d)", layer, c->d.n_layers);
+  const int64_t bytes = (int64_t)n_tokens * c->d.hidden * 4;
+  const char *xb = (const char *)x, *yb = (const char *)y;
+  if (xb < yb + bytes && yb < xb + bytes) return fail(MOE_EINVAL, "y overlaps x");
+  if (hipSetDevice(c->device) != hipSuccess) return fail(MOE_EHIP, "hipSetDevice failed");
+  if (n_tokens == 1) return forward_decode(c, x, router_w, layer, y, delta, topk_idx, topk_w);
+  return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
+}
+
+int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                      int32_t layer, float *y, moe_counters *delta) {
+  return moe_layer_forward_dbg(c, x, n_tokens, router_w, layer, y, delta, nullptr, nullptr);
+}
+
+int moe_cache_counters(const moe_cache *c, int32_t layer, moe_counters *out) {
+  if (!c || !out) return fail(MOE_EINVAL, "NULL argument");
+  if (layer < -1 || layer >= c->d.n_layers) return fail(MOE_EINVAL, "layer out of range");
+  moe_counters s{};
+  for (int32_t l = 0; l < c->d.n_layers; ++l) {
+    if (layer >= 0 && l != layer) continue;
+    const moe_counters &a = c->lru[l].counters();
+    s.hits += a.hits;
+    s.misses += a.misses;
+    s.evictions += a.evictions;
+    s.materialized_bytes += a.materialized_bytes;
+  }
+  *out = s;
+  return MOE_OK;
+}
+
+int moe_cache_read_trace(moe_cache *c, moe_step_rec *buf, int64_t cap, int64_t *n_out) {
+  if (!c || !n_out || cap < 0 || (cap > 0 && !buf)) return fail(MOE_EINVAL, "bad arguments");
+  const int64_t avail = (int64_t)(c->trace.size() - c->trace_head);
+  const int64_t n = std::min(avail, cap);
+  if (n > 0) std::memcpy(buf, c->trace.data() + c->trace_head, n * sizeof(moe_step_rec));
+  c->trace_head += n;
+  if (c->trace_head == c->trace.size()) {
+    c->trace.clear();
+    c->trace_head = 0;
+  }
+  *n_out = n;
+  return MOE_OK;
+}
+
+int moe_cache_reset(moe_cache *c) {
+  if (!c) return fail(MOE_EINVAL, "handle is NULL");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  HIP_TRY(c, hipStreamSynchronize(c->side));
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  int rc = drain_timing(c);
+  if (rc) return rc;
+  for (auto &t : c->lru) t.reset();
+  c->trace.clear();
+  c->trace_head = 0;
+  for (auto &s : c->stats) s = moe_kernel_stats{};
+  return MOE_OK;
+}
+
+int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
+  if (!c || !out || kind < 0 || kind >= MOE_KIND_COUNT) return fail(MOE_EINVAL, "bad arguments");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  HIP_TRY(c, hipStreamSynchronize(c->side));
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  int rc = drain_timing(c);
+  if (rc) return rc;
+  *out = c->stats[kind];
+  return MOE_OK;
+}
+
+void moe_cache_destroy(moe_cache *c) { free_all(c); }
+
+}  // extern "C"
+
+namespace {
+
+int forward_prefill(moe_cache *c, const float *, int32_t, const float *, int32_t, float *,
+                    moe_counters *, int32_t *, float *) {
+  (void)c;
+  return fail(MOE_EINVAL, "n_tokens > 1 (prefill) is not built yet");
+}
+
+}  // namespace

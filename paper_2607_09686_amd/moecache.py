@@ -1,0 +1,254 @@
+"""ctypes binding of libmoecache (include/moecache.h): argument marshalling only.
+
+Every step of a layer call (routing, the slot table, the copies, the FFN)
+runs inside the library; this module converts torch tensors and numpy arrays
+to pointers and raises on non-zero status codes.  PyTorch provides device
+memory and streams.  There is no fallback: if the library is missing or
+cannot be loaded, every entry point raises.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoecache.so")
+
+MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
+MOE_Q8_0, MOE_Q4_0 = 8, 2
+MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING = 1, 2, 4
+KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY = 0, 1, 2, 3
+KIND_NAMES = {KIND_ROUTER: "router", KIND_GATEUP: "gateup", KIND_DOWN: "down", KIND_COPY: "copy"}
+QTYPES = {"q8_0": MOE_Q8_0, "q4_0": MOE_Q4_0}
+
+
+class MoeError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"moecache error {code}: {msg}")
+        self.code = code
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("qtype", ctypes.c_int32), ("host_store", ctypes.c_void_p),
+                ("store_bytes", ctypes.c_uint64), ("hip_stream", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32)]
+
+
+class Counters(ctypes.Structure):
+    _fields_ = [("hits", ctypes.c_uint64), ("misses", ctypes.c_uint64),
+                ("evictions", ctypes.c_uint64), ("materialized_bytes", ctypes.c_uint64)]
+
+    def as_tuple(self):
+        return (self.hits, self.misses, self.evictions, self.materialized_bytes)
+
+    def __repr__(self):
+        return "Counters(hits=%d, misses=%d, evictions=%d, materialized_bytes=%d)" % self.as_tuple()
+
+
+class StepRec(ctypes.Structure):
+    _fields_ = [("layer", ctypes.c_int32), ("step", ctypes.c_int32), ("expert", ctypes.c_int32),
+                ("hit", ctypes.c_int32), ("slot", ctypes.c_int32), ("evicted", ctypes.c_int32)]
+
+
+class KernelStats(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_uint64), ("total_ms", ctypes.c_double),
+                ("bytes", ctypes.c_uint64), ("flops", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libmoecache.so (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run paper_2607_09686_amd.build.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    P = ctypes.POINTER
+    sig = {
+        "moe_cache_create": ([P(ModelDesc), i32, P(vp)], ctypes.c_int),
+        "moe_layer_forward": ([vp, vp, i32, vp, i32, vp, P(Counters)], ctypes.c_int),
+        "moe_layer_forward_dbg": ([vp, vp, i32, vp, i32, vp, P(Counters), vp, vp], ctypes.c_int),
+        "moe_cache_counters": ([vp, i32, P(Counters)], ctypes.c_int),
+        "moe_cache_read_trace": ([vp, P(StepRec), i64, P(i64)], ctypes.c_int),
+        "moe_cache_reset": ([vp], ctypes.c_int),
+        "moe_cache_kernel_stats": ([vp, i32, P(KernelStats)], ctypes.c_int),
+        "moe_cache_destroy": ([vp], None),
+        "moe_last_error": ([], ctypes.c_char_p),
+        "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
+        "moe_host_free": ([vp], ctypes.c_int),
+        "moe_lru_create": ([i32, i32, u64, i32, P(vp)], ctypes.c_int),
+        "moe_lru_step": ([vp, P(i32), i32, P(StepRec), P(i32)], ctypes.c_int),
+        "moe_lru_counters": ([vp, P(Counters)], ctypes.c_int),
+        "moe_lru_destroy": ([vp], None),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _check(rc):
+    if rc != MOE_OK:
+        msg = lib().moe_last_error()
+        raise MoeError(rc, msg.decode() if msg else "")
+
+
+def _stream_handle(stream):
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream  # torch.cuda.Stream
+
+
+def _dev_ptr(t, dtype_name, numel, what):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{what} must live on the GPU")
+    if str(t.dtype) != f"torch.{dtype_name}":
+        raise TypeError(f"{what} must be {dtype_name}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{what} has {t.numel()} elements, expected {numel}")
+    return t.data_ptr()
+
+
+class HostBuffer:
+    """Pinned host memory from moe_host_alloc, exposed as a numpy uint8 array."""
+
+    def __init__(self, nbytes):
+        p = ctypes.c_void_p()
+        _check(lib().moe_host_alloc(nbytes, ctypes.byref(p)))
+        self.ptr = p.value
+        self.nbytes = nbytes
+        self.array = np.ctypeslib.as_array((ctypes.c_uint8 * nbytes).from_address(self.ptr))
+
+    def free(self):
+        if self.ptr:
+            self.array = None
+            _check(lib().moe_host_free(self.ptr))
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class MoeCache:
+    """A per-layer expert-slot cache over an expert store (moe_cache_create)."""
+
+    def __init__(self, n_layers, n_experts, top_k, hidden, inter, qtype, store_ptr, store_bytes,
+                 budget_slots, stream=None, residual=False, trace=False, timing=False):
+        self.hidden, self.n_experts, self.top_k = hidden, n_experts, top_k
+        flags = (MOE_F_RESIDUAL if residual else 0) | (MOE_F_TRACE if trace else 0) | \
+                (MOE_F_TIMING if timing else 0)
+        q = QTYPES[qtype] if isinstance(qtype, str) else int(qtype)
+        self._desc = ModelDesc(n_layers, n_experts, top_k, hidden, inter, q, store_ptr, store_bytes,
+                               _stream_handle(stream), flags)
+        h = ctypes.c_void_p()
+        _check(lib().moe_cache_create(ctypes.byref(self._desc), budget_slots, ctypes.byref(h)))
+        self._h = h.value
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise RuntimeError("cache is closed")
+        return self._h
+
+    def layer_forward(self, x, router_w, layer, y, n_tokens=None, routes=False):
+        """y <- MoE layer(x); returns the counter delta (and routes if asked)."""
+        T = (x.numel() // self.hidden) if n_tokens is None else n_tokens
+        xp = _dev_ptr(x, "float32", T * self.hidden, "x")
+        wp = _dev_ptr(router_w, "float32", self.hidden * self.n_experts, "router_w")
+        yp = _dev_ptr(y, "float32", T * self.hidden, "y")
+        delta = Counters()
+        if not routes:
+            _check(lib().moe_layer_forward(self.handle, xp, T, wp, layer, yp, ctypes.byref(delta)))
+            return delta
+        idx = np.empty((T, self.top_k), np.int32)
+        w = np.empty((T, self.top_k), np.float32)
+        _check(lib().moe_layer_forward_dbg(self.handle, xp, T, wp, layer, yp, ctypes.byref(delta),
+                                           idx.ctypes.data, w.ctypes.data))
+        return delta, idx, w
+
+    def counters(self, layer=-1):
+        c = Counters()
+        _check(lib().moe_cache_counters(self.handle, layer, ctypes.byref(c)))
+        return c
+
+    def read_trace(self, cap=1 << 20):
+        out = []
+        buf = (StepRec * 65536)()
+        n = ctypes.c_int64()
+        while len(out) < cap:
+            _check(lib().moe_cache_read_trace(self.handle, buf, min(65536, cap - len(out)),
+                                              ctypes.byref(n)))
+            out.extend((r.layer, r.step, r.expert, r.hit, r.slot, r.evicted) for r in buf[:n.value])
+            if n.value == 0:
+                break
+        return out
+
+    def reset(self):
+        _check(lib().moe_cache_reset(self.handle))
+
+    def kernel_stats(self, kind):
+        s = KernelStats()
+        _check(lib().moe_cache_kernel_stats(self.handle, kind, ctypes.byref(s)))
+        return s
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().moe_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class SlotTable:
+    """The library's LRU slot table alone (moe_lru_*), usable without a GPU."""
+
+    def __init__(self, n_experts, n_slots, payload_bytes, layer=0):
+        h = ctypes.c_void_p()
+        _check(lib().moe_lru_create(n_experts, n_slots, payload_bytes, layer, ctypes.byref(h)))
+        self._h = h.value
+
+    def step(self, ids):
+        ids = np.ascontiguousarray(ids, np.int32)
+        out = (StepRec * max(1, ids.size))()
+        n = ctypes.c_int32()
+        _check(lib().moe_lru_step(self._h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                  ids.size, out, ctypes.byref(n)))
+        return [(r.layer, r.step, r.expert, r.hit, r.slot, r.evicted) for r in out[:n.value]]
+
+    def counters(self):
+        c = Counters()
+        _check(lib().moe_lru_counters(self._h, ctypes.byref(c)))
+        return c
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().moe_lru_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
