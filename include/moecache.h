@@ -53,6 +53,8 @@ extern "C" {
 #define MOE_F_RESIDUAL 1u /* y = x + moe(x) instead of y = moe(x) */
 #define MOE_F_TRACE 2u    /* keep one moe_step_rec per routed expert per call */
 #define MOE_F_TIMING 4u   /* bracket router, FFN kernels and copies with HIP events */
+#define MOE_F_PRENORM 8u  /* route and run the experts on x / sqrt(mean(x^2) + 1e-6) (per
+                             token, unit gain); the residual of MOE_F_RESIDUAL adds raw x */
 
 typedef struct moe_cache moe_cache; /* opaque, owned by the library */
 
@@ -160,6 +162,13 @@ const char *moe_last_error(void);
  * hipHostMalloc.  MOE_ENOMEM if it cannot be pinned. */
 int moe_host_alloc(uint64_t bytes, void **out);
 int moe_host_free(void *p);
+
+/* Host-to-device bandwidth of the copy path used for misses: n_chunks copies
+ * of chunk_bytes each, read consecutively from host_src (pinned), spread
+ * round-robin over n_streams new streams into one device buffer, timed with
+ * HIP events from the first copy to the last.  *gb_per_s = bytes / time. */
+int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, int32_t n_streams,
+                  double *gb_per_s);
 
 /* The slot table alone, with no HIP dependency (used to check it on the CPU).
  * Same rule as inside moe_layer_forward: for one call with routed experts ids

@@ -14,7 +14,10 @@ GPU path is timed against):
 The stack feeds each layer the previous layer's output plus its input
 (h_{l+1} = h_l + y_l, rounded to fp32 at the layer boundary, since a layer
 takes fp32 hidden states); this reading keeps the true layer-to-layer
-dependency of decoding.
+dependency of decoding.  With ``prenorm`` a layer routes and runs its experts
+on the RMS-normalised input x / sqrt(mean(x^2) + 1e-6) (unit gain), the
+pre-norm residual block of MoE transformers without attention; without it a
+deep stack of SwiGLU experts grows its activations without bound.
 
 ``moe_layer_bf16`` is the prefill variant: the dequantised weights d*q, the
 inputs x and the SwiGLU activations are each rounded to bfloat16 (nearest,
@@ -48,6 +51,15 @@ class Shape:
         return quant.payload_bytes(self.qtype, self.hidden, self.inter)
 
 
+EPS = 1e-6
+
+
+def rms_normalize(x):
+    """x / sqrt(mean(x^2) + 1e-6) per row, in fp64."""
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + EPS)
+
+
 def _experts(store, shape, layer, ids, bf16=False):
     out = {}
     for e in ids:
@@ -57,7 +69,7 @@ def _experts(store, shape, layer, ids, bf16=False):
     return out
 
 
-def moe_layer(x, router_w, store, shape, layer, lru=None, routes=None, tokens=None):
+def moe_layer(x, router_w, store, shape, layer, lru=None, routes=None, tokens=None, prenorm=False):
     """One layer call.
 
     x [T, H] fp32; router_w [H, E] fp32; store: the whole uint8 expert store.
@@ -66,10 +78,12 @@ def moe_layer(x, router_w, store, shape, layer, lru=None, routes=None, tokens=No
     (used when the GPU took the other side of a near-tie).
     ``tokens``: optional subset of token indices whose y is computed (the
     routing and the cache step always cover all tokens).
+    ``prenorm``: route and run the experts on rms_normalize(x).
     Returns dict(y [T,H] fp64 (rows outside ``tokens`` are nan), idx, w, gap, records).
     """
     shape = Shape.of(shape)
     x = np.atleast_2d(np.asarray(x, dtype=np.float32))
+    x = rms_normalize(x) if prenorm else x.astype(np.float64)
     idx, w, gap = router.route(x, router_w, shape.top_k)
     if routes is not None:
         idx, w = routes
@@ -80,14 +94,17 @@ def moe_layer(x, router_w, store, shape, layer, lru=None, routes=None, tokens=No
     ex = _experts(store, shape, layer, need)
     y = np.full((T, shape.hidden), np.nan)
     for t in tokens:
-        y[t] = ffn.combine(x[t].astype(np.float64), [ex[int(e)] for e in idx[t]], w[t])
+        y[t] = ffn.combine(x[t], [ex[int(e)] for e in idx[t]], w[t])
     return dict(y=y, idx=idx, w=w, gap=gap, records=records)
 
 
-def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, tokens=None):
-    """Prefill variant of ``moe_layer`` with bf16 rounding of weights, inputs and activations."""
+def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, tokens=None,
+                   prenorm=False):
+    """Prefill variant of ``moe_layer`` with bf16 rounding of weights, inputs and activations
+    (the inputs are rounded after the optional normalisation)."""
     shape = Shape.of(shape)
     x = np.atleast_2d(np.asarray(x, dtype=np.float32))
+    x = rms_normalize(x) if prenorm else x.astype(np.float64)
     idx, w, gap = router.route(x, router_w, shape.top_k)
     if routes is not None:
         idx, w = routes
@@ -96,7 +113,7 @@ def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, toke
     tokens = list(range(T) if tokens is None else tokens)
     need = sorted({int(e) for t in tokens for e in idx[t]})
     ex = _experts(store, shape, layer, need, bf16=True)
-    xb = bf16_round(x.astype(np.float64))
+    xb = bf16_round(x)
     y = np.full((T, shape.hidden), np.nan)
     for t in tokens:
         acc = np.zeros(shape.hidden)
@@ -108,7 +125,7 @@ def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, toke
     return dict(y=y, idx=idx, w=w, gap=gap, records=records)
 
 
-def run_stack(x_tokens, routers, store, shape, n_slots, decode=True, bf16=False):
+def run_stack(x_tokens, routers, store, shape, n_slots, decode=True, bf16=False, prenorm=False):
     """Decode (one token per layer call) or prefill (all tokens per call) through
     every layer from a cold cache.
 
@@ -126,7 +143,7 @@ def run_stack(x_tokens, routers, store, shape, n_slots, decode=True, bf16=False)
     for toks in calls:
         h = np.asarray(x_tokens[toks], dtype=np.float32)
         for l in range(L):
-            out = fn(h, routers[l], store, shape, l, lrus[l])
+            out = fn(h, routers[l], store, shape, l, lrus[l], prenorm=prenorm)
             inputs[(toks[0], l)] = h.copy()
             routes[(toks[0], l)] = (out["idx"], out["w"], out["gap"])
             records.extend(out["records"])

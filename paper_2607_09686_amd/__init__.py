@@ -4,4 +4,5 @@ The library is ``libmoecache.so`` (``include/moecache.h``), built in-tree by
 ``paper_2607_09686_amd.build``.  ``moecache`` is its ctypes binding.
 """
 from .moecache import (HostBuffer, MoeCache, MoeError, SlotTable, Counters,  # noqa: F401
-                       KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY, KIND_NAMES, lib)
+                       KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY, KIND_NAMES, lib,
+                       probe_h2d)

@@ -94,7 +94,7 @@ constexpr int kRouterRowsPerBlock = 64;
 __global__ __launch_bounds__(kThreads) void router_decode_kernel(
     const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int k,
     float *__restrict__ partial, uint32_t *counter, int32_t *idx, float *w, int32_t *host_idx,
-    float *host_w) {
+    float *host_w, float *inv_rms, int prenorm) {
   __shared__ float red[kThreads];
   __shared__ float zs[256];
   __shared__ int is_last;
@@ -122,11 +122,23 @@ __global__ __launch_bounds__(kThreads) void router_decode_kernel(
   __syncthreads();
   if (!is_last) return;
   __threadfence();
+  // RMS scale of the token (pre-norm): z(x / rms) = z(x) / rms
+  float ss = 0.f;
+  if (prenorm)
+    for (int i = tid; i < H; i += kThreads) ss = fmaf(x[i], x[i], ss);
+  red[tid] = ss;
+  __syncthreads();
+  for (int off = kThreads / 2; off >= 1; off >>= 1) {
+    if (tid < off) red[tid] += red[tid + off];
+    __syncthreads();
+  }
+  const float inv = prenorm ? 1.f / sqrtf(red[0] / (float)H + 1e-6f) : 1.f;
+  if (tid == 0) *inv_rms = inv;
   if (tid < E) {
     float s = 0.f;
     for (int b = 0; b < (int)gridDim.x; ++b)
       s += __hip_atomic_load(partial + b * E + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    zs[tid] = s;
+    zs[tid] = s * inv;
   }
   __syncthreads();
   if (tid == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -294,9 +306,10 @@ __device__ __forceinline__ float pair_dot(const uint8_t *p, const float *xs, flo
 
 __device__ __forceinline__ float silu(float s) { return s / (1.f + expf(-s)); }
 
-// Stage a K-vector in LDS plus the sum of each 32-wide block of it.
-__device__ __forceinline__ void stage_vec(const float *__restrict__ v, int K, float *xs, float *xsum) {
-  for (int i = threadIdx.x; i < K; i += kThreads) xs[i] = v[i];
+// Stage scale*v (K floats) in LDS plus the sum of each 32-wide block of it.
+__device__ __forceinline__ void stage_vec(const float *__restrict__ v, float scale, int K, float *xs,
+                                          float *xsum) {
+  for (int i = threadIdx.x; i < K; i += kThreads) xs[i] = v[i] * scale;
   __syncthreads();
   for (int b = threadIdx.x; b < K / 32; b += kThreads) {
     float s = 0.f;
@@ -307,7 +320,7 @@ __device__ __forceinline__ void stage_vec(const float *__restrict__ v, int K, fl
 
 struct GateUpParams {
   ExpertList L;
-  const float *x;
+  const float *x, *inv_rms;
   float *h;
   int H, I, rows;  // rows of gate (and of up) per block
 };
@@ -323,7 +336,7 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   const int64_t rowb = (int64_t)nb * Fmt<QT>::kBlockBytes;
   const int64_t mat = (int64_t)a.I * rowb;
   const uint8_t *base = a.L.payload[ei];
-  stage_vec(a.x, H, xs, xsum);
+  stage_vec(a.x, *a.inv_rms, H, xs, xsum);
   __syncthreads();
   const int items = 2 * a.rows * np;
   for (int it = threadIdx.x; it < items; it += kThreads) {
@@ -408,9 +421,9 @@ int router_decode_grid(int H) { return (H + kRouterRowsPerBlock - 1) / kRouterRo
 
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
                                 uint32_t *counter, int32_t *idx, float *w, int32_t *host_idx,
-                                float *host_w, hipStream_t s) {
+                                float *host_w, float *inv_rms, bool prenorm, hipStream_t s) {
   hipLaunchKernelGGL(router_decode_kernel, dim3(router_decode_grid(H)), dim3(kThreads), 0, s, x, wr,
-                     H, E, k, partial, counter, idx, w, host_idx, host_w);
+                     H, E, k, partial, counter, idx, w, host_idx, host_w, inv_rms, (int)prenorm);
   return hipGetLastError();
 }
 
@@ -426,9 +439,9 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
   return hipGetLastError();
 }
 
-hipError_t launch_gateup(int qtype, const float *x, int H, int I, const ExpertList &L, float *h,
-                         hipStream_t s) {
-  GateUpParams a{L, x, h, H, I, 0};
+hipError_t launch_gateup(int qtype, const float *x, const float *inv_rms, int H, int I,
+                         const ExpertList &L, float *h, hipStream_t s) {
+  GateUpParams a{L, x, inv_rms, h, H, I, 0};
   a.rows = pick_rows(I, L.n, 16);
   const int np = H / 64;
   size_t lds = sizeof(float) * ((size_t)H + H / 32 + 2 * (size_t)a.rows * np);

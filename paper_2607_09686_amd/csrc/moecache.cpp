@@ -56,7 +56,7 @@ struct moe_cache {
 
   uint8_t *slots = nullptr;  // [L][C][P]
   float *partial = nullptr;  // router split partials [grid][E]
-  uint32_t *counter = nullptr;
+  uint32_t *counter = nullptr;  // [0]: router block counter; float at [8]: 1/rms of the token
   int32_t *topk_idx = nullptr;  // device [cap_tokens][k]
   float *topk_w = nullptr;
   float *zbuf = nullptr;  // prefill logits [cap_tokens][E]
@@ -77,6 +77,7 @@ struct moe_cache {
   moe_kernel_stats stats[MOE_KIND_COUNT]{};
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
+  float *inv_rms() const { return reinterpret_cast<float *>(counter + 8); }
 };
 
 namespace {
@@ -205,19 +206,22 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
-  if (c->d.flags & MOE_F_TIMING) {
-    int rc = drain_timing(c);  // the previous call's spans ended before its router sync
-    if (rc) return rc;
-  }
   {
     Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
             2ull * d.hidden * d.n_experts);
     HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->counter,
-                                    c->topk_idx, c->topk_w, c->host_idx, c->host_w, c->main));
+                                    c->topk_idx, c->topk_w, c->host_idx, c->host_w, c->inv_rms(),
+                                    (d.flags & MOE_F_PRENORM) != 0, c->main));
     sp.end();
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
   HIP_TRY(c, hipEventSynchronize(c->ev_route));
+  if (c->d.flags & MOE_F_TIMING) {
+    // every span queued so far has completed: earlier calls' FFN kernels ran
+    // before this router on the same stream, and their copies before those kernels
+    int rc = drain_timing(c);
+    if (rc) return rc;
+  }
 
   int32_t ids[kMaxRouted];
   for (int i = 0; i < k; ++i) {
@@ -270,7 +274,7 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
     if (pass == 1) HIP_TRY(c, hipStreamWaitEvent(c->main, c->ev_copy, 0));
     {
       Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
-      HIP_TRY(c, launch_gateup(d.qtype, x, d.hidden, d.inter, L, c->h, c->main));
+      HIP_TRY(c, launch_gateup(d.qtype, x, c->inv_rms(), d.hidden, d.inter, L, c->h, c->main));
       sp.end();
     }
     {
@@ -458,6 +462,49 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
 }
 
 void moe_cache_destroy(moe_cache *c) { free_all(c); }
+
+int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, int32_t n_streams,
+                  double *gb_per_s) {
+  if (!host_src || !gb_per_s || chunk_bytes == 0 || n_chunks < 1 || n_streams < 1 || n_streams > 16)
+    return fail(MOE_EINVAL, "moe_probe_h2d: bad arguments");
+  uint8_t *dst = nullptr;
+  const uint64_t dst_bytes = chunk_bytes * (uint64_t)std::min(n_chunks, n_streams);
+  if (hipMalloc(&dst, dst_bytes) != hipSuccess) return fail(MOE_ENOMEM, "probe buffer");
+  std::vector<hipStream_t> st(n_streams, nullptr);
+  hipEvent_t start = nullptr, stop = nullptr;
+  std::vector<hipEvent_t> done(n_streams, nullptr);
+  int rc = MOE_OK;
+  float ms = 0.f;
+  auto cleanup = [&]() {
+    for (auto s_ : st)
+      if (s_) (void)hipStreamDestroy(s_);
+    for (auto e_ : done)
+      if (e_) (void)hipEventDestroy(e_);
+    if (start) (void)hipEventDestroy(start);
+    if (stop) (void)hipEventDestroy(stop);
+    (void)hipFree(dst);
+  };
+  const uint8_t *src = static_cast<const uint8_t *>(host_src);
+  bool ok = hipEventCreate(&start) == hipSuccess && hipEventCreate(&stop) == hipSuccess;
+  for (int i = 0; ok && i < n_streams; ++i)
+    ok = hipStreamCreateWithFlags(&st[i], hipStreamNonBlocking) == hipSuccess &&
+         hipEventCreateWithFlags(&done[i], hipEventDisableTiming) == hipSuccess;
+  ok = ok && hipDeviceSynchronize() == hipSuccess && hipEventRecord(start, st[0]) == hipSuccess;
+  for (int i = 1; ok && i < n_streams; ++i) ok = hipStreamWaitEvent(st[i], start, 0) == hipSuccess;
+  for (int j = 0; ok && j < n_chunks; ++j) {
+    int s_ = j % n_streams;
+    ok = hipMemcpyAsync(dst + (uint64_t)s_ * chunk_bytes, src + (uint64_t)j * chunk_bytes, chunk_bytes,
+                        hipMemcpyDefault, st[s_]) == hipSuccess;
+  }
+  for (int i = 1; ok && i < n_streams; ++i)
+    ok = hipEventRecord(done[i], st[i]) == hipSuccess && hipStreamWaitEvent(st[0], done[i], 0) == hipSuccess;
+  ok = ok && hipEventRecord(stop, st[0]) == hipSuccess && hipEventSynchronize(stop) == hipSuccess &&
+       hipEventElapsedTime(&ms, start, stop) == hipSuccess;
+  if (!ok) rc = fail(MOE_EHIP, "moe_probe_h2d: HIP call failed");
+  else *gb_per_s = (double)chunk_bytes * n_chunks / (ms * 1e6);
+  cleanup();
+  return rc;
+}
 
 }  // extern "C"
 

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libmoecache.so")
 
 MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
 MOE_Q8_0, MOE_Q4_0 = 8, 2
-MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING = 1, 2, 4
+MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING, MOE_F_PRENORM = 1, 2, 4, 8
 KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY = 0, 1, 2, 3
 KIND_NAMES = {KIND_ROUTER: "router", KIND_GATEUP: "gateup", KIND_DOWN: "down", KIND_COPY: "copy"}
 QTYPES = {"q8_0": MOE_Q8_0, "q4_0": MOE_Q4_0}
@@ -82,6 +82,7 @@ def lib():
         "moe_last_error": ([], ctypes.c_char_p),
         "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
         "moe_host_free": ([vp], ctypes.c_int),
+        "moe_probe_h2d": ([vp, u64, i32, i32, P(ctypes.c_double)], ctypes.c_int),
         "moe_lru_create": ([i32, i32, u64, i32, P(vp)], ctypes.c_int),
         "moe_lru_step": ([vp, P(i32), i32, P(StepRec), P(i32)], ctypes.c_int),
         "moe_lru_counters": ([vp, P(Counters)], ctypes.c_int),
@@ -151,10 +152,11 @@ class MoeCache:
     """A per-layer expert-slot cache over an expert store (moe_cache_create)."""
 
     def __init__(self, n_layers, n_experts, top_k, hidden, inter, qtype, store_ptr, store_bytes,
-                 budget_slots, stream=None, residual=False, trace=False, timing=False):
+                 budget_slots, stream=None, residual=False, trace=False, timing=False,
+                 prenorm=False):
         self.hidden, self.n_experts, self.top_k = hidden, n_experts, top_k
         flags = (MOE_F_RESIDUAL if residual else 0) | (MOE_F_TRACE if trace else 0) | \
-                (MOE_F_TIMING if timing else 0)
+                (MOE_F_TIMING if timing else 0) | (MOE_F_PRENORM if prenorm else 0)
         q = QTYPES[qtype] if isinstance(qtype, str) else int(qtype)
         self._desc = ModelDesc(n_layers, n_experts, top_k, hidden, inter, q, store_ptr, store_bytes,
                                _stream_handle(stream), flags)
@@ -219,6 +221,13 @@ class MoeCache:
             self.close()
         except Exception:
             pass
+
+
+def probe_h2d(host_ptr, chunk_bytes, n_chunks, n_streams=1):
+    """GB/s of host-to-device copies from pinned memory (moe_probe_h2d)."""
+    g = ctypes.c_double()
+    _check(lib().moe_probe_h2d(host_ptr, chunk_bytes, n_chunks, n_streams, ctypes.byref(g)))
+    return g.value
 
 
 class SlotTable:

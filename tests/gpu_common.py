@@ -61,9 +61,10 @@ def softmax_of(z, ids):
     return e / e.sum()
 
 
-def check_routes(x, wr, k, idx_gpu, w_gpu):
-    """Compare one call's routes. Returns (oracle_idx, oracle_w, flipped_tokens)."""
-    z = oracle_router.logits(x, wr)
+def check_routes(x, wr, k, idx_gpu, w_gpu, prenorm=False):
+    """Compare one call's routes. Returns (oracle_idx, oracle_w, z, flipped_tokens)."""
+    from oracle.layer import rms_normalize
+    z = oracle_router.logits(rms_normalize(x) if prenorm else x, wr)
     idx, w, gap = oracle_router.topk(z, k)
     flipped = []
     for t in range(idx.shape[0]):
@@ -99,7 +100,7 @@ def replay_trace(calls_by_layer, wl, budget):
 
 
 def oracle_layer_y(x, wr, store, wl, layer, idx_or, w_or, z, idx_gpu, flipped, bf16=False,
-                   tokens=None):
+                   tokens=None, prenorm=False):
     """Oracle y of one layer call; for tokens whose top-k flipped at a near-tie the
     GPU's set is used, weighted by the oracle's softmax over that set."""
     idx_use = idx_or.copy()
@@ -108,32 +109,33 @@ def oracle_layer_y(x, wr, store, wl, layer, idx_or, w_or, z, idx_gpu, flipped, b
         idx_use[t] = idx_gpu[t]
         w_use[t] = softmax_of(z[t], idx_gpu[t])
     fn = moe_layer_bf16 if bf16 else moe_layer
-    return fn(x, wr, store, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=tokens)["y"]
+    return fn(x, wr, store, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=tokens,
+              prenorm=prenorm)["y"]
 
 
-def decode_chain(cache, wl, store_ptr, X, routers_dev, record_inputs=True, residual=True):
-    """Run the decode chain h_{l+1} = h_l + y_l on the GPU for every token; returns
-    (final h [T,H] np, inputs {(t,l): np}, routes {(t,l): (idx, w)}, y {(t,l): np})."""
+def decode_chain(cache, wl, X, routers_dev, record_inputs=True):
+    """Decode every token through every layer on the GPU with the library's residual
+    flag (h_{l+1} = h_l + moe(h_l)), as the benchmark does.  Returns
+    (final h [T,H], inputs [T,L,H] fp32 or None, idx [T,L,k], w [T,L,k])."""
     torch = torch_cuda()
     T, H = X.shape
-    inputs, routes, ys = {}, {}, {}
+    L, k = wl.n_layers, wl.top_k
+    inputs = np.empty((T, L, H), np.float32) if record_inputs else None
+    idx_all = np.empty((T, L, k), np.int32)
+    w_all = np.empty((T, L, k), np.float32)
     h = torch.empty(H, dtype=torch.float32, device="cuda")
     y = torch.empty(H, dtype=torch.float32, device="cuda")
     out = np.empty_like(X)
     for t in range(T):
         h.copy_(torch.from_numpy(X[t]))
-        for l in range(wl.n_layers):
-            _, idx, w = cache.layer_forward(h, routers_dev[l], l, y, n_tokens=1, routes=True)
+        for l in range(L):
             if record_inputs:
-                inputs[(t, l)] = h.cpu().numpy()
-                ys[(t, l)] = y.cpu().numpy()
-            routes[(t, l)] = (idx, w)
-            if residual:
-                h, y = y, h
-            else:
-                h.add_(y)
+                inputs[t, l] = h.cpu().numpy()
+            _, idx, w = cache.layer_forward(h, routers_dev[l], l, y, n_tokens=1, routes=True)
+            idx_all[t, l], w_all[t, l] = idx[0], w[0]
+            h, y = y, h
         out[t] = h.cpu().numpy()
-    return out, inputs, routes, ys
+    return out, inputs, idx_all, w_all
 
 
 __all__ = ["log", "store_buffer", "make_cache", "check_routes", "check_y", "replay_trace",

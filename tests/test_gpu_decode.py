@@ -11,16 +11,17 @@ pytestmark = pytest.mark.gpu
 
 
 def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, store=None,
-               timing=False):
+               timing=False, prenorm=False):
     torch = torch_cuda()
     n_tokens = wl.n_tokens if n_tokens is None else n_tokens
     log(f"decode {wl.name} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
-        f"{wl.qtype} L={wl.n_layers} C={budget} T={n_tokens} residual={residual}")
+        f"{wl.qtype} L={wl.n_layers} C={budget} T={n_tokens} residual={residual} prenorm={prenorm}")
     keep, ptr, arr = store if store is not None else store_buffer(wl, device=device_store)
     R = synth.router(wl)
     X = synth.hidden(wl, n_tokens=n_tokens)
     Rd = torch.from_numpy(R).cuda()
-    cache = make_cache(wl, ptr, budget, trace=True, residual=residual, timing=timing)
+    cache = make_cache(wl, ptr, budget, trace=True, residual=residual, timing=timing,
+                       prenorm=prenorm)
     calls = [[] for _ in range(wl.n_layers)]
     worst = 0.0
     y = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
@@ -33,8 +34,9 @@ def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, st
             yg = y.cpu().numpy().astype(np.float64)
             if residual:
                 yg = yg - xh.astype(np.float64)
-            idx_or, w_or, z, flipped = check_routes(xh[None], R[l], wl.top_k, idx, w)
-            yo = oracle_layer_y(xh[None], R[l], arr, wl, l, idx_or, w_or, z, idx, flipped)
+            idx_or, w_or, z, flipped = check_routes(xh[None], R[l], wl.top_k, idx, w, prenorm)
+            yo = oracle_layer_y(xh[None], R[l], arr, wl, l, idx_or, w_or, z, idx, flipped,
+                                prenorm=prenorm)
             worst = max(worst, check_y(yg[None], yo, f"token {t} layer {l}"))
             calls[l].append(idx[0])
             assert delta.hits + delta.misses == len(set(idx[0].tolist()))
@@ -58,6 +60,13 @@ def test_tiny_decode_parity():
 def test_tiny_residual_mode():
     wl = synth.WORKLOADS["tiny"]
     run_decode(wl, wl.budget_slots, residual=True, n_tokens=16)[0].close()
+
+
+def test_prenorm_residual_multi_layer():
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=4, name="tiny4")
+    run_decode(wl, 4, residual=True, prenorm=True, n_tokens=16)[0].close()
+    wl = wl.with_(qtype="q4_0", name="tiny4_q4")
+    run_decode(wl, 5, residual=True, prenorm=True, n_tokens=8)[0].close()
 
 
 def test_full_cache_reaches_hit_rate_one():

@@ -164,3 +164,27 @@ def test_stack_is_residual_chain():
         y1 = layer.moe_layer(h1, R[1], store, shape, 1)["y"]
         np.testing.assert_array_equal(out["h"][t], (h1.astype(np.float64) + y1).astype(np.float32)[0])
         assert not np.array_equal(out["h"][t], x[t])
+
+
+def test_prenorm_definition_and_scale_invariance():
+    from oracle.layer import rms_normalize
+    # a vector of +-c has mean square c^2, so it normalises to +-1/sqrt(1 + 1e-6/c^2)
+    for c in (1.0, 3.0, 1e-2):
+        v = np.array([c, -c, c, c, -c, -c, c, -c])
+        np.testing.assert_allclose(rms_normalize(v), np.sign(v) / np.sqrt(1 + 1e-6 / c ** 2),
+                                   rtol=1e-15)
+    wl = synth.WORKLOADS["tiny"]
+    store = _random_store(wl)
+    shape = Shape.of(wl)
+    x = synth.hidden(wl, n_tokens=3)
+    wr = synth.router(wl)[0]
+    a = layer.moe_layer(x, wr, store, shape, 0, prenorm=True)
+    b = layer.moe_layer((4 * x).astype(np.float32), wr, store, shape, 0, prenorm=True)
+    np.testing.assert_array_equal(a["idx"], b["idx"])
+    np.testing.assert_allclose(a["y"], b["y"], rtol=1e-5, atol=1e-9)
+    # a stack with pre-norm stays bounded over many layers
+    wl48 = synth.WORKLOADS["tiny"].with_(n_layers=24)
+    st = _random_store(wl48)
+    out = layer.run_stack(synth.hidden(wl48, n_tokens=2), synth.router(wl48), st, wl48, 4,
+                          prenorm=True)
+    assert np.all(np.isfinite(out["h"])) and np.abs(out["h"]).max() < 100
