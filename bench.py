@@ -46,6 +46,10 @@ def parse():
     ap.add_argument("--budget", type=int, default=None, help="slots per layer (default: workload's)")
     ap.add_argument("--rho", type=float, default=None)
     ap.add_argument("--no-timing", action="store_true", help="no HIP events around kernels")
+    ap.add_argument("--copy-mode", default="kernel", choices=["kernel", "side", "sdma"],
+                    help="kernel: copy kernel on the compute stream (default); side: "
+                         "hipMemcpyAsync on a side stream overlapped with the hit experts; "
+                         "sdma: hipMemcpyAsync on the compute stream")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=None,
@@ -96,7 +100,7 @@ def main():
     timing = not args.no_timing
     cache = MoeCache(wl.n_layers, wl.n_experts, wl.top_k, wl.hidden, wl.inter, wl.qtype, hb.ptr,
                      wl.store_bytes, budget, stream=torch.cuda.current_stream(), residual=True,
-                     prenorm=True, timing=timing)
+                     prenorm=True, timing=timing, copy_mode=args.copy_mode)
     h = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
     y = torch.empty_like(h)
 
@@ -157,6 +161,7 @@ def main():
         "config": {"workload": wl.name, "n_layers": wl.n_layers, "hidden": wl.hidden,
                    "n_experts": wl.n_experts, "top_k": wl.top_k, "inter": wl.inter,
                    "qtype": wl.qtype, "budget_slots": budget, "n_tokens": wl.n_tokens, "rho": rho,
+                   "copy_mode": args.copy_mode,
                    "global_batch": 1, "seq_len": wl.n_tokens, "parallelism": "none"},
     }
     if timing:

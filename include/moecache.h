@@ -55,6 +55,14 @@ extern "C" {
 #define MOE_F_TIMING 4u   /* bracket router, FFN kernels and copies with HIP events */
 #define MOE_F_PRENORM 8u  /* route and run the experts on x / sqrt(mean(x^2) + 1e-6) (per
                              token, unit gain); the residual of MOE_F_RESIDUAL adds raw x */
+/* How decode copies the missed experts into their slots (default: one copy
+ * kernel for all of a call's misses on the caller's stream, then gate/up and
+ * down over all routed experts; nothing crosses streams): */
+#define MOE_F_SIDE_COPY 16u /* hipMemcpyAsync per miss on a library side stream while the
+                               hit experts run on the caller's stream, which then waits
+                               for the copies before the missed experts */
+#define MOE_F_SDMA_COPY 32u /* hipMemcpyAsync per miss on the caller's stream (copy
+                               engine instead of the copy kernel) */
 
 typedef struct moe_cache moe_cache; /* opaque, owned by the library */
 

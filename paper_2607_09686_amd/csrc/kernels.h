@@ -15,26 +15,39 @@ struct ExpertList {
   int32_t n;
 };
 
-// Decode router: one token.  partial: [grid][E] fp32 scratch; counter: one
-// uint32, zero on entry (left zero on exit).  Writes idx/w [k] to device and,
-// if non-null, to host-mapped mirrors.
+// Decode router: one token, two launches.  partial: [grid][E] fp32 scratch.
+// Writes idx/w [k] to device and, if non-null, to host-mapped mirrors.
 int router_decode_grid(int H);
-// inv_rms: device scalar written with 1/sqrt(mean(x^2)+1e-6) when prenorm,
-// else 1; the logits are scaled by it before top-k.
+// Also writes the digits xq [3][H] and block scales xsc [H/32] of x * s,
+// s = 1/sqrt(mean(x^2)+1e-6) when prenorm else 1; the logits are scaled by s.
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
-                                uint32_t *counter, int32_t *idx, float *w, int32_t *host_idx,
-                                float *host_w, float *inv_rms, bool prenorm, hipStream_t s);
+                                int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
+                                float *xsc, bool prenorm, hipStream_t s);
 
 // Prefill router: z = x W_r for T tokens into z [T][E], then top-k rows.
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k, float *z,
                                  int32_t *idx, float *w, hipStream_t s);
 
-// Decode FFN.  h: [k][I] fp32 scratch (row pos of each listed expert written
-// by gate/up, read by down).  mode of down: 0 y = sum, 1 y = x + sum, 2 y += sum.
-// x is scaled by *inv_rms (written by the router) when staged.
-hipError_t launch_gateup(int qtype, const float *x, const float *inv_rms, int H, int I,
-                         const ExpertList &L, float *h, hipStream_t s);
-hipError_t launch_down(int qtype, const float *h, int H, int I, const ExpertList &L, const float *w,
-                       const float *x, float *y, int mode, hipStream_t s);
+// Device scratch of the decode FFN (owned by the cache handle).
+struct DecodeScratch {
+  int8_t *xq;   // [3][H] digits of the (scaled) token, written by the router
+  float *xsc;   // [H/32]
+  float *h;     // [k][I] SwiGLU activations, written by gate/up
+  int8_t *hq;   // [3][k*I] their digits, written by gate/up
+  float *hsc;   // [k*I/32]
+};
+
+// Decode FFN.  Gate/up writes h rows (and their digits) at each listed
+// expert's top-k position; down reads the digits.  mode of down: 0 y = sum,
+// 1 y = x + sum, 2 y += sum.
+hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
+                         hipStream_t s);
+hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
+                       const float *w, const float *x, float *y, int mode, hipStream_t s);
+
+// Copy n payloads of `bytes` (multiple of 16, 16-byte aligned) src[i] -> dst[i]
+// with a copy kernel of `grid` blocks (host-pinned or device sources).
+hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
+                              int grid, hipStream_t s);
 
 }  // namespace moecache

@@ -2,8 +2,12 @@
 //
 // Router: z = x W_r (fp32), top-k by (-z, id) with wave shuffles, softmax over
 // the chosen k.  Decode FFN: block-dequant GEMV straight from the GGUF-style
-// Q8_0 / Q4_0 blocks in the slots, x staged in LDS, fp32 accumulation, fixed
-// summation order (results do not depend on scheduling).
+// Q8_0 / Q4_0 blocks in the slots.  The fp32 input vector of a GEMV is first
+// split, per 32-wide block b with scale s_b = max|v|/127, into three int8
+// "digits" v = s_b (D1 + D2/254 + D3/254^2) + O(6e-8 max|v|); each block's
+// dot product with the int8 (or 4-bit) weights is then three exact int32
+// dot4 sums, recombined in fp32 and scaled by d * s_b.  Fixed summation
+// order throughout: results do not depend on scheduling.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -87,25 +91,56 @@ __device__ void wave_topk(const float *z, int E, int k, int32_t *idx, float *w, 
   }
 }
 
+// Three int8 digits of v for the 32-wide block this lane's group of 32 lanes
+// holds (all 32 lanes call it together): s = max|v|/127 over the group,
+// D1 = rint(v/s), D2 = rint(254 (v/s - D1)), D3 = rint(254 (254 (v/s - D1) - D2)).
+// Returns s (0 for an all-zero block, digits 0).
+__device__ __forceinline__ float block_digits(float v, int8_t &d1, int8_t &d2, int8_t &d3) {
+  float m = fabsf(v);
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+  const float s = m * (1.f / 127.f);
+  const float t = s > 0.f ? v / s : 0.f;
+  const float a = __builtin_rintf(t);
+  const float r1 = (t - a) * 254.f;
+  const float b = __builtin_rintf(r1);
+  const float c = __builtin_rintf((r1 - b) * 254.f);
+  d1 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, a));
+  d2 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, b));
+  d3 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, c));
+  return s;
+}
+
 // ---------------------------------------------------------------- router ---
 
-constexpr int kRouterRowsPerBlock = 64;
+constexpr int kRouterRowsPerBlock = 32;
 
-__global__ __launch_bounds__(kThreads) void router_decode_kernel(
-    const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int k,
-    float *__restrict__ partial, uint32_t *counter, int32_t *idx, float *w, int32_t *host_idx,
-    float *host_w, float *inv_rms, int prenorm) {
+// Decode router, first kernel: block b accumulates z over rows [32b, 32b+32)
+// of W_r into partial[b][E] (no cross-block communication inside a launch:
+// on a multi-XCD GPU a device-scope fence costs more than a second launch).
+__global__ __launch_bounds__(kThreads) void router_partial_kernel(const float *__restrict__ x,
+                                                                  const float *__restrict__ wr,
+                                                                  int H, int E,
+                                                                  float *__restrict__ partial) {
   __shared__ float red[kThreads];
-  __shared__ float zs[256];
-  __shared__ int is_last;
   const int tid = threadIdx.x;
   const int phases = kThreads / E;  // E <= 256
   const int c = tid % E, ph = tid / E;
   const int r0 = blockIdx.x * kRouterRowsPerBlock;
   const int r1 = min(H, r0 + kRouterRowsPerBlock);
   float acc = 0.f;
-  if (ph < phases)
-    for (int r = r0 + ph; r < r1; r += phases) acc = fmaf(x[r], wr[(int64_t)r * E + c], acc);
+  if (ph < phases) {
+    float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+#pragma unroll
+    for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
+      const int r = r0 + ph + phases * j;
+      const bool ok = r < r1;
+      xv[j] = ok ? x[r] : 0.f;
+      wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
+  }
   red[tid] = acc;
   __syncthreads();
   if (tid < E) {
@@ -113,35 +148,82 @@ __global__ __launch_bounds__(kThreads) void router_decode_kernel(
     for (int p = 0; p < phases; ++p) s += red[p * E + tid];
     partial[blockIdx.x * E + tid] = s;
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t prev = atomicAdd(counter, 1u);
-    is_last = prev == gridDim.x - 1;
+}
+
+// Decode router, second kernel (one block): z = sum of the partials in block
+// order, scaled by 1/rms(x) (pre-norm); the scaled input as int8 digits with
+// per-block scales for the gate/up kernel; top-k + softmax.
+__global__ __launch_bounds__(kThreads) void router_finish_kernel(
+    const float *__restrict__ x, const float *__restrict__ partial, int nb, int H, int E, int k,
+    int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *__restrict__ xq,
+    float *__restrict__ xsc, int prenorm) {
+  extern __shared__ float xs_l[];  // [H]
+  __shared__ float red[kThreads];
+  __shared__ float zs[256];
+  __shared__ float wsum[kThreads / kWave];
+  const int tid = threadIdx.x;
+  const int phases = kThreads / E;
+  const int c = tid % E, ph = tid / E;
+  // loads: x (8 per lane per round) and the partials (16 per lane per round)
+  for (int i0 = 0; i0 < H; i0 += 8 * kThreads) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = i0 + j * kThreads + tid;
+      v[j] = i < H ? x[i] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = i0 + j * kThreads + tid;
+      if (i < H) xs_l[i] = v[j];
+    }
   }
+  const int per = (nb + phases - 1) / phases;
+  float s = 0.f;
+  if (ph < phases) {
+    const int b0 = ph * per, b1 = min(nb, b0 + per);
+    for (int b = b0; b < b1; b += 16) {
+      float v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) s += v[j];
+    }
+  }
+  red[tid] = s;
   __syncthreads();
-  if (!is_last) return;
-  __threadfence();
-  // RMS scale of the token (pre-norm): z(x / rms) = z(x) / rms
   float ss = 0.f;
   if (prenorm)
-    for (int i = tid; i < H; i += kThreads) ss = fmaf(x[i], x[i], ss);
-  red[tid] = ss;
+    for (int i = tid; i < H; i += kThreads) ss = fmaf(xs_l[i], xs_l[i], ss);
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
+  if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = ss;
   __syncthreads();
-  for (int off = kThreads / 2; off >= 1; off >>= 1) {
-    if (tid < off) red[tid] += red[tid + off];
-    __syncthreads();
-  }
-  const float inv = prenorm ? 1.f / sqrtf(red[0] / (float)H + 1e-6f) : 1.f;
-  if (tid == 0) *inv_rms = inv;
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
+  const float inv = prenorm ? 1.f / sqrtf(tot / (float)H + 1e-6f) : 1.f;
   if (tid < E) {
-    float s = 0.f;
-    for (int b = 0; b < (int)gridDim.x; ++b)
-      s += __hip_atomic_load(partial + b * E + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    zs[tid] = s * inv;
+    float z = 0.f;
+    for (int p = 0; p < phases; ++p) z += red[p * E + tid];
+    zs[tid] = z * inv;
+  }
+  // lanes 0..31 / 32..63 of a wave each hold one 32-wide block of x * inv
+  for (int b0 = 0; b0 < H / 32; b0 += 2 * (kThreads / kWave)) {
+    const int lane = tid & (kWave - 1);
+    const int b = b0 + 2 * (tid / kWave) + lane / 32;
+    const int i = 32 * b + (lane & 31);
+    const float v = b < H / 32 ? xs_l[i] * inv : 0.f;
+    int8_t d1, d2, d3;
+    const float sc = block_digits(v, d1, d2, d3);
+    if (b < H / 32) {
+      xq[i] = d1;
+      xq[H + i] = d2;
+      xq[2 * H + i] = d3;
+      if ((lane & 31) == 0) xsc[b] = sc;
+    }
   }
   __syncthreads();
-  if (tid == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (tid < kWave) wave_topk(zs, E, k, idx, w, host_idx, host_w);
 }
 
@@ -204,8 +286,9 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__rest
 //
 // A "pair" is two consecutive 32-weight blocks of one row (64 weights): 68
 // bytes for Q8_0, 36 for Q4_0, always 4-byte aligned because rows hold an
-// even number of blocks.  One thread turns one pair into one partial dot
-// product; partials of a row are then summed in pair order.
+// even number of blocks.  A lane turns a pair into a partial dot product with
+// the matching 64 inputs, given as three planes of int8 digits (16 dwords per
+// plane per pair) and two block scales.
 
 template <int QT>
 struct Fmt;
@@ -222,197 +305,340 @@ template <int QT>
 __device__ __forceinline__ void load_pair(const uint8_t *p, uint32_t (&wd)[Fmt<QT>::kPairDwords]) {
   const uint32_t *q = reinterpret_cast<const uint32_t *>(p);
 #pragma unroll
-  for (int i = 0; i < Fmt<QT>::kPairDwords; ++i) wd[i] = __builtin_nontemporal_load(q + i);
+  for (int i = 0; i < Fmt<QT>::kPairDwords; ++i) wd[i] = q[i];
 }
 
-// sum_j u_j * xs[j] over the four unsigned bytes of v.
-__device__ __forceinline__ float dot_u8x4(uint32_t v, const float *xs, float acc) {
-  acc = fmaf((float)(v & 0xffu), xs[0], acc);
-  acc = fmaf((float)((v >> 8) & 0xffu), xs[1], acc);
-  acc = fmaf((float)((v >> 16) & 0xffu), xs[2], acc);
-  acc = fmaf((float)(v >> 24), xs[3], acc);
-  return acc;
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
-// Q8_0 pair: bytes 0-1 d0 | 2-33 q0[0..31] | 34-35 d1 | 36-67 q1[0..31].
-// q is signed; with u = q ^ 0x80 (= q + 128), sum q x = sum u x - 128 sum x.
-__device__ __forceinline__ float pair_dot_q8(const uint32_t (&wd)[17], const float *xs,
-                                             float xsum0, float xsum1) {
-  const uint32_t f = 0x80808080u;
-  float d0 = half_bits_to_float(wd[0] & 0xffffu);
-  float d1 = half_bits_to_float(wd[8] >> 16);
-  uint32_t u0 = wd[0] ^ f;
-  float a0 = 0.f;
-  a0 = fmaf((float)((u0 >> 16) & 0xffu), xs[0], a0);
-  a0 = fmaf((float)(u0 >> 24), xs[1], a0);
-#pragma unroll
-  for (int i = 1; i < 8; ++i) a0 = dot_u8x4(wd[i] ^ f, xs + 2 + 4 * (i - 1), a0);
-  uint32_t u8 = wd[8] ^ f;
-  a0 = fmaf((float)(u8 & 0xffu), xs[30], a0);
-  a0 = fmaf((float)((u8 >> 8) & 0xffu), xs[31], a0);
-  float a1 = 0.f;
-#pragma unroll
-  for (int i = 9; i < 17; ++i) a1 = dot_u8x4(wd[i] ^ f, xs + 32 + 4 * (i - 9), a1);
-  return d0 * (a0 - 128.f * xsum0) + d1 * (a1 - 128.f * xsum1);
+// fp32 value of a block's digit dot products I1 + I2/254 + I3/254^2.
+__device__ __forceinline__ float recombine(int i1, int i2, int i3) {
+  return fmaf((float)i3, 1.f / 64516.f, fmaf((float)i2, 1.f / 254.f, (float)i1));
 }
 
-// Q4_0 pair: bytes 0-1 d0 | 2-17 nibbles of block 0 | 18-19 d1 | 20-35 block 1.
-// Nibble byte j: low -> element j, high -> element j+16; weight d*(n-8).
-__device__ __forceinline__ float nib_dot(uint32_t v, const float *xs, float acc) {
-  // v holds nibble bytes j..j+3; xs points at x[j] of the block
-  uint32_t lo = v & 0x0f0f0f0fu, hi = (v >> 4) & 0x0f0f0f0fu;
-  acc = dot_u8x4(lo, xs, acc);
-  acc = dot_u8x4(hi, xs + 16, acc);
-  return acc;
-}
-
-__device__ __forceinline__ float pair_dot_q4(const uint32_t (&wd)[9], const float *xs,
-                                             float xsum0, float xsum1) {
-  float d0 = half_bits_to_float(wd[0] & 0xffffu);
-  float d1 = half_bits_to_float(wd[4] >> 16);
-  float a0 = 0.f;
-  {  // nibble bytes 0,1 are the high half of dword 0
-    uint32_t v = wd[0] >> 16;
-    a0 = fmaf((float)(v & 0xfu), xs[0], a0);
-    a0 = fmaf((float)((v >> 4) & 0xfu), xs[16], a0);
-    a0 = fmaf((float)((v >> 8) & 0xfu), xs[1], a0);
-    a0 = fmaf((float)((v >> 12) & 0xfu), xs[17], a0);
-  }
-#pragma unroll
-  for (int i = 1; i < 4; ++i) a0 = nib_dot(wd[i], xs + 2 + 4 * (i - 1), a0);
-  {  // nibble bytes 14,15 are the low half of dword 4
-    uint32_t v = wd[4] & 0xffffu;
-    a0 = fmaf((float)(v & 0xfu), xs[14], a0);
-    a0 = fmaf((float)((v >> 4) & 0xfu), xs[30], a0);
-    a0 = fmaf((float)((v >> 8) & 0xfu), xs[15], a0);
-    a0 = fmaf((float)((v >> 12) & 0xfu), xs[31], a0);
-  }
-  float a1 = 0.f;
-#pragma unroll
-  for (int i = 5; i < 9; ++i) a1 = nib_dot(wd[i], xs + 32 + 4 * (i - 5), a1);
-  return d0 * (a0 - 8.f * xsum0) + d1 * (a1 - 8.f * xsum1);
-}
-
+// Partial dot of one pair with the inputs: D[c][j] = digit plane c, dword j of
+// the pair's 64 inputs; sc0/sc1 the two input block scales; dsum[c][0..1]
+// (Q4_0 only) the digit sums of the two blocks, for the offset 8.
 template <int QT>
-__device__ __forceinline__ float pair_dot(const uint8_t *p, const float *xs, float xsum0,
-                                          float xsum1) {
-  uint32_t wd[Fmt<QT>::kPairDwords];
-  load_pair<QT>(p, wd);
-  if constexpr (QT == 8)
-    return pair_dot_q8(wd, xs, xsum0, xsum1);
-  else
-    return pair_dot_q4(wd, xs, xsum0, xsum1);
+__device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwords],
+                                          const uint32_t *D, const float sc0, const float sc1,
+                                          const int *ds0, const int *ds1, int dstride) {
+  if constexpr (QT == 8) {
+    // bytes 0-1 d0 | 2-33 q0 | 34-35 d1 | 36-67 q1
+    const float d0 = half_bits_to_float(wd[0] & 0xffffu), d1 = half_bits_to_float(wd[8] >> 16);
+    int a1 = 0, a2 = 0, a3 = 0, b1 = 0, b2 = 0, b3 = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t q = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2);
+      a1 = sdot4(q, D[j], a1);
+      a2 = sdot4(q, D[16 + j], a2);
+      a3 = sdot4(q, D[32 + j], a3);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t q = wd[9 + j];
+      b1 = sdot4(q, D[8 + j], b1);
+      b2 = sdot4(q, D[24 + j], b2);
+      b3 = sdot4(q, D[40 + j], b3);
+    }
+    return fmaf(d0 * sc0, recombine(a1, a2, a3), d1 * sc1 * recombine(b1, b2, b3));
+  } else {
+    // bytes 0-1 d0 | 2-17 nibbles of block 0 | 18-19 d1 | 20-35 block 1;
+    // nibble byte j: low -> element j, high -> element j+16; weight d*(n-8)
+    const float d0 = half_bits_to_float(wd[0] & 0xffffu), d1 = half_bits_to_float(wd[4] >> 16);
+    int a1 = 0, a2 = 0, a3 = 0, b1 = 0, b2 = 0, b3 = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t v = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2);
+      const uint32_t lo = v & 0x0f0f0f0fu, hi = (v >> 4) & 0x0f0f0f0fu;
+      a1 = sdot4(hi, D[4 + j], sdot4(lo, D[j], a1));
+      a2 = sdot4(hi, D[20 + j], sdot4(lo, D[16 + j], a2));
+      a3 = sdot4(hi, D[36 + j], sdot4(lo, D[32 + j], a3));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t v = wd[5 + j];
+      const uint32_t lo = v & 0x0f0f0f0fu, hi = (v >> 4) & 0x0f0f0f0fu;
+      b1 = sdot4(hi, D[12 + j], sdot4(lo, D[8 + j], b1));
+      b2 = sdot4(hi, D[28 + j], sdot4(lo, D[24 + j], b2));
+      b3 = sdot4(hi, D[44 + j], sdot4(lo, D[40 + j], b3));
+    }
+    a1 -= 8 * ds0[0];
+    a2 -= 8 * ds0[dstride];
+    a3 -= 8 * ds0[2 * dstride];
+    b1 -= 8 * ds1[0];
+    b2 -= 8 * ds1[dstride];
+    b3 -= 8 * ds1[2 * dstride];
+    return fmaf(d0 * sc0, recombine(a1, a2, a3), d1 * sc1 * recombine(b1, b2, b3));
+  }
+}
+
+// The 48 digit dwords of pair p from LDS planes (plane c of length n bytes).
+__device__ __forceinline__ void load_digits(const uint8_t *planes, int64_t n, int p,
+                                            uint32_t (&D)[48]) {
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(planes + c * n + 64 * p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint4 v = src[i];
+      D[16 * c + 4 * i] = v.x;
+      D[16 * c + 4 * i + 1] = v.y;
+      D[16 * c + 4 * i + 2] = v.z;
+      D[16 * c + 4 * i + 3] = v.w;
+    }
+  }
 }
 
 __device__ __forceinline__ float silu(float s) { return s / (1.f + expf(-s)); }
 
-// Stage scale*v (K floats) in LDS plus the sum of each 32-wide block of it.
-__device__ __forceinline__ void stage_vec(const float *__restrict__ v, float scale, int K, float *xs,
-                                          float *xsum) {
-  for (int i = threadIdx.x; i < K; i += kThreads) xs[i] = v[i] * scale;
-  __syncthreads();
-  for (int b = threadIdx.x; b < K / 32; b += kThreads) {
-    float s = 0.f;
-    for (int j = 0; j < 32; ++j) s += xs[32 * b + j];
-    xsum[b] = s;
+// Sum over the `lanes` consecutive lanes of a group (power of 2), butterfly
+// order: the same on every run.
+__device__ __forceinline__ float group_sum(float v, int lanes) {
+  for (int off = lanes >> 1; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Stage n bytes of digit planes (3 planes, plane stride src_stride, the
+// wanted range starting at src_off) and their block scales into LDS; for Q4_0
+// also the digit sum of every 32-wide block.
+__device__ __forceinline__ void stage_digits(const int8_t *__restrict__ q, int64_t src_stride,
+                                             int64_t src_off, int n, const float *__restrict__ sc,
+                                             uint8_t *qL, float *scL, int *dsL, bool sums,
+                                             int nthreads) {
+  for (int c = 0; c < 3; ++c) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(q + c * src_stride + src_off);
+    uint4 *dst = reinterpret_cast<uint4 *>(qL + c * n);
+    for (int i = threadIdx.x; i < n / 16; i += nthreads) dst[i] = src[i];
+  }
+  for (int i = threadIdx.x; i < n / 32; i += nthreads) scL[i] = sc[i];
+  if (sums) {
+    __syncthreads();
+    for (int i = threadIdx.x; i < 3 * (n / 32); i += nthreads) {
+      const int c = i / (n / 32), b = i % (n / 32);
+      const int8_t *v = reinterpret_cast<const int8_t *>(qL + c * n + 32 * b);
+      int t = 0;
+#pragma unroll 8
+      for (int j = 0; j < 32; ++j) t += v[j];
+      dsL[c * (n / 32) + b] = t;
+    }
   }
 }
 
 struct GateUpParams {
   ExpertList L;
-  const float *x, *inv_rms;
-  float *h;
-  int H, I, rows;  // rows of gate (and of up) per block
+  const int8_t *xq;  // input digits [3][H]
+  const float *xsc;  // input block scales [H/32]
+  float *h;          // SwiGLU activations [k][I]
+  int8_t *hq;        // their digits [3][k*I]
+  float *hsc;        // their block scales [k*I/32]
+  int H, I, k;
+  int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs per lane
 };
 
-// grid: n experts x (I / rows).  h[pos][r] = silu(g_r) * u_r.
+constexpr int kGateUpThreads = 512;
+
+// One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
+// lanes handles pairs l, l+lanes, ... of both rows.  A block covers whole
+// 32-row groups of h (512/lanes rows), so it also writes their digits.
+// grid: n experts x ceil(I / rows_per_block).
 template <int QT>
-__global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
-  extern __shared__ float smem[];
+__global__ __launch_bounds__(kGateUpThreads) void gateup_kernel(GateUpParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
   const int H = a.H, nb = H / 32, np = nb / 2;
-  float *xs = smem, *xsum = xs + H, *part = xsum + nb;  // part[2][rows][np]
-  const int tiles = a.I / a.rows;
-  const int ei = blockIdx.x / tiles, r0 = (blockIdx.x % tiles) * a.rows;
-  const int64_t rowb = (int64_t)nb * Fmt<QT>::kBlockBytes;
-  const int64_t mat = (int64_t)a.I * rowb;
-  const uint8_t *base = a.L.payload[ei];
-  stage_vec(a.x, *a.inv_rms, H, xs, xsum);
-  __syncthreads();
-  const int items = 2 * a.rows * np;
-  for (int it = threadIdx.x; it < items; it += kThreads) {
-    int m = it / (a.rows * np), rem = it % (a.rows * np);
-    int r = rem / np, p = rem % np;
-    const uint8_t *ptr = base + m * mat + (int64_t)(r0 + r) * rowb + (int64_t)p * 2 * Fmt<QT>::kBlockBytes;
-    part[it] = pair_dot<QT>(ptr, xs + 64 * p, xsum[2 * p], xsum[2 * p + 1]);
-  }
-  __syncthreads();
-  for (int r = threadIdx.x; r < a.rows; r += kThreads) {
-    float g = 0.f, u = 0.f;
-    for (int p = 0; p < np; ++p) {
-      g += part[r * np + p];
-      u += part[(a.rows + r) * np + p];
+  uint8_t *qL = smem8;                                    // [3][H]
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * H);  // [H/32]
+  int *dsL = reinterpret_cast<int *>(scL + nb);           // [3][H/32]
+  float *hL = reinterpret_cast<float *>(dsL + 3 * nb);    // [rows per block]
+  const int upb = kGateUpThreads / a.lanes;
+  const int bpe = (a.I + upb - 1) / upb;
+  const int ei = blockIdx.x / bpe, r0 = (blockIdx.x % bpe) * upb;
+  const int r = r0 + threadIdx.x / a.lanes;
+  const int l = threadIdx.x & (a.lanes - 1);
+  const bool active = r < a.I;
+  const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
+  const uint8_t *gate = a.L.payload[ei] + (int64_t)r * rowb, *up = gate + mat;
+  uint32_t wg[2][PD], wu[2][PD];
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const int p = l + m * a.lanes;
+    if (active && m < a.mpairs && p < np) {
+      load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
+      load_pair<QT>(up + (int64_t)p * 2 * BB, wu[m]);
     }
-    a.h[(int64_t)a.L.pos[ei] * a.I + r0 + r] = silu(g) * u;
+  }
+  stage_digits(a.xq, H, 0, H, a.xsc, qL, scL, dsL, QT == 2, kGateUpThreads);
+  __syncthreads();
+  float g = 0.f, u = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += 2) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const int p = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && p < np) {
+          load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
+          load_pair<QT>(up + (int64_t)p * 2 * BB, wu[m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int p = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && p < np) {
+        uint32_t D[48];
+        load_digits(qL, H, p, D);
+        const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
+        g += pair_dot<QT>(wg[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+        u += pair_dot<QT>(wu[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+      }
+    }
+  }
+  g = group_sum(g, a.lanes);
+  u = group_sum(u, a.lanes);
+  if (l == 0) hL[threadIdx.x / a.lanes] = active ? silu(g) * u : 0.f;
+  __syncthreads();
+  // the block's rows of h, and their digits (one 32-lane group per 32 rows)
+  if ((int)threadIdx.x < upb) {
+    const int rr = r0 + threadIdx.x;
+    const float v = hL[threadIdx.x];
+    int8_t d1, d2, d3;
+    const float sc = block_digits(v, d1, d2, d3);
+    if (rr < a.I) {
+      const int64_t i = (int64_t)a.L.pos[ei] * a.I + rr, KI = (int64_t)a.k * a.I;
+      a.h[i] = v;
+      a.hq[i] = d1;
+      a.hq[KI + i] = d2;
+      a.hq[2 * KI + i] = d3;
+      if ((rr & 31) == 0) a.hsc[i / 32] = sc;
+    }
   }
 }
 
 struct DownParams {
   ExpertList L;
-  const float *h, *w, *x;
+  const int8_t *hq;  // activation digits [3][k*I]
+  const float *hsc;  // their block scales [k*I/32]
+  const float *w, *x;
   float *y;
-  int H, I, rows, mode;
+  int H, I, k, mode;
+  int lanes, mpairs;  // as in the gate/up kernel
+  int rows;           // output rows per block: rows * n * lanes <= 256
 };
 
-// grid: H / rows.  y[j] (+)= sum_i w[pos_i] * (W_down,i h_i)_j, experts in list order.
+// One unit = (output row j, expert i), `lanes` lanes, lane l handling pairs
+// l, l+lanes, ... (three in flight).  grid: ceil(H / rows).
+// y[j] (+)= sum over the listed experts, in list order, of w[pos_i] (W_down,i h_i)_j.
 template <int QT>
 __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
-  extern __shared__ float smem[];
+  extern __shared__ __align__(16) uint8_t smem8[];
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
   const int I = a.I, nb = I / 32, np = nb / 2, n = a.L.n;
-  float *hs = smem, *hsum = hs + n * I, *part = hsum + n * nb;  // part[n][rows][np]
+  uint8_t *qL = smem8;                                        // [n][3][I]
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * I);  // [n][I/32]
+  int *dsL = reinterpret_cast<int *>(scL + n * nb);           // [n][3][I/32]
+  float *res = reinterpret_cast<float *>(dsL + 3 * n * nb);   // [rows][n]
   const int j0 = blockIdx.x * a.rows;
-  const int64_t rowb = (int64_t)nb * Fmt<QT>::kBlockBytes;
-  const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * Fmt<QT>::kBlockBytes);
-  for (int i = 0; i < n; ++i) {
-    for (int c = threadIdx.x; c < I; c += kThreads) hs[i * I + c] = a.h[(int64_t)a.L.pos[i] * I + c];
+  const int unit = threadIdx.x / a.lanes, l = threadIdx.x & (a.lanes - 1);
+  const int i = unit % n, rr = unit / n, j = j0 + rr;
+  const bool active = rr < a.rows && j < a.H;
+  const int64_t rowb = (int64_t)nb * BB;
+  const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
+  const uint8_t *row = a.L.payload[i] + 2 * mat + (int64_t)j * rowb;
+  uint32_t wd[3][PD];
+#pragma unroll
+  for (int m = 0; m < 3; ++m) {
+    const int p = l + m * a.lanes;
+    if (active && m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
   }
+  for (int e = 0; e < n; ++e)
+    stage_digits(a.hq, (int64_t)a.k * I, (int64_t)a.L.pos[e] * I, I, a.hsc + (int64_t)a.L.pos[e] * nb,
+                 qL + 3 * e * I, scL + e * nb, dsL + 3 * e * nb, QT == 2, kThreads);
   __syncthreads();
-  for (int b = threadIdx.x; b < n * nb; b += kThreads) {
-    float s = 0.f;
-    for (int j = 0; j < 32; ++j) s += hs[32 * b + j];
-    hsum[b] = s;
-  }
-  __syncthreads();
-  const int items = n * a.rows * np;
-  for (int it = threadIdx.x; it < items; it += kThreads) {
-    int i = it / (a.rows * np), rem = it % (a.rows * np);
-    int r = rem / np, p = rem % np;
-    const uint8_t *ptr = a.L.payload[i] + 2 * mat + (int64_t)(j0 + r) * rowb +
-                         (int64_t)p * 2 * Fmt<QT>::kBlockBytes;
-    part[it] = pair_dot<QT>(ptr, hs + i * I + 64 * p, hsum[i * nb + 2 * p], hsum[i * nb + 2 * p + 1]);
-  }
-  __syncthreads();
-  for (int r = threadIdx.x; r < a.rows; r += kThreads) {
-    const int j = j0 + r;
-    float acc = a.mode == 2 ? a.y[j] : (a.mode == 1 ? a.x[j] : 0.f);
-    for (int i = 0; i < n; ++i) {
-      float s = 0.f;
-      for (int p = 0; p < np; ++p) s += part[(i * a.rows + r) * np + p];
-      acc = fmaf(a.w[a.L.pos[i]], s, acc);
+  float acc = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += 3) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < 3; ++m) {
+        const int p = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
+      }
     }
-    a.y[j] = acc;
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      const int p = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && p < np) {
+        uint32_t D[48];
+        load_digits(qL + 3 * i * I, I, p, D);
+        const int *ds = dsL + 3 * i * nb;
+        acc += pair_dot<QT>(wd[m], D, scL[i * nb + 2 * p], scL[i * nb + 2 * p + 1], ds + 2 * p,
+                            ds + 2 * p + 1, nb);
+      }
+    }
+  }
+  acc = group_sum(acc, a.lanes);
+  if (active && l == 0) res[rr * n + i] = acc;
+  __syncthreads();
+  for (int t = threadIdx.x; t < a.rows; t += kThreads) {
+    const int jj = j0 + t;
+    if (jj >= a.H) continue;
+    float v = a.mode == 2 ? a.y[jj] : (a.mode == 1 ? a.x[jj] : 0.f);
+    for (int ii = 0; ii < n; ++ii) v = fmaf(a.w[a.L.pos[ii]], res[t * n + ii], v);
+    a.y[jj] = v;
   }
 }
 
-int pick_rows(int total, int per_tile_blocks, int max_rows) {
-  // largest power-of-two row count <= max_rows dividing total that still
-  // gives at least 512 blocks, else the smallest that divides
-  int best = 0;
-  for (int r = 1; r <= max_rows; r <<= 1)
-    if (total % r == 0) {
-      if (best == 0) best = r;
-      if ((int64_t)per_tile_blocks * (total / r) >= 512) best = r;
+// Copy the payloads of the listed misses (P bytes each, 16-byte aligned) from
+// the store into their slots: 16-byte loads and stores, four in flight per
+// thread, grid-strided over all misses' bytes.
+struct CopyParams {
+  const uint4 *src[kMaxRouted];
+  uint4 *dst[kMaxRouted];
+  int n;
+  int64_t p16;  // payload size in 16-byte units
+};
+
+__global__ __launch_bounds__(kThreads) void materialize_kernel(CopyParams a) {
+  const int64_t total = a.p16 * a.n;
+  const int64_t st = (int64_t)gridDim.x * kThreads;
+  int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  for (; i + 3 * st < total; i += 4 * st) {
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = i + j * st, e = g / a.p16;
+      v[j] = a.src[e][g - e * a.p16];
     }
-  return best;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = i + j * st, e = g / a.p16;
+      a.dst[e][g - e * a.p16] = v[j];
+    }
+  }
+  for (; i < total; i += st) {
+    const int64_t e = i / a.p16;
+    a.dst[e][i - e * a.p16] = a.src[e][i - e * a.p16];
+  }
+}
+
+// Lanes per row (a power of two) and pairs per lane for rows of np pairs,
+// when a lane keeps `in_flight` pairs of a row loading at once: few load
+// rounds first, then few idle lanes, then fewer lanes.
+void pick_lanes(int np, int in_flight, int max_lanes, int &lanes, int &mpairs) {
+  double best = -1e9;
+  lanes = max_lanes;
+  mpairs = (np + max_lanes - 1) / max_lanes;
+  for (int L = 1; L <= max_lanes; L <<= 1) {
+    const int M = (np + L - 1) / L;
+    const int rounds = (M + in_flight - 1) / in_flight;
+    const double score = (double)np / (L * M) - 0.25 * (rounds - 1) - 0.001 * L;
+    if (score > best) {
+      best = score;
+      lanes = L;
+      mpairs = M;
+    }
+  }
 }
 
 }  // namespace
@@ -420,10 +646,14 @@ int pick_rows(int total, int per_tile_blocks, int max_rows) {
 int router_decode_grid(int H) { return (H + kRouterRowsPerBlock - 1) / kRouterRowsPerBlock; }
 
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
-                                uint32_t *counter, int32_t *idx, float *w, int32_t *host_idx,
-                                float *host_w, float *inv_rms, bool prenorm, hipStream_t s) {
-  hipLaunchKernelGGL(router_decode_kernel, dim3(router_decode_grid(H)), dim3(kThreads), 0, s, x, wr,
-                     H, E, k, partial, counter, idx, w, host_idx, host_w, inv_rms, (int)prenorm);
+                                int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
+                                float *xsc, bool prenorm, hipStream_t s) {
+  const int nb = router_decode_grid(H);
+  hipLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, x, wr, H, E, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), sizeof(float) * (size_t)H, s, x,
+                     partial, nb, H, E, k, idx, w, host_idx, host_w, xq, xsc, (int)prenorm);
   return hipGetLastError();
 }
 
@@ -439,31 +669,47 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
   return hipGetLastError();
 }
 
-hipError_t launch_gateup(int qtype, const float *x, const float *inv_rms, int H, int I,
-                         const ExpertList &L, float *h, hipStream_t s) {
-  GateUpParams a{L, x, inv_rms, h, H, I, 0};
-  a.rows = pick_rows(I, L.n, 16);
+hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
+                         hipStream_t s) {
   const int np = H / 64;
-  size_t lds = sizeof(float) * ((size_t)H + H / 32 + 2 * (size_t)a.rows * np);
-  dim3 grid(L.n * (I / a.rows));
+  GateUpParams a{L, S.xq, S.xsc, S.h, S.hq, S.hsc, H, I, k, 0, 0};
+  pick_lanes(np, 2, 16, a.lanes, a.mpairs);
+  const int upb = kGateUpThreads / a.lanes;  // a multiple of 32 rows
+  const size_t lds = 3 * (size_t)H + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
+  dim3 grid(L.n * ((I + upb - 1) / upb));
   if (qtype == 8)
-    hipLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kThreads), lds, s, a);
+    hipLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kGateUpThreads), lds, s, a);
   else
-    hipLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kThreads), lds, s, a);
+    hipLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kGateUpThreads), lds, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_down(int qtype, const float *h, int H, int I, const ExpertList &L, const float *w,
-                       const float *x, float *y, int mode, hipStream_t s) {
-  DownParams a{L, h, w, x, y, H, I, 0, mode};
-  a.rows = pick_rows(H, 1, 16);
-  const int np = I / 64, nb = I / 32;
-  size_t lds = sizeof(float) * ((size_t)L.n * I + (size_t)L.n * nb + (size_t)L.n * a.rows * np);
-  dim3 grid(H / a.rows);
+hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
+                       const float *w, const float *x, float *y, int mode, hipStream_t s) {
+  const int np = I / 64;
+  DownParams a{L, S.hq, S.hsc, w, x, y, H, I, k, mode, 0, 0, 0};
+  pick_lanes(np, 3, 64, a.lanes, a.mpairs);
+  a.rows = kThreads / (a.lanes * L.n);
+  if (a.rows < 1) return hipErrorInvalidValue;
+  const size_t lds = 3 * (size_t)L.n * I + 4 * (size_t)L.n * (I / 32) * 4 + 4 * (size_t)a.rows * L.n;
+  dim3 grid((H + a.rows - 1) / a.rows);
   if (qtype == 8)
     hipLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, a);
   else
     hipLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
+                              int grid, hipStream_t s) {
+  CopyParams a{};
+  for (int i = 0; i < n; ++i) {
+    a.src[i] = reinterpret_cast<const uint4 *>(src[i]);
+    a.dst[i] = reinterpret_cast<uint4 *>(dst[i]);
+  }
+  a.n = n;
+  a.p16 = bytes / 16;
+  hipLaunchKernelGGL(materialize_kernel, dim3(grid), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

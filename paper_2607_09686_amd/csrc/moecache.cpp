@@ -36,6 +36,8 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
+constexpr int kCopyGrid = 64;  // copy-kernel blocks: enough requests in flight to fill PCIe
+
 struct TimedSpan {
   int kind;
   hipEvent_t start, stop;
@@ -56,7 +58,10 @@ struct moe_cache {
 
   uint8_t *slots = nullptr;  // [L][C][P]
   float *partial = nullptr;  // router split partials [grid][E]
-  uint32_t *counter = nullptr;  // [0]: router block counter; float at [8]: 1/rms of the token
+  int8_t *xq = nullptr;         // decode: digits of the scaled token [3][H]
+  float *xsc = nullptr;         //   and their block scales [H/32]
+  int8_t *hq = nullptr;         // decode: digits of the activations [3][k*I]
+  float *hsc = nullptr;         //   and their block scales [k*I/32]
   int32_t *topk_idx = nullptr;  // device [cap_tokens][k]
   float *topk_w = nullptr;
   float *zbuf = nullptr;  // prefill logits [cap_tokens][E]
@@ -77,7 +82,7 @@ struct moe_cache {
   moe_kernel_stats stats[MOE_KIND_COUNT]{};
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
-  float *inv_rms() const { return reinterpret_cast<float *>(counter + 8); }
+  DecodeScratch scratch() const { return DecodeScratch{xq, xsc, h, hq, hsc}; }
 };
 
 namespace {
@@ -103,10 +108,18 @@ hipEvent_t get_event(moe_cache *c) {
   return e;
 }
 
-// Fold completed timing spans into the totals.  Only called once the spans'
-// streams have been synchronised (or are known complete).
-int drain_timing(moe_cache *c) {
+// Fold completed timing spans into the totals; spans whose stop event has not
+// completed yet stay pending (wait = true synchronises them first).
+int drain_timing(moe_cache *c, bool wait = false) {
+  std::vector<TimedSpan> keep;
   for (auto &sp : c->pending) {
+    if (wait) HIP_TRY(c, hipEventSynchronize(sp.stop));
+    const hipError_t q = hipEventQuery(sp.stop);
+    if (q == hipErrorNotReady) {
+      keep.push_back(sp);
+      continue;
+    }
+    HIP_TRY(c, q);
     float ms = 0.f;
     HIP_TRY(c, hipEventElapsedTime(&ms, sp.start, sp.stop));
     auto &st = c->stats[sp.kind];
@@ -117,7 +130,7 @@ int drain_timing(moe_cache *c) {
     c->ev_pool.push_back(sp.start);
     c->ev_pool.push_back(sp.stop);
   }
-  c->pending.clear();
+  c->pending.swap(keep);
   return MOE_OK;
 }
 
@@ -165,11 +178,14 @@ void free_all(moe_cache *c) {
   }
   (void)hipFree(c->slots);
   (void)hipFree(c->partial);
-  (void)hipFree(c->counter);
   (void)hipFree(c->topk_idx);
   (void)hipFree(c->topk_w);
   (void)hipFree(c->zbuf);
   (void)hipFree(c->h);
+  (void)hipFree(c->xq);
+  (void)hipFree(c->xsc);
+  (void)hipFree(c->hq);
+  (void)hipFree(c->hsc);
   if (c->host_idx) (void)hipHostFree(c->host_idx);
   if (c->host_w) (void)hipHostFree(c->host_w);
   if (c->ev_route) (void)hipEventDestroy(c->ev_route);
@@ -206,19 +222,34 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
+  for (int i = 0; i < k; ++i) reinterpret_cast<volatile int32_t *>(c->host_idx)[i] = -1;
   {
     Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
             2ull * d.hidden * d.n_experts);
-    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->counter,
-                                    c->topk_idx, c->topk_w, c->host_idx, c->host_w, c->inv_rms(),
+    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->topk_idx,
+                                    c->topk_w, c->host_idx, c->host_w, c->xq, c->xsc,
                                     (d.flags & MOE_F_PRENORM) != 0, c->main));
     sp.end();
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
-  HIP_TRY(c, hipEventSynchronize(c->ev_route));
+  // Wait for the routes: spin on the host-mapped ids the router writes (each
+  // was set to -1 before the launch); this wakes the host sooner than an
+  // event wait.  After a while without them, fall back to the event, which
+  // also reports a failed launch.
+  {
+    volatile int32_t *hid = c->host_idx;
+    bool ready = false;
+    for (long spin = 0; !ready; ++spin) {
+      ready = true;
+      for (int i = 0; i < k; ++i) ready = ready && hid[i] >= 0;
+      if (!ready && (spin & 0xfff) == 0xfff && hipEventQuery(c->ev_route) != hipErrorNotReady) {
+        HIP_TRY(c, hipEventSynchronize(c->ev_route));
+        ready = true;
+      }
+    }
+  }
+  if (dbg_w) HIP_TRY(c, hipEventSynchronize(c->ev_route));
   if (c->d.flags & MOE_F_TIMING) {
-    // every span queued so far has completed: earlier calls' FFN kernels ran
-    // before this router on the same stream, and their copies before those kernels
     int rc = drain_timing(c);
     if (rc) return rc;
   }
@@ -239,51 +270,83 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
   c->recs.clear();
   t.step(ids, k, c->recs);
 
-  // hit/miss per routed position, and the miss copies (ascending expert order)
-  ExpertList hits{}, misses{};
+  // hit/miss per routed position (top-k order)
+  ExpertList hits{}, misses{}, all{};
   int n_copy = 0;
   for (const auto &r : c->recs) n_copy += r.hit ? 0 : 1;
-  if (n_copy) {
-    Span sp(c, c->side, MOE_KIND_COPY, n_copy, (uint64_t)n_copy * c->P, 0);
-    for (const auto &r : c->recs) {
-      if (r.hit) continue;
-      const uint8_t *src = c->store + ((int64_t)layer * d.n_experts + r.expert) * c->P;
-      HIP_TRY(c, hipMemcpyAsync(c->slot_ptr(layer, r.slot), src, c->P, hipMemcpyDefault, c->side));
-    }
-    sp.end();
-    HIP_TRY(c, hipEventRecord(c->ev_copy, c->side));
-  }
   for (int i = 0; i < k; ++i) {
     const int32_t e = ids[i];
-    const int32_t s = t.slot_of(e);
     bool hit = false;
     for (const auto &r : c->recs)
       if (r.expert == e) hit = r.hit;
     ExpertList &L = hit ? hits : misses;
-    L.payload[L.n] = c->slot_ptr(layer, s);
-    L.pos[L.n] = i;
-    ++L.n;
+    L.payload[L.n] = all.payload[all.n] = c->slot_ptr(layer, t.slot_of(e));
+    L.pos[L.n++] = all.pos[all.n++] = i;
   }
   const bool resid = d.flags & MOE_F_RESIDUAL;
   const uint64_t gu_bytes = 2ull * c->M, dn_bytes = (uint64_t)c->M;
   const uint64_t gu_flops = 4ull * d.hidden * d.inter, dn_flops = 2ull * d.hidden * d.inter;
-  bool wrote = false;
-  for (int pass = 0; pass < 2; ++pass) {
-    ExpertList &L = pass == 0 ? hits : misses;
-    if (!L.n) continue;
-    if (pass == 1) HIP_TRY(c, hipStreamWaitEvent(c->main, c->ev_copy, 0));
-    {
-      Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
-      HIP_TRY(c, launch_gateup(d.qtype, x, c->inv_rms(), d.hidden, d.inter, L, c->h, c->main));
-      sp.end();
+  auto gateup = [&](const ExpertList &L) -> int {
+    Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
+    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->main));
+    sp.end();
+    return MOE_OK;
+  };
+  auto down = [&](const ExpertList &L, int mode) -> int {
+    Span sp(c, c->main, MOE_KIND_DOWN, 1, L.n * dn_bytes, L.n * dn_flops);
+    HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->topk_w, x, y,
+                           mode, c->main));
+    sp.end();
+    return MOE_OK;
+  };
+  // misses in ascending expert order (the records' order)
+  auto copy_misses = [&](hipStream_t s) -> int {
+    Span sp(c, s, MOE_KIND_COPY, n_copy, (uint64_t)n_copy * c->P, 0);
+    for (const auto &r : c->recs) {
+      if (r.hit) continue;
+      const uint8_t *src = c->store + ((int64_t)layer * d.n_experts + r.expert) * c->P;
+      HIP_TRY(c, hipMemcpyAsync(c->slot_ptr(layer, r.slot), src, c->P, hipMemcpyDefault, s));
     }
-    {
-      Span sp(c, c->main, MOE_KIND_DOWN, 1, L.n * dn_bytes, L.n * dn_flops);
-      int mode = wrote ? 2 : (resid ? 1 : 0);
-      HIP_TRY(c, launch_down(d.qtype, c->h, d.hidden, d.inter, L, c->topk_w, x, y, mode, c->main));
-      sp.end();
+    sp.end();
+    return MOE_OK;
+  };
+  int rc = MOE_OK;
+  if (d.flags & MOE_F_SIDE_COPY) {
+    // copies on the side stream, overlapped with the hit experts on the caller's stream
+    if (n_copy) {
+      if ((rc = copy_misses(c->side))) return rc;
+      HIP_TRY(c, hipEventRecord(c->ev_copy, c->side));
     }
-    wrote = true;
+    bool wrote = false;
+    if (hits.n) {
+      if ((rc = gateup(hits)) || (rc = down(hits, resid ? 1 : 0))) return rc;
+      wrote = true;
+    }
+    if (misses.n) {
+      HIP_TRY(c, hipStreamWaitEvent(c->main, c->ev_copy, 0));
+      if ((rc = gateup(misses)) || (rc = down(misses, wrote ? 2 : (resid ? 1 : 0)))) return rc;
+    }
+  } else {
+    // everything on the caller's stream: the miss copies first (the critical
+    // path), then gate/up and down over all routed experts in top-k order
+    if (n_copy) {
+      if (d.flags & MOE_F_SDMA_COPY) {
+        if ((rc = copy_misses(c->main))) return rc;
+      } else {
+        const uint8_t *src[kMaxRouted];
+        uint8_t *dst[kMaxRouted];
+        int n = 0;
+        for (const auto &r : c->recs) {
+          if (r.hit) continue;
+          src[n] = c->store + ((int64_t)layer * d.n_experts + r.expert) * c->P;
+          dst[n++] = c->slot_ptr(layer, r.slot);
+        }
+        Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
+        HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main));
+        sp.end();
+      }
+    }
+    if ((rc = gateup(all)) || (rc = down(all, resid ? 1 : 0))) return rc;
   }
 
   if (d.flags & MOE_F_TRACE) c->trace.insert(c->trace.end(), c->recs.begin(), c->recs.end());
@@ -360,16 +423,18 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
   }
   const int grid = router_decode_grid(desc->hidden);
   if (hipMalloc(&c->partial, (size_t)grid * desc->n_experts * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->counter, 64) != hipSuccess ||
       hipMalloc(&c->h, (size_t)desc->top_k * desc->inter * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->xq, 3 * (size_t)desc->hidden) != hipSuccess ||
+      hipMalloc(&c->xsc, (size_t)desc->hidden / 32 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->hq, 3 * (size_t)desc->top_k * desc->inter) != hipSuccess ||
+      hipMalloc(&c->hsc, (size_t)desc->top_k * desc->inter / 32 * sizeof(float)) != hipSuccess ||
       hipHostMalloc(&c->host_idx, kMaxRouted * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->host_w, kMaxRouted * sizeof(float), hipHostMallocCoherent) != hipSuccess) {
     (void)hipGetLastError();
     free_all(c);
     return fail(MOE_ENOMEM, "cannot allocate scratch buffers");
   }
-  if (hipMemset(c->counter, 0, 64) != hipSuccess ||
-      hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+  if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_route, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_copy, hipEventDisableTiming) != hipSuccess) {
     free_all(c);
@@ -441,7 +506,7 @@ int moe_cache_reset(moe_cache *c) {
   if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
   HIP_TRY(c, hipStreamSynchronize(c->side));
   HIP_TRY(c, hipStreamSynchronize(c->main));
-  int rc = drain_timing(c);
+  int rc = drain_timing(c, true);
   if (rc) return rc;
   for (auto &t : c->lru) t.reset();
   c->trace.clear();
@@ -455,7 +520,7 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
   if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
   HIP_TRY(c, hipStreamSynchronize(c->side));
   HIP_TRY(c, hipStreamSynchronize(c->main));
-  int rc = drain_timing(c);
+  int rc = drain_timing(c, true);
   if (rc) return rc;
   *out = c->stats[kind];
   return MOE_OK;

@@ -11,17 +11,18 @@ pytestmark = pytest.mark.gpu
 
 
 def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, store=None,
-               timing=False, prenorm=False):
+               timing=False, prenorm=False, copy_mode="kernel"):
     torch = torch_cuda()
     n_tokens = wl.n_tokens if n_tokens is None else n_tokens
     log(f"decode {wl.name} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
-        f"{wl.qtype} L={wl.n_layers} C={budget} T={n_tokens} residual={residual} prenorm={prenorm}")
+        f"{wl.qtype} L={wl.n_layers} C={budget} T={n_tokens} residual={residual} prenorm={prenorm} "
+        f"copy={copy_mode}")
     keep, ptr, arr = store if store is not None else store_buffer(wl, device=device_store)
     R = synth.router(wl)
     X = synth.hidden(wl, n_tokens=n_tokens)
     Rd = torch.from_numpy(R).cuda()
     cache = make_cache(wl, ptr, budget, trace=True, residual=residual, timing=timing,
-                       prenorm=prenorm)
+                       prenorm=prenorm, copy_mode=copy_mode)
     calls = [[] for _ in range(wl.n_layers)]
     worst = 0.0
     y = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
@@ -49,9 +50,10 @@ def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, st
     return cache, calls, worst
 
 
-def test_tiny_decode_parity():
+@pytest.mark.parametrize("copy_mode", ["kernel", "side", "sdma"])
+def test_tiny_decode_parity(copy_mode):
     wl = synth.WORKLOADS["tiny"]
-    cache, calls, worst = run_decode(wl, wl.budget_slots)
+    cache, calls, worst = run_decode(wl, wl.budget_slots, copy_mode=copy_mode)
     c = cache.counters()
     assert c.misses > 0 and c.hits > 0 and c.evictions > 0
     cache.close()
@@ -62,11 +64,12 @@ def test_tiny_residual_mode():
     run_decode(wl, wl.budget_slots, residual=True, n_tokens=16)[0].close()
 
 
-def test_prenorm_residual_multi_layer():
+@pytest.mark.parametrize("copy_mode", ["kernel", "side", "sdma"])
+def test_prenorm_residual_multi_layer(copy_mode):
     wl = synth.WORKLOADS["tiny"].with_(n_layers=4, name="tiny4")
-    run_decode(wl, 4, residual=True, prenorm=True, n_tokens=16)[0].close()
+    run_decode(wl, 4, residual=True, prenorm=True, n_tokens=16, copy_mode=copy_mode)[0].close()
     wl = wl.with_(qtype="q4_0", name="tiny4_q4")
-    run_decode(wl, 5, residual=True, prenorm=True, n_tokens=8)[0].close()
+    run_decode(wl, 5, residual=True, prenorm=True, n_tokens=8, copy_mode=copy_mode)[0].close()
 
 
 def test_full_cache_reaches_hit_rate_one():
@@ -95,13 +98,15 @@ def test_q4_0_tiny():
     run_decode(wl, wl.budget_slots, n_tokens=24)[0].close()
 
 
-@pytest.mark.parametrize("shape", [(64, 64, 1, 1, 1), (320, 192, 5, 3, 3), (1024, 384, 40, 6, 9)])
+@pytest.mark.parametrize("shape", [(64, 64, 1, 1, 1), (320, 192, 5, 3, 3), (1024, 384, 40, 6, 9),
+                                   (768, 1408, 256, 8, 40), (2816, 704, 64, 16, 17),
+                                   (8192, 64, 3, 2, 2), (128, 8192, 4, 1, 1)])
 def test_other_shapes(shape):
     H, I, E, k, C = shape
     for qt in ("q8_0", "q4_0"):
         wl = synth.WORKLOADS["tiny"].with_(hidden=H, inter=I, n_experts=E, top_k=k, qtype=qt,
                                            name=f"shape{H}x{I}x{E}")
-        run_decode(wl, C, n_tokens=12)[0].close()
+        run_decode(wl, C, n_tokens=6)[0].close()
 
 
 def test_multi_layer_and_reset():
