@@ -46,14 +46,20 @@ def parse():
     ap.add_argument("--budget", type=int, default=None, help="slots per layer (default: workload's)")
     ap.add_argument("--rho", type=float, default=None)
     ap.add_argument("--no-timing", action="store_true", help="no HIP events around kernels")
+    ap.add_argument("--timing-stride", type=int, default=16,
+                    help="bracket one layer call in this many with HIP events")
     ap.add_argument("--copy-mode", default="kernel", choices=["kernel", "side", "sdma"],
                     help="kernel: copy kernel on the compute stream (default); side: "
                          "hipMemcpyAsync on a side stream overlapped with the hit experts; "
                          "sdma: hipMemcpyAsync on the compute stream")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per gate/up launch (from rocprofv3 --pmc)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "gateup_a3b_q8_traffic.json"),
+                    help="JSON with the measured HBM bytes per gate/up launch (rocprofv3 --pmc); used "
+                         "only if it was taken on the current kernels.hip and this workload")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the run, copy 256 MiB device-to-device 4 times with torch (a plain "
+                         "copy kernel of known size, to scale the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -101,6 +107,8 @@ def main():
     cache = MoeCache(wl.n_layers, wl.n_experts, wl.top_k, wl.hidden, wl.inter, wl.qtype, hb.ptr,
                      wl.store_bytes, budget, stream=torch.cuda.current_stream(), residual=True,
                      prenorm=True, timing=timing, copy_mode=args.copy_mode)
+    if timing:
+        cache.set_timing_stride(args.timing_stride)
     h = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
     y = torch.empty_like(h)
 
@@ -171,7 +179,13 @@ def main():
         achieved = per_launch_bytes / avg_s / 1e9
         traffic = None
         if args.traffic and os.path.exists(args.traffic):
-            traffic = json.load(open(args.traffic)).get("gateup_bytes_per_launch")
+            import hashlib
+            t = json.load(open(args.traffic))
+            src = os.path.join(ROOT, "paper_2607_09686_amd", "csrc", "kernels.hip")
+            cur = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+            if t.get("kernels_hip_sha256_16") == cur and t.get("workload") == wl.name and \
+                    budget == wl.budget_slots:
+                traffic = t["traffic_bytes_per_launch"]
         result["roofline"] = {"bound": "hbm", "kernel": "gateup_kernel<8>" if wl.qtype == "q8_0"
                               else "gateup_kernel<2>", "achieved": achieved, "peak": HBM_PEAK_GBS,
                               "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -197,6 +211,14 @@ def main():
             "kernels": stats,
         })
     cache.close()
+    if args.calibrate_copy:
+        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        for _ in range(4):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     if not args.no_cpu_baseline:
         from threadpoolctl import threadpool_info

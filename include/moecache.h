@@ -160,6 +160,10 @@ int moe_cache_reset(moe_cache *c);
  * Synchronises with the handle's streams first. */
 int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out);
 
+/* With MOE_F_TIMING, bracket only one layer call in every `every` (>= 1,
+ * default 1) with events, so the timing itself barely perturbs the run. */
+int moe_cache_set_timing_stride(moe_cache *c, int32_t every);
+
 /* Waits for the handle's work, frees everything the library allocated. NULL-safe. */
 void moe_cache_destroy(moe_cache *c);
 

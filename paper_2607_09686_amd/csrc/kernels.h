@@ -9,6 +9,12 @@ namespace moecache {
 
 constexpr int kMaxRouted = 16;  // experts per FFN launch (top_k <= 16 in decode)
 
+// Optional events recorded by the runtime right at the start of the first
+// kernel and the end of the last kernel of a launch wrapper (null: none).
+struct Timing {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
 struct ExpertList {
   const uint8_t *payload[kMaxRouted];  // slot holding the expert's [gate|up|down] payload
   int32_t pos[kMaxRouted];             // top-k position of the expert for token 0
@@ -22,7 +28,7 @@ int router_decode_grid(int H);
 // s = 1/sqrt(mean(x^2)+1e-6) when prenorm else 1; the logits are scaled by s.
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
-                                float *xsc, bool prenorm, hipStream_t s);
+                                float *xsc, bool prenorm, hipStream_t s, const Timing &t = {});
 
 // Prefill router: z = x W_r for T tokens into z [T][E], then top-k rows.
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k, float *z,
@@ -41,13 +47,14 @@ struct DecodeScratch {
 // expert's top-k position; down reads the digits.  mode of down: 0 y = sum,
 // 1 y = x + sum, 2 y += sum.
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                         hipStream_t s);
+                         hipStream_t s, const Timing &t = {});
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                       const float *w, const float *x, float *y, int mode, hipStream_t s);
+                       const float *w, const float *x, float *y, int mode, hipStream_t s,
+                       const Timing &t = {});
 
 // Copy n payloads of `bytes` (multiple of 16, 16-byte aligned) src[i] -> dst[i]
 // with a copy kernel of `grid` blocks (host-pinned or device sources).
 hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
-                              int grid, hipStream_t s);
+                              int grid, hipStream_t s, const Timing &t = {});
 
 }  // namespace moecache

@@ -8,6 +8,7 @@
 // dot product with the int8 (or 4-bit) weights is then three exact int32
 // dot4 sums, recombined in fp32 and scaled by d * s_b.  Fixed summation
 // order throughout: results do not depend on scheduling.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -647,13 +648,15 @@ int router_decode_grid(int H) { return (H + kRouterRowsPerBlock - 1) / kRouterRo
 
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
-                                float *xsc, bool prenorm, hipStream_t s) {
+                                float *xsc, bool prenorm, hipStream_t s, const Timing &t) {
   const int nb = router_decode_grid(H);
-  hipLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, x, wr, H, E, partial);
+  hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
+                        wr, H, E, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), sizeof(float) * (size_t)H, s, x,
-                     partial, nb, H, E, k, idx, w, host_idx, host_w, xq, xsc, (int)prenorm);
+  hipExtLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), sizeof(float) * (size_t)H, s,
+                        nullptr, t.stop, 0, x, partial, nb, H, E, k, idx, w, host_idx, host_w, xq, xsc,
+                        (int)prenorm);
   return hipGetLastError();
 }
 
@@ -670,7 +673,7 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
 }
 
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                         hipStream_t s) {
+                         hipStream_t s, const Timing &t) {
   const int np = H / 64;
   GateUpParams a{L, S.xq, S.xsc, S.h, S.hq, S.hsc, H, I, k, 0, 0};
   pick_lanes(np, 2, 16, a.lanes, a.mpairs);
@@ -678,14 +681,15 @@ hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
   const size_t lds = 3 * (size_t)H + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
   dim3 grid(L.n * ((I + upb - 1) / upb));
   if (qtype == 8)
-    hipLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kGateUpThreads), lds, s, a);
+    hipExtLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kGateUpThreads), lds, s, t.start, t.stop, 0, a);
   else
-    hipLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kGateUpThreads), lds, s, a);
+    hipExtLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kGateUpThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                       const float *w, const float *x, float *y, int mode, hipStream_t s) {
+                       const float *w, const float *x, float *y, int mode, hipStream_t s,
+                       const Timing &t) {
   const int np = I / 64;
   DownParams a{L, S.hq, S.hsc, w, x, y, H, I, k, mode, 0, 0, 0};
   pick_lanes(np, 3, 64, a.lanes, a.mpairs);
@@ -694,14 +698,14 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
   const size_t lds = 3 * (size_t)L.n * I + 4 * (size_t)L.n * (I / 32) * 4 + 4 * (size_t)a.rows * L.n;
   dim3 grid((H + a.rows - 1) / a.rows);
   if (qtype == 8)
-    hipLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, a);
+    hipExtLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
-    hipLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, a);
+    hipExtLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 
 hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
-                              int grid, hipStream_t s) {
+                              int grid, hipStream_t s, const Timing &t) {
   CopyParams a{};
   for (int i = 0; i < n; ++i) {
     a.src[i] = reinterpret_cast<const uint4 *>(src[i]);
@@ -709,7 +713,7 @@ hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, in
   }
   a.n = n;
   a.p16 = bytes / 16;
-  hipLaunchKernelGGL(materialize_kernel, dim3(grid), dim3(kThreads), 0, s, a);
+  hipExtLaunchKernelGGL(materialize_kernel, dim3(grid), dim3(kThreads), 0, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 

@@ -80,6 +80,9 @@ struct moe_cache {
   std::vector<hipEvent_t> ev_pool;
   std::vector<TimedSpan> pending;
   moe_kernel_stats stats[MOE_KIND_COUNT]{};
+  int32_t timing_every = 1;
+  uint64_t n_calls = 0;
+  bool timing_now = false;  // this call is bracketed
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
   DecodeScratch scratch() const { return DecodeScratch{xq, xsc, h, hq, hsc}; }
@@ -134,6 +137,9 @@ int drain_timing(moe_cache *c, bool wait = false) {
   return MOE_OK;
 }
 
+// Events of one timed launch wrapper.  Kernel launches take them through
+// hipExtLaunchKernelGGL (the runtime stamps the kernels' own start and end);
+// host-side copies record them on the stream around the copies.
 struct Span {
   moe_cache *c;
   hipStream_t s;
@@ -141,12 +147,19 @@ struct Span {
   bool on = false;
   Span(moe_cache *c_, hipStream_t s_, int kind, uint64_t launches, uint64_t bytes, uint64_t flops)
       : c(c_), s(s_) {
-    if (!(c->d.flags & MOE_F_TIMING)) return;
+    if (!c->timing_now) return;
     sp = TimedSpan{kind, get_event(c), get_event(c), launches, bytes, flops};
-    on = sp.start && sp.stop && hipEventRecord(sp.start, s) == hipSuccess;
+    on = sp.start && sp.stop;
   }
-  void end() {
-    if (on && hipEventRecord(sp.stop, s) == hipSuccess) c->pending.push_back(sp);
+  Timing timing() const { return on ? Timing{sp.start, sp.stop} : Timing{}; }
+  void record_start() {
+    if (on && hipEventRecord(sp.start, s) != hipSuccess) on = false;
+  }
+  void record_stop() {
+    if (on && hipEventRecord(sp.stop, s) != hipSuccess) on = false;
+  }
+  void end() {  // the launch (or the stop record) succeeded: keep the span
+    if (on) c->pending.push_back(sp);
     on = false;
   }
 };
@@ -222,13 +235,14 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
+  c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
   for (int i = 0; i < k; ++i) reinterpret_cast<volatile int32_t *>(c->host_idx)[i] = -1;
   {
     Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
             2ull * d.hidden * d.n_experts);
     HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->topk_idx,
                                     c->topk_w, c->host_idx, c->host_w, c->xq, c->xsc,
-                                    (d.flags & MOE_F_PRENORM) != 0, c->main));
+                                    (d.flags & MOE_F_PRENORM) != 0, c->main, sp.timing()));
     sp.end();
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
@@ -288,25 +302,28 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
   const uint64_t gu_flops = 4ull * d.hidden * d.inter, dn_flops = 2ull * d.hidden * d.inter;
   auto gateup = [&](const ExpertList &L) -> int {
     Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
-    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->main));
+    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->main,
+                             sp.timing()));
     sp.end();
     return MOE_OK;
   };
   auto down = [&](const ExpertList &L, int mode) -> int {
     Span sp(c, c->main, MOE_KIND_DOWN, 1, L.n * dn_bytes, L.n * dn_flops);
     HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->topk_w, x, y,
-                           mode, c->main));
+                           mode, c->main, sp.timing()));
     sp.end();
     return MOE_OK;
   };
   // misses in ascending expert order (the records' order)
   auto copy_misses = [&](hipStream_t s) -> int {
     Span sp(c, s, MOE_KIND_COPY, n_copy, (uint64_t)n_copy * c->P, 0);
+    sp.record_start();
     for (const auto &r : c->recs) {
       if (r.hit) continue;
       const uint8_t *src = c->store + ((int64_t)layer * d.n_experts + r.expert) * c->P;
       HIP_TRY(c, hipMemcpyAsync(c->slot_ptr(layer, r.slot), src, c->P, hipMemcpyDefault, s));
     }
+    sp.record_stop();
     sp.end();
     return MOE_OK;
   };
@@ -342,7 +359,7 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
           dst[n++] = c->slot_ptr(layer, r.slot);
         }
         Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
-        HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main));
+        HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main, sp.timing()));
         sp.end();
       }
     }
@@ -509,6 +526,7 @@ int moe_cache_reset(moe_cache *c) {
   int rc = drain_timing(c, true);
   if (rc) return rc;
   for (auto &t : c->lru) t.reset();
+  c->n_calls = 0;
   c->trace.clear();
   c->trace_head = 0;
   for (auto &s : c->stats) s = moe_kernel_stats{};
@@ -527,6 +545,13 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
 }
 
 void moe_cache_destroy(moe_cache *c) { free_all(c); }
+
+int moe_cache_set_timing_stride(moe_cache *c, int32_t every) {
+  if (!c || every < 1) return fail(MOE_EINVAL, "timing stride must be >= 1");
+  c->timing_every = every;
+  c->n_calls = 0;
+  return MOE_OK;
+}
 
 int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, int32_t n_streams,
                   double *gb_per_s) {

@@ -81,6 +81,7 @@ def lib():
         "moe_cache_reset": ([vp], ctypes.c_int),
         "moe_cache_kernel_stats": ([vp, i32, P(KernelStats)], ctypes.c_int),
         "moe_cache_destroy": ([vp], None),
+        "moe_cache_set_timing_stride": ([vp, i32], ctypes.c_int),
         "moe_last_error": ([], ctypes.c_char_p),
         "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
         "moe_host_free": ([vp], ctypes.c_int),
@@ -208,6 +209,9 @@ class MoeCache:
 
     def reset(self):
         _check(lib().moe_cache_reset(self.handle))
+
+    def set_timing_stride(self, every):
+        _check(lib().moe_cache_set_timing_stride(self.handle, every))
 
     def kernel_stats(self, kind):
         s = KernelStats()
