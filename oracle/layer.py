@@ -19,10 +19,11 @@ on the RMS-normalised input x / sqrt(mean(x^2) + 1e-6) (unit gain), the
 pre-norm residual block of MoE transformers without attention; without it a
 deep stack of SwiGLU experts grows its activations without bound.
 
-``moe_layer_bf16`` is the prefill variant: the dequantised weights d*q, the
-inputs x and the SwiGLU activations are each rounded to bfloat16 (nearest,
-ties to even) before the products, as the MFMA tiles hold them; all sums stay
-exact (fp64).
+``moe_layer_bf16`` is the prefill variant: the dequantised weights d*q are
+rounded to bfloat16 (nearest, ties to even), as the MFMA weight tiles hold
+them; inputs, activations and all sums stay exact (fp64).  (The MFMA path
+carries its activations as two bf16 terms, hi + lo, about 16 significant bits,
+so it is compared against exact activations.)
 """
 from dataclasses import dataclass
 
@@ -100,8 +101,7 @@ def moe_layer(x, router_w, store, shape, layer, lru=None, routes=None, tokens=No
 
 def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, tokens=None,
                    prenorm=False):
-    """Prefill variant of ``moe_layer`` with bf16 rounding of weights, inputs and activations
-    (the inputs are rounded after the optional normalisation)."""
+    """Prefill variant of ``moe_layer``: the dequantised weights rounded to bf16."""
     shape = Shape.of(shape)
     x = np.atleast_2d(np.asarray(x, dtype=np.float32))
     x = rms_normalize(x) if prenorm else x.astype(np.float64)
@@ -113,15 +113,9 @@ def moe_layer_bf16(x, router_w, store, shape, layer, lru=None, routes=None, toke
     tokens = list(range(T) if tokens is None else tokens)
     need = sorted({int(e) for t in tokens for e in idx[t]})
     ex = _experts(store, shape, layer, need, bf16=True)
-    xb = bf16_round(x)
     y = np.full((T, shape.hidden), np.nan)
     for t in tokens:
-        acc = np.zeros(shape.hidden)
-        for e, we in zip(idx[t], w[t]):
-            wg, wu, wd = ex[int(e)]
-            a = bf16_round(ffn.silu(wg @ xb[t]) * (wu @ xb[t]))
-            acc += we * (wd @ a)
-        y[t] = acc
+        y[t] = ffn.combine(x[t], [ex[int(e)] for e in idx[t]], w[t])
     return dict(y=y, idx=idx, w=w, gap=gap, records=records)
 
 

@@ -1,6 +1,7 @@
 // Launch wrappers of the HIP kernels (internal to libmoecache).
 #pragma once
 
+#include <hip/hip_bf16.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -30,9 +31,35 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
                                 float *xsc, bool prenorm, hipStream_t s, const Timing &t = {});
 
-// Prefill router: z = x W_r for T tokens into z [T][E], then top-k rows.
-hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k, float *z,
-                                 int32_t *idx, float *w, hipStream_t s);
+// Prefill router: z = (x W_r) * tscale[t] (tscale nullable) for T tokens
+// into z [T][E], then top-k rows into idx/w [T][k].
+hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
+                                 const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s);
+
+// Prefill.  inv[t] = 1/rms (or 1) and xb [2][T][H] = x * inv as bf16 hi and lo terms.
+hipError_t launch_prefill_prep(const float *x, int T, int H, bool prenorm, float *inv, __bf16 *xb,
+                               hipStream_t s);
+// Stable grouping of the T*k (token, expert) pairs by expert: counts [E],
+// offsets [E+1], perm [T*k] (pair ids t*k + j).
+hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, int32_t *offsets,
+                        int32_t *perm, hipStream_t s);
+// The experts of one wave (count <= pf_max_experts()).
+struct PfWave {
+  const uint8_t *payload[256];
+  int32_t row0[256], n[256];
+  int32_t count;
+};
+int pf_max_experts();
+int max_copy();  // payloads per launch_materialize call
+// ab: [2][T*k][I] activations as bf16 hi and lo terms (rows in perm order).
+hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
+                            __bf16 *ab, int T, int H, int I, int k, hipStream_t s,
+                            const Timing &t = {});
+hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *ab,
+                          const float *w, float *P, int pairs, int H, int I, hipStream_t s,
+                          const Timing &t = {});
+hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, int H, int k,
+                             bool residual, hipStream_t s);
 
 // Device scratch of the decode FFN (owned by the cache handle).
 struct DecodeScratch {
@@ -52,8 +79,8 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
                        const float *w, const float *x, float *y, int mode, hipStream_t s,
                        const Timing &t = {});
 
-// Copy n payloads of `bytes` (multiple of 16, 16-byte aligned) src[i] -> dst[i]
-// with a copy kernel of `grid` blocks (host-pinned or device sources).
+// Copy n <= max_copy() payloads of `bytes` (multiple of 16, 16-byte aligned)
+// src[i] -> dst[i] with a copy kernel of `grid` blocks (host-pinned or device sources).
 hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
                               int grid, hipStream_t s, const Timing &t = {});
 

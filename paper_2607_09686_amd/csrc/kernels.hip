@@ -234,6 +234,7 @@ constexpr int kPfTok = 32, kPfRows = 32;
 __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__restrict__ x,
                                                                  const float *__restrict__ wr,
                                                                  int T, int H, int E,
+                                                                 const float *__restrict__ tscale,
                                                                  float *__restrict__ z) {
   __shared__ float xs[kPfTok][kPfRows + 1];
   __shared__ float ws[kPfRows][256];
@@ -271,7 +272,8 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
   if (ph < phases)
     for (int i = 0; i < per && i < kPfTok; ++i) {
       int tt = ph * per + i;
-      if (tt < kPfTok && t0 + tt < T) z[(int64_t)(t0 + tt) * E + c] = acc[i];
+      if (tt < kPfTok && t0 + tt < T)
+        z[(int64_t)(t0 + tt) * E + c] = acc[i] * (tscale ? tscale[t0 + tt] : 1.f);
     }
 }
 
@@ -593,9 +595,10 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
 // Copy the payloads of the listed misses (P bytes each, 16-byte aligned) from
 // the store into their slots: 16-byte loads and stores, four in flight per
 // thread, grid-strided over all misses' bytes.
+constexpr int kMaxCopy = 64;
 struct CopyParams {
-  const uint4 *src[kMaxRouted];
-  uint4 *dst[kMaxRouted];
+  const uint4 *src[kMaxCopy];
+  uint4 *dst[kMaxCopy];
   int n;
   int64_t p16;  // payload size in 16-byte units
 };
@@ -620,6 +623,407 @@ __global__ __launch_bounds__(kThreads) void materialize_kernel(CopyParams a) {
   for (; i < total; i += st) {
     const int64_t e = i / a.p16;
     a.dst[e][i - e * a.p16] = a.src[e][i - e * a.p16];
+  }
+}
+
+// ---------------------------------------------------------------- prefill ---
+//
+// A multi-token layer call: per-token RMS scale and the scaled input as two
+// bf16 terms (hi = bf16(v), lo = bf16(v - hi): about 16 significant bits),
+// router logits + top-k, grouping of the (token, expert) pairs by expert (a
+// stable counting sort: pairs keep token order), then, wave by wave of at
+// most C experts, the copy kernel for the wave's misses and two MFMA grouped
+// GEMMs with the weights dequantised to bf16 on the fly (each activation tile
+// is multiplied as hi and lo, both into the same fp32 accumulators):
+//   gate/up:  A_e = silu(X_e W_gate^T) * (X_e W_up^T)   [n_e, I], kept as hi + lo
+//   down:     P[pair] = w_pair * (A_e W_down^T)[row]     [n_e, H]
+// and finally y[t] = (x[t] +) sum over the token's k pairs, in rank order.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// inv[t] = 1/sqrt(mean(x_t^2) + 1e-6) (or 1); v = x_t * inv[t] as
+// xb[t] = bf16(v) and xb[T*H + t] = bf16(v - bf16(v)).
+__global__ __launch_bounds__(kThreads) void prefill_prep_kernel(const float *__restrict__ x, int T,
+                                                                int H, int prenorm,
+                                                                float *__restrict__ inv,
+                                                                __bf16 *__restrict__ xb) {
+  __shared__ float wsum[kThreads / kWave];
+  const int t = blockIdx.x;
+  const float *xt = x + (int64_t)t * H;
+  float ss = 0.f;
+  if (prenorm)
+    for (int i = threadIdx.x; i < H; i += kThreads) ss = fmaf(xt[i], xt[i], ss);
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0) wsum[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
+  const float s = prenorm ? 1.f / sqrtf(tot / (float)H + 1e-6f) : 1.f;
+  if (threadIdx.x == 0) inv[t] = s;
+  for (int i = threadIdx.x; i < H; i += kThreads) {
+    const float v = xt[i] * s;
+    const __bf16 hi = (__bf16)v;
+    xb[(int64_t)t * H + i] = hi;
+    xb[(int64_t)T * H + (int64_t)t * H + i] = (__bf16)(v - (float)hi);
+  }
+}
+
+// counts[e] = number of pairs routed to e (one block per expert).
+__global__ __launch_bounds__(kThreads) void group_count_kernel(const int32_t *__restrict__ idx,
+                                                               int npairs,
+                                                               int32_t *__restrict__ counts) {
+  __shared__ int wsum[kThreads / kWave];
+  const int e = blockIdx.x;
+  int c = 0;
+  for (int i = threadIdx.x; i < npairs; i += kThreads) c += idx[i] == e;
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) c += __shfl_xor(c, off, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0) wsum[threadIdx.x / kWave] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int tot = 0;
+    for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
+    counts[e] = tot;
+  }
+}
+
+// perm[offsets[e] + r] = the r-th pair (in pair order) routed to e;
+// offsets[e] = sum of counts below e, offsets[E] = npairs (block 0 writes it).
+__global__ __launch_bounds__(kThreads) void group_scatter_kernel(const int32_t *__restrict__ idx,
+                                                                 int npairs, int E,
+                                                                 const int32_t *__restrict__ counts,
+                                                                 int32_t *__restrict__ offsets,
+                                                                 int32_t *__restrict__ perm) {
+  __shared__ int wcnt[kThreads / kWave];
+  __shared__ int base_s;
+  const int e = blockIdx.x;
+  if (threadIdx.x == 0) {
+    int off = 0;
+    for (int i = 0; i < e; ++i) off += counts[i];
+    base_s = off;
+    offsets[e] = off;
+    if (e == E - 1) offsets[E] = off + counts[e];
+  }
+  __syncthreads();
+  int base = base_s;
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  for (int i0 = 0; i0 < npairs; i0 += kThreads) {
+    const int i = i0 + threadIdx.x;
+    const bool hit = i < npairs && idx[i] == e;
+    const uint64_t mask = __ballot(hit);
+    const int before = __popcll(mask & ((1ull << lane) - 1ull));
+    if (lane == 0) wcnt[wv] = __popcll(mask);
+    __syncthreads();
+    int woff = 0;
+    for (int w = 0; w < wv; ++w) woff += wcnt[w];
+    int tot = 0;
+    for (int w = 0; w < kThreads / kWave; ++w) tot += wcnt[w];
+    if (hit) perm[base + woff + before] = i;
+    base += tot;
+    __syncthreads();
+  }
+}
+
+// One wave's experts for the grouped GEMMs (kernel argument).
+constexpr int kPfMaxExperts = 96;
+struct PfExperts {
+  const uint8_t *payload[kPfMaxExperts];
+  int32_t row0[kPfMaxExperts];  // first row of the expert's pairs in perm / Ab
+  int32_t n[kPfMaxExperts];     // pairs (tokens) routed to it
+  int32_t count;
+};
+
+constexpr int kPfBM = 128;  // tokens per tile
+constexpr int kPfBK = 64;   // one pair of weight blocks per row
+constexpr int kPfLd = kPfBK + 8;  // LDS row stride in bf16 (padding against bank conflicts)
+
+// (expert, M-tile) of a flat M-tile index; returns false past the end.
+__device__ __forceinline__ bool pf_tile(const PfExperts &X, int mt, int &j, int &m0) {
+  for (j = 0; j < X.count; ++j) {
+    const int tiles = (X.n[j] + kPfBM - 1) / kPfBM;
+    if (mt < tiles) {
+      m0 = mt * kPfBM;
+      return true;
+    }
+    mt -= tiles;
+  }
+  return false;
+}
+
+// Dequantise one 32-weight block (half a pair) of a weight row to bf16.  The
+// thread loads the 9 dwords of its half of the pair: half 0 = bytes 0..35,
+// half 1 = bytes 32..67 (Q8_0) / half 0 = bytes 0..19, half 1 = 16..35 (Q4_0).
+template <int QT>
+__device__ __forceinline__ void load_half(const uint8_t *pair, int half, uint32_t (&v)[9]) {
+  const uint32_t *q = reinterpret_cast<const uint32_t *>(pair) + (QT == 8 ? 8 * half : 4 * half);
+  constexpr int n = QT == 8 ? 9 : 5;
+#pragma unroll
+  for (int i = 0; i < n; ++i) v[i] = q[i];
+}
+
+// The 32 bf16 weights of one block (as loaded by load_half) into dst (16-byte
+// aligned), rounded to nearest even from the exact fp32 value d*q.
+template <int QT>
+__device__ __forceinline__ void dequant_half(const uint32_t (&v)[9], int half, __bf16 *dst) {
+  __bf16 o[32];
+  if constexpr (QT == 8) {
+    // half 0 holds bytes 0..35: d = bytes 0-1, q = bytes 2..33;
+    // half 1 holds bytes 32..67: d = bytes 34-35, q = bytes 36..67
+    const float d = half_bits_to_float(half == 0 ? (v[0] & 0xffffu) : (v[0] >> 16));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t w = half == 0 ? __builtin_amdgcn_alignbyte(v[j + 1], v[j], 2) : v[j + 1];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o[4 * j + b] = (__bf16)(d * (float)(int8_t)((w >> (8 * b)) & 0xff));
+    }
+  } else {
+    // half 0 holds bytes 0..19: d = bytes 0-1, nibble bytes 2..17;
+    // half 1 holds bytes 16..35: d = bytes 18-19, nibble bytes 20..35
+    const float d = half_bits_to_float(half == 0 ? (v[0] & 0xffffu) : (v[0] >> 16));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w = half == 0 ? __builtin_amdgcn_alignbyte(v[j + 1], v[j], 2) : v[j + 1];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const uint32_t byte = (w >> (8 * b)) & 0xff;
+        o[4 * j + b] = (__bf16)(d * (float)((int)(byte & 0xf) - 8));
+        o[16 + 4 * j + b] = (__bf16)(d * (float)((int)(byte >> 4) - 8));
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    *reinterpret_cast<uint4 *>(dst + 8 * i) = *reinterpret_cast<const uint4 *>(o + 8 * i);
+}
+
+struct PfGateUpParams {
+  PfExperts X;
+  const int32_t *perm;
+  const __bf16 *xb;  // [2][T][H]: hi then lo
+  __bf16 *ab;        // [2][pairs][I]: hi then lo
+  int T, pairs, H, I, k;
+};
+
+// grid: (M-tiles of the wave's experts, I / 64).  256 threads = 4 waves; wave w
+// owns tile rows [32w, 32w+32) (two 16-row MFMA tiles) and all 4+4 16-column
+// tiles of gate and up.  K loop over H in steps of 64 (one weight pair).
+template <int QT>
+__global__ __launch_bounds__(kThreads) void pf_gateup_kernel(PfGateUpParams a) {
+  __shared__ __align__(16) __bf16 As[2][2][kPfBM][kPfLd];  // [buffer][hi, lo]
+  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];       // rows 0..63 gate, 64..127 up
+  constexpr int BB = Fmt<QT>::kBlockBytes;
+  int j, m0;
+  if (!pf_tile(a.X, blockIdx.x, j, m0)) return;
+  const int n0 = blockIdx.y * 64;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int nb = a.H / 32;
+  const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
+  const int64_t lo_off = (int64_t)a.T * a.H;
+  // A: 4 chunks of 16 bytes per thread per plane; B: one 32-weight block per thread
+  const int brow = tid >> 1, bhalf = tid & 1;
+  const uint8_t *bptr = a.X.payload[j] + (brow >= 64 ? mat : 0) + (int64_t)(n0 + (brow & 63)) * rowb;
+  int arow_tok[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = tid + c * kThreads, r = ch >> 3;
+    arow_tok[c] = m0 + r < n ? a.perm[row0 + m0 + r] / a.k : -1;
+  }
+  uint4 av[2][4];
+  uint32_t bv[9];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = tid + c * kThreads, c16 = ch & 7;
+      const int64_t o = (int64_t)arow_tok[c] * a.H + kt * kPfBK + 8 * c16;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+        av[pl][c] = arow_tok[c] >= 0 ? *reinterpret_cast<const uint4 *>(a.xb + pl * lo_off + o)
+                                     : make_uint4(0, 0, 0, 0);
+    }
+    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, bv);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) *reinterpret_cast<uint4 *>(&As[buf][pl][r][8 * c16]) = av[pl][c];
+    }
+    dequant_half<QT>(bv, bhalf, &Bs[buf][brow][32 * bhalf]);
+  };
+  f32x4 accg[2][4], accu[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      accg[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      accu[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  const int KT = a.H / kPfBK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) gload(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 bg[4], bu[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        bg[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+        bu[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][64 + 16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+      }
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
+              &As[buf][pl][32 * wv + 16 * i + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bg[q], accg[i][q], 0, 0, 0);
+            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bu[q], accu[i][q], 0, 0, 0);
+          }
+        }
+    }
+    if (kt + 1 < KT) lstore(buf ^ 1);
+    __syncthreads();
+  }
+  // C layout (16x16): lane holds rows 4*(lane/16) + r, column lane % 16
+  const int64_t plane = (int64_t)a.pairs * a.I;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+        if (m < n) {
+          const float g = accg[i][q][r], u = accu[i][q][r];
+          const float v = silu(g) * u;
+          const __bf16 hi = (__bf16)v;
+          const int64_t o = (int64_t)(row0 + m) * a.I + n0 + 16 * q + (lane & 15);
+          a.ab[o] = hi;
+          a.ab[plane + o] = (__bf16)(v - (float)hi);
+        }
+      }
+}
+
+struct PfDownParams {
+  PfExperts X;
+  const int32_t *perm;
+  const __bf16 *ab;  // [2][pairs][I]: hi then lo
+  const float *w;    // [pairs] routing weights (pair = t*k + j)
+  float *P;          // [pairs][H]
+  int pairs, H, I;
+};
+
+// grid: (M-tiles, H / 128).  Wave w owns rows [32w, 32w+32) and the 8
+// 16-column tiles; K loop over I in steps of 64.
+template <int QT>
+__global__ __launch_bounds__(kThreads) void pf_down_kernel(PfDownParams a) {
+  __shared__ __align__(16) __bf16 As[2][2][kPfBM][kPfLd];
+  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];
+  constexpr int BB = Fmt<QT>::kBlockBytes;
+  int j, m0;
+  if (!pf_tile(a.X, blockIdx.x, j, m0)) return;
+  const int n0 = blockIdx.y * 128;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int nbI = a.I / 32;
+  const int64_t rowb = (int64_t)nbI * BB;
+  const int64_t mat = (int64_t)a.I * ((int64_t)(a.H / 32) * BB);
+  const int64_t plane = (int64_t)a.pairs * a.I;
+  const int brow = tid >> 1, bhalf = tid & 1;
+  const uint8_t *bptr = a.X.payload[j] + 2 * mat + (int64_t)(n0 + brow) * rowb;
+  bool arow_ok[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) arow_ok[c] = m0 + ((tid + c * kThreads) >> 3) < n;
+  uint4 av[2][4];
+  uint32_t bv[9];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
+      const int64_t o = (int64_t)(row0 + m0 + r) * a.I + kt * kPfBK + 8 * c16;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+        av[pl][c] = arow_ok[c] ? *reinterpret_cast<const uint4 *>(a.ab + pl * plane + o)
+                               : make_uint4(0, 0, 0, 0);
+    }
+    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, bv);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) *reinterpret_cast<uint4 *>(&As[buf][pl][r][8 * c16]) = av[pl][c];
+    }
+    dequant_half<QT>(bv, bhalf, &Bs[buf][brow][32 * bhalf]);
+  };
+  f32x4 acc[2][8];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int KT = a.I / kPfBK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) gload(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 bf[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        bf[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
+              &As[buf][pl][32 * wv + 16 * i + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[q], acc[i][q], 0, 0, 0);
+        }
+    }
+    if (kt + 1 < KT) lstore(buf ^ 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+      if (m < n) {
+        const int pair = a.perm[row0 + m];
+        const float wt = a.w[pair];
+        float *dst = a.P + (int64_t)pair * a.H + n0 + (lane & 15);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) dst[16 * q] = wt * acc[i][q][r];
+      }
+    }
+}
+
+// y[t] = (x[t] if residual) + sum_j P[t*k + j], j = 0..k-1 in rank order.
+__global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__restrict__ P,
+                                                              const float *__restrict__ x,
+                                                              float *__restrict__ y, int H, int k,
+                                                              int residual) {
+  const int t = blockIdx.x;
+  for (int i = threadIdx.x; i < H; i += kThreads) {
+    float v = residual ? x[(int64_t)t * H + i] : 0.f;
+    for (int jj = 0; jj < k; ++jj) v += P[((int64_t)t * k + jj) * H + i];
+    y[(int64_t)t * H + i] = v;
   }
 }
 
@@ -660,10 +1064,10 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
   return hipGetLastError();
 }
 
-hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k, float *z,
-                                 int32_t *idx, float *w, hipStream_t s) {
+hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
+                                 const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s) {
   hipLaunchKernelGGL(router_logits_kernel, dim3((T + kPfTok - 1) / kPfTok), dim3(kThreads), 0, s, x,
-                     wr, T, H, E, z);
+                     wr, T, H, E, tscale, z);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int wpb = kThreads / kWave;
@@ -716,5 +1120,86 @@ hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, in
   hipExtLaunchKernelGGL(materialize_kernel, dim3(grid), dim3(kThreads), 0, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
+
+hipError_t launch_prefill_prep(const float *x, int T, int H, bool prenorm, float *inv, __bf16 *xb,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(prefill_prep_kernel, dim3(T), dim3(kThreads), 0, s, x, T, H, (int)prenorm, inv, xb);
+  return hipGetLastError();
+}
+
+hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, int32_t *offsets,
+                        int32_t *perm, hipStream_t s) {
+  hipLaunchKernelGGL(group_count_kernel, dim3(E), dim3(kThreads), 0, s, idx, npairs, counts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_scatter_kernel, dim3(E), dim3(kThreads), 0, s, idx, npairs, E, counts,
+                     offsets, perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
+                            __bf16 *ab, int T, int H, int I, int k, hipStream_t s, const Timing &t) {
+  PfGateUpParams a{};
+  a.X.count = W.count;
+  int tiles = 0;
+  for (int i = 0; i < W.count; ++i) {
+    a.X.payload[i] = W.payload[i];
+    a.X.row0[i] = W.row0[i];
+    a.X.n[i] = W.n[i];
+    tiles += (W.n[i] + kPfBM - 1) / kPfBM;
+  }
+  a.perm = perm;
+  a.xb = xb;
+  a.ab = ab;
+  a.T = T;
+  a.pairs = T * k;
+  a.H = H;
+  a.I = I;
+  a.k = k;
+  if (tiles == 0) return hipSuccess;
+  dim3 grid(tiles, I / 64);
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(pf_gateup_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(pf_gateup_kernel<2>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *ab,
+                          const float *w, float *P, int pairs, int H, int I, hipStream_t s,
+                          const Timing &t) {
+  PfDownParams a{};
+  a.X.count = W.count;
+  int tiles = 0;
+  for (int i = 0; i < W.count; ++i) {
+    a.X.payload[i] = W.payload[i];
+    a.X.row0[i] = W.row0[i];
+    a.X.n[i] = W.n[i];
+    tiles += (W.n[i] + kPfBM - 1) / kPfBM;
+  }
+  a.perm = perm;
+  a.ab = ab;
+  a.w = w;
+  a.P = P;
+  a.pairs = pairs;
+  a.H = H;
+  a.I = I;
+  if (tiles == 0) return hipSuccess;
+  dim3 grid(tiles, H / 128);
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(pf_down_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(pf_down_kernel<2>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, int H, int k,
+                             bool residual, hipStream_t s) {
+  hipLaunchKernelGGL(pf_combine_kernel, dim3(T), dim3(kThreads), 0, s, P, x, y, H, k, (int)residual);
+  return hipGetLastError();
+}
+
+int pf_max_experts() { return kPfMaxExperts; }
+int max_copy() { return kMaxCopy; }
 
 }  // namespace moecache

@@ -66,6 +66,16 @@ struct moe_cache {
   float *topk_w = nullptr;
   float *zbuf = nullptr;  // prefill logits [cap_tokens][E]
   int64_t cap_tokens = 0;
+  // prefill buffers (grown on demand)
+  int64_t pf_cap = 0;
+  float *pf_inv = nullptr;      // [T]
+  __bf16 *pf_xb = nullptr;      // [2][T][H] (hi, lo)
+  int32_t *pf_counts = nullptr; // [E]
+  int32_t *pf_off = nullptr;    // [E+1]
+  int32_t *pf_perm = nullptr;   // [T*k]
+  __bf16 *pf_ab = nullptr;      // [2][T*k][I] (hi, lo)
+  float *pf_P = nullptr;        // [T*k][H]
+  int32_t *pf_host_off = nullptr;  // pinned [E+1]
   float *h = nullptr;  // decode SwiGLU activations [k][I]
   int32_t *host_idx = nullptr;  // host mirrors [k] (decode)
   float *host_w = nullptr;
@@ -195,6 +205,14 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->topk_w);
   (void)hipFree(c->zbuf);
   (void)hipFree(c->h);
+  (void)hipFree(c->pf_inv);
+  (void)hipFree(c->pf_xb);
+  (void)hipFree(c->pf_counts);
+  (void)hipFree(c->pf_off);
+  (void)hipFree(c->pf_perm);
+  (void)hipFree(c->pf_ab);
+  (void)hipFree(c->pf_P);
+  if (c->pf_host_off) (void)hipHostFree(c->pf_host_off);
   (void)hipFree(c->xq);
   (void)hipFree(c->xsc);
   (void)hipFree(c->hq);
@@ -376,8 +394,8 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
   return MOE_OK;
 }
 
-int forward_prefill(moe_cache *, const float *, int32_t, const float *, int32_t, float *,
-                    moe_counters *, int32_t *, float *);
+int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer,
+                    float *y, moe_counters *delta, int32_t *dbg_idx, float *dbg_w);
 
 }  // namespace
 
@@ -600,10 +618,179 @@ int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, 
 
 namespace {
 
-int forward_prefill(moe_cache *c, const float *, int32_t, const float *, int32_t, float *,
-                    moe_counters *, int32_t *, float *) {
-  (void)c;
-  return fail(MOE_EINVAL, "n_tokens > 1 (prefill) is not built yet");
+int ensure_prefill(moe_cache *c, int64_t T) {
+  if (T <= c->pf_cap) return MOE_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  void *ptrs[] = {c->pf_inv, c->pf_xb, c->pf_counts, c->pf_off, c->pf_perm, c->pf_ab, c->pf_P};
+  for (void *q : ptrs) (void)hipFree(q);
+  c->pf_inv = nullptr;
+  c->pf_xb = nullptr;
+  c->pf_counts = c->pf_off = c->pf_perm = nullptr;
+  c->pf_ab = nullptr;
+  c->pf_P = nullptr;
+  c->pf_cap = 0;
+  const int64_t H = c->d.hidden, I = c->d.inter, E = c->d.n_experts, k = c->d.top_k;
+  if (hipMalloc(&c->pf_inv, T * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->pf_xb, 2 * T * H * sizeof(__bf16)) != hipSuccess ||
+      hipMalloc(&c->pf_counts, E * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->pf_off, (E + 1) * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->pf_perm, T * k * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->pf_ab, 2 * T * k * I * sizeof(__bf16)) != hipSuccess ||
+      hipMalloc(&c->pf_P, T * k * H * sizeof(float)) != hipSuccess ||
+      (!c->pf_host_off &&
+       hipHostMalloc(&c->pf_host_off, 257 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)) {
+    (void)hipGetLastError();
+    return fail(MOE_ENOMEM, "cannot allocate prefill buffers for %lld tokens", (long long)T);
+  }
+  c->pf_cap = T;
+  return MOE_OK;
+}
+
+// A multi-token layer call.  The routed experts S of all tokens go through the
+// slot table once; experts are then processed in waves so that a slot is
+// overwritten only after the expert that held it (if routed in this call) has
+// been computed: a wave closes when the next miss would evict an expert of
+// the wave that has not run yet.
+int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
+                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  const moe_model_desc &d = c->d;
+  const int k = d.top_k, E = d.n_experts, H = d.hidden, I = d.inter;
+  int rc = ensure_tokens(c, T);
+  if (!rc) rc = ensure_prefill(c, T);
+  if (rc) return rc;
+  c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
+  const bool prenorm = d.flags & MOE_F_PRENORM;
+  {
+    Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)H * E * 4 + (uint64_t)T * H * 4,
+            2ull * T * H * E);
+    sp.record_start();
+    HIP_TRY(c, launch_prefill_prep(x, T, H, prenorm, c->pf_inv, c->pf_xb, c->main));
+    HIP_TRY(c, launch_router_prefill(x, wr, T, H, E, k, prenorm ? c->pf_inv : nullptr, c->zbuf,
+                                     c->topk_idx, c->topk_w, c->main));
+    HIP_TRY(c, launch_group(c->topk_idx, T * k, E, c->pf_counts, c->pf_off, c->pf_perm, c->main));
+    sp.record_stop();
+    sp.end();
+  }
+  HIP_TRY(c, hipMemcpyAsync(c->pf_host_off, c->pf_off, (E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
+                            c->main));
+  HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
+  HIP_TRY(c, hipEventSynchronize(c->ev_route));
+  if (d.flags & MOE_F_TIMING) {
+    rc = drain_timing(c);
+    if (rc) return rc;
+  }
+  const int32_t *off = c->pf_host_off;
+  if (off[0] != 0 || off[E] != T * k) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "grouping produced offsets [%d, %d] for %d pairs", off[0], off[E], T * k);
+  }
+  std::vector<int32_t> S;
+  for (int e = 0; e < E; ++e) {
+    if (off[e + 1] < off[e]) {
+      c->poisoned = true;
+      return fail(MOE_EHIP, "grouping produced decreasing offsets");
+    }
+    if (off[e + 1] > off[e]) S.push_back(e);
+  }
+  SlotLru &t = c->lru[layer];
+  const moe_counters before = t.counters();
+  c->recs.clear();
+  t.step(S.data(), (int32_t)S.size(), c->recs);
+
+  // waves of record indices; hits first (they need no copy)
+  std::vector<char> in_S(E, 0), done(E, 0), in_cur(E, 0);
+  for (int e : S) in_S[e] = 1;
+  std::vector<std::vector<int>> waves(1);
+  for (size_t i = 0; i < c->recs.size(); ++i)
+    if (c->recs[i].hit) {
+      waves.back().push_back((int)i);
+      in_cur[c->recs[i].expert] = 1;
+    }
+  for (size_t i = 0; i < c->recs.size(); ++i) {
+    const moe_step_rec &r = c->recs[i];
+    if (r.hit) continue;
+    const int v = r.evicted;
+    if (v >= 0 && in_S[v] && !done[v]) {  // v is in the current wave: run it first
+      for (int q : waves.back()) {
+        done[c->recs[q].expert] = 1;
+        in_cur[c->recs[q].expert] = 0;
+      }
+      waves.emplace_back();
+    }
+    waves.back().push_back((int)i);
+    in_cur[r.expert] = 1;
+  }
+
+  const int copy_cap = max_copy(), ex_cap = pf_max_experts();
+  const uint64_t M = (uint64_t)c->M;
+  for (const auto &wave : waves) {
+    if (wave.empty()) continue;
+    // copies of the wave's misses (the slot each takes is free or held by a computed expert)
+    std::vector<int> miss;
+    for (int q : wave)
+      if (!c->recs[q].hit) miss.push_back(q);
+    for (size_t m0 = 0; m0 < miss.size(); m0 += copy_cap) {
+      const int n = (int)std::min<size_t>(copy_cap, miss.size() - m0);
+      const uint8_t *src[256];
+      uint8_t *dst[256];
+      for (int q = 0; q < n; ++q) {
+        const moe_step_rec &r = c->recs[miss[m0 + q]];
+        src[q] = c->store + ((int64_t)layer * E + r.expert) * c->P;
+        dst[q] = c->slot_ptr(layer, r.slot);
+      }
+      Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
+      if (d.flags & (MOE_F_SDMA_COPY | MOE_F_SIDE_COPY)) {
+        sp.record_start();
+        for (int q = 0; q < n; ++q)
+          HIP_TRY(c, hipMemcpyAsync(dst[q], src[q], c->P, hipMemcpyDefault, c->main));
+        sp.record_stop();
+      } else {
+        HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main, sp.timing()));
+      }
+      sp.end();
+    }
+    for (size_t e0 = 0; e0 < wave.size(); e0 += ex_cap) {
+      PfWave W{};
+      uint64_t rows = 0;
+      for (size_t q = e0; q < wave.size() && W.count < ex_cap; ++q) {
+        const moe_step_rec &r = c->recs[wave[q]];
+        W.payload[W.count] = c->slot_ptr(layer, r.slot);
+        W.row0[W.count] = off[r.expert];
+        W.n[W.count] = off[r.expert + 1] - off[r.expert];
+        rows += W.n[W.count];
+        ++W.count;
+      }
+      {
+        Span sp(c, c->main, MOE_KIND_GATEUP, 1, W.count * 2 * M, rows * 4ull * H * I);
+        HIP_TRY(c, launch_pf_gateup(d.qtype, W, c->pf_perm, c->pf_xb, c->pf_ab, T, H, I, k, c->main,
+                                    sp.timing()));
+        sp.end();
+      }
+      {
+        Span sp(c, c->main, MOE_KIND_DOWN, 1, W.count * M, rows * 2ull * H * I);
+        HIP_TRY(c, launch_pf_down(d.qtype, W, c->pf_perm, c->pf_ab, c->topk_w, c->pf_P, T * k, H, I,
+                                  c->main, sp.timing()));
+        sp.end();
+      }
+    }
+  }
+  HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
+  if (dbg_idx || dbg_w) {
+    if (dbg_idx)
+      HIP_TRY(c, hipMemcpyAsync(dbg_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t),
+                                hipMemcpyDeviceToHost, c->main));
+    if (dbg_w)
+      HIP_TRY(c, hipMemcpyAsync(dbg_w, c->topk_w, (size_t)T * k * sizeof(float), hipMemcpyDeviceToHost,
+                                c->main));
+    HIP_TRY(c, hipStreamSynchronize(c->main));
+  }
+  if (d.flags & MOE_F_TRACE) c->trace.insert(c->trace.end(), c->recs.begin(), c->recs.end());
+  if (delta) {
+    const moe_counters &a = t.counters();
+    *delta = moe_counters{a.hits - before.hits, a.misses - before.misses, a.evictions - before.evictions,
+                          a.materialized_bytes - before.materialized_bytes};
+  }
+  return MOE_OK;
 }
 
 }  // namespace

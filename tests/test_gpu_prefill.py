@@ -1,0 +1,147 @@
+"""GPU parity of the prefill path (many tokens per layer call): bf16 MFMA grouped
+GEMMs compared with the bf16-emulating oracle; routes, waves of slot reuse inside a
+call (more routed experts than slots), trace and counters exact."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_common import (TIE_GAP, check_y, log, make_cache, softmax_of, store_buffer, torch_cuda)
+from oracle import router as oracle_router
+from oracle.layer import Shape, moe_layer_bf16, rms_normalize
+from oracle.lru import LayerLRU
+
+pytestmark = pytest.mark.gpu
+
+
+def oracle_routes(x, wr, k, prenorm):
+    z = oracle_router.logits(rms_normalize(x) if prenorm else x, wr)
+    idx, w, gap = oracle_router.topk(z, k)
+    return z, idx, w, gap
+
+
+def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens=None):
+    """Routes of every token, y of `tokens` (default all) against the bf16 oracle."""
+    z, idx, w, gap = oracle_routes(x, wr, wl.top_k, prenorm)
+    flips = 0
+    idx_use, w_use = idx.copy(), w.copy()
+    for t in range(x.shape[0]):
+        if set(idx[t].tolist()) != set(idx_g[t].tolist()):
+            assert gap[t] < TIE_GAP, f"token {t}: top-k differs with gap {gap[t]}"
+            idx_use[t] = idx_g[t]
+            w_use[t] = softmax_of(z[t], idx_g[t])
+            flips += 1
+    toks = list(range(x.shape[0])) if tokens is None else list(tokens)
+    yo = moe_layer_bf16(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
+                        prenorm=prenorm)["y"][toks]
+    yg = y_g[toks].astype(np.float64)
+    if residual:
+        yg = yg - x[toks].astype(np.float64)
+    err = check_y(yg, yo, f"layer {layer}")
+    return flips, err
+
+
+def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=None, seed_shift=0):
+    torch = torch_cuda()
+    log(f"prefill {wl.qtype} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
+        f"L={wl.n_layers} C={budget} T={T} calls={calls} prenorm={prenorm} residual={residual}")
+    keep, ptr, arr = store if store is not None else store_buffer(wl)
+    R = synth.router(wl)
+    cache = make_cache(wl, ptr, budget, trace=True, residual=residual, prenorm=prenorm)
+    lrus = [LayerLRU(wl.n_experts, budget, wl.payload_bytes, l) for l in range(wl.n_layers)]
+    want = []
+    worst = 0.0
+    for c in range(calls):
+        X = synth.hidden(wl.with_(hidden_seed=wl.hidden_seed + 7 * c + seed_shift), rho=-1.0,
+                         n_tokens=T)
+        for l in range(wl.n_layers):
+            x = torch.from_numpy(X).cuda()
+            y = torch.empty_like(x)
+            delta, idx, w = cache.layer_forward(x, torch.from_numpy(R[l]).cuda(), l, y,
+                                                n_tokens=T, routes=True)
+            torch.cuda.synchronize()
+            flips, err = check_call(X, R[l], arr, wl, l, idx, w, y.cpu().numpy(), prenorm, residual)
+            worst = max(worst, err)
+            want.extend(lrus[l].step(np.unique(idx)))
+            assert delta.materialized_bytes == delta.misses * wl.payload_bytes
+    got = cache.read_trace()
+    assert got == want
+    tot = sum((lr.counters for lr in lrus[1:]), lrus[0].counters)
+    assert cache.counters().as_tuple() == tot.as_tuple()
+    log(f"  ok: worst err/rms {worst:.2e}; counters {cache.counters()}")
+    cache.close()
+    return worst
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("T,budget", [(2, 4), (37, 4), (300, 16), (300, 3), (129, 6)])
+def test_prefill_small(qtype, T, budget):
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, name="tiny_pf")
+    run_prefill(wl, max(budget, wl.top_k), T)
+
+
+def test_prefill_warm_cache_prenorm_residual_multilayer():
+    # (H, I large enough that one bf16 rounding flip of an input, ~4e-3 of its value,
+    # stays far below the tolerance; at H 256 a single flip moves y by ~2e-3 x RMS)
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=3, hidden=1024, inter=384, name="pf3")
+    run_prefill(wl, 5, 200, calls=3, prenorm=True, residual=True)
+
+
+@pytest.mark.parametrize("shape", [(1024, 384, 40, 6, 9, 260), (768, 1408, 64, 8, 20, 96)])
+def test_prefill_other_shapes(shape):
+    H, I, E, k, C, T = shape
+    for qt in ("q8_0", "q4_0"):
+        wl = synth.WORKLOADS["tiny"].with_(hidden=H, inter=I, n_experts=E, top_k=k, qtype=qt,
+                                           name=f"pf{H}x{I}x{E}")
+        run_prefill(wl, C, T)
+
+
+def test_a3b_prefill_full_size():
+    """4096 tokens through all 48 layers of the A3B stack, 45 slots, cold cache,
+    pre-norm residual chain on the GPU; every route and the whole trace checked,
+    outputs of sampled tokens in sampled layers against the bf16 oracle."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["a3b_prefill"]
+    keep, ptr, arr = store_buffer(wl)
+    R = synth.router(wl)
+    X = synth.hidden(wl)
+    cache = make_cache(wl, ptr, wl.budget_slots, trace=True, residual=True, prenorm=True)
+    T, L = X.shape[0], wl.n_layers
+    check_layers = {0, L // 2, L - 1}
+    inputs, outputs, routes = {}, {}, []
+    h = torch.from_numpy(X).cuda()
+    y = torch.empty_like(h)
+    log(f"a3b prefill: {T} tokens x {L} layers, C={wl.budget_slots}")
+    for l in range(L):
+        xin = h.cpu().numpy()
+        delta, idx, w = cache.layer_forward(h, torch.from_numpy(R[l]).cuda(), l, y, n_tokens=T,
+                                            routes=True)
+        routes.append((xin, idx, w))
+        if l in check_layers:
+            inputs[l] = xin
+            outputs[l] = y.cpu().numpy()
+        assert delta.misses == len(np.unique(idx))   # every layer starts cold
+        h, y = y, h
+    assert np.all(np.isfinite(h.cpu().numpy()))
+    log("  routes")
+    flips = 0
+    for l, (xin, idx, w) in enumerate(routes):
+        z, io, wo, gap = oracle_routes(xin, R[l], wl.top_k, True)
+        for t in np.nonzero(np.any(np.sort(io, 1) != np.sort(idx, 1), axis=1))[0]:
+            assert gap[t] < TIE_GAP, f"layer {l} token {t}: gap {gap[t]}"
+            flips += 1
+    log(f"  near-tie flips: {flips}; trace")
+    want = []
+    for l, (xin, idx, w) in enumerate(routes):
+        lru = LayerLRU(wl.n_experts, wl.budget_slots, wl.payload_bytes, l)
+        want.extend(lru.step(np.unique(idx)))
+    assert cache.read_trace() == want
+    rng = np.random.default_rng(5)
+    worst = 0.0
+    for l in sorted(check_layers):
+        toks = sorted(rng.choice(T, size=6, replace=False).tolist())
+        xin, idx, w = routes[l]
+        _, err = check_call(xin, R[l], arr, wl, l, idx, w, outputs[l], True, True, tokens=toks)
+        worst = max(worst, err)
+    log(f"  ok: worst err/rms {worst:.2e}; counters {cache.counters()}")
+    cache.close()
+    keep.free()

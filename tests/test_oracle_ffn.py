@@ -49,19 +49,30 @@ def test_closed_form_single_expert():
 
 
 def test_closed_form_bf16_variant():
+    # weights that are not bf16-representable: d = 1 + 2^-9 (exact in fp16) times q = 1
+    # rounds to 1 (ties to even) in bf16; the activation path stays exact
     H, I, E = 64, 32, 1
     store, s = _closed_form_store(H, I)
+    st = store.copy()
+    d = int(np.float16(1 + 2.0 ** -9).view(np.uint16))
+    mb = quant.matrix_bytes("q8_0", I, H)
+    gate = st[:mb].reshape(-1, 34)                      # gate matrix blocks only
+    gate[:, 0], gate[:, 1] = d & 0xFF, d >> 8
     shape = Shape("q8_0", E, H, I, 1)
     rng = np.random.default_rng(1)
-    x = torch.from_numpy(rng.standard_normal((3, H)).astype(np.float32)).to(torch.bfloat16).float().numpy()
+    x = rng.standard_normal((3, H)).astype(np.float32)
     wr = np.zeros((H, E), np.float32)
-    out = layer.moe_layer_bf16(x, wr, store, shape, 0)
+    exact = layer.moe_layer(x, wr, st, shape, 0)["y"]
+    out = layer.moe_layer_bf16(x, wr, st, shape, 0)
     j = np.arange(H)
     for t in range(3):
-        g = x[t, 2 * (j % I)].astype(np.float64)
+        g = x[t, 2 * (j % I)].astype(np.float64)          # bf16(1 + 2^-9) = 1
         u = x[t, 2 * (j % I) + 1].astype(np.float64)
-        a = torch.from_numpy(g * expit(g) * u).to(torch.bfloat16).double().numpy()
-        np.testing.assert_array_equal(out["y"][t], s * a)
+        np.testing.assert_allclose(out["y"][t], s * g * expit(g) * u, rtol=1e-14, atol=1e-15)
+        assert not np.allclose(exact[t], out["y"][t], rtol=1e-5, atol=0)  # the rounding matters
+    # weights already bf16-exact: the variant equals the exact layer
+    np.testing.assert_allclose(layer.moe_layer_bf16(x, wr, store, shape, 0)["y"],
+                               layer.moe_layer(x, wr, store, shape, 0)["y"], rtol=1e-14, atol=1e-15)
 
 
 def _random_store(wl):
