@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 
 
 def log(msg):
@@ -42,7 +43,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="a3b_decode", choices=["a3b_decode", "q4_decode", "tiny"])
+    ap.add_argument("--workload", default="a3b_decode",
+                    choices=["a3b_decode", "q4_decode", "tiny", "a3b_prefill"])
     ap.add_argument("--budget", type=int, default=None, help="slots per layer (default: workload's)")
     ap.add_argument("--rho", type=float, default=None)
     ap.add_argument("--no-timing", action="store_true", help="no HIP events around kernels")
@@ -112,9 +114,20 @@ def main():
     h = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
     y = torch.empty_like(h)
 
+    prefill = wl.mode == "prefill"
+    if prefill:
+        h = torch.empty_like(Xd)
+        y = torch.empty_like(Xd)
+
     def step():
         nonlocal h, y
         cache.reset()
+        if prefill:  # the whole chunk through every layer
+            h.copy_(Xd)
+            for l in range(wl.n_layers):
+                cache.layer_forward(h, Rd[l], l, y, n_tokens=wl.n_tokens)
+                h, y = y, h
+            return
         for t in range(wl.n_tokens):
             h.copy_(Xd[t])
             for l in range(wl.n_layers):
@@ -154,7 +167,9 @@ def main():
             stats[name] = dict(a, avg_us=1e3 * a["total_ms"] / a["launches"],
                                gb_per_s=a["bytes"] / (a["total_ms"] * 1e6) if a["total_ms"] else None)
     result = {
-        "metric": "MoE-layer decode tokens/s; expert-FFN HBM GB/s; materialized bytes/token",
+        "metric": ("MoE-layer prefill tokens/s; expert-FFN MFMA utilisation; materialized bytes/token"
+                   if prefill else
+                   "MoE-layer decode tokens/s; expert-FFN HBM GB/s; materialized bytes/token"),
         "value": tokens / dt,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -164,15 +179,27 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if prefill else "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "n_layers": wl.n_layers, "hidden": wl.hidden,
                    "n_experts": wl.n_experts, "top_k": wl.top_k, "inter": wl.inter,
                    "qtype": wl.qtype, "budget_slots": budget, "n_tokens": wl.n_tokens, "rho": rho,
                    "copy_mode": args.copy_mode,
-                   "global_batch": 1, "seq_len": wl.n_tokens, "parallelism": "none"},
+                   "global_batch": wl.n_tokens if prefill else 1, "seq_len": wl.n_tokens,
+                   "parallelism": "none"},
     }
-    if timing:
+    if timing and prefill:
+        gu = stats["gateup"]
+        avg_s = gu["total_ms"] / 1e3 / max(1, gu["launches"])
+        per_launch_flops = gu["flops"] / max(1, gu["launches"])
+        achieved = per_launch_flops / avg_s / 1e12
+        result["roofline"] = {"bound": "mfma", "kernel": "pf_gateup_kernel<8>", "achieved": achieved,
+                              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": achieved / BF16_PEAK_TFLOPS, "traffic": None,
+                              "flops_per_launch": per_launch_flops, "avg_launch_us": avg_s * 1e6}
+        ffn_ms = stats["gateup"]["total_ms"] + stats["down"]["total_ms"]
+        ffn_bytes = stats["gateup"]["bytes"] + stats["down"]["bytes"]
+    elif timing:
         gu = stats["gateup"]
         per_launch_bytes = gu["bytes"] / max(1, gu["launches"])
         avg_s = gu["total_ms"] / 1e3 / max(1, gu["launches"])
@@ -203,6 +230,10 @@ def main():
     }
     if timing and "copy" in stats:
         cp = stats["copy"]
+        if prefill:
+            fl = stats["gateup"]["flops"] + stats["down"]["flops"]
+            result["extra"]["expert_ffn_tflops"] = fl / (ffn_ms * 1e9)
+            result["extra"]["expert_ffn_frac_of_bf16_peak"] = fl / (ffn_ms * 1e9) / BF16_PEAK_TFLOPS
         result["extra"].update({
             "expert_ffn_gb_per_s": ffn_bytes / (ffn_ms * 1e6),
             "expert_ffn_frac_of_hbm_peak": ffn_bytes / (ffn_ms * 1e6) / HBM_PEAK_GBS,
@@ -226,7 +257,10 @@ def main():
         n = args.cpu_sample_tokens
         log(f"cpu baseline: oracle on the first {n} tokens through all {wl.n_layers} layers")
         tc = time.perf_counter()
-        run_stack(X[:n], R, hb.array, wl, budget, prenorm=True)
+        if prefill:  # a bounded sample: n tokens of the chunk as one multi-token call per layer
+            run_stack(X[:n], R, hb.array, wl, budget, decode=False, bf16=True, prenorm=True)
+        else:
+            run_stack(X[:n], R, hb.array, wl, budget, prenorm=True)
         cdt = time.perf_counter() - tc
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
         result["cpu_baseline"] = {"value": n / cdt, "unit": "tokens/s", "cores": threads,

@@ -31,8 +31,10 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
                                 float *xsc, bool prenorm, hipStream_t s, const Timing &t = {});
 
-// Prefill router: z = (x W_r) * tscale[t] (tscale nullable) for T tokens
-// into z [T][E], then top-k rows into idx/w [T][k].
+// Prefill router: partial logits over router_slices() slices of H into
+// z [slices][T][E], then per token z = tscale[t] * (sum of slices) (tscale
+// nullable) and top-k rows into idx/w [T][k].
+int router_slices();
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s);
 

@@ -228,61 +228,80 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
   if (tid < kWave) wave_topk(zs, E, k, idx, w, host_idx, host_w);
 }
 
-// z[T][E] = x[T][H] W_r[H][E]: a block owns 32 tokens and all E columns.
-constexpr int kPfTok = 32, kPfRows = 32;
+// Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]:
+// a block owns 32 tokens, 128 expert columns (blockIdx.y) and one of
+// kPfSlices slices of H (blockIdx.z); thread (tt, cc) keeps a 4-token x
+// 4-expert tile of accumulators; K runs over the slice in 32-row steps
+// through LDS.  The top-k kernel adds the slices in order.
+constexpr int kPfTok = 32, kPfRows = 32, kPfCols = 128, kPfSlices = 4;
 
 __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__restrict__ x,
                                                                  const float *__restrict__ wr,
                                                                  int T, int H, int E,
-                                                                 const float *__restrict__ tscale,
-                                                                 float *__restrict__ z) {
-  __shared__ float xs[kPfTok][kPfRows + 1];
-  __shared__ float ws[kPfRows][256];
+                                                                 float *__restrict__ zp) {
+  __shared__ float xs[kPfRows][kPfTok + 1];   // [k][token]
+  __shared__ float ws[kPfRows][kPfCols + 4];  // [k][col]
   const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * kPfTok;
-  const int phases = kThreads / E;
-  const int c = tid % E, ph = tid / E;
-  const int per = (kPfTok + phases - 1) / phases;  // tokens per thread
-  float acc[kPfTok];
+  const int t0 = blockIdx.x * kPfTok, c0 = blockIdx.y * kPfCols;
+  const int tt = (tid / 32) * 4, cc = (tid % 32) * 4;  // 8 x 32 threads, 4 x 4 each
+  float acc[4][4];
 #pragma unroll
-  for (int i = 0; i < kPfTok; ++i) acc[i] = 0.f;
-  for (int r0 = 0; r0 < H; r0 += kPfRows) {
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  const int per = (H / kPfSlices + kPfRows - 1) / kPfRows * kPfRows;
+  const int rbeg = blockIdx.z * per, rend = min(H, rbeg + per);
+  for (int r0 = rbeg; r0 < rend; r0 += kPfRows) {
     for (int i = tid; i < kPfTok * kPfRows; i += kThreads) {
-      int tt = i / kPfRows, rr = i % kPfRows;
-      xs[tt][rr] = (t0 + tt < T && r0 + rr < H) ? x[(int64_t)(t0 + tt) * H + r0 + rr] : 0.f;
+      const int t = i / kPfRows, rr = i % kPfRows;
+      xs[rr][t] = (t0 + t < T && r0 + rr < rend) ? x[(int64_t)(t0 + t) * H + r0 + rr] : 0.f;
     }
-    for (int i = tid; i < kPfRows * E; i += kThreads) {
-      int rr = i / E, cc = i % E;
-      ws[rr][cc] = r0 + rr < H ? wr[(int64_t)(r0 + rr) * E + cc] : 0.f;
+    for (int i = tid; i < kPfRows * kPfCols; i += kThreads) {
+      const int rr = i / kPfCols, col = i % kPfCols;
+      ws[rr][col] = (r0 + rr < rend && c0 + col < E) ? wr[(int64_t)(r0 + rr) * E + c0 + col] : 0.f;
     }
     __syncthreads();
-    if (ph < phases) {
+#pragma unroll 8
+    for (int rr = 0; rr < kPfRows; ++rr) {
+      float xv[4], wv[4];
 #pragma unroll
-      for (int i = 0; i < kPfTok; ++i) {
-        int tt = ph * per + i;
-        if (i < per && tt < kPfTok) {
-          float a = acc[i];
-          for (int rr = 0; rr < kPfRows; ++rr) a = fmaf(xs[tt][rr], ws[rr][c], a);
-          acc[i] = a;
-        }
-      }
+      for (int i = 0; i < 4; ++i) xv[i] = xs[rr][tt + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wv[j] = ws[rr][cc + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(xv[i], wv[j], acc[i][j]);
     }
     __syncthreads();
   }
-  if (ph < phases)
-    for (int i = 0; i < per && i < kPfTok; ++i) {
-      int tt = ph * per + i;
-      if (tt < kPfTok && t0 + tt < T)
-        z[(int64_t)(t0 + tt) * E + c] = acc[i] * (tscale ? tscale[t0 + tt] : 1.f);
-    }
+  float *z = zp + (int64_t)blockIdx.z * T * E;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = t0 + tt + i;
+    if (t >= T) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (c0 + cc + j < E) z[(int64_t)t * E + c0 + cc + j] = acc[i][j];
+  }
 }
 
-__global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__restrict__ z, int T,
-                                                             int E, int k, int32_t *idx, float *w) {
-  const int wave = threadIdx.x / kWave;
+// z[t] = tscale[t] * sum of the slices in order; top-k of each token row.
+__global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__restrict__ zp, int T,
+                                                             int E, int k,
+                                                             const float *__restrict__ tscale,
+                                                             int32_t *idx, float *w) {
+  __shared__ float zs[kThreads / kWave][256];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int t = blockIdx.x * (kThreads / kWave) + wave;
   if (t >= T) return;
-  wave_topk(z + (int64_t)t * E, E, k, idx + (int64_t)t * k, w + (int64_t)t * k, nullptr, nullptr);
+  const float sc = tscale ? tscale[t] : 1.f;
+  for (int e = lane; e < E; e += kWave) {
+    float v = 0.f;
+    for (int sl = 0; sl < kPfSlices; ++sl) v += zp[((int64_t)sl * T + t) * E + e];
+    zs[wave][e] = v * sc;
+  }
+  wave_topk(zs[wave], E, k, idx + (int64_t)t * k, w + (int64_t)t * k, nullptr, nullptr);
 }
 
 // ------------------------------------------------------------ decode FFN ---
@@ -1066,13 +1085,14 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
 
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s) {
-  hipLaunchKernelGGL(router_logits_kernel, dim3((T + kPfTok - 1) / kPfTok), dim3(kThreads), 0, s, x,
-                     wr, T, H, E, tscale, z);
+  hipLaunchKernelGGL(router_logits_kernel,
+                     dim3((T + kPfTok - 1) / kPfTok, (E + kPfCols - 1) / kPfCols, kPfSlices),
+                     dim3(kThreads), 0, s, x, wr, T, H, E, z);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int wpb = kThreads / kWave;
   hipLaunchKernelGGL(topk_rows_kernel, dim3((T + wpb - 1) / wpb), dim3(kThreads), 0, s, z, T, E, k,
-                     idx, w);
+                     tscale, idx, w);
   return hipGetLastError();
 }
 
@@ -1200,6 +1220,7 @@ hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, in
 }
 
 int pf_max_experts() { return kPfMaxExperts; }
+int router_slices() { return kPfSlices; }
 int max_copy() { return kMaxCopy; }
 
 }  // namespace moecache

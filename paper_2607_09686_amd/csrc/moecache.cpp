@@ -76,6 +76,7 @@ struct moe_cache {
   __bf16 *pf_ab = nullptr;      // [2][T*k][I] (hi, lo)
   float *pf_P = nullptr;        // [T*k][H]
   int32_t *pf_host_off = nullptr;  // pinned [E+1]
+  std::vector<hipEvent_t> pf_ev;   // per-chunk events (copy done, compute done)
   float *h = nullptr;  // decode SwiGLU activations [k][I]
   int32_t *host_idx = nullptr;  // host mirrors [k] (decode)
   float *host_w = nullptr;
@@ -213,6 +214,7 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->pf_ab);
   (void)hipFree(c->pf_P);
   if (c->pf_host_off) (void)hipHostFree(c->pf_host_off);
+  for (auto e : c->pf_ev) (void)hipEventDestroy(e);
   (void)hipFree(c->xq);
   (void)hipFree(c->xsc);
   (void)hipFree(c->hq);
@@ -243,7 +245,7 @@ int ensure_tokens(moe_cache *c, int64_t T) {
   const int64_t k = c->d.top_k, E = c->d.n_experts;
   if (hipMalloc(&c->topk_idx, T * k * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->topk_w, T * k * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->zbuf, T * E * sizeof(float)) != hipSuccess)
+      hipMalloc(&c->zbuf, router_slices() * T * E * sizeof(float)) != hipSuccess)
     return fail(MOE_ENOMEM, "cannot allocate routing buffers for %lld tokens", (long long)T);
   c->cap_tokens = T;
   return MOE_OK;
@@ -647,10 +649,12 @@ int ensure_prefill(moe_cache *c, int64_t T) {
 }
 
 // A multi-token layer call.  The routed experts S of all tokens go through the
-// slot table once; experts are then processed in waves so that a slot is
-// overwritten only after the expert that held it (if routed in this call) has
-// been computed: a wave closes when the next miss would evict an expert of
-// the wave that has not run yet.
+// slot table once.  The experts are then processed in chunks: the copy kernel
+// of a chunk's misses runs on the caller's stream while the MFMA GEMMs of
+// earlier chunks run on the side stream.  A copy overwrites a slot only after
+// the expert that held it (if it is routed in this call) has been computed:
+// the copy stream waits for that expert's chunk, and a chunk is closed early
+// when one of its own experts would be evicted by the next miss.
 int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
                     moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
@@ -697,83 +701,105 @@ int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, in
   c->recs.clear();
   t.step(S.data(), (int32_t)S.size(), c->recs);
 
-  // waves of record indices; hits first (they need no copy)
-  std::vector<char> in_S(E, 0), done(E, 0), in_cur(E, 0);
-  for (int e : S) in_S[e] = 1;
-  std::vector<std::vector<int>> waves(1);
+  // chunks of record indices: the hits first (no copy), then the misses in order
+  struct Chunk {
+    std::vector<int> recs;
+    int copy_dep = -1;  // chunk whose computation must finish before this chunk's copies
+  };
+  const int per_chunk = std::max(1, std::min(c->C / 3, pf_max_experts()));
+  std::vector<Chunk> chunks(1);
+  std::vector<int> chunk_of(E, -1);
   for (size_t i = 0; i < c->recs.size(); ++i)
     if (c->recs[i].hit) {
-      waves.back().push_back((int)i);
-      in_cur[c->recs[i].expert] = 1;
+      if ((int)chunks.back().recs.size() == pf_max_experts()) chunks.emplace_back();
+      chunks.back().recs.push_back((int)i);
+      chunk_of[c->recs[i].expert] = (int)chunks.size() - 1;
     }
+  if (!chunks.back().recs.empty()) chunks.emplace_back();
+  int misses_in_cur = 0;
   for (size_t i = 0; i < c->recs.size(); ++i) {
     const moe_step_rec &r = c->recs[i];
     if (r.hit) continue;
-    const int v = r.evicted;
-    if (v >= 0 && in_S[v] && !done[v]) {  // v is in the current wave: run it first
-      for (int q : waves.back()) {
-        done[c->recs[q].expert] = 1;
-        in_cur[c->recs[q].expert] = 0;
-      }
-      waves.emplace_back();
+    const int dep = r.evicted >= 0 ? chunk_of[r.evicted] : -1;  // -1: not routed in this call
+    if ((dep >= 0 && dep == (int)chunks.size() - 1) || misses_in_cur == per_chunk) {
+      chunks.emplace_back();
+      misses_in_cur = 0;
     }
-    waves.back().push_back((int)i);
-    in_cur[r.expert] = 1;
+    Chunk &ch = chunks.back();
+    ch.recs.push_back((int)i);
+    ch.copy_dep = std::max(ch.copy_dep, dep);
+    chunk_of[r.expert] = (int)chunks.size() - 1;
+    ++misses_in_cur;
   }
-
-  const int copy_cap = max_copy(), ex_cap = pf_max_experts();
+  while (!chunks.empty() && chunks.back().recs.empty()) chunks.pop_back();
+  while (c->pf_ev.size() < 2 * chunks.size()) {
+    hipEvent_t e = nullptr;
+    HIP_TRY(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    c->pf_ev.push_back(e);
+  }
+  // chunk i: pf_ev[2i] = its copies done (caller's stream), pf_ev[2i+1] = computed (side)
+  HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_route, 0));
+  const int copy_cap = max_copy();
   const uint64_t M = (uint64_t)c->M;
-  for (const auto &wave : waves) {
-    if (wave.empty()) continue;
-    // copies of the wave's misses (the slot each takes is free or held by a computed expert)
+  int waited = -1;
+  for (size_t ci = 0; ci < chunks.size(); ++ci) {
+    const Chunk &ch = chunks[ci];
     std::vector<int> miss;
-    for (int q : wave)
+    for (int q : ch.recs)
       if (!c->recs[q].hit) miss.push_back(q);
-    for (size_t m0 = 0; m0 < miss.size(); m0 += copy_cap) {
-      const int n = (int)std::min<size_t>(copy_cap, miss.size() - m0);
-      const uint8_t *src[256];
-      uint8_t *dst[256];
-      for (int q = 0; q < n; ++q) {
-        const moe_step_rec &r = c->recs[miss[m0 + q]];
-        src[q] = c->store + ((int64_t)layer * E + r.expert) * c->P;
-        dst[q] = c->slot_ptr(layer, r.slot);
+    if (!miss.empty()) {
+      if (ch.copy_dep > waited) {
+        HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * ch.copy_dep + 1], 0));
+        waited = ch.copy_dep;
       }
-      Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
-      if (d.flags & (MOE_F_SDMA_COPY | MOE_F_SIDE_COPY)) {
-        sp.record_start();
-        for (int q = 0; q < n; ++q)
-          HIP_TRY(c, hipMemcpyAsync(dst[q], src[q], c->P, hipMemcpyDefault, c->main));
-        sp.record_stop();
-      } else {
-        HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main, sp.timing()));
+      for (size_t m0 = 0; m0 < miss.size(); m0 += copy_cap) {
+        const int n = (int)std::min<size_t>(copy_cap, miss.size() - m0);
+        const uint8_t *src[256];
+        uint8_t *dst[256];
+        for (int q = 0; q < n; ++q) {
+          const moe_step_rec &r = c->recs[miss[m0 + q]];
+          src[q] = c->store + ((int64_t)layer * E + r.expert) * c->P;
+          dst[q] = c->slot_ptr(layer, r.slot);
+        }
+        Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
+        if (d.flags & (MOE_F_SDMA_COPY | MOE_F_SIDE_COPY)) {
+          sp.record_start();
+          for (int q = 0; q < n; ++q)
+            HIP_TRY(c, hipMemcpyAsync(dst[q], src[q], c->P, hipMemcpyDefault, c->main));
+          sp.record_stop();
+        } else {
+          HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main, sp.timing()));
+        }
+        sp.end();
       }
+      HIP_TRY(c, hipEventRecord(c->pf_ev[2 * ci], c->main));
+      HIP_TRY(c, hipStreamWaitEvent(c->side, c->pf_ev[2 * ci], 0));
+    }
+    PfWave W{};
+    uint64_t rows = 0;
+    for (int q : ch.recs) {
+      const moe_step_rec &r = c->recs[q];
+      W.payload[W.count] = c->slot_ptr(layer, r.slot);
+      W.row0[W.count] = off[r.expert];
+      W.n[W.count] = off[r.expert + 1] - off[r.expert];
+      rows += W.n[W.count];
+      ++W.count;
+    }
+    {
+      Span sp(c, c->side, MOE_KIND_GATEUP, 1, W.count * 2 * M, rows * 4ull * H * I);
+      HIP_TRY(c, launch_pf_gateup(d.qtype, W, c->pf_perm, c->pf_xb, c->pf_ab, T, H, I, k, c->side,
+                                  sp.timing()));
       sp.end();
     }
-    for (size_t e0 = 0; e0 < wave.size(); e0 += ex_cap) {
-      PfWave W{};
-      uint64_t rows = 0;
-      for (size_t q = e0; q < wave.size() && W.count < ex_cap; ++q) {
-        const moe_step_rec &r = c->recs[wave[q]];
-        W.payload[W.count] = c->slot_ptr(layer, r.slot);
-        W.row0[W.count] = off[r.expert];
-        W.n[W.count] = off[r.expert + 1] - off[r.expert];
-        rows += W.n[W.count];
-        ++W.count;
-      }
-      {
-        Span sp(c, c->main, MOE_KIND_GATEUP, 1, W.count * 2 * M, rows * 4ull * H * I);
-        HIP_TRY(c, launch_pf_gateup(d.qtype, W, c->pf_perm, c->pf_xb, c->pf_ab, T, H, I, k, c->main,
-                                    sp.timing()));
-        sp.end();
-      }
-      {
-        Span sp(c, c->main, MOE_KIND_DOWN, 1, W.count * M, rows * 2ull * H * I);
-        HIP_TRY(c, launch_pf_down(d.qtype, W, c->pf_perm, c->pf_ab, c->topk_w, c->pf_P, T * k, H, I,
-                                  c->main, sp.timing()));
-        sp.end();
-      }
+    {
+      Span sp(c, c->side, MOE_KIND_DOWN, 1, W.count * M, rows * 2ull * H * I);
+      HIP_TRY(c, launch_pf_down(d.qtype, W, c->pf_perm, c->pf_ab, c->topk_w, c->pf_P, T * k, H, I,
+                                c->side, sp.timing()));
+      sp.end();
     }
+    HIP_TRY(c, hipEventRecord(c->pf_ev[2 * ci + 1], c->side));
   }
+  if (!chunks.empty()) HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * chunks.size() - 1], 0));
   HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
   if (dbg_idx || dbg_w) {
     if (dbg_idx)
