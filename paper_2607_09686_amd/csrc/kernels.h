@@ -68,13 +68,11 @@ struct DecodeScratch {
   int8_t *xq;   // [3][H] digits of the (scaled) token, written by the router
   float *xsc;   // [H/32]
   float *h;     // [k][I] SwiGLU activations, written by gate/up
-  int8_t *hq;   // [3][k*I] their digits, written by gate/up
-  float *hsc;   // [k*I/32]
 };
 
-// Decode FFN.  Gate/up writes h rows (and their digits) at each listed
-// expert's top-k position; down reads the digits.  mode of down: 0 y = sum,
-// 1 y = x + sum, 2 y += sum.
+// Decode FFN.  Gate/up writes h rows at each listed expert's top-k position;
+// down forms their digits while staging them (n * I <= 12288).  mode of
+// down: 0 y = sum, 1 y = x + sum, 2 y += sum.
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
                          hipStream_t s, const Timing &t = {});
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,

@@ -92,24 +92,57 @@ __device__ void wave_topk(const float *z, int E, int k, int32_t *idx, float *w, 
   }
 }
 
-// Three int8 digits of v for the 32-wide block this lane's group of 32 lanes
-// holds (all 32 lanes call it together): s = max|v|/127 over the group,
-// D1 = rint(v/s), D2 = rint(254 (v/s - D1)), D3 = rint(254 (254 (v/s - D1) - D2)).
-// Returns s (0 for an all-zero block, digits 0).
-__device__ __forceinline__ float block_digits(float v, int8_t &d1, int8_t &d2, int8_t &d3) {
-  float m = fabsf(v);
-#pragma unroll
-  for (int off = 16; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
-  const float s = m * (1.f / 127.f);
-  const float t = s > 0.f ? v / s : 0.f;
+// The three int8 digits of v in a block of scale s, given rs = 1/s (0 for an
+// all-zero block): with t = v rs, D1 = rint(t), D2 = rint(254 (t - D1)),
+// D3 = rint(254 (254 (t - D1) - D2)).
+__device__ __forceinline__ void digits_of(float v, float rs, int &d1, int &d2, int &d3) {
+  const float t = v * rs;
   const float a = __builtin_rintf(t);
   const float r1 = (t - a) * 254.f;
   const float b = __builtin_rintf(r1);
   const float c = __builtin_rintf((r1 - b) * 254.f);
-  d1 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, a));
-  d2 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, b));
-  d3 = (int8_t)(int)fminf(127.f, fmaxf(-127.f, c));
+  d1 = (int)fminf(127.f, fmaxf(-127.f, a));
+  d2 = (int)fminf(127.f, fmaxf(-127.f, b));
+  d3 = (int)fminf(127.f, fmaxf(-127.f, c));
+}
+
+// Digits of a 32-wide block held by an aligned group of 8 lanes, four
+// consecutive values per lane: s = max|v|/127 over the block (three xor
+// shuffles; a max is exact in any order), then the digits of the lane's four
+// values packed into one dword per plane (byte j = value j).  Returns s
+// (0 for an all-zero block, digits 0).  All 8 lanes of the group call it.
+__device__ __forceinline__ float octet_digits(float4 v, uint32_t (&dw)[3]) {
+  float m = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
+  m = fmaxf(m, __shfl_xor(m, 1, kWave));
+  m = fmaxf(m, __shfl_xor(m, 2, kWave));
+  m = fmaxf(m, __shfl_xor(m, 4, kWave));
+  const float s = m * (1.f / 127.f);
+  const float rs = m > 0.f ? 127.f * __builtin_amdgcn_rcpf(m) : 0.f;
+  const float vv[4] = {v.x, v.y, v.z, v.w};
+  dw[0] = dw[1] = dw[2] = 0u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int d1, d2, d3;
+    digits_of(vv[j], rs, d1, d2, d3);
+    dw[0] |= ((uint32_t)d1 & 0xffu) << (8 * j);
+    dw[1] |= ((uint32_t)d2 & 0xffu) << (8 * j);
+    dw[2] |= ((uint32_t)d3 & 0xffu) << (8 * j);
+  }
   return s;
+}
+
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+}
+
+// Sum of the four signed bytes of a dword, summed over the aligned group of 8
+// lanes (the digit sum of a 32-wide block for the Q4_0 offset).
+__device__ __forceinline__ int octet_byte_sum(uint32_t dw) {
+  int t = sdot4(dw, 0x01010101u, 0);
+  t += __shfl_xor(t, 1, kWave);
+  t += __shfl_xor(t, 2, kWave);
+  t += __shfl_xor(t, 4, kWave);
+  return t;
 }
 
 // ---------------------------------------------------------------- router ---
@@ -153,31 +186,26 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(const float *_
 
 // Decode router, second kernel (one block): z = sum of the partials in block
 // order, scaled by 1/rms(x) (pre-norm); the scaled input as int8 digits with
-// per-block scales for the gate/up kernel; top-k + softmax.
+// per-block scales for the gate/up kernel; top-k + softmax.  Every global
+// load is issued up front; thread tid holds float4 number tid + 256 m of x,
+// which is the slice of block (tid/8 + 32 m) that octet_digits wants.
+constexpr int kMaxX4 = 8;  // H <= 8192
 __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     const float *__restrict__ x, const float *__restrict__ partial, int nb, int H, int E, int k,
     int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *__restrict__ xq,
     float *__restrict__ xsc, int prenorm) {
-  extern __shared__ float xs_l[];  // [H]
   __shared__ float red[kThreads];
   __shared__ float zs[256];
   __shared__ float wsum[kThreads / kWave];
   const int tid = threadIdx.x;
   const int phases = kThreads / E;
   const int c = tid % E, ph = tid / E;
-  // loads: x (8 per lane per round) and the partials (16 per lane per round)
-  for (int i0 = 0; i0 < H; i0 += 8 * kThreads) {
-    float v[8];
+  const int H4 = H / 4;
+  float4 xv[kMaxX4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int i = i0 + j * kThreads + tid;
-      v[j] = i < H ? x[i] : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int i = i0 + j * kThreads + tid;
-      if (i < H) xs_l[i] = v[j];
-    }
+  for (int m = 0; m < kMaxX4; ++m) {
+    const int i = tid + m * kThreads;
+    xv[m] = i < H4 ? reinterpret_cast<const float4 *>(x)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   const int per = (nb + phases - 1) / phases;
   float s = 0.f;
@@ -192,10 +220,16 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     }
   }
   red[tid] = s;
-  __syncthreads();
   float ss = 0.f;
-  if (prenorm)
-    for (int i = tid; i < H; i += kThreads) ss = fmaf(xs_l[i], xs_l[i], ss);
+  if (prenorm) {
+#pragma unroll
+    for (int m = 0; m < kMaxX4; ++m) {
+      ss = fmaf(xv[m].x, xv[m].x, ss);
+      ss = fmaf(xv[m].y, xv[m].y, ss);
+      ss = fmaf(xv[m].z, xv[m].z, ss);
+      ss = fmaf(xv[m].w, xv[m].w, ss);
+    }
+  }
 #pragma unroll
   for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
   if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = ss;
@@ -209,19 +243,18 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     for (int p = 0; p < phases; ++p) z += red[p * E + tid];
     zs[tid] = z * inv;
   }
-  // lanes 0..31 / 32..63 of a wave each hold one 32-wide block of x * inv
-  for (int b0 = 0; b0 < H / 32; b0 += 2 * (kThreads / kWave)) {
-    const int lane = tid & (kWave - 1);
-    const int b = b0 + 2 * (tid / kWave) + lane / 32;
-    const int i = 32 * b + (lane & 31);
-    const float v = b < H / 32 ? xs_l[i] * inv : 0.f;
-    int8_t d1, d2, d3;
-    const float sc = block_digits(v, d1, d2, d3);
-    if (b < H / 32) {
-      xq[i] = d1;
-      xq[H + i] = d2;
-      xq[2 * H + i] = d3;
-      if ((lane & 31) == 0) xsc[b] = sc;
+#pragma unroll
+  for (int m = 0; m < kMaxX4; ++m) {
+    const int i = tid + m * kThreads;  // float4 index; block i / 8
+    if (m * kThreads < H4) {           // uniform over the block (H4 is a multiple of 16)
+      const float4 v = make_float4(xv[m].x * inv, xv[m].y * inv, xv[m].z * inv, xv[m].w * inv);
+      uint32_t dw[3];
+      const float sc = octet_digits(v, dw);
+      if (i < H4) {
+#pragma unroll
+        for (int p = 0; p < 3; ++p) reinterpret_cast<uint32_t *>(xq + (int64_t)p * H)[i] = dw[p];
+        if ((i & 7) == 0) xsc[i / 8] = sc;
+      }
     }
   }
   __syncthreads();
@@ -314,24 +347,44 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__rest
 
 template <int QT>
 struct Fmt;
+// kGateUpFlight / kDownFlight: pairs per lane loading at once in the gate/up
+// kernel (per matrix) and in the down kernel, about 270 and 210 bytes.
 template <>
 struct Fmt<8> {
-  static constexpr int kBlockBytes = 34, kPairDwords = 17;
+  static constexpr int kBlockBytes = 34, kPairDwords = 17, kGateUpFlight = 2, kDownFlight = 3;
 };
 template <>
 struct Fmt<2> {
-  static constexpr int kBlockBytes = 18, kPairDwords = 9;
+  static constexpr int kBlockBytes = 18, kPairDwords = 9, kGateUpFlight = 4, kDownFlight = 6;
 };
+
+// LDS image of a digit vector of n values: three planes of n/64 pairs, each
+// pair's 64 digit bytes at a pitch of 80 bytes, so that the 16-byte reads of
+// eight lanes taking consecutive pairs fall on distinct banks.
+constexpr int kPairPitch = 80;
+__device__ __forceinline__ int plane_bytes(int n) { return (n / 64) * kPairPitch; }
+// Offset in a plane of the value at index i (any i; a 4-aligned i starts a dword).
+__device__ __forceinline__ int pad_off(int i) { return (i >> 6) * kPairPitch + (i & 63); }
+
+// A pair is only 4-byte aligned; the 16-byte loads below rely on the
+// unaligned global access that gfx9 runtimes enable (one dwordx4 instead of
+// four dword loads: a quarter of the address work per byte).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef u32x4 u32x4_a4 __attribute__((aligned(4)));
 
 template <int QT>
 __device__ __forceinline__ void load_pair(const uint8_t *p, uint32_t (&wd)[Fmt<QT>::kPairDwords]) {
-  const uint32_t *q = reinterpret_cast<const uint32_t *>(p);
+  constexpr int PD = Fmt<QT>::kPairDwords;
+  const u32x4_a4 *q = reinterpret_cast<const u32x4_a4 *>(p);
 #pragma unroll
-  for (int i = 0; i < Fmt<QT>::kPairDwords; ++i) wd[i] = q[i];
-}
-
-__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
-  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+  for (int i = 0; i < PD / 4; ++i) {
+    const u32x4 v = q[i];
+    wd[4 * i] = v.x;
+    wd[4 * i + 1] = v.y;
+    wd[4 * i + 2] = v.z;
+    wd[4 * i + 3] = v.w;
+  }
+  wd[PD - 1] = reinterpret_cast<const uint32_t *>(p)[PD - 1];
 }
 
 // fp32 value of a block's digit dot products I1 + I2/254 + I3/254^2.
@@ -396,12 +449,12 @@ __device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwo
   }
 }
 
-// The 48 digit dwords of pair p from LDS planes (plane c of length n bytes).
-__device__ __forceinline__ void load_digits(const uint8_t *planes, int64_t n, int p,
+// The 48 digit dwords of pair p from an LDS digit image (plane stride pb bytes).
+__device__ __forceinline__ void load_digits(const uint8_t *planes, int pb, int p,
                                             uint32_t (&D)[48]) {
 #pragma unroll
   for (int c = 0; c < 3; ++c) {
-    const uint4 *src = reinterpret_cast<const uint4 *>(planes + c * n + 64 * p);
+    const uint4 *src = reinterpret_cast<const uint4 *>(planes + c * pb + kPairPitch * p);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint4 v = src[i];
@@ -422,29 +475,49 @@ __device__ __forceinline__ float group_sum(float v, int lanes) {
   return v;
 }
 
-// Stage n bytes of digit planes (3 planes, plane stride src_stride, the
-// wanted range starting at src_off) and their block scales into LDS; for Q4_0
-// also the digit sum of every 32-wide block.
-__device__ __forceinline__ void stage_digits(const int8_t *__restrict__ q, int64_t src_stride,
-                                             int64_t src_off, int n, const float *__restrict__ sc,
-                                             uint8_t *qL, float *scL, int *dsL, bool sums,
-                                             int nthreads) {
-  for (int c = 0; c < 3; ++c) {
-    const uint4 *src = reinterpret_cast<const uint4 *>(q + c * src_stride + src_off);
-    uint4 *dst = reinterpret_cast<uint4 *>(qL + c * n);
-    for (int i = threadIdx.x; i < n / 16; i += nthreads) dst[i] = src[i];
+// Stage the token's digit planes ([3][H] bytes, contiguous) into an LDS digit
+// image, and the block scales: every global load is issued before the first
+// LDS store (one memory round trip).
+constexpr int kMaxTok16 = 6;  // 3 * 8192 / 16 / 256
+__device__ __forceinline__ void stage_token(const int8_t *__restrict__ q,
+                                            const float *__restrict__ sc, int H, uint8_t *qL,
+                                            float *scL) {
+  const int n16 = 3 * H / 16, nsc = H / 32, per = H / 16, pb = plane_bytes(H);
+  const uint4 *src = reinterpret_cast<const uint4 *>(q);
+  uint4 v[kMaxTok16];
+#pragma unroll
+  for (int m = 0; m < kMaxTok16; ++m) {
+    const int i = threadIdx.x + m * kThreads;
+    v[m] = i < n16 ? src[i] : make_uint4(0u, 0u, 0u, 0u);
   }
-  for (int i = threadIdx.x; i < n / 32; i += nthreads) scL[i] = sc[i];
-  if (sums) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < 3 * (n / 32); i += nthreads) {
-      const int c = i / (n / 32), b = i % (n / 32);
-      const int8_t *v = reinterpret_cast<const int8_t *>(qL + c * n + 32 * b);
-      int t = 0;
-#pragma unroll 8
-      for (int j = 0; j < 32; ++j) t += v[j];
-      dsL[c * (n / 32) + b] = t;
+  const float s = (int)threadIdx.x < nsc ? sc[threadIdx.x] : 0.f;
+#pragma unroll
+  for (int m = 0; m < kMaxTok16; ++m) {
+    const int i = threadIdx.x + m * kThreads;
+    if (i < n16) {
+      const int c = (i >= per) + (i >= 2 * per);
+      *reinterpret_cast<uint4 *>(qL + c * pb + pad_off(16 * (i - c * per))) = v[m];
     }
+  }
+  if ((int)threadIdx.x < nsc) scL[threadIdx.x] = s;
+}
+
+// Digit sums of every 32-wide block of a staged digit image of n values
+// (Q4_0 offset): dsL[c][b] = sum of the 32 digits of block b in plane c.
+__device__ __forceinline__ void digit_sums(const uint8_t *qL, int n, int *dsL) {
+  const int nb = n / 32, pb = plane_bytes(n);
+  for (int i = threadIdx.x; i < 3 * nb; i += kThreads) {
+    const int c = i / nb, b = i - c * nb;
+    const uint4 *v = reinterpret_cast<const uint4 *>(qL + c * pb + pad_off(32 * b));
+    const uint4 u0 = v[0], u1 = v[1];
+    int t = sdot4(u0.x, 0x01010101u, 0);
+    t = sdot4(u0.y, 0x01010101u, t);
+    t = sdot4(u0.z, 0x01010101u, t);
+    t = sdot4(u0.w, 0x01010101u, t);
+    t = sdot4(u1.x, 0x01010101u, t);
+    t = sdot4(u1.y, 0x01010101u, t);
+    t = sdot4(u1.z, 0x01010101u, t);
+    dsL[i] = sdot4(u1.w, 0x01010101u, t);
   }
 }
 
@@ -453,51 +526,50 @@ struct GateUpParams {
   const int8_t *xq;  // input digits [3][H]
   const float *xsc;  // input block scales [H/32]
   float *h;          // SwiGLU activations [k][I]
-  int8_t *hq;        // their digits [3][k*I]
-  float *hsc;        // their block scales [k*I/32]
   int H, I, k;
-  int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs per lane
+  int lanes, mpairs;  // lanes per row (power of 2, <= 32), pairs per lane
+  int lanes_log2;
 };
 
-constexpr int kGateUpThreads = 512;
-
 // One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
-// lanes handles pairs l, l+lanes, ... of both rows.  A block covers whole
-// 32-row groups of h (512/lanes rows), so it also writes their digits.
-// grid: n experts x ceil(I / rows_per_block).
+// lanes handles pairs l, l+lanes, ... of both rows (F of each in flight).
+// grid: n experts x ceil(I / (256 / lanes)).
 template <int QT>
-__global__ __launch_bounds__(kGateUpThreads) void gateup_kernel(GateUpParams a) {
+__global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
-  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
-  const int H = a.H, nb = H / 32, np = nb / 2;
-  uint8_t *qL = smem8;                                    // [3][H]
-  float *scL = reinterpret_cast<float *>(smem8 + 3 * H);  // [H/32]
-  int *dsL = reinterpret_cast<int *>(scL + nb);           // [3][H/32]
-  float *hL = reinterpret_cast<float *>(dsL + 3 * nb);    // [rows per block]
-  const int upb = kGateUpThreads / a.lanes;
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kGateUpFlight;
+  const int H = a.H, nb = H / 32, np = nb / 2, pb = plane_bytes(H);
+  uint8_t *qL = smem8;                                     // digit image of the token
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);  // [H/32]
+  int *dsL = reinterpret_cast<int *>(scL + nb);            // [3][H/32]
+  const int upb = kThreads / a.lanes;
   const int bpe = (a.I + upb - 1) / upb;
-  const int ei = blockIdx.x / bpe, r0 = (blockIdx.x % bpe) * upb;
-  const int r = r0 + threadIdx.x / a.lanes;
+  const int ei = blockIdx.x / bpe;
+  const int r = (blockIdx.x - ei * bpe) * upb + (threadIdx.x >> a.lanes_log2);
   const int l = threadIdx.x & (a.lanes - 1);
   const bool active = r < a.I;
   const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
   const uint8_t *gate = a.L.payload[ei] + (int64_t)r * rowb, *up = gate + mat;
-  uint32_t wg[2][PD], wu[2][PD];
+  uint32_t wg[F][PD], wu[F][PD];
 #pragma unroll
-  for (int m = 0; m < 2; ++m) {
+  for (int m = 0; m < F; ++m) {
     const int p = l + m * a.lanes;
     if (active && m < a.mpairs && p < np) {
       load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
       load_pair<QT>(up + (int64_t)p * 2 * BB, wu[m]);
     }
   }
-  stage_digits(a.xq, H, 0, H, a.xsc, qL, scL, dsL, QT == 2, kGateUpThreads);
+  stage_token(a.xq, a.xsc, H, qL, scL);
   __syncthreads();
+  if constexpr (QT == 2) {
+    digit_sums(qL, H, dsL);
+    __syncthreads();
+  }
   float g = 0.f, u = 0.f;
-  for (int m0 = 0; m0 < a.mpairs; m0 += 2) {
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
     if (m0 > 0) {
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
+      for (int m = 0; m < F; ++m) {
         const int p = l + (m0 + m) * a.lanes;
         if (active && m0 + m < a.mpairs && p < np) {
           load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
@@ -506,11 +578,11 @@ __global__ __launch_bounds__(kGateUpThreads) void gateup_kernel(GateUpParams a) 
       }
     }
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
+    for (int m = 0; m < F; ++m) {
       const int p = l + (m0 + m) * a.lanes;
       if (active && m0 + m < a.mpairs && p < np) {
         uint32_t D[48];
-        load_digits(qL, H, p, D);
+        load_digits(qL, pb, p, D);
         const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
         g += pair_dot<QT>(wg[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
         u += pair_dot<QT>(wu[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
@@ -519,80 +591,107 @@ __global__ __launch_bounds__(kGateUpThreads) void gateup_kernel(GateUpParams a) 
   }
   g = group_sum(g, a.lanes);
   u = group_sum(u, a.lanes);
-  if (l == 0) hL[threadIdx.x / a.lanes] = active ? silu(g) * u : 0.f;
-  __syncthreads();
-  // the block's rows of h, and their digits (one 32-lane group per 32 rows)
-  if ((int)threadIdx.x < upb) {
-    const int rr = r0 + threadIdx.x;
-    const float v = hL[threadIdx.x];
-    int8_t d1, d2, d3;
-    const float sc = block_digits(v, d1, d2, d3);
-    if (rr < a.I) {
-      const int64_t i = (int64_t)a.L.pos[ei] * a.I + rr, KI = (int64_t)a.k * a.I;
-      a.h[i] = v;
-      a.hq[i] = d1;
-      a.hq[KI + i] = d2;
-      a.hq[2 * KI + i] = d3;
-      if ((rr & 31) == 0) a.hsc[i / 32] = sc;
+  if (active && l == 0) a.h[(int64_t)a.L.pos[ei] * a.I + r] = silu(g) * u;
+}
+
+// Stage the activations of the listed experts into LDS as digit images
+// qL [n] (each three planes of plane_bytes(I)), block scales scL [n][I/32]
+// and (Q4_0) digit sums dsL [n][3][I/32]: group g = (expert, 32-wide block) of the n * I/32 groups is
+// taken by lanes 8(g % 32) .. +8 in pass g / 32, four values per lane; all
+// global loads are issued before the first digit is formed.
+constexpr int kMaxHPass = 12;  // k * I <= 12288: 384 groups, 32 per pass
+__device__ __forceinline__ void stage_h(const float *__restrict__ h, const ExpertList &L, int I,
+                                        uint8_t *qL, float *scL, int *dsL, bool sums) {
+  const int nb = I / 32, G = L.n * nb, pb = plane_bytes(I);
+  const int o = threadIdx.x & 7, g0 = threadIdx.x >> 3;
+  // (expert, block) of group g as floor((g + 0.5) / nb) in fp32: exact for
+  // g < 2^12 (the rounding error stays far below the 0.5/nb margin)
+  const float rnb = 1.f / (float)nb;
+  float4 v[kMaxHPass];
+  int dst[kMaxHPass], sci[kMaxHPass], dsi[kMaxHPass];
+#pragma unroll
+  for (int m = 0; m < kMaxHPass; ++m) {
+    const int g = g0 + 32 * m;
+    const int e = (int)(((float)g + 0.5f) * rnb), b = g - e * nb;
+    dst[m] = 3 * e * pb + pad_off(32 * b + 4 * o);
+    sci[m] = e * nb + b;
+    dsi[m] = 3 * e * nb + b;
+    v[m] = g < G ? *reinterpret_cast<const float4 *>(h + (int64_t)L.pos[min(e, L.n - 1)] * I +
+                                                     32 * b + 4 * o)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int m = 0; m < kMaxHPass; ++m) {
+    if (g0 + 32 * m < G) {  // uniform over the 8 lanes of a group
+      uint32_t dw[3];
+      const float s = octet_digits(v[m], dw);
+#pragma unroll
+      for (int c = 0; c < 3; ++c) *reinterpret_cast<uint32_t *>(qL + dst[m] + c * pb) = dw[c];
+      if (o == 0) scL[sci[m]] = s;
+      if (sums) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+          const int t = octet_byte_sum(dw[c]);
+          if (o == 0) dsL[dsi[m] + c * nb] = t;
+        }
+      }
     }
   }
 }
 
 struct DownParams {
   ExpertList L;
-  const int8_t *hq;  // activation digits [3][k*I]
-  const float *hsc;  // their block scales [k*I/32]
+  const float *h;  // SwiGLU activations [k][I]
   const float *w, *x;
   float *y;
   int H, I, k, mode;
   int lanes, mpairs;  // as in the gate/up kernel
   int rows;           // output rows per block: rows * n * lanes <= 256
+  int lanes_log2;
 };
 
 // One unit = (output row j, expert i), `lanes` lanes, lane l handling pairs
-// l, l+lanes, ... (three in flight).  grid: ceil(H / rows).
+// l, l+lanes, ... (F in flight).  grid: ceil(H / rows).
 // y[j] (+)= sum over the listed experts, in list order, of w[pos_i] (W_down,i h_i)_j.
 template <int QT>
 __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
-  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
-  const int I = a.I, nb = I / 32, np = nb / 2, n = a.L.n;
-  uint8_t *qL = smem8;                                        // [n][3][I]
-  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * I);  // [n][I/32]
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kDownFlight;
+  const int I = a.I, nb = I / 32, np = nb / 2, n = a.L.n, pb = plane_bytes(I);
+  uint8_t *qL = smem8;                                         // n digit images
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * pb);  // [n][I/32]
   int *dsL = reinterpret_cast<int *>(scL + n * nb);           // [n][3][I/32]
   float *res = reinterpret_cast<float *>(dsL + 3 * n * nb);   // [rows][n]
   const int j0 = blockIdx.x * a.rows;
-  const int unit = threadIdx.x / a.lanes, l = threadIdx.x & (a.lanes - 1);
+  const int unit = threadIdx.x >> a.lanes_log2, l = threadIdx.x & (a.lanes - 1);
   const int i = unit % n, rr = unit / n, j = j0 + rr;
   const bool active = rr < a.rows && j < a.H;
   const int64_t rowb = (int64_t)nb * BB;
   const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
   const uint8_t *row = a.L.payload[i] + 2 * mat + (int64_t)j * rowb;
-  uint32_t wd[3][PD];
+  uint32_t wd[F][PD];
 #pragma unroll
-  for (int m = 0; m < 3; ++m) {
+  for (int m = 0; m < F; ++m) {
     const int p = l + m * a.lanes;
     if (active && m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
   }
-  for (int e = 0; e < n; ++e)
-    stage_digits(a.hq, (int64_t)a.k * I, (int64_t)a.L.pos[e] * I, I, a.hsc + (int64_t)a.L.pos[e] * nb,
-                 qL + 3 * e * I, scL + e * nb, dsL + 3 * e * nb, QT == 2, kThreads);
+  stage_h(a.h, a.L, I, qL, scL, dsL, QT == 2);
   __syncthreads();
   float acc = 0.f;
-  for (int m0 = 0; m0 < a.mpairs; m0 += 3) {
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
     if (m0 > 0) {
 #pragma unroll
-      for (int m = 0; m < 3; ++m) {
+      for (int m = 0; m < F; ++m) {
         const int p = l + (m0 + m) * a.lanes;
         if (active && m0 + m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
       }
     }
 #pragma unroll
-    for (int m = 0; m < 3; ++m) {
+    for (int m = 0; m < F; ++m) {
       const int p = l + (m0 + m) * a.lanes;
       if (active && m0 + m < a.mpairs && p < np) {
         uint32_t D[48];
-        load_digits(qL + 3 * i * I, I, p, D);
+        load_digits(qL + 3 * i * pb, pb, p, D);
         const int *ds = dsL + 3 * i * nb;
         acc += pair_dot<QT>(wd[m], D, scL[i * nb + 2 * p], scL[i * nb + 2 * p + 1], ds + 2 * p,
                             ds + 2 * p + 1, nb);
@@ -1049,6 +1148,14 @@ __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__res
 // Lanes per row (a power of two) and pairs per lane for rows of np pairs,
 // when a lane keeps `in_flight` pairs of a row loading at once: few load
 // rounds first, then few idle lanes, then fewer lanes.
+#ifndef MOE_GATEUP_MAX_LANES
+#define MOE_GATEUP_MAX_LANES 32
+#endif
+#ifndef MOE_DOWN_MAX_LANES
+#define MOE_DOWN_MAX_LANES 64
+#endif
+constexpr int kGateUpMaxLanes = MOE_GATEUP_MAX_LANES, kDownMaxLanes = MOE_DOWN_MAX_LANES;
+
 void pick_lanes(int np, int in_flight, int max_lanes, int &lanes, int &mpairs) {
   double best = -1e9;
   lanes = max_lanes;
@@ -1099,15 +1206,17 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
                          hipStream_t s, const Timing &t) {
   const int np = H / 64;
-  GateUpParams a{L, S.xq, S.xsc, S.h, S.hq, S.hsc, H, I, k, 0, 0};
-  pick_lanes(np, 2, 16, a.lanes, a.mpairs);
-  const int upb = kGateUpThreads / a.lanes;  // a multiple of 32 rows
-  const size_t lds = 3 * (size_t)H + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
+  GateUpParams a{L, S.xq, S.xsc, S.h, H, I, k, 0, 0, 0};
+  pick_lanes(np, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes,
+             a.lanes, a.mpairs);
+  while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
+  const int upb = kThreads / a.lanes;
+  const size_t lds = 3 * (size_t)np * kPairPitch + 4 * (size_t)(H / 32) * 4;
   dim3 grid(L.n * ((I + upb - 1) / upb));
   if (qtype == 8)
-    hipExtLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kGateUpThreads), lds, s, t.start, t.stop, 0, a);
+    hipExtLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
-    hipExtLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kGateUpThreads), lds, s, t.start, t.stop, 0, a);
+    hipExtLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 
@@ -1115,11 +1224,15 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
                        const float *w, const float *x, float *y, int mode, hipStream_t s,
                        const Timing &t) {
   const int np = I / 64;
-  DownParams a{L, S.hq, S.hsc, w, x, y, H, I, k, mode, 0, 0, 0};
-  pick_lanes(np, 3, 64, a.lanes, a.mpairs);
+  if (L.n * I > 32 * 32 * kMaxHPass) return hipErrorInvalidValue;
+  DownParams a{L, S.h, w, x, y, H, I, k, mode, 0, 0, 0, 0};
+  pick_lanes(np, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
+             a.mpairs);
+  while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
   a.rows = kThreads / (a.lanes * L.n);
   if (a.rows < 1) return hipErrorInvalidValue;
-  const size_t lds = 3 * (size_t)L.n * I + 4 * (size_t)L.n * (I / 32) * 4 + 4 * (size_t)a.rows * L.n;
+  const size_t lds = 3 * (size_t)L.n * np * kPairPitch + 4 * (size_t)L.n * (I / 32) * 4 +
+                     4 * (size_t)a.rows * L.n;
   dim3 grid((H + a.rows - 1) / a.rows);
   if (qtype == 8)
     hipExtLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);

@@ -60,8 +60,6 @@ struct moe_cache {
   float *partial = nullptr;  // router split partials [grid][E]
   int8_t *xq = nullptr;         // decode: digits of the scaled token [3][H]
   float *xsc = nullptr;         //   and their block scales [H/32]
-  int8_t *hq = nullptr;         // decode: digits of the activations [3][k*I]
-  float *hsc = nullptr;         //   and their block scales [k*I/32]
   int32_t *topk_idx = nullptr;  // device [cap_tokens][k]
   float *topk_w = nullptr;
   float *zbuf = nullptr;  // prefill logits [cap_tokens][E]
@@ -96,7 +94,7 @@ struct moe_cache {
   bool timing_now = false;  // this call is bracketed
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
-  DecodeScratch scratch() const { return DecodeScratch{xq, xsc, h, hq, hsc}; }
+  DecodeScratch scratch() const { return DecodeScratch{xq, xsc, h}; }
 };
 
 namespace {
@@ -217,8 +215,6 @@ void free_all(moe_cache *c) {
   for (auto e : c->pf_ev) (void)hipEventDestroy(e);
   (void)hipFree(c->xq);
   (void)hipFree(c->xsc);
-  (void)hipFree(c->hq);
-  (void)hipFree(c->hsc);
   if (c->host_idx) (void)hipHostFree(c->host_idx);
   if (c->host_w) (void)hipHostFree(c->host_w);
   if (c->ev_route) (void)hipEventDestroy(c->ev_route);
@@ -463,8 +459,6 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
       hipMalloc(&c->h, (size_t)desc->top_k * desc->inter * sizeof(float)) != hipSuccess ||
       hipMalloc(&c->xq, 3 * (size_t)desc->hidden) != hipSuccess ||
       hipMalloc(&c->xsc, (size_t)desc->hidden / 32 * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->hq, 3 * (size_t)desc->top_k * desc->inter) != hipSuccess ||
-      hipMalloc(&c->hsc, (size_t)desc->top_k * desc->inter / 32 * sizeof(float)) != hipSuccess ||
       hipHostMalloc(&c->host_idx, kMaxRouted * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->host_w, kMaxRouted * sizeof(float), hipHostMallocCoherent) != hipSuccess) {
     (void)hipGetLastError();

@@ -62,6 +62,19 @@ class KernelStats(ctypes.Structure):
 _lib = None
 
 
+def _check_one_hip_runtime():
+    """Raise if more than one copy of the HIP runtime is mapped in this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            paths = {ln.split()[-1] for ln in f if "libamdhip64.so" in ln}
+    except OSError:
+        return
+    real = {os.path.realpath(p) for p in paths}
+    if len(real) > 1:
+        raise RuntimeError("two HIP runtimes are loaded (%s); import torch before the "
+                           "library is first loaded" % ", ".join(sorted(real)))
+
+
 def lib():
     """Load libmoecache.so (raises if it is not built)."""
     global _lib
@@ -69,7 +82,13 @@ def lib():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run paper_2607_09686_amd.build.build()")
+    # torch ships its own HIP runtime (soname libamdhip64.so.7).  Loading torch
+    # first makes the library bind to that same runtime, so device pointers and
+    # streams from torch are valid in it; loaded the other way round, the process
+    # would hold two HIP runtimes and torch's would fail to see the GPU.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
+    _check_one_hip_runtime()
     vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
     P = ctypes.POINTER
     sig = {
