@@ -130,12 +130,20 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
  *   layer    0..n_layers-1
  *   y        device, [n_tokens][hidden] fp32, written; must not overlap x
  *   delta    host, nullable: this call's counter increments
- * n_tokens == 1 takes the decode path (fp32 activations, GEMV kernels);
- * n_tokens > 1 the prefill path (bf16 MFMA grouped GEMM: weights, x and the
- * SwiGLU activations rounded to bf16, fp32 accumulation).
- * Work is queued on desc.hip_stream; the host blocks once per call, until the
- * routes are known.  y is ready when that stream passes this call; delta is
- * final on return.  Routing reads x, so x must be ready on that stream. */
+ * n_tokens == 1 takes the decode path (GEMV kernels on fp32 activations held
+ * as three int8 digits per value); n_tokens > 1 the prefill path (bf16 MFMA
+ * grouped GEMM: weights rounded to bf16, x and the SwiGLU activations carried
+ * as two bf16 terms, fp32 accumulation).
+ * Work is queued on desc.hip_stream and y is ready when that stream passes
+ * this call.  Decode with the default copy kernel does not block the host:
+ * the layer's slot table lives in device memory and is stepped by the
+ * router's last kernel.  A routing failure there (no finite logit among the
+ * top_k) makes the call do no work and is returned by the next call that
+ * synchronises (a call with delta or routes, counters, trace, stats, reset or
+ * a prefill call), which poisons the handle.  The SIDE/SDMA copy modes and
+ * prefill block until the routes are known.  A non-NULL delta makes the call
+ * wait for its own completion.  Routing reads x, so x must be ready on that
+ * stream. */
 int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
                       int32_t layer, float *y, moe_counters *delta);
 

@@ -22,14 +22,44 @@ struct ExpertList {
   int32_t n;
 };
 
-// Decode router: one token, two launches.  partial: [grid][E] fp32 scratch.
+// Work of one decode call written on the device by the slot-table step and
+// read by the copy, gate/up and down kernels.
+struct WorkList {
+  int32_t n_copy, pad;
+  const uint8_t *src[kMaxRouted];  // misses in ascending expert order
+  uint8_t *dst[kMaxRouted];
+  ExpertList list;  // the k routed experts in rank order (n = 0 after a routing error)
+};
+
+// Device-resident slot table of one layer (the rule of slot_lru.h) and where
+// a call's results go.  trace: 6 int32 per record (moe_step_rec), nullable.
+struct LruDev {
+  int32_t *slot_of;    // [E], -1 if not resident
+  int32_t *expert_in;  // [C], -1 if free
+  int64_t *stamp;      // [E]
+  int64_t *meta;       // [3]: clock, step number, slots in use
+  uint64_t *cnt;       // [4]: hits, misses, evictions, materialised bytes
+  int32_t *trace;
+  uint64_t *trace_n;   // records written so far
+  int32_t *err;        // set to 1 + (bad id & 0xffff) when a routed id is out of range
+  const uint8_t *store;  // the layer's E payloads in the store
+  uint8_t *slots;        // the layer's C slots
+  WorkList *work;
+  int64_t P;
+  int32_t C, layer;
+};
+
+// Decode router: one token, two launches.  partial: [grid * E + 1] fp32 scratch.
 // Writes idx/w [k] to device and, if non-null, to host-mapped mirrors.
 int router_decode_grid(int H);
 // Also writes the digits xq [3][H] and block scales xsc [H/32] of x * s,
 // s = 1/sqrt(mean(x^2)+1e-6) when prenorm else 1; the logits are scaled by s.
+// With lru non-null the finishing block also runs the layer's slot-table
+// step and writes lru->work (E <= 256, C <= E).
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
-                                float *xsc, bool prenorm, hipStream_t s, const Timing &t = {});
+                                float *xsc, bool prenorm, const LruDev *lru, hipStream_t s,
+                                const Timing &t = {});
 
 // Prefill router: partial logits over router_slices() slices of H into
 // z [slices][T][E], then per token z = tscale[t] * (sum of slices) (tscale
@@ -67,21 +97,29 @@ hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, in
 struct DecodeScratch {
   int8_t *xq;   // [3][H] digits of the (scaled) token, written by the router
   float *xsc;   // [H/32]
-  float *h;     // [k][I] SwiGLU activations, written by gate/up
+  int8_t *hq;   // [3][k*I] digits of the SwiGLU activations, written by gate/up
+  float *hsc;   // [k*I/16] their 16-wide block scales
+  int32_t *hds; // [3][k*I/16] digit sums of those blocks (Q4_0 offset)
 };
 
-// Decode FFN.  Gate/up writes h rows at each listed expert's top-k position;
-// down forms their digits while staging them (n * I <= 12288).  mode of
-// down: 0 y = sum, 1 y = x + sum, 2 y += sum.
+// Decode FFN.  Gate/up writes the activations of its rows, as digits of
+// 16-wide blocks, at each listed expert's top-k position; down stages them
+// (n * I <= 12288).  mode of down: 0 y = sum, 1 y = x + sum, 2 y += sum.
+// With Ld non-null the kernels read the list from device memory (L.n is then
+// only the launch size; a device list with n = 0 makes them do nothing).
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                         hipStream_t s, const Timing &t = {});
+                         const ExpertList *Ld, hipStream_t s, const Timing &t = {});
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                       const float *w, const float *x, float *y, int mode, hipStream_t s,
-                       const Timing &t = {});
+                       const ExpertList *Ld, const float *w, const float *x, float *y, int mode,
+                       hipStream_t s, const Timing &t = {});
 
 // Copy n <= max_copy() payloads of `bytes` (multiple of 16, 16-byte aligned)
 // src[i] -> dst[i] with a copy kernel of `grid` blocks (host-pinned or device sources).
 hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, int n, int64_t bytes,
                               int grid, hipStream_t s, const Timing &t = {});
+// The copies a device work list names (n_copy of them); acc (nullable) gets
+// += copies, += bytes.
+hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, uint64_t *acc,
+                                   hipStream_t s, const Timing &t = {});
 
 }  // namespace moecache

@@ -35,7 +35,8 @@ __device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
 }
 
 // Top-k over z[0..E) by one wave (E <= 256).  Writes ids in rank order and the
-// softmax over the chosen logits.  Must be called by all 64 lanes of a wave.
+// softmax over the chosen logits (idx2/w2: optional further copies of them).
+// Must be called by all 64 lanes of a wave.
 __device__ void wave_topk(const float *z, int E, int k, int32_t *idx, float *w, int32_t *idx2,
                           float *w2) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -135,130 +136,290 @@ __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
   return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
-// Sum of the four signed bytes of a dword, summed over the aligned group of 8
-// lanes (the digit sum of a 32-wide block for the Q4_0 offset).
-__device__ __forceinline__ int octet_byte_sum(uint32_t dw) {
-  int t = sdot4(dw, 0x01010101u, 0);
-  t += __shfl_xor(t, 1, kWave);
-  t += __shfl_xor(t, 2, kWave);
-  t += __shfl_xor(t, 4, kWave);
-  return t;
-}
-
 // ---------------------------------------------------------------- router ---
 
 constexpr int kRouterRowsPerBlock = 32;
 
+constexpr int kMaxX4 = 8;  // H <= 8192
+
 // Decode router, first kernel: block b accumulates z over rows [32b, 32b+32)
 // of W_r into partial[b][E] (no cross-block communication inside a launch:
 // on a multi-XCD GPU a device-scope fence costs more than a second launch).
-__global__ __launch_bounds__(kThreads) void router_partial_kernel(const float *__restrict__ x,
-                                                                  const float *__restrict__ wr,
-                                                                  int H, int E,
-                                                                  float *__restrict__ partial) {
+// Every block also forms s = 1/sqrt(mean(x^2) + 1e-6) (or 1) from the whole x,
+// in the same order, so all blocks hold the same s; block b writes the digits
+// of its 32-wide block of x * s, and block 0 writes s at partial[nb * E].
+__global__ __launch_bounds__(kThreads) void router_partial_kernel(
+    const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int prenorm,
+    float *__restrict__ partial, int8_t *__restrict__ xq, float *__restrict__ xsc) {
   __shared__ float red[kThreads];
+  __shared__ float wsum[kThreads / kWave];
   const int tid = threadIdx.x;
   const int phases = kThreads / E;  // E <= 256
   const int c = tid % E, ph = tid / E;
   const int r0 = blockIdx.x * kRouterRowsPerBlock;
   const int r1 = min(H, r0 + kRouterRowsPerBlock);
-  float acc = 0.f;
-  if (ph < phases) {
-    float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
-#pragma unroll
-    for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
-      const int r = r0 + ph + phases * j;
-      const bool ok = r < r1;
-      xv[j] = ok ? x[r] : 0.f;
-      wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
-  }
-  red[tid] = acc;
-  __syncthreads();
-  if (tid < E) {
-    float s = 0.f;
-    for (int p = 0; p < phases; ++p) s += red[p * E + tid];
-    partial[blockIdx.x * E + tid] = s;
-  }
-}
-
-// Decode router, second kernel (one block): z = sum of the partials in block
-// order, scaled by 1/rms(x) (pre-norm); the scaled input as int8 digits with
-// per-block scales for the gate/up kernel; top-k + softmax.  Every global
-// load is issued up front; thread tid holds float4 number tid + 256 m of x,
-// which is the slice of block (tid/8 + 32 m) that octet_digits wants.
-constexpr int kMaxX4 = 8;  // H <= 8192
-__global__ __launch_bounds__(kThreads) void router_finish_kernel(
-    const float *__restrict__ x, const float *__restrict__ partial, int nb, int H, int E, int k,
-    int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *__restrict__ xq,
-    float *__restrict__ xsc, int prenorm) {
-  __shared__ float red[kThreads];
-  __shared__ float zs[256];
-  __shared__ float wsum[kThreads / kWave];
-  const int tid = threadIdx.x;
-  const int phases = kThreads / E;
-  const int c = tid % E, ph = tid / E;
   const int H4 = H / 4;
-  float4 xv[kMaxX4];
+  const float4 *x4 = reinterpret_cast<const float4 *>(x);
+  float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+#pragma unroll
+  for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
+    const int r = r0 + ph + phases * j;
+    const bool ok = ph < phases && r < r1;
+    xv[j] = ok ? x[r] : 0.f;
+    wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
+  }
+  float4 xa[kMaxX4];
 #pragma unroll
   for (int m = 0; m < kMaxX4; ++m) {
     const int i = tid + m * kThreads;
-    xv[m] = i < H4 ? reinterpret_cast<const float4 *>(x)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    xa[m] = prenorm && i < H4 ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  const int per = (nb + phases - 1) / phases;
-  float s = 0.f;
-  if (ph < phases) {
-    const int b0 = ph * per, b1 = min(nb, b0 + per);
-    for (int b = b0; b < b1; b += 16) {
-      float v[16];
+  const float4 mine = tid < 8 ? x4[r0 / 4 + tid] : make_float4(0.f, 0.f, 0.f, 0.f);
+  float acc = 0.f;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) s += v[j];
-    }
-  }
-  red[tid] = s;
+  for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
   float ss = 0.f;
-  if (prenorm) {
 #pragma unroll
-    for (int m = 0; m < kMaxX4; ++m) {
-      ss = fmaf(xv[m].x, xv[m].x, ss);
-      ss = fmaf(xv[m].y, xv[m].y, ss);
-      ss = fmaf(xv[m].z, xv[m].z, ss);
-      ss = fmaf(xv[m].w, xv[m].w, ss);
-    }
+  for (int m = 0; m < kMaxX4; ++m) {
+    ss = fmaf(xa[m].x, xa[m].x, ss);
+    ss = fmaf(xa[m].y, xa[m].y, ss);
+    ss = fmaf(xa[m].z, xa[m].z, ss);
+    ss = fmaf(xa[m].w, xa[m].w, ss);
   }
 #pragma unroll
   for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
   if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = ss;
+  red[tid] = acc;
   __syncthreads();
   float tot = 0.f;
 #pragma unroll
   for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
   const float inv = prenorm ? 1.f / sqrtf(tot / (float)H + 1e-6f) : 1.f;
   if (tid < E) {
+    float sum = 0.f;
+    for (int p = 0; p < phases; ++p) sum += red[p * E + tid];
+    partial[blockIdx.x * E + tid] = sum;
+  }
+  if (tid < 8) {  // one octet: the block's 32 values
+    const float4 v = make_float4(mine.x * inv, mine.y * inv, mine.z * inv, mine.w * inv);
+    uint32_t dw[3];
+    const float sc = octet_digits(v, dw);
+#pragma unroll
+    for (int p = 0; p < 3; ++p) reinterpret_cast<uint32_t *>(xq + (int64_t)p * H + r0)[tid] = dw[p];
+    if (tid == 0) xsc[blockIdx.x] = sc;
+  }
+  if (blockIdx.x == 0 && tid == 0) partial[(int64_t)gridDim.x * E] = inv;
+}
+
+// Decode router, second kernel (one block): z = s * (sum of the partials in
+// block order); top-k + softmax; with lru.slot_of set, the layer's slot-table
+// step.  Every global load is issued up front (the table state included).
+//
+// Top-k by rank: expert e is chosen iff fewer than k experts beat it in the
+// (logit descending, id ascending) order, and its rank is its position.  The
+// order is that of one 64-bit key per expert: the order-preserving bit image
+// of the logit (NaN taken as -inf, -0 as +0) above 255 - id.  A non-finite
+// chosen logit is a routing failure.
+//
+// Slot-table step (one thread per expert): the same rule as the host table
+// (stamp the routed set S in ascending order; a routed expert holding a slot
+// is a hit; misses in ascending order take the lowest free slot, else the
+// slot of the resident expert with the smallest stamp).  Stamps are unique
+// and all of S is stamped after every other resident, so the victims are the
+// oldest residents outside S, in stamp order, for the misses beyond the free
+// slots in expert order.
+__device__ __forceinline__ uint64_t rank_key(float z, int e) {
+  z = z != z ? -INFINITY : z + 0.f;
+  uint32_t u = __float_as_uint(z);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 8) | (uint64_t)(255 - e);
+}
+
+__global__ __launch_bounds__(kThreads) void router_finish_kernel(
+    const float *__restrict__ partial, int nb, int E, int k, int32_t *idx, float *w,
+    int32_t *host_idx, float *host_w, LruDev lru) {
+  __shared__ float red[kThreads];
+  __shared__ float zs[256];
+  __shared__ uint64_t keyZ[256];
+  __shared__ int32_t selL[kMaxRouted], vicL[kMaxRouted], vslL[kMaxRouted];
+  __shared__ float zselL[kMaxRouted];
+  __shared__ int32_t cntL[2][kThreads / kWave];
+  __shared__ int64_t keyL[256];
+  __shared__ int32_t badL;
+  const int tid = threadIdx.x;
+  const int phases = kThreads / E;
+  const int c = tid % E, ph = tid / E;
+  const bool dev = lru.slot_of != nullptr;
+  // the table state first: its latency hides behind the routing work
+  int so = -1;
+  int64_t st = 0, clock0 = 0, step = 0, used = 0;
+  uint64_t tn = 0;
+  if (dev) {
+    if (tid < E) {
+      so = lru.slot_of[tid];
+      st = lru.stamp[tid];
+    }
+    clock0 = lru.meta[0];
+    step = lru.meta[1];
+    used = lru.meta[2];
+    if (lru.trace) tn = *lru.trace_n;
+  }
+  const float inv = partial[(int64_t)nb * E];
+  const int per = (nb + phases - 1) / phases;
+  float sacc = 0.f;
+  if (ph < phases) {
+    const int b0 = ph * per, b1 = min(nb, b0 + per);
+    for (int b = b0; b < b1; b += 48) {  // one round trip up to 48 partials per lane
+      float v[48];
+#pragma unroll
+      for (int j = 0; j < 48; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 48; ++j) sacc += v[j];
+    }
+  }
+  red[tid] = sacc;
+  __syncthreads();
+  if (tid < E) {
     float z = 0.f;
     for (int p = 0; p < phases; ++p) z += red[p * E + tid];
-    zs[tid] = z * inv;
+    z *= inv;
+    zs[tid] = z;
+    keyZ[tid] = rank_key(z, tid);
   }
+  __syncthreads();
+  // rank of expert c over the experts [ph E / phases, (ph+1) E / phases)
+  {
+    int r = 0;
+    if (ph < phases) {
+      const uint64_t kc = keyZ[c];
+      const int f0 = ph * E / phases, f1 = (ph + 1) * E / phases;
+      int f = f0;
+      for (; f + 8 <= f1; f += 8) {  // eight independent LDS reads per step
+        uint64_t v[8];
 #pragma unroll
-  for (int m = 0; m < kMaxX4; ++m) {
-    const int i = tid + m * kThreads;  // float4 index; block i / 8
-    if (m * kThreads < H4) {           // uniform over the block (H4 is a multiple of 16)
-      const float4 v = make_float4(xv[m].x * inv, xv[m].y * inv, xv[m].z * inv, xv[m].w * inv);
-      uint32_t dw[3];
-      const float sc = octet_digits(v, dw);
-      if (i < H4) {
+        for (int j = 0; j < 8; ++j) v[j] = keyZ[f + j];
 #pragma unroll
-        for (int p = 0; p < 3; ++p) reinterpret_cast<uint32_t *>(xq + (int64_t)p * H)[i] = dw[p];
-        if ((i & 7) == 0) xsc[i / 8] = sc;
+        for (int j = 0; j < 8; ++j) r += v[j] > kc ? 1 : 0;
       }
+      for (; f < f1; ++f) r += keyZ[f] > kc ? 1 : 0;
+    }
+    __syncthreads();
+    red[tid] = __int_as_float(r);
+  }
+  __syncthreads();
+  int rank = E;
+  if (tid < E) {
+    rank = 0;
+    for (int p = 0; p < phases; ++p) rank += __float_as_int(red[p * E + tid]);
+    if (rank < k) {
+      selL[rank] = tid;
+      zselL[rank] = zs[tid];
     }
   }
   __syncthreads();
-  if (tid < kWave) wave_topk(zs, E, k, idx, w, host_idx, host_w);
+  if (tid < kWave) {  // softmax over the chosen logits (the first is the largest)
+    const bool ok = __ballot(tid < k && !isfinite(zselL[tid < k ? tid : 0])) == 0;
+    const float ex = tid < k && ok ? expf(zselL[tid] - zselL[0]) : 0.f;
+    float sum = ex;
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+    if (tid < k) {
+      const int32_t id = ok ? selL[tid] : 0x7fffffff;
+      const float wi = ok ? ex / sum : 0.f;
+      idx[tid] = id;
+      w[tid] = wi;
+      if (host_idx) host_idx[tid] = id;
+      if (host_w) host_w[tid] = wi;
+    }
+    if (tid == 0) badL = ok ? 0 : 1;
+  }
+  if (!dev) return;  // uniform
+  __syncthreads();
+  if (badL) {  // no work for this call; reported at the next synchronisation
+    if (tid == 0) {
+      *lru.err = 1;
+      lru.work->n_copy = 0;
+      lru.work->list.n = 0;
+    }
+    return;
+  }
+  const int lane = tid & (kWave - 1), wv = tid / kWave;
+  const bool inS = rank < k;
+  const bool miss = inS && so < 0;
+  const bool cand = tid < E && so >= 0 && !inS;
+  const uint64_t bS = __ballot(inS), bM = __ballot(miss), lt = (1ull << lane) - 1ull;
+  if (lane == 0) {
+    cntL[0][wv] = __popcll(bS);
+    cntL[1][wv] = __popcll(bM);
+  }
+  for (int sl = tid; sl < lru.C; sl += kThreads) keyL[sl] = INT64_MAX;
+  __syncthreads();
+  int rS = __popcll(bS & lt), rM = __popcll(bM & lt), nM = 0;
+#pragma unroll
+  for (int v = 0; v < kThreads / kWave; ++v) {
+    if (v < wv) {
+      rS += cntL[0][v];
+      rM += cntL[1][v];
+    }
+    nM += cntL[1][v];
+  }
+  if (cand) keyL[so] = st;
+  const int nfree = lru.C - (int)used;
+  const int nev = max(0, nM - nfree);
+  __syncthreads();
+  bool evicted = false;
+  if (cand && nev > 0) {
+    int cr = 0;  // residents outside S with an older stamp (stamps are unique)
+    for (int sl = 0; sl < lru.C; ++sl) cr += keyL[sl] < st ? 1 : 0;
+    if (cr < nev) {
+      evicted = true;
+      vicL[cr] = tid;
+      vslL[cr] = so;
+    }
+  }
+  __syncthreads();
+  int fs = so, fev = -1;
+  if (miss) {
+    if (rM < nfree) {
+      fs = (int)used + rM;
+    } else {
+      fs = vslL[rM - nfree];
+      fev = vicL[rM - nfree];
+    }
+  }
+  if (evicted) lru.slot_of[tid] = -1;
+  if (inS) {
+    lru.stamp[tid] = clock0 + rS + 1;
+    if (miss) {
+      lru.slot_of[tid] = fs;
+      lru.expert_in[fs] = tid;
+      lru.work->src[rM] = lru.store + (int64_t)tid * lru.P;
+      lru.work->dst[rM] = lru.slots + (int64_t)fs * lru.P;
+    }
+    lru.work->list.payload[rank] = lru.slots + (int64_t)fs * lru.P;
+    lru.work->list.pos[rank] = rank;
+    if (lru.trace) {
+      int32_t *r = lru.trace + 6 * (int64_t)(tn + rS);
+      r[0] = lru.layer;
+      r[1] = (int32_t)step;
+      r[2] = tid;
+      r[3] = miss ? 0 : 1;
+      r[4] = fs;
+      r[5] = fev;
+    }
+  }
+  if (tid == 0) {
+    lru.work->list.n = k;
+    lru.work->n_copy = nM;
+    lru.cnt[0] += (uint64_t)(k - nM);
+    lru.cnt[1] += (uint64_t)nM;
+    lru.cnt[2] += (uint64_t)nev;
+    lru.cnt[3] += (uint64_t)nM * (uint64_t)lru.P;
+    lru.meta[0] = clock0 + k;
+    lru.meta[1] = step + 1;
+    lru.meta[2] = used + min(nM, nfree);
+    if (lru.trace) *lru.trace_n = tn + (uint64_t)k;
+  }
 }
 
 // Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]:
@@ -449,6 +610,59 @@ __device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwo
   }
 }
 
+// As pair_dot, with inputs in 16-wide digit blocks: sc[0..3] the scales of
+// the pair's four 16-value quarters, ds[c * dstride + q] (Q4_0 only) their
+// digit sums.  A Q4_0 block's low nibbles are its first 16 values and its
+// high nibbles the last 16, so each nibble half meets one input block.
+template <int QT>
+__device__ __forceinline__ float pair_dot16(const uint32_t (&wd)[Fmt<QT>::kPairDwords],
+                                            const uint32_t *D, const float *sc, const int *ds,
+                                            int dstride) {
+  int A[4][3] = {};  // [quarter][digit plane]
+  float d0, d1;
+  if constexpr (QT == 8) {
+    d0 = half_bits_to_float(wd[0] & 0xffffu);
+    d1 = half_bits_to_float(wd[8] >> 16);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t q = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2);
+#pragma unroll
+      for (int c = 0; c < 3; ++c) A[j >> 2][c] = sdot4(q, D[16 * c + j], A[j >> 2][c]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t q = wd[9 + j];
+#pragma unroll
+      for (int c = 0; c < 3; ++c) A[2 + (j >> 2)][c] = sdot4(q, D[16 * c + 8 + j], A[2 + (j >> 2)][c]);
+    }
+  } else {
+    d0 = half_bits_to_float(wd[0] & 0xffffu);
+    d1 = half_bits_to_float(wd[4] >> 16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t v0 = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2), v1 = wd[5 + j];
+      const uint32_t lo0 = v0 & 0x0f0f0f0fu, hi0 = (v0 >> 4) & 0x0f0f0f0fu;
+      const uint32_t lo1 = v1 & 0x0f0f0f0fu, hi1 = (v1 >> 4) & 0x0f0f0f0fu;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        A[0][c] = sdot4(lo0, D[16 * c + j], A[0][c]);
+        A[1][c] = sdot4(hi0, D[16 * c + 4 + j], A[1][c]);
+        A[2][c] = sdot4(lo1, D[16 * c + 8 + j], A[2][c]);
+        A[3][c] = sdot4(hi1, D[16 * c + 12 + j], A[3][c]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) A[q][c] -= 8 * ds[c * dstride + q];
+  }
+  const float r0 = fmaf(sc[0], recombine(A[0][0], A[0][1], A[0][2]),
+                        sc[1] * recombine(A[1][0], A[1][1], A[1][2]));
+  const float r1 = fmaf(sc[2], recombine(A[2][0], A[2][1], A[2][2]),
+                        sc[3] * recombine(A[3][0], A[3][1], A[3][2]));
+  return fmaf(d0, r0, d1 * r1);
+}
+
 // The 48 digit dwords of pair p from an LDS digit image (plane stride pb bytes).
 __device__ __forceinline__ void load_digits(const uint8_t *planes, int pb, int p,
                                             uint32_t (&D)[48]) {
@@ -523,17 +737,21 @@ __device__ __forceinline__ void digit_sums(const uint8_t *qL, int n, int *dsL) {
 
 struct GateUpParams {
   ExpertList L;
+  const ExpertList *Ld;  // device list (nullable): read instead of L
   const int8_t *xq;  // input digits [3][H]
   const float *xsc;  // input block scales [H/32]
-  float *h;          // SwiGLU activations [k][I]
+  int8_t *hq;        // activation digits [3][k*I]
+  float *hsc;        // their 16-wide block scales [k*I/16]
+  int32_t *hds;      // their digit sums [3][k*I/16] (Q4_0)
   int H, I, k;
-  int lanes, mpairs;  // lanes per row (power of 2, <= 32), pairs per lane
+  int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs per lane
   int lanes_log2;
 };
 
 // One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
 // lanes handles pairs l, l+lanes, ... of both rows (F of each in flight).
-// grid: n experts x ceil(I / (256 / lanes)).
+// A block covers 256 / lanes >= 16 consecutive rows, so it also forms the
+// digits of its whole 16-wide blocks of h.  grid: n experts x ceil(I / (256 / lanes)).
 template <int QT>
 __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
@@ -542,14 +760,18 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   uint8_t *qL = smem8;                                     // digit image of the token
   float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);  // [H/32]
   int *dsL = reinterpret_cast<int *>(scL + nb);            // [3][H/32]
+  float *hL = reinterpret_cast<float *>(dsL + 3 * nb);     // [256 / lanes]
+  const ExpertList &L = a.Ld ? *a.Ld : a.L;
   const int upb = kThreads / a.lanes;
   const int bpe = (a.I + upb - 1) / upb;
   const int ei = blockIdx.x / bpe;
-  const int r = (blockIdx.x - ei * bpe) * upb + (threadIdx.x >> a.lanes_log2);
+  if (ei >= L.n) return;  // uniform over the block
+  const int r0 = (blockIdx.x - ei * bpe) * upb;
+  const int r = r0 + (threadIdx.x >> a.lanes_log2);
   const int l = threadIdx.x & (a.lanes - 1);
   const bool active = r < a.I;
   const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
-  const uint8_t *gate = a.L.payload[ei] + (int64_t)r * rowb, *up = gate + mat;
+  const uint8_t *gate = L.payload[ei] + (int64_t)r * rowb, *up = gate + mat;
   uint32_t wg[F][PD], wu[F][PD];
 #pragma unroll
   for (int m = 0; m < F; ++m) {
@@ -591,57 +813,138 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   }
   g = group_sum(g, a.lanes);
   u = group_sum(u, a.lanes);
-  if (active && l == 0) a.h[(int64_t)a.L.pos[ei] * a.I + r] = silu(g) * u;
-}
-
-// Stage the activations of the listed experts into LDS as digit images
-// qL [n] (each three planes of plane_bytes(I)), block scales scL [n][I/32]
-// and (Q4_0) digit sums dsL [n][3][I/32]: group g = (expert, 32-wide block) of the n * I/32 groups is
-// taken by lanes 8(g % 32) .. +8 in pass g / 32, four values per lane; all
-// global loads are issued before the first digit is formed.
-constexpr int kMaxHPass = 12;  // k * I <= 12288: 384 groups, 32 per pass
-__device__ __forceinline__ void stage_h(const float *__restrict__ h, const ExpertList &L, int I,
-                                        uint8_t *qL, float *scL, int *dsL, bool sums) {
-  const int nb = I / 32, G = L.n * nb, pb = plane_bytes(I);
-  const int o = threadIdx.x & 7, g0 = threadIdx.x >> 3;
-  // (expert, block) of group g as floor((g + 0.5) / nb) in fp32: exact for
-  // g < 2^12 (the rounding error stays far below the 0.5/nb margin)
-  const float rnb = 1.f / (float)nb;
-  float4 v[kMaxHPass];
-  int dst[kMaxHPass], sci[kMaxHPass], dsi[kMaxHPass];
+  if (l == 0) hL[threadIdx.x >> a.lanes_log2] = active ? silu(g) * u : 0.f;
+  __syncthreads();
+  // digits of the block's rows: one value per thread, 16-lane groups
+  if ((int)threadIdx.x < upb) {
+    const float v = hL[threadIdx.x];
+    float m = fabsf(v);
 #pragma unroll
-  for (int m = 0; m < kMaxHPass; ++m) {
-    const int g = g0 + 32 * m;
-    const int e = (int)(((float)g + 0.5f) * rnb), b = g - e * nb;
-    dst[m] = 3 * e * pb + pad_off(32 * b + 4 * o);
-    sci[m] = e * nb + b;
-    dsi[m] = 3 * e * nb + b;
-    v[m] = g < G ? *reinterpret_cast<const float4 *>(h + (int64_t)L.pos[min(e, L.n - 1)] * I +
-                                                     32 * b + 4 * o)
-                 : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
+    for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+    const float rs = m > 0.f ? 127.f * __builtin_amdgcn_rcpf(m) : 0.f;
+    int d1, d2, d3;
+    digits_of(v, rs, d1, d2, d3);
+    int t1 = d1, t2 = d2, t3 = d3;
+    if constexpr (QT == 2) {
 #pragma unroll
-  for (int m = 0; m < kMaxHPass; ++m) {
-    if (g0 + 32 * m < G) {  // uniform over the 8 lanes of a group
-      uint32_t dw[3];
-      const float s = octet_digits(v[m], dw);
-#pragma unroll
-      for (int c = 0; c < 3; ++c) *reinterpret_cast<uint32_t *>(qL + dst[m] + c * pb) = dw[c];
-      if (o == 0) scL[sci[m]] = s;
-      if (sums) {
-#pragma unroll
-        for (int c = 0; c < 3; ++c) {
-          const int t = octet_byte_sum(dw[c]);
-          if (o == 0) dsL[dsi[m] + c * nb] = t;
+      for (int off = 1; off < 16; off <<= 1) {
+        t1 += __shfl_xor(t1, off, kWave);
+        t2 += __shfl_xor(t2, off, kWave);
+        t3 += __shfl_xor(t3, off, kWave);
+      }
+    }
+    const int rr = r0 + threadIdx.x;
+    if (rr < a.I) {
+      const int64_t i = (int64_t)L.pos[ei] * a.I + rr, KI = (int64_t)a.k * a.I;
+      a.hq[i] = (int8_t)d1;
+      a.hq[KI + i] = (int8_t)d2;
+      a.hq[2 * KI + i] = (int8_t)d3;
+      if ((rr & 15) == 0) {
+        a.hsc[i / 16] = m * (1.f / 127.f);
+        if constexpr (QT == 2) {
+          a.hds[i / 16] = t1;
+          a.hds[KI / 16 + i / 16] = t2;
+          a.hds[2 * (KI / 16) + i / 16] = t3;
         }
       }
     }
   }
 }
 
+// Stage the activation digits of the listed experts into LDS: digit images
+// qL [n] (three planes of plane_bytes(I) each), scales scL [n][I/16] and
+// (Q4_0) digit sums dsL [n][3][I/16].  Split in two so that the caller can
+// issue these loads ahead of its weight loads and store them afterwards.
+constexpr int kMaxDig16 = 9;  // 3 * 12288 / 16 / 256
+constexpr int kMaxSc4 = 1;    // 12288 / 16 / 4 / 256
+constexpr int kMaxDs4 = 3;    // 3 * 12288 / 16 / 4 / 256
+struct HStage {
+  uint4 d[kMaxDig16];
+  float4 s[kMaxSc4];
+  int4 q[kMaxDs4];
+};
+
+// Unit u of n groups of `per` units -> (group, index) by floor((u + 0.5) / per)
+// in fp32: exact here (u < 2^12, so the rounding error stays far below the
+// 0.5/per margin).
+__device__ __forceinline__ int split_unit(int u, float rper, int per, int &j) {
+  const int g = (int)(((float)u + 0.5f) * rper);
+  j = u - g * per;
+  return g;
+}
+
+__device__ __forceinline__ void stage_h_load(const int8_t *__restrict__ hq,
+                                             const float *__restrict__ hsc,
+                                             const int32_t *__restrict__ hds, const ExpertList &L,
+                                             int I, int k, bool sums, HStage &st) {
+  const int64_t KI = (int64_t)k * I;
+  const int n = L.n, u16 = I / 16, u64 = I / 64;
+  const float r16 = 1.f / (float)u16, r64 = 1.f / (float)u64;
+#pragma unroll
+  for (int m = 0; m < kMaxDig16; ++m) {
+    const int u = threadIdx.x + m * kThreads;  // (expert, plane, unit)
+    int j;
+    const int ec = split_unit(u, r16, u16, j);
+    const int e = min(ec / 3, n - 1), c = ec - 3 * (ec / 3);
+    st.d[m] = u < 3 * n * u16
+                  ? *reinterpret_cast<const uint4 *>(hq + c * KI + (int64_t)L.pos[e] * I + 16 * j)
+                  : make_uint4(0u, 0u, 0u, 0u);
+  }
+#pragma unroll
+  for (int m = 0; m < kMaxSc4; ++m) {
+    const int u = threadIdx.x + m * kThreads;  // (expert, 4 scales)
+    int j;
+    const int e = min(split_unit(u, r64, u64, j), n - 1);
+    st.s[m] = u < n * u64 ? *reinterpret_cast<const float4 *>(hsc + (int64_t)L.pos[e] * u16 + 4 * j)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (sums) {
+#pragma unroll
+    for (int m = 0; m < kMaxDs4; ++m) {
+      const int u = threadIdx.x + m * kThreads;  // (expert, plane, 4 sums)
+      int j;
+      const int ec = split_unit(u, r64, u64, j);
+      const int e = min(ec / 3, n - 1), c = ec - 3 * (ec / 3);
+      st.q[m] = u < 3 * n * u64 ? *reinterpret_cast<const int4 *>(hds + c * (KI / 16) +
+                                                                  (int64_t)L.pos[e] * u16 + 4 * j)
+                                : make_int4(0, 0, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void stage_h_store(const HStage &st, int n, int I, bool sums, uint8_t *qL,
+                                              float *scL, int *dsL) {
+  const int u16 = I / 16, u64 = I / 64, pb = plane_bytes(I);
+  const float r16 = 1.f / (float)u16;
+#pragma unroll
+  for (int m = 0; m < kMaxDig16; ++m) {
+    const int u = threadIdx.x + m * kThreads;
+    if (u < 3 * n * u16) {
+      int j;
+      const int ec = split_unit(u, r16, u16, j);
+      *reinterpret_cast<uint4 *>(qL + ec * pb + pad_off(16 * j)) = st.d[m];
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < kMaxSc4; ++m) {
+    const int u = threadIdx.x + m * kThreads;
+    if (u < n * u64) reinterpret_cast<float4 *>(scL)[u] = st.s[m];
+  }
+  if (sums) {
+#pragma unroll
+    for (int m = 0; m < kMaxDs4; ++m) {
+      const int u = threadIdx.x + m * kThreads;
+      if (u < 3 * n * u64) reinterpret_cast<int4 *>(dsL)[u] = st.q[m];
+    }
+  }
+}
+
 struct DownParams {
   ExpertList L;
-  const float *h;  // SwiGLU activations [k][I]
+  const ExpertList *Ld;  // device list (nullable): read instead of L
+  const int8_t *hq;   // activation digits [3][k*I]
+  const float *hsc;   // their 16-wide block scales [k*I/16]
+  const int32_t *hds; // their digit sums [3][k*I/16] (Q4_0)
   const float *w, *x;
   float *y;
   int H, I, k, mode;
@@ -657,25 +960,29 @@ template <int QT>
 __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
   constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kDownFlight;
+  const ExpertList &L = a.Ld ? *a.Ld : a.L;
+  if (L.n != a.L.n) return;  // a device list emptied by a routing error
   const int I = a.I, nb = I / 32, np = nb / 2, n = a.L.n, pb = plane_bytes(I);
   uint8_t *qL = smem8;                                         // n digit images
-  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * pb);  // [n][I/32]
-  int *dsL = reinterpret_cast<int *>(scL + n * nb);           // [n][3][I/32]
-  float *res = reinterpret_cast<float *>(dsL + 3 * n * nb);   // [rows][n]
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * pb);  // [n][I/16]
+  int *dsL = reinterpret_cast<int *>(scL + n * (I / 16));      // [n][3][I/16]
+  float *res = reinterpret_cast<float *>(dsL + 3 * n * (I / 16));  // [rows][n]
   const int j0 = blockIdx.x * a.rows;
   const int unit = threadIdx.x >> a.lanes_log2, l = threadIdx.x & (a.lanes - 1);
   const int i = unit % n, rr = unit / n, j = j0 + rr;
   const bool active = rr < a.rows && j < a.H;
   const int64_t rowb = (int64_t)nb * BB;
   const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
-  const uint8_t *row = a.L.payload[i] + 2 * mat + (int64_t)j * rowb;
+  const uint8_t *row = L.payload[i] + 2 * mat + (int64_t)j * rowb;
+  HStage st;
+  stage_h_load(a.hq, a.hsc, a.hds, L, I, a.k, QT == 2, st);  // ahead of the weights
   uint32_t wd[F][PD];
 #pragma unroll
   for (int m = 0; m < F; ++m) {
     const int p = l + m * a.lanes;
     if (active && m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
   }
-  stage_h(a.h, a.L, I, qL, scL, dsL, QT == 2);
+  stage_h_store(st, n, I, QT == 2, qL, scL, dsL);
   __syncthreads();
   float acc = 0.f;
   for (int m0 = 0; m0 < a.mpairs; m0 += F) {
@@ -692,9 +999,8 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
       if (active && m0 + m < a.mpairs && p < np) {
         uint32_t D[48];
         load_digits(qL + 3 * i * pb, pb, p, D);
-        const int *ds = dsL + 3 * i * nb;
-        acc += pair_dot<QT>(wd[m], D, scL[i * nb + 2 * p], scL[i * nb + 2 * p + 1], ds + 2 * p,
-                            ds + 2 * p + 1, nb);
+        acc += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p,
+                              dsL + 3 * i * (I / 16) + 4 * p, I / 16);
       }
     }
   }
@@ -705,7 +1011,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
     const int jj = j0 + t;
     if (jj >= a.H) continue;
     float v = a.mode == 2 ? a.y[jj] : (a.mode == 1 ? a.x[jj] : 0.f);
-    for (int ii = 0; ii < n; ++ii) v = fmaf(a.w[a.L.pos[ii]], res[t * n + ii], v);
+    for (int ii = 0; ii < n; ++ii) v = fmaf(a.w[L.pos[ii]], res[t * n + ii], v);
     a.y[jj] = v;
   }
 }
@@ -741,6 +1047,38 @@ __global__ __launch_bounds__(kThreads) void materialize_kernel(CopyParams a) {
   for (; i < total; i += st) {
     const int64_t e = i / a.p16;
     a.dst[e][i - e * a.p16] = a.src[e][i - e * a.p16];
+  }
+}
+
+// The same copy for the misses a device work list names.
+__global__ __launch_bounds__(kThreads) void materialize_list_kernel(const WorkList *w, int64_t p16,
+                                                                    uint64_t *acc) {
+  const int n = w->n_copy;
+  if (acc && blockIdx.x == 0 && threadIdx.x == 0) {
+    atomicAdd(reinterpret_cast<unsigned long long *>(acc), (unsigned long long)n);
+    atomicAdd(reinterpret_cast<unsigned long long *>(acc + 1), (unsigned long long)(n * p16 * 16));
+  }
+  const int64_t total = p16 * n;
+  const int64_t st = (int64_t)gridDim.x * kThreads;
+  int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const uint4 *const *src = reinterpret_cast<const uint4 *const *>(w->src);
+  uint4 *const *dst = reinterpret_cast<uint4 *const *>(w->dst);
+  for (; i + 3 * st < total; i += 4 * st) {
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = i + j * st, e = g / p16;
+      v[j] = src[e][g - e * p16];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = i + j * st, e = g / p16;
+      dst[e][g - e * p16] = v[j];
+    }
+  }
+  for (; i < total; i += st) {
+    const int64_t e = i / p16;
+    dst[e][i - e * p16] = src[e][i - e * p16];
   }
 }
 
@@ -1149,7 +1487,7 @@ __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__res
 // when a lane keeps `in_flight` pairs of a row loading at once: few load
 // rounds first, then few idle lanes, then fewer lanes.
 #ifndef MOE_GATEUP_MAX_LANES
-#define MOE_GATEUP_MAX_LANES 32
+#define MOE_GATEUP_MAX_LANES 16
 #endif
 #ifndef MOE_DOWN_MAX_LANES
 #define MOE_DOWN_MAX_LANES 64
@@ -1178,15 +1516,16 @@ int router_decode_grid(int H) { return (H + kRouterRowsPerBlock - 1) / kRouterRo
 
 hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, int k, float *partial,
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
-                                float *xsc, bool prenorm, hipStream_t s, const Timing &t) {
+                                float *xsc, bool prenorm, const LruDev *lru, hipStream_t s,
+                                const Timing &t) {
+  const LruDev none{};
   const int nb = router_decode_grid(H);
   hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
-                        wr, H, E, partial);
+                        wr, H, E, (int)prenorm, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), sizeof(float) * (size_t)H, s,
-                        nullptr, t.stop, 0, x, partial, nb, H, E, k, idx, w, host_idx, host_w, xq, xsc,
-                        (int)prenorm);
+  hipExtLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0, partial,
+                        nb, E, k, idx, w, host_idx, host_w, lru ? *lru : none);
   return hipGetLastError();
 }
 
@@ -1204,14 +1543,14 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
 }
 
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                         hipStream_t s, const Timing &t) {
+                         const ExpertList *Ld, hipStream_t s, const Timing &t) {
   const int np = H / 64;
-  GateUpParams a{L, S.xq, S.xsc, S.h, H, I, k, 0, 0, 0};
+  GateUpParams a{L, Ld, S.xq, S.xsc, S.hq, S.hsc, S.hds, H, I, k, 0, 0, 0};
   pick_lanes(np, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes,
              a.lanes, a.mpairs);
   while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
   const int upb = kThreads / a.lanes;
-  const size_t lds = 3 * (size_t)np * kPairPitch + 4 * (size_t)(H / 32) * 4;
+  const size_t lds = 3 * (size_t)np * kPairPitch + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
   dim3 grid(L.n * ((I + upb - 1) / upb));
   if (qtype == 8)
     hipExtLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
@@ -1221,23 +1560,30 @@ hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
 }
 
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
-                       const float *w, const float *x, float *y, int mode, hipStream_t s,
-                       const Timing &t) {
+                       const ExpertList *Ld, const float *w, const float *x, float *y, int mode,
+                       hipStream_t s, const Timing &t) {
   const int np = I / 64;
-  if (L.n * I > 32 * 32 * kMaxHPass) return hipErrorInvalidValue;
-  DownParams a{L, S.h, w, x, y, H, I, k, mode, 0, 0, 0, 0};
+  if (3 * L.n * I / 16 > kMaxDig16 * kThreads) return hipErrorInvalidValue;
+  DownParams a{L, Ld, S.hq, S.hsc, S.hds, w, x, y, H, I, k, mode, 0, 0, 0, 0};
   pick_lanes(np, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
              a.mpairs);
   while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
   a.rows = kThreads / (a.lanes * L.n);
   if (a.rows < 1) return hipErrorInvalidValue;
-  const size_t lds = 3 * (size_t)L.n * np * kPairPitch + 4 * (size_t)L.n * (I / 32) * 4 +
+  const size_t lds = 3 * (size_t)L.n * np * kPairPitch + 4 * (size_t)L.n * (I / 16) * 4 +
                      4 * (size_t)a.rows * L.n;
   dim3 grid((H + a.rows - 1) / a.rows);
   if (qtype == 8)
     hipExtLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
     hipExtLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, uint64_t *acc,
+                                   hipStream_t s, const Timing &t) {
+  hipExtLaunchKernelGGL(materialize_list_kernel, dim3(grid), dim3(kThreads), 0, s, t.start, t.stop, 0,
+                        w, bytes / 16, acc);
   return hipGetLastError();
 }
 

@@ -2,10 +2,14 @@
 //
 // One handle = one model's expert store (pinned host memory, caller-owned),
 // per-layer HBM slot slabs, per-layer LRU slot tables, a side stream for the
-// miss copies, and small scratch buffers.  A layer call is: router kernel on
-// the caller's stream -> host waits for the routes -> LRU step -> miss copies
-// on the side stream -> FFN for hit experts on the caller's stream (overlaps
-// the copies) -> caller's stream waits for the copies -> FFN for the misses.
+// miss copies, and small scratch buffers.
+//
+// Decode with the default copy kernel keeps the slot tables in device memory:
+// a layer call is four launches on the caller's stream (router partials;
+// router finish + slot-table step, which writes the call's work list; copy
+// kernel for the misses; gate/up; down) and the host never waits.  The other
+// copy modes and prefill run the slot table on the host, after waiting for
+// the routes; around a prefill call the layer's table moves to the host and back.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -57,7 +61,7 @@ struct moe_cache {
   const uint8_t *store = nullptr;
 
   uint8_t *slots = nullptr;  // [L][C][P]
-  float *partial = nullptr;  // router split partials [grid][E]
+  float *partial = nullptr;  // router split partials [grid][E], then 1/rms
   int8_t *xq = nullptr;         // decode: digits of the scaled token [3][H]
   float *xsc = nullptr;         //   and their block scales [H/32]
   int32_t *topk_idx = nullptr;  // device [cap_tokens][k]
@@ -75,7 +79,23 @@ struct moe_cache {
   float *pf_P = nullptr;        // [T*k][H]
   int32_t *pf_host_off = nullptr;  // pinned [E+1]
   std::vector<hipEvent_t> pf_ev;   // per-chunk events (copy done, compute done)
-  float *h = nullptr;  // decode SwiGLU activations [k][I]
+  int8_t *hq = nullptr;   // decode: digits of the SwiGLU activations [3][k*I]
+  float *hsc = nullptr;   //   their 16-wide block scales [k*I/16]
+  int32_t *hds = nullptr; //   and digit sums [3][k*I/16]
+  // device-resident slot tables (decode with the copy kernel)
+  bool dev_lru = false;
+  int32_t *dl_slot_of = nullptr;    // [L][E]
+  int32_t *dl_expert_in = nullptr;  // [L][C]
+  int64_t *dl_stamp = nullptr;      // [L][E]
+  int64_t *dl_meta = nullptr;       // [L][3] clock, step, used
+  uint64_t *dl_cnt = nullptr;       // [L][4]
+  int32_t *dl_trace = nullptr;      // [dl_trace_cap][6]
+  uint64_t *dl_trace_n = nullptr;
+  int32_t *dl_err = nullptr;
+  uint64_t *dl_copy_acc = nullptr;  // [2] copies and bytes of the timed copy launches
+  WorkList *dl_work = nullptr;
+  int64_t dl_trace_cap = 0, dl_trace_pending = 0;
+  uint8_t *dl_stage = nullptr;      // pinned staging of one layer's table
   int32_t *host_idx = nullptr;  // host mirrors [k] (decode)
   float *host_w = nullptr;
   hipEvent_t ev_route = nullptr, ev_copy = nullptr;
@@ -94,7 +114,7 @@ struct moe_cache {
   bool timing_now = false;  // this call is bracketed
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
-  DecodeScratch scratch() const { return DecodeScratch{xq, xsc, h}; }
+  DecodeScratch scratch() const { return DecodeScratch{xq, xsc, hq, hsc, hds}; }
 };
 
 namespace {
@@ -203,7 +223,9 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->topk_idx);
   (void)hipFree(c->topk_w);
   (void)hipFree(c->zbuf);
-  (void)hipFree(c->h);
+  (void)hipFree(c->hq);
+  (void)hipFree(c->hsc);
+  (void)hipFree(c->hds);
   (void)hipFree(c->pf_inv);
   (void)hipFree(c->pf_xb);
   (void)hipFree(c->pf_counts);
@@ -215,6 +237,17 @@ void free_all(moe_cache *c) {
   for (auto e : c->pf_ev) (void)hipEventDestroy(e);
   (void)hipFree(c->xq);
   (void)hipFree(c->xsc);
+  (void)hipFree(c->dl_slot_of);
+  (void)hipFree(c->dl_expert_in);
+  (void)hipFree(c->dl_stamp);
+  (void)hipFree(c->dl_meta);
+  (void)hipFree(c->dl_cnt);
+  (void)hipFree(c->dl_trace);
+  (void)hipFree(c->dl_trace_n);
+  (void)hipFree(c->dl_err);
+  (void)hipFree(c->dl_copy_acc);
+  (void)hipFree(c->dl_work);
+  if (c->dl_stage) (void)hipHostFree(c->dl_stage);
   if (c->host_idx) (void)hipHostFree(c->host_idx);
   if (c->host_w) (void)hipHostFree(c->host_w);
   if (c->ev_route) (void)hipEventDestroy(c->ev_route);
@@ -247,8 +280,232 @@ int ensure_tokens(moe_cache *c, int64_t T) {
   return MOE_OK;
 }
 
+// ---- device-resident slot tables ----
+
+constexpr int64_t kTraceCap = 1 << 16;  // device trace records kept between drains
+
+size_t table_bytes(const moe_cache *c) {
+  const int64_t E = c->d.n_experts;
+  return (size_t)(4 * E + 4 * c->C + 8 * E + 8 * 3 + 8 * 4);
+}
+
+int alloc_dev_tables(moe_cache *c) {
+  const int64_t L = c->d.n_layers, E = c->d.n_experts, C = c->C;
+  if (hipMalloc(&c->dl_slot_of, L * E * 4) != hipSuccess ||
+      hipMalloc(&c->dl_expert_in, L * C * 4) != hipSuccess ||
+      hipMalloc(&c->dl_stamp, L * E * 8) != hipSuccess || hipMalloc(&c->dl_meta, L * 3 * 8) != hipSuccess ||
+      hipMalloc(&c->dl_cnt, L * 4 * 8) != hipSuccess || hipMalloc(&c->dl_trace_n, 8) != hipSuccess ||
+      hipMalloc(&c->dl_err, 4) != hipSuccess || hipMalloc(&c->dl_copy_acc, 16) != hipSuccess ||
+      hipMalloc(&c->dl_work, sizeof(WorkList)) != hipSuccess ||
+      hipHostMalloc(&c->dl_stage, table_bytes(c), hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MOE_ENOMEM, "cannot allocate the device slot tables");
+  }
+  if (c->d.flags & MOE_F_TRACE) {
+    if (hipMalloc(&c->dl_trace, kTraceCap * 6 * 4) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(MOE_ENOMEM, "cannot allocate the device trace");
+    }
+    c->dl_trace_cap = kTraceCap;
+  }
+  return MOE_OK;
+}
+
+// Empty tables, zero counters (queued on the caller's stream).
+int clear_dev_tables(moe_cache *c) {
+  const int64_t L = c->d.n_layers, E = c->d.n_experts, C = c->C;
+  HIP_TRY(c, hipMemsetAsync(c->dl_slot_of, 0xff, L * E * 4, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_expert_in, 0xff, L * C * 4, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_stamp, 0, L * E * 8, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_meta, 0, L * 3 * 8, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_cnt, 0, L * 4 * 8, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_trace_n, 0, 8, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_err, 0, 4, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_copy_acc, 0, 16, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_work, 0, sizeof(WorkList), c->main));
+  c->dl_trace_pending = 0;
+  return MOE_OK;
+}
+
+// After a synchronisation: report a routing error the device recorded.
+int check_dev_error(moe_cache *c) {
+  if (!c->dev_lru) return MOE_OK;
+  int32_t err = 0;
+  HIP_TRY(c, hipMemcpy(&err, c->dl_err, 4, hipMemcpyDeviceToHost));
+  if (err) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "router produced expert id %d (non-finite logits?)", (int16_t)(err - 1));
+  }
+  return MOE_OK;
+}
+
+// Synchronise with the caller's stream and check for a recorded error.
+int sync_dev(moe_cache *c) {
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  return check_dev_error(c);
+}
+
+// Move the device trace records into the host trace (synchronises).
+int drain_dev_trace(moe_cache *c) {
+  if (!c->dev_lru || !c->dl_trace) return MOE_OK;
+  int rc = sync_dev(c);
+  if (rc) return rc;
+  uint64_t n = 0;
+  HIP_TRY(c, hipMemcpy(&n, c->dl_trace_n, 8, hipMemcpyDeviceToHost));
+  if ((int64_t)n > c->dl_trace_cap) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "device trace overflow (%llu records)", (unsigned long long)n);
+  }
+  if (n) {
+    const size_t at = c->trace.size();
+    c->trace.resize(at + n);
+    static_assert(sizeof(moe_step_rec) == 24, "moe_step_rec is six int32");
+    HIP_TRY(c, hipMemcpy(c->trace.data() + at, c->dl_trace, n * sizeof(moe_step_rec),
+                         hipMemcpyDeviceToHost));
+    HIP_TRY(c, hipMemsetAsync(c->dl_trace_n, 0, 8, c->main));
+    HIP_TRY(c, hipStreamSynchronize(c->main));
+  }
+  c->dl_trace_pending = 0;
+  return MOE_OK;
+}
+
+LruDev dev_table(moe_cache *c, int32_t layer) {
+  const int64_t E = c->d.n_experts, C = c->C;
+  LruDev L{};
+  L.slot_of = c->dl_slot_of + layer * E;
+  L.expert_in = c->dl_expert_in + layer * C;
+  L.stamp = c->dl_stamp + layer * E;
+  L.meta = c->dl_meta + layer * 3;
+  L.cnt = c->dl_cnt + layer * 4;
+  L.trace = c->dl_trace;
+  L.trace_n = c->dl_trace_n;
+  L.err = c->dl_err;
+  L.store = c->store + (int64_t)layer * E * c->P;
+  L.slots = c->slot_ptr(layer, 0);
+  L.work = c->dl_work;
+  L.P = c->P;
+  L.C = (int32_t)C;
+  L.layer = layer;
+  return L;
+}
+
+// Copy a layer's device table into the host table (synchronises first).
+int pull_table(moe_cache *c, int32_t layer) {
+  int rc = drain_dev_trace(c);
+  if (!rc) rc = sync_dev(c);
+  if (rc) return rc;
+  const LruDev L = dev_table(c, layer);
+  const int64_t E = c->d.n_experts, C = c->C;
+  SlotLru::State st;
+  st.slot_of.resize(E);
+  st.expert_in.resize(C);
+  std::vector<int64_t> stamp(E), meta(3);
+  std::vector<uint64_t> cnt(4);
+  HIP_TRY(c, hipMemcpy(st.slot_of.data(), L.slot_of, E * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(st.expert_in.data(), L.expert_in, C * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(stamp.data(), L.stamp, E * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(meta.data(), L.meta, 3 * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(cnt.data(), L.cnt, 4 * 8, hipMemcpyDeviceToHost));
+  st.stamp.assign(stamp.begin(), stamp.end());
+  st.clock = (uint64_t)meta[0];
+  st.step = (int32_t)meta[1];
+  st.used = (int32_t)meta[2];
+  st.cnt = moe_counters{cnt[0], cnt[1], cnt[2], cnt[3]};
+  c->lru[layer].set_state(st);
+  return MOE_OK;
+}
+
+// Queue the host table of a layer back to the device (pinned staging; the
+// next pull synchronises before the staging is reused).
+int push_table(moe_cache *c, int32_t layer) {
+  const LruDev L = dev_table(c, layer);
+  const int64_t E = c->d.n_experts, C = c->C;
+  const SlotLru::State st = c->lru[layer].state();
+  uint8_t *p = c->dl_stage;
+  int32_t *so = reinterpret_cast<int32_t *>(p), *ei = so + E;
+  int64_t *stamp = reinterpret_cast<int64_t *>(p + 4 * E + 4 * C), *meta = stamp + E;
+  uint64_t *cnt = reinterpret_cast<uint64_t *>(meta + 3);
+  std::copy(st.slot_of.begin(), st.slot_of.end(), so);
+  std::copy(st.expert_in.begin(), st.expert_in.end(), ei);
+  for (int64_t e = 0; e < E; ++e) stamp[e] = (int64_t)st.stamp[e];
+  meta[0] = (int64_t)st.clock;
+  meta[1] = st.step;
+  meta[2] = st.used;
+  cnt[0] = st.cnt.hits;
+  cnt[1] = st.cnt.misses;
+  cnt[2] = st.cnt.evictions;
+  cnt[3] = st.cnt.materialized_bytes;
+  HIP_TRY(c, hipMemcpyAsync(L.slot_of, so, E * 4, hipMemcpyHostToDevice, c->main));
+  HIP_TRY(c, hipMemcpyAsync(L.expert_in, ei, C * 4, hipMemcpyHostToDevice, c->main));
+  HIP_TRY(c, hipMemcpyAsync(L.stamp, stamp, E * 8, hipMemcpyHostToDevice, c->main));
+  HIP_TRY(c, hipMemcpyAsync(L.meta, meta, 3 * 8, hipMemcpyHostToDevice, c->main));
+  HIP_TRY(c, hipMemcpyAsync(L.cnt, cnt, 4 * 8, hipMemcpyHostToDevice, c->main));
+  return MOE_OK;
+}
+
+// Decode call with the slot table on the device: four launches, no host wait
+// (unless the caller asks for the counter delta or the routes).
+int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t layer, float *y,
+                       moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  const moe_model_desc &d = c->d;
+  const int k = d.top_k;
+  c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
+  uint64_t before[4] = {0, 0, 0, 0};
+  int rc = MOE_OK;
+  if (delta) {
+    if ((rc = sync_dev(c))) return rc;
+    HIP_TRY(c, hipMemcpy(before, c->dl_cnt + 4 * layer, 32, hipMemcpyDeviceToHost));
+  }
+  if (c->dl_trace && c->dl_trace_pending + k > c->dl_trace_cap && (rc = drain_dev_trace(c)))
+    return rc;
+  const LruDev L = dev_table(c, layer);
+  {
+    Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
+            2ull * d.hidden * d.n_experts);
+    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->topk_idx,
+                                    c->topk_w, nullptr, nullptr, c->xq, c->xsc,
+                                    (d.flags & MOE_F_PRENORM) != 0, &L, c->main, sp.timing()));
+    sp.end();
+  }
+  if (c->dl_trace) c->dl_trace_pending += k;
+  {
+    Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
+    HIP_TRY(c, launch_materialize_list(c->dl_work, c->P, kCopyGrid, c->timing_now ? c->dl_copy_acc : nullptr,
+                                       c->main, sp.timing()));
+    sp.end();
+  }
+  ExpertList shape{};
+  shape.n = k;
+  {
+    Span sp(c, c->main, MOE_KIND_GATEUP, 1, (uint64_t)k * 2 * c->M, 4ull * k * d.hidden * d.inter);
+    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, k, shape, &c->dl_work->list,
+                             c->main, sp.timing()));
+    sp.end();
+  }
+  {
+    Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * d.hidden * d.inter);
+    HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, k, shape, &c->dl_work->list,
+                           c->topk_w, x, y, (d.flags & MOE_F_RESIDUAL) ? 1 : 0, c->main, sp.timing()));
+    sp.end();
+  }
+  if ((d.flags & MOE_F_TIMING) && (rc = drain_timing(c))) return rc;
+  if (delta || dbg_idx || dbg_w) {
+    if ((rc = sync_dev(c))) return rc;
+    if (dbg_idx) HIP_TRY(c, hipMemcpy(dbg_idx, c->topk_idx, k * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (dbg_w) HIP_TRY(c, hipMemcpy(dbg_w, c->topk_w, k * sizeof(float), hipMemcpyDeviceToHost));
+    if (delta) {
+      uint64_t after[4];
+      HIP_TRY(c, hipMemcpy(after, c->dl_cnt + 4 * layer, 32, hipMemcpyDeviceToHost));
+      *delta = moe_counters{after[0] - before[0], after[1] - before[1], after[2] - before[2],
+                            after[3] - before[3]};
+    }
+  }
+  return MOE_OK;
+}
+
 int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer, float *y,
                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  if (c->dev_lru) return forward_decode_dev(c, x, wr, layer, y, delta, dbg_idx, dbg_w);
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
   c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
@@ -258,7 +515,7 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
             2ull * d.hidden * d.n_experts);
     HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->topk_idx,
                                     c->topk_w, c->host_idx, c->host_w, c->xq, c->xsc,
-                                    (d.flags & MOE_F_PRENORM) != 0, c->main, sp.timing()));
+                                    (d.flags & MOE_F_PRENORM) != 0, nullptr, c->main, sp.timing()));
     sp.end();
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
@@ -318,15 +575,15 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
   const uint64_t gu_flops = 4ull * d.hidden * d.inter, dn_flops = 2ull * d.hidden * d.inter;
   auto gateup = [&](const ExpertList &L) -> int {
     Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
-    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->main,
+    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, nullptr, c->main,
                              sp.timing()));
     sp.end();
     return MOE_OK;
   };
   auto down = [&](const ExpertList &L, int mode) -> int {
     Span sp(c, c->main, MOE_KIND_DOWN, 1, L.n * dn_bytes, L.n * dn_flops);
-    HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, c->topk_w, x, y,
-                           mode, c->main, sp.timing()));
+    HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, d.top_k, L, nullptr, c->topk_w, x,
+                           y, mode, c->main, sp.timing()));
     sp.end();
     return MOE_OK;
   };
@@ -455,8 +712,10 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
     return fail(MOE_ENOMEM, "cannot allocate %lld bytes of expert slots", (long long)slot_bytes);
   }
   const int grid = router_decode_grid(desc->hidden);
-  if (hipMalloc(&c->partial, (size_t)grid * desc->n_experts * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->h, (size_t)desc->top_k * desc->inter * sizeof(float)) != hipSuccess ||
+  if (hipMalloc(&c->partial, ((size_t)grid * desc->n_experts + 1) * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->hq, 3 * (size_t)desc->top_k * desc->inter) != hipSuccess ||
+      hipMalloc(&c->hsc, (size_t)desc->top_k * desc->inter / 16 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->hds, 3 * (size_t)desc->top_k * desc->inter / 16 * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->xq, 3 * (size_t)desc->hidden) != hipSuccess ||
       hipMalloc(&c->xsc, (size_t)desc->hidden / 32 * sizeof(float)) != hipSuccess ||
       hipHostMalloc(&c->host_idx, kMaxRouted * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
@@ -472,6 +731,12 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
     return fail(MOE_EHIP, "HIP setup failed");
   }
   rc = ensure_tokens(c, 1);
+  c->dev_lru = !(desc->flags & (MOE_F_SIDE_COPY | MOE_F_SDMA_COPY));
+  if (!rc && c->dev_lru) {
+    rc = alloc_dev_tables(c);
+    if (!rc) rc = clear_dev_tables(c);
+    if (!rc && hipStreamSynchronize(c->main) != hipSuccess) rc = fail(MOE_EHIP, "stream synchronisation failed");
+  }
   if (rc) {
     free_all(c);
     return rc;
@@ -502,13 +767,24 @@ int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const floa
   return moe_layer_forward_dbg(c, x, n_tokens, router_w, layer, y, delta, nullptr, nullptr);
 }
 
-int moe_cache_counters(const moe_cache *c, int32_t layer, moe_counters *out) {
-  if (!c || !out) return fail(MOE_EINVAL, "NULL argument");
-  if (layer < -1 || layer >= c->d.n_layers) return fail(MOE_EINVAL, "layer out of range");
+int moe_cache_counters(const moe_cache *cc, int32_t layer, moe_counters *out) {
+  if (!cc || !out) return fail(MOE_EINVAL, "NULL argument");
+  if (layer < -1 || layer >= cc->d.n_layers) return fail(MOE_EINVAL, "layer out of range");
+  moe_cache *c = const_cast<moe_cache *>(cc);  // synchronises, reads device tables
+  std::vector<uint64_t> dev;
+  if (c->dev_lru) {
+    if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+    int rc = sync_dev(c);
+    if (rc) return rc;
+    dev.resize(4 * (size_t)c->d.n_layers);
+    HIP_TRY(c, hipMemcpy(dev.data(), c->dl_cnt, dev.size() * 8, hipMemcpyDeviceToHost));
+  }
   moe_counters s{};
   for (int32_t l = 0; l < c->d.n_layers; ++l) {
     if (layer >= 0 && l != layer) continue;
-    const moe_counters &a = c->lru[l].counters();
+    const moe_counters a = c->dev_lru ? moe_counters{dev[4 * l], dev[4 * l + 1], dev[4 * l + 2],
+                                                     dev[4 * l + 3]}
+                                      : c->lru[l].counters();
     s.hits += a.hits;
     s.misses += a.misses;
     s.evictions += a.evictions;
@@ -520,6 +796,11 @@ int moe_cache_counters(const moe_cache *c, int32_t layer, moe_counters *out) {
 
 int moe_cache_read_trace(moe_cache *c, moe_step_rec *buf, int64_t cap, int64_t *n_out) {
   if (!c || !n_out || cap < 0 || (cap > 0 && !buf)) return fail(MOE_EINVAL, "bad arguments");
+  if (c->dev_lru) {
+    if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+    int rc = drain_dev_trace(c);
+    if (rc) return rc;
+  }
   const int64_t avail = (int64_t)(c->trace.size() - c->trace_head);
   const int64_t n = std::min(avail, cap);
   if (n > 0) std::memcpy(buf, c->trace.data() + c->trace_head, n * sizeof(moe_step_rec));
@@ -538,8 +819,14 @@ int moe_cache_reset(moe_cache *c) {
   HIP_TRY(c, hipStreamSynchronize(c->side));
   HIP_TRY(c, hipStreamSynchronize(c->main));
   int rc = drain_timing(c, true);
+  if (!rc) rc = check_dev_error(c);
   if (rc) return rc;
   for (auto &t : c->lru) t.reset();
+  if (c->dev_lru) {
+    rc = clear_dev_tables(c);
+    if (rc) return rc;
+    HIP_TRY(c, hipStreamSynchronize(c->main));
+  }
   c->n_calls = 0;
   c->trace.clear();
   c->trace_head = 0;
@@ -553,8 +840,15 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
   HIP_TRY(c, hipStreamSynchronize(c->side));
   HIP_TRY(c, hipStreamSynchronize(c->main));
   int rc = drain_timing(c, true);
+  if (!rc) rc = check_dev_error(c);
   if (rc) return rc;
   *out = c->stats[kind];
+  if (c->dev_lru && kind == MOE_KIND_COPY) {  // the copy kernel counts its own work
+    uint64_t acc[2];
+    HIP_TRY(c, hipMemcpy(acc, c->dl_copy_acc, 16, hipMemcpyDeviceToHost));
+    out->launches = acc[0];
+    out->bytes = acc[1];
+  }
   return MOE_OK;
 }
 
@@ -649,8 +943,8 @@ int ensure_prefill(moe_cache *c, int64_t T) {
 // the expert that held it (if it is routed in this call) has been computed:
 // the copy stream waits for that expert's chunk, and a chunk is closed early
 // when one of its own experts would be evicted by the next miss.
-int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
-                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer,
+                         float *y, moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
   const int k = d.top_k, E = d.n_experts, H = d.hidden, I = d.inter;
   int rc = ensure_tokens(c, T);
@@ -811,6 +1105,20 @@ int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, in
                           a.materialized_bytes - before.materialized_bytes};
   }
   return MOE_OK;
+}
+
+// Prefill runs the layer's slot table on the host: with device tables, move
+// the table to the host for the call and queue it back afterwards.
+int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
+                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  int rc = c->dev_lru ? pull_table(c, layer) : MOE_OK;
+  if (rc) return rc;
+  rc = forward_prefill_impl(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
+  if (c->dev_lru) {
+    const int rc2 = push_table(c, layer);
+    if (!rc) rc = rc2;
+  }
+  return rc;
 }
 
 }  // namespace

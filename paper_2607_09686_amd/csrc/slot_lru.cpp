@@ -22,6 +22,28 @@ void SlotLru::reset() {
   cnt_ = moe_counters{};
 }
 
+SlotLru::State SlotLru::state() const {
+  State s;
+  s.slot_of = slot_of_;
+  s.expert_in = expert_in_;
+  s.stamp = stamp_;
+  s.clock = clock_;
+  s.step = step_no_;
+  s.used = used_;
+  s.cnt = cnt_;
+  return s;
+}
+
+void SlotLru::set_state(const State &s) {
+  slot_of_ = s.slot_of;
+  expert_in_ = s.expert_in;
+  stamp_ = s.stamp;
+  clock_ = s.clock;
+  step_no_ = s.step;
+  used_ = s.used;
+  cnt_ = s.cnt;
+}
+
 void SlotLru::step(const int32_t *ids, int32_t n, std::vector<moe_step_rec> &out) {
   // distinct ids, ascending (bitmap over the expert range)
   for (int32_t i = 0; i < n; ++i) mark_[ids[i]] = 1;

@@ -27,6 +27,17 @@ class SlotLru {
   void step(const int32_t *ids, int32_t n, std::vector<moe_step_rec> &out);
   void reset();
 
+  // Whole state of the table, for moving it to and from device memory.
+  struct State {
+    std::vector<int32_t> slot_of, expert_in;
+    std::vector<uint64_t> stamp;
+    uint64_t clock = 0;
+    int32_t step = 0, used = 0;
+    moe_counters cnt{};
+  };
+  State state() const;
+  void set_state(const State &s);  // sizes must match n_experts / n_slots
+
   const moe_counters &counters() const { return cnt_; }
   int32_t slot_of(int32_t e) const { return slot_of_[e]; }
   int32_t n_slots() const { return n_slots_; }

@@ -193,16 +193,22 @@ class MoeCache:
             raise RuntimeError("cache is closed")
         return self._h
 
-    def layer_forward(self, x, router_w, layer, y, n_tokens=None, routes=False):
-        """y <- MoE layer(x); returns the counter delta (and routes if asked)."""
+    def layer_forward(self, x, router_w, layer, y, n_tokens=None, routes=False, counters=False):
+        """y <- MoE layer(x).
+
+        Returns None, or the call's counter delta if counters=True, or
+        (delta, idx, w) if routes=True.  Asking for either makes the call wait
+        for its own completion; without them a decode call only queues work.
+        """
         T = (x.numel() // self.hidden) if n_tokens is None else n_tokens
         xp = _dev_ptr(x, "float32", T * self.hidden, "x")
         wp = _dev_ptr(router_w, "float32", self.hidden * self.n_experts, "router_w")
         yp = _dev_ptr(y, "float32", T * self.hidden, "y")
         delta = Counters()
         if not routes:
-            _check(lib().moe_layer_forward(self.handle, xp, T, wp, layer, yp, ctypes.byref(delta)))
-            return delta
+            _check(lib().moe_layer_forward(self.handle, xp, T, wp, layer, yp,
+                                           ctypes.byref(delta) if counters else None))
+            return delta if counters else None
         idx = np.empty((T, self.top_k), np.int32)
         w = np.empty((T, self.top_k), np.float32)
         _check(lib().moe_layer_forward_dbg(self.handle, xp, T, wp, layer, yp, ctypes.byref(delta),

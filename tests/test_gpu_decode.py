@@ -167,6 +167,59 @@ def test_deterministic_outputs():
     np.testing.assert_array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
 
 
+def test_queued_calls_match_waited_calls():
+    """Decode calls that only queue work (no routes or counters asked for, so the
+    slot tables are stepped on the device with no host wait) give bit-identical
+    outputs, trace and counters to calls that wait for every result."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=3, name="tiny3q")
+    keep, ptr, arr = store_buffer(wl)
+    R = torch.from_numpy(synth.router(wl)).cuda()
+    X = torch.from_numpy(synth.hidden(wl, n_tokens=24)).cuda()
+    res = []
+    for wait in (True, False):
+        cache = make_cache(wl, ptr, 5, trace=True, residual=True, prenorm=True)
+        outs = []
+        for t in range(X.shape[0]):
+            x = X[t].contiguous()
+            for l in range(wl.n_layers):
+                y = torch.empty_like(x)
+                cache.layer_forward(x, R[l], l, y, routes=wait)
+                x = y
+            outs.append(x)
+        out = torch.stack(outs).cpu().numpy()
+        res.append((out, sorted(cache.read_trace()), cache.counters().as_tuple()))
+        cache.close()
+    assert np.all(np.isfinite(res[0][0]))
+    np.testing.assert_array_equal(res[0][0].view(np.uint32), res[1][0].view(np.uint32))
+    assert res[0][1] == res[1][1] and len(res[0][1]) == 24 * 3 * wl.top_k
+    assert res[0][2] == res[1][2]
+
+
+@pytest.mark.parametrize("copy_mode", ["kernel", "side"])
+def test_nonfinite_input_is_reported(copy_mode):
+    """All-NaN logits leave no valid expert: the host-table modes fail the call, the
+    device-table mode does no work for it and fails at the next synchronising call;
+    the handle is poisoned afterwards either way."""
+    torch = torch_cuda()
+    from paper_2607_09686_amd import MoeError, moecache
+    wl = synth.WORKLOADS["tiny"]
+    keep, ptr, arr = store_buffer(wl)
+    R = torch.from_numpy(synth.router(wl)).cuda()
+    cache = make_cache(wl, ptr, 4, trace=True, copy_mode=copy_mode)
+    x = torch.full((wl.hidden,), float("nan"), dtype=torch.float32, device="cuda")
+    y = torch.zeros(wl.hidden, dtype=torch.float32, device="cuda")
+    with pytest.raises(MoeError) as e:
+        cache.layer_forward(x, R[0], 0, y)
+        cache.counters()
+    assert e.value.code == moecache.MOE_EHIP
+    x = torch.from_numpy(synth.hidden(wl, n_tokens=1)[0]).cuda()
+    with pytest.raises(MoeError) as e:
+        cache.layer_forward(x, R[0], 0, y)
+    assert e.value.code == moecache.MOE_ESTATE
+    cache.close()
+
+
 def test_timing_totals():
     wl = synth.WORKLOADS["tiny"]
     from paper_2607_09686_amd import KIND_COPY, KIND_DOWN, KIND_GATEUP, KIND_ROUTER

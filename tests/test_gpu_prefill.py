@@ -5,7 +5,8 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_common import (TIE_GAP, check_y, log, make_cache, softmax_of, store_buffer, torch_cuda)
+from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, softmax_of, store_buffer,
+                        torch_cuda)
 from oracle import router as oracle_router
 from oracle.layer import Shape, moe_layer_bf16, rms_normalize
 from oracle.lru import LayerLRU
@@ -70,6 +71,46 @@ def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=Non
     log(f"  ok: worst err/rms {worst:.2e}; counters {cache.counters()}")
     cache.close()
     return worst
+
+
+def test_prefill_and_decode_share_slot_tables():
+    """Prefill calls (slot table stepped on the host) and decode calls (stepped on
+    the device) interleaved on one handle: the trace, in call order, and the
+    counters equal one oracle table per layer stepped through all calls."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=2, name="tiny_mix")
+    budget = 6
+    keep, ptr, arr = store_buffer(wl)
+    R = synth.router(wl)
+    Rd = [torch.from_numpy(R[l]).cuda() for l in range(wl.n_layers)]
+    cache = make_cache(wl, ptr, budget, trace=True)
+    lrus = [LayerLRU(wl.n_experts, budget, wl.payload_bytes, l) for l in range(wl.n_layers)]
+    want = []
+    for phase, T in enumerate((37, 1, 20, 1, 2)):
+        n_calls = 9 if T == 1 else 1
+        X = synth.hidden(wl.with_(hidden_seed=wl.hidden_seed + 11 * phase), rho=-1.0,
+                         n_tokens=max(T, n_calls))
+        for c in range(n_calls):
+            xs = np.ascontiguousarray(X[c:c + 1] if T == 1 else X)
+            for l in range(wl.n_layers):
+                x = torch.from_numpy(xs).cuda()
+                y = torch.empty_like(x)
+                delta, idx, w = cache.layer_forward(x, Rd[l], l, y, n_tokens=xs.shape[0],
+                                                    routes=True)
+                if T == 1:
+                    check_routes(xs, R[l], wl.top_k, idx, w)
+                else:
+                    z, io, wo, gap = oracle_routes(xs, R[l], wl.top_k, False)
+                    for t in range(xs.shape[0]):
+                        if set(io[t].tolist()) != set(idx[t].tolist()):
+                            assert gap[t] < TIE_GAP
+                step = lrus[l].step(np.unique(idx))
+                want.extend(step)
+                assert delta.hits == sum(r[3] for r in step)
+    assert cache.read_trace() == want
+    tot = sum((lr.counters for lr in lrus[1:]), lrus[0].counters)
+    assert cache.counters().as_tuple() == tot.as_tuple()
+    cache.close()
 
 
 @pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
