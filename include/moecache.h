@@ -63,6 +63,9 @@ extern "C" {
                                for the copies before the missed experts */
 #define MOE_F_SDMA_COPY 32u /* hipMemcpyAsync per miss on the caller's stream (copy
                                engine instead of the copy kernel) */
+#define MOE_F_SPLIT_COPY 64u /* decode, default copy mode: the copy kernel and gate/up as
+                                two launches instead of one launch that copies the misses
+                                and runs gate/up for every routed expert (results equal) */
 
 typedef struct moe_cache moe_cache; /* opaque, owned by the library */
 

@@ -28,6 +28,8 @@ struct WorkList {
   int32_t n_copy, pad;
   const uint8_t *src[kMaxRouted];  // misses in ascending expert order
   uint8_t *dst[kMaxRouted];
+  int32_t miss_pos[kMaxRouted];    // top-k position of each miss
+  int32_t hit[kMaxRouted];         // per top-k position: 1 hit, 0 miss
   ExpertList list;  // the k routed experts in rank order (n = 0 after a routing error)
 };
 
@@ -112,6 +114,17 @@ hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
                        const ExpertList *Ld, const float *w, const float *x, float *y, int mode,
                        hipStream_t s, const Timing &t = {});
+
+// Decode copy + gate/up in one launch (device work list): `copy_blocks` blocks
+// stream the misses' payloads host -> slot and form the SwiGLU activations of
+// the missed experts from the gate/up rows they carry; further blocks run
+// gate/up for the hit experts from their slots meanwhile.  Writes the same
+// activation digits as launch_gateup.  Returns hipErrorInvalidValue for a
+// shape it does not take (fusable_copy_gateup false).
+bool fusable_copy_gateup(int qtype, int H, int I);
+hipError_t launch_copy_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
+                              const WorkList *w, int64_t payload_bytes, int copy_blocks,
+                              uint64_t *acc, hipStream_t s, const Timing &t = {});
 
 // Copy n <= max_copy() payloads of `bytes` (multiple of 16, 16-byte aligned)
 // src[i] -> dst[i] with a copy kernel of `grid` blocks (host-pinned or device sources).

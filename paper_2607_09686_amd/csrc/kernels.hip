@@ -11,6 +11,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -390,11 +391,13 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
   if (evicted) lru.slot_of[tid] = -1;
   if (inS) {
     lru.stamp[tid] = clock0 + rS + 1;
+    lru.work->hit[rank] = miss ? 0 : 1;
     if (miss) {
       lru.slot_of[tid] = fs;
       lru.expert_in[fs] = tid;
       lru.work->src[rM] = lru.store + (int64_t)tid * lru.P;
       lru.work->dst[rM] = lru.slots + (int64_t)fs * lru.P;
+      lru.work->miss_pos[rM] = rank;
     }
     lru.work->list.payload[rank] = lru.slots + (int64_t)fs * lru.P;
     lru.work->list.pos[rank] = rank;
@@ -748,25 +751,62 @@ struct GateUpParams {
   int lanes_log2;
 };
 
+// Digits of SwiGLU activations in 16-wide blocks, called by 16 consecutive
+// lanes holding the values of rows row0 .. row0+15 of the expert at top-k
+// position pos (one value each, lane l has row row0 + l).
+template <int QT>
+__device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I, int k, int8_t *hq,
+                                               float *hsc, int32_t *hds) {
+  float m = fabsf(v);
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+  const float rs = m > 0.f ? 127.f * __builtin_amdgcn_rcpf(m) : 0.f;
+  int d1, d2, d3;
+  digits_of(v, rs, d1, d2, d3);
+  int t1 = d1, t2 = d2, t3 = d3;
+  if constexpr (QT == 2) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      t1 += __shfl_xor(t1, off, kWave);
+      t2 += __shfl_xor(t2, off, kWave);
+      t3 += __shfl_xor(t3, off, kWave);
+    }
+  }
+  if (row < I) {
+    const int64_t i = (int64_t)pos * I + row, KI = (int64_t)k * I;
+    hq[i] = (int8_t)d1;
+    hq[KI + i] = (int8_t)d2;
+    hq[2 * KI + i] = (int8_t)d3;
+    if ((row & 15) == 0) {
+      hsc[i / 16] = m * (1.f / 127.f);
+      if constexpr (QT == 2) {
+        hds[i / 16] = t1;
+        hds[KI / 16 + i / 16] = t2;
+        hds[2 * (KI / 16) + i / 16] = t3;
+      }
+    }
+  }
+}
+
 // One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
 // lanes handles pairs l, l+lanes, ... of both rows (F of each in flight).
 // A block covers 256 / lanes >= 16 consecutive rows, so it also forms the
-// digits of its whole 16-wide blocks of h.  grid: n experts x ceil(I / (256 / lanes)).
+// digits of its whole 16-wide blocks of h.  Block blk of the launch: expert
+// blk / bpe, rows from (blk % bpe) * (256 / lanes).
 template <int QT>
-__global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
-  extern __shared__ __align__(16) uint8_t smem8[];
+__device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertList &L, int blk,
+                                            uint8_t *smem8) {
   constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kGateUpFlight;
   const int H = a.H, nb = H / 32, np = nb / 2, pb = plane_bytes(H);
   uint8_t *qL = smem8;                                     // digit image of the token
   float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);  // [H/32]
   int *dsL = reinterpret_cast<int *>(scL + nb);            // [3][H/32]
   float *hL = reinterpret_cast<float *>(dsL + 3 * nb);     // [256 / lanes]
-  const ExpertList &L = a.Ld ? *a.Ld : a.L;
   const int upb = kThreads / a.lanes;
   const int bpe = (a.I + upb - 1) / upb;
-  const int ei = blockIdx.x / bpe;
+  const int ei = blk / bpe;
   if (ei >= L.n) return;  // uniform over the block
-  const int r0 = (blockIdx.x - ei * bpe) * upb;
+  const int r0 = (blk - ei * bpe) * upb;
   const int r = r0 + (threadIdx.x >> a.lanes_log2);
   const int l = threadIdx.x & (a.lanes - 1);
   const bool active = r < a.I;
@@ -816,38 +856,167 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   if (l == 0) hL[threadIdx.x >> a.lanes_log2] = active ? silu(g) * u : 0.f;
   __syncthreads();
   // digits of the block's rows: one value per thread, 16-lane groups
-  if ((int)threadIdx.x < upb) {
-    const float v = hL[threadIdx.x];
-    float m = fabsf(v);
+  if ((int)threadIdx.x < upb)
+    store_h_digits<QT>(hL[threadIdx.x], L.pos[ei], r0 + threadIdx.x, a.I, a.k, a.hq, a.hsc, a.hds);
+}
+
+template <int QT>
+__global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  gateup_body<QT>(a, a.Ld ? *a.Ld : a.L, blockIdx.x, smem8);
+}
+
+// ---------------------------------------------------- copy + gate/up fused ---
+//
+// Blocks [0, copy_blocks) move the misses' payloads in "chunks": two spans of
+// R rows (R * rowb bytes each) -- the same rows of W_gate and W_up for the
+// first I/16 "units" of a miss (one unit = one 16-row block of h, 16/R
+// chunks), then the down matrix in units of the same byte size.  A chunk is
+// loaded with coalesced 16-byte loads (the copy kernel's pattern), stored to
+// the slot and, for gate/up rows, to LDS, where the block computes its R rows
+// of h while the next chunk is in flight.  Unit u of the launch goes to
+// block u % copy_blocks.  Blocks from copy_blocks on are the gate/up blocks of
+// the hit experts (gateup_body); those of missed positions exit.
+constexpr int kChunkSlots = 9;  // 16-byte loads per lane per chunk: 2 * R * rowb <= 9 * 4096
+
+struct CopyGateUpParams {
+  GateUpParams g;     // token digits, activation outputs, shape, hit-block lanes
+  const WorkList *W;
+  int64_t P;
+  int copy_blocks, R;  // rows per chunk
+  uint64_t *acc;      // nullable: += copies, += bytes
+};
+
+template <int QT>
+__global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  const WorkList &W = *a.W;
+  if ((int)blockIdx.x >= a.copy_blocks) {  // gate/up of a hit expert
+    const int blk = blockIdx.x - a.copy_blocks;
+    const int upb = kThreads / a.g.lanes, bpe = (a.g.I + upb - 1) / upb, ei = blk / bpe;
+    if (ei >= W.list.n || !W.hit[ei]) return;
+    gateup_body<QT>(a.g, W.list, blk, smem8);
+    return;
+  }
+  const int n = W.n_copy;
+  if (n == 0) return;
+  if (a.acc && blockIdx.x == 0 && threadIdx.x == 0) {
+    atomicAdd(reinterpret_cast<unsigned long long *>(a.acc), (unsigned long long)n);
+    atomicAdd(reinterpret_cast<unsigned long long *>(a.acc + 1), (unsigned long long)(n * a.P));
+  }
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
+  const int H = a.g.H, I = a.g.I, nb = H / 32, np = nb / 2, pb = plane_bytes(H);
+  uint8_t *qL = smem8;
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);
+  int *dsL = reinterpret_cast<int *>(scL + nb);
+  float *hL = reinterpret_cast<float *>(dsL + 3 * nb);  // [16]
+  uint8_t *cL = reinterpret_cast<uint8_t *>(hL + 16);    // one chunk: 2 spans
+  const int R = a.R, cpu = 16 / R;                        // chunks per unit
+  const int64_t rowb = (int64_t)nb * BB, M = (int64_t)I * rowb, half = R * rowb;
+  const int h16 = (int)(half / 16), c16 = 2 * h16;        // 16-byte pieces per span / chunk
+  const int upm = I / 16 + I / 32;                         // units per miss
+  const int n_units = n * upm;
+  int u = blockIdx.x;
+  if (u >= n_units) return;  // uniform
+  stage_token(a.g.xq, a.g.xsc, H, qL, scL);
+  // the two spans of chunk c of unit u (source and slot), and whether it holds gate/up rows
+  auto spans = [&](int uu, int c, const uint8_t *&s0, const uint8_t *&s1, uint8_t *&d0, uint8_t *&d1,
+                   int &miss, int &g) -> bool {
+    miss = uu / upm;
+    const int j = uu - miss * upm;
+    int64_t o0, o1;
+    const bool gu = j < I / 16;
+    if (gu) {
+      g = j;
+      o0 = (int64_t)(16 * j + c * R) * rowb;
+      o1 = M + o0;
+    } else {
+      g = -1;
+      o0 = 2 * M + ((int64_t)(j - I / 16) * cpu + c) * 2 * half;
+      o1 = o0 + half;
+    }
+    s0 = W.src[miss] + o0;
+    s1 = W.src[miss] + o1;
+    d0 = W.dst[miss] + o0;
+    d1 = W.dst[miss] + o1;
+    return gu;
+  };
+  uint4 buf[kChunkSlots];
+  auto load_chunk = [&](const uint8_t *s0, const uint8_t *s1) {
 #pragma unroll
-    for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
-    const float rs = m > 0.f ? 127.f * __builtin_amdgcn_rcpf(m) : 0.f;
-    int d1, d2, d3;
-    digits_of(v, rs, d1, d2, d3);
-    int t1 = d1, t2 = d2, t3 = d3;
-    if constexpr (QT == 2) {
+    for (int m = 0; m < kChunkSlots; ++m) {
+      const int q = threadIdx.x + m * kThreads;
+      const uint8_t *p = q < h16 ? s0 + 16 * (int64_t)q : s1 + 16 * (int64_t)(q - h16);
+      buf[m] = q < c16 ? *reinterpret_cast<const uint4 *>(p) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  const uint8_t *s0, *s1;
+  uint8_t *d0, *d1;
+  int miss, g, c = 0;
+  bool gu = spans(u, 0, s0, s1, d0, d1, miss, g);
+  load_chunk(s0, s1);
+  if constexpr (QT == 2) {
+    __syncthreads();
+    digit_sums(qL, H, dsL);
+  }
+  // the gate/up kernel's lanes and pair order, so h is bit-identical to its result
+  const int L = a.g.lanes, rr = threadIdx.x >> a.g.lanes_log2, l = threadIdx.x & (L - 1);
+  for (;;) {
+    // the chunk in buf: to its slot, and (gate/up rows) to LDS
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        t1 += __shfl_xor(t1, off, kWave);
-        t2 += __shfl_xor(t2, off, kWave);
-        t3 += __shfl_xor(t3, off, kWave);
+    for (int m = 0; m < kChunkSlots; ++m) {
+      const int q = threadIdx.x + m * kThreads;
+      if (q < c16) {
+        uint8_t *p = q < h16 ? d0 + 16 * (int64_t)q : d1 + 16 * (int64_t)(q - h16);
+        *reinterpret_cast<uint4 *>(p) = buf[m];
+        if (gu) reinterpret_cast<uint4 *>(cL)[q] = buf[m];
       }
     }
-    const int rr = r0 + threadIdx.x;
-    if (rr < a.I) {
-      const int64_t i = (int64_t)L.pos[ei] * a.I + rr, KI = (int64_t)a.k * a.I;
-      a.hq[i] = (int8_t)d1;
-      a.hq[KI + i] = (int8_t)d2;
-      a.hq[2 * KI + i] = (int8_t)d3;
-      if ((rr & 15) == 0) {
-        a.hsc[i / 16] = m * (1.f / 127.f);
-        if constexpr (QT == 2) {
-          a.hds[i / 16] = t1;
-          a.hds[KI / 16 + i / 16] = t2;
-          a.hds[2 * (KI / 16) + i / 16] = t3;
+    const bool cur_gu = gu;
+    const int cur_c = c, cur_miss = miss, cur_g = g;
+    // next chunk of this block, loads issued before the compute below
+    if (++c == cpu) {
+      c = 0;
+      u += a.copy_blocks;
+    }
+    const bool more = u < n_units;
+    if (more) {
+      gu = spans(u, c, s0, s1, d0, d1, miss, g);
+      load_chunk(s0, s1);
+    }
+    __syncthreads();  // chunk in LDS
+    if (cur_gu) {
+      // R rows of h from the chunk: L lanes per row, pairs l, l+L, ...
+      float gs = 0.f, us = 0.f;
+      const int rrc = rr < R ? rr : 0;
+      const uint8_t *grow = cL + (int64_t)rrc * rowb, *urow = grow + half;
+      for (int p = rr < R ? l : np; p < np; p += L) {
+        uint32_t wg[PD], wu[PD];
+        const uint32_t *gp = reinterpret_cast<const uint32_t *>(grow + (int64_t)p * 2 * BB);
+        const uint32_t *up = reinterpret_cast<const uint32_t *>(urow + (int64_t)p * 2 * BB);
+#pragma unroll
+        for (int i = 0; i < PD; ++i) {
+          wg[i] = gp[i];
+          wu[i] = up[i];
         }
+        uint32_t D[48];
+        load_digits(qL, pb, p, D);
+        const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
+        gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+        us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+      }
+      gs = group_sum(gs, L);
+      us = group_sum(us, L);
+      if (l == 0 && rr < R) hL[cur_c * R + rr] = silu(gs) * us;
+      if (cur_c == cpu - 1) {
+        __syncthreads();
+        if (threadIdx.x < 16)
+          store_h_digits<QT>(hL[threadIdx.x], W.miss_pos[cur_miss], 16 * cur_g + threadIdx.x, I,
+                             a.g.k, a.g.hq, a.g.hsc, a.g.hds);
       }
     }
+    __syncthreads();  // LDS free for the next chunk
+    if (!more) break;
   }
 }
 
@@ -1577,6 +1746,38 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
     hipExtLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
     hipExtLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+bool fusable_copy_gateup(int qtype, int H, int I) {
+  const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
+  return 2 * 4 * rowb <= (int64_t)kChunkSlots * kThreads * 16 && I % 32 == 0;
+}
+
+hipError_t launch_copy_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
+                              const WorkList *w, int64_t payload_bytes, int copy_blocks,
+                              uint64_t *acc, hipStream_t s, const Timing &t) {
+  if (!fusable_copy_gateup(qtype, H, I) || copy_blocks < 1) return hipErrorInvalidValue;
+  const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
+  const int R = 2 * 8 * rowb <= (int64_t)kChunkSlots * kThreads * 16 ? 8 : 4;
+  CopyGateUpParams a{};
+  a.g = GateUpParams{ExpertList{}, nullptr, S.xq, S.xsc, S.hq, S.hsc, S.hds, H, I, k, 0, 0, 0};
+  pick_lanes(H / 64, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes,
+             a.g.lanes, a.g.mpairs);
+  while ((1 << a.g.lanes_log2) < a.g.lanes) ++a.g.lanes_log2;
+  a.W = w;
+  a.P = payload_bytes;
+  a.copy_blocks = copy_blocks;
+  a.R = R;
+  a.acc = acc;
+  const int upb = kThreads / a.g.lanes;
+  const size_t image = 3 * (size_t)(H / 64) * kPairPitch + 16 * (size_t)(H / 32);
+  const size_t lds = std::max(image + 4 * (size_t)upb, image + 64 + 2 * (size_t)R * rowb);
+  dim3 grid(copy_blocks + k * ((I + upb - 1) / upb));
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(copy_gateup_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(copy_gateup_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 

@@ -6,8 +6,9 @@
 //
 // Decode with the default copy kernel keeps the slot tables in device memory:
 // a layer call is four launches on the caller's stream (router partials;
-// router finish + slot-table step, which writes the call's work list; copy
-// kernel for the misses; gate/up; down) and the host never waits.  The other
+// router finish + slot-table step, which writes the call's work list; the
+// misses' copies fused with gate/up for all routed experts; down) and the host
+// never waits.  The other
 // copy modes and prefill run the slot table on the host, after waiting for
 // the routes; around a prefill call the layer's table moves to the host and back.
 #include <hip/hip_runtime.h>
@@ -468,15 +469,21 @@ int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t la
     sp.end();
   }
   if (c->dl_trace) c->dl_trace_pending += k;
-  {
-    Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
-    HIP_TRY(c, launch_materialize_list(c->dl_work, c->P, kCopyGrid, c->timing_now ? c->dl_copy_acc : nullptr,
-                                       c->main, sp.timing()));
-    sp.end();
-  }
   ExpertList shape{};
   shape.n = k;
-  {
+  uint64_t *acc = c->timing_now ? c->dl_copy_acc : nullptr;
+  if (!(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup(d.qtype, d.hidden, d.inter)) {
+    // one launch: the misses' copies, their gate/up on the fly, the hits' gate/up alongside
+    Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
+    HIP_TRY(c, launch_copy_gateup(d.qtype, c->scratch(), d.hidden, d.inter, k, c->dl_work, c->P,
+                                  kCopyGrid, acc, c->main, sp.timing()));
+    sp.end();
+  } else {
+    {
+      Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);
+      HIP_TRY(c, launch_materialize_list(c->dl_work, c->P, kCopyGrid, acc, c->main, sp.timing()));
+      sp.end();
+    }
     Span sp(c, c->main, MOE_KIND_GATEUP, 1, (uint64_t)k * 2 * c->M, 4ull * k * d.hidden * d.inter);
     HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, k, shape, &c->dl_work->list,
                              c->main, sp.timing()));

@@ -17,8 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libmoecache.so")
 MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
 MOE_Q8_0, MOE_Q4_0 = 8, 2
 MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING, MOE_F_PRENORM = 1, 2, 4, 8
-MOE_F_SIDE_COPY, MOE_F_SDMA_COPY = 16, 32
-COPY_MODES = {"kernel": 0, "side": MOE_F_SIDE_COPY, "sdma": MOE_F_SDMA_COPY}
+MOE_F_SIDE_COPY, MOE_F_SDMA_COPY, MOE_F_SPLIT_COPY = 16, 32, 64
+COPY_MODES = {"kernel": 0, "split": MOE_F_SPLIT_COPY, "side": MOE_F_SIDE_COPY, "sdma": MOE_F_SDMA_COPY}
 KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY = 0, 1, 2, 3
 KIND_NAMES = {KIND_ROUTER: "router", KIND_GATEUP: "gateup", KIND_DOWN: "down", KIND_COPY: "copy"}
 QTYPES = {"q8_0": MOE_Q8_0, "q4_0": MOE_Q4_0}

@@ -50,7 +50,7 @@ def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, st
     return cache, calls, worst
 
 
-@pytest.mark.parametrize("copy_mode", ["kernel", "side", "sdma"])
+@pytest.mark.parametrize("copy_mode", ["kernel", "split", "side", "sdma"])
 def test_tiny_decode_parity(copy_mode):
     wl = synth.WORKLOADS["tiny"]
     cache, calls, worst = run_decode(wl, wl.budget_slots, copy_mode=copy_mode)
@@ -64,7 +64,7 @@ def test_tiny_residual_mode():
     run_decode(wl, wl.budget_slots, residual=True, n_tokens=16)[0].close()
 
 
-@pytest.mark.parametrize("copy_mode", ["kernel", "side", "sdma"])
+@pytest.mark.parametrize("copy_mode", ["kernel", "split", "side", "sdma"])
 def test_prenorm_residual_multi_layer(copy_mode):
     wl = synth.WORKLOADS["tiny"].with_(n_layers=4, name="tiny4")
     run_decode(wl, 4, residual=True, prenorm=True, n_tokens=16, copy_mode=copy_mode)[0].close()
@@ -107,6 +107,35 @@ def test_other_shapes(shape):
         wl = synth.WORKLOADS["tiny"].with_(hidden=H, inter=I, n_experts=E, top_k=k, qtype=qt,
                                            name=f"shape{H}x{I}x{E}")
         run_decode(wl, C, n_tokens=6)[0].close()
+
+
+@pytest.mark.parametrize("shape", [(320, 192, 5, 3, 3), (2816, 704, 64, 16, 17), (4096, 256, 32, 4, 6)])
+def test_split_copy_matches_fused(shape):
+    """The default decode launch (miss copies fused with gate/up) and the split
+    launches (copy kernel, then gate/up) give bit-identical outputs and equal traces."""
+    torch = torch_cuda()
+    H, I, E, k, C = shape
+    for qt in ("q8_0", "q4_0"):
+        wl = synth.WORKLOADS["tiny"].with_(hidden=H, inter=I, n_experts=E, top_k=k, qtype=qt,
+                                           n_layers=2, name=f"fuse{H}x{I}x{E}")
+        keep, ptr, arr = store_buffer(wl)
+        R = torch.from_numpy(synth.router(wl)).cuda()
+        X = torch.from_numpy(synth.hidden(wl, n_tokens=10)).cuda()
+        res = []
+        for mode in ("kernel", "split"):
+            cache = make_cache(wl, ptr, C, trace=True, residual=True, prenorm=True, copy_mode=mode)
+            outs = []
+            for t in range(X.shape[0]):
+                x = X[t].contiguous()
+                for l in range(wl.n_layers):
+                    y = torch.empty_like(x)
+                    cache.layer_forward(x, R[l], l, y)
+                    x = y
+                outs.append(x)
+            res.append((torch.stack(outs).cpu().numpy(), sorted(cache.read_trace())))
+            cache.close()
+        np.testing.assert_array_equal(res[0][0].view(np.uint32), res[1][0].view(np.uint32))
+        assert res[0][1] == res[1][1]
 
 
 def test_multi_layer_and_reset():
@@ -220,16 +249,22 @@ def test_nonfinite_input_is_reported(copy_mode):
     cache.close()
 
 
-def test_timing_totals():
+@pytest.mark.parametrize("copy_mode", ["kernel", "split"])
+def test_timing_totals(copy_mode):
+    """Event totals: copies and bytes counted by the copy launch itself; gate/up is a
+    launch of its own only in the split mode (inside the copy launch otherwise)."""
     wl = synth.WORKLOADS["tiny"]
     from paper_2607_09686_amd import KIND_COPY, KIND_DOWN, KIND_GATEUP, KIND_ROUTER
-    cache, calls, _ = run_decode(wl, wl.budget_slots, n_tokens=8, timing=True)
+    cache, calls, _ = run_decode(wl, wl.budget_slots, n_tokens=8, timing=True, copy_mode=copy_mode)
     c = cache.counters()
     cp = cache.kernel_stats(KIND_COPY)
     assert cp.launches == c.misses and cp.bytes == c.materialized_bytes and cp.total_ms > 0
     assert cache.kernel_stats(KIND_ROUTER).launches == 8
     gu = cache.kernel_stats(KIND_GATEUP)
-    assert gu.bytes == 8 * wl.top_k * 2 * wl.payload_bytes // 3 and gu.total_ms > 0
+    if copy_mode == "split":
+        assert gu.bytes == 8 * wl.top_k * 2 * wl.payload_bytes // 3 and gu.total_ms > 0
+    else:
+        assert gu.launches == 0 and gu.bytes == 0
     assert cache.kernel_stats(KIND_DOWN).bytes == 8 * wl.top_k * wl.payload_bytes // 3
     cache.close()
 
