@@ -257,7 +257,7 @@ def main():
             "expert_ffn_kernels": "gate/up + down" if "gateup" in stats else
                                   "down (gate/up runs inside the copy launch)",
             "copy_gb_per_s": cp["gb_per_s"],
-            "copy_frac_of_measured_h2d": (cp["gb_per_s"] or 0) / h2d_peak,
+            "copy_frac_of_best_measured_h2d": (cp["gb_per_s"] or 0) / max(h2d_peak, h2d_big or 0),
             "kernels": stats,
         })
     cache.close()

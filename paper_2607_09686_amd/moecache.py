@@ -12,7 +12,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmoecache.so")
+# MOECACHE_LIB: an alternative build of the library to load instead of the in-tree one
+LIB_PATH = os.environ.get("MOECACHE_LIB") or os.path.join(_HERE, "libmoecache.so")
 
 MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
 MOE_Q8_0, MOE_Q4_0 = 8, 2
