@@ -535,11 +535,18 @@ __device__ __forceinline__ int pad_off(int i) { return (i >> 6) * kPairPitch + (
 // four dword loads: a quarter of the address work per byte).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef u32x4 u32x4_a4 __attribute__((aligned(4)));
+// Weight pointers come out of the work lists as generic pointers; loads
+// through them would be flat loads, which also count against the LDS wait
+// counter (every LDS wait would then wait for the weights as well).  Slots
+// are device memory: the weights are read through global-address-space
+// pointers.
+typedef __attribute__((address_space(1))) const u32x4_a4 g_u32x4_a4;
+typedef __attribute__((address_space(1))) const uint32_t g_u32;
 
 template <int QT>
 __device__ __forceinline__ void load_pair(const uint8_t *p, uint32_t (&wd)[Fmt<QT>::kPairDwords]) {
   constexpr int PD = Fmt<QT>::kPairDwords;
-  const u32x4_a4 *q = reinterpret_cast<const u32x4_a4 *>(p);
+  g_u32x4_a4 *q = (g_u32x4_a4 *)p;
 #pragma unroll
   for (int i = 0; i < PD / 4; ++i) {
     const u32x4 v = q[i];
@@ -548,7 +555,7 @@ __device__ __forceinline__ void load_pair(const uint8_t *p, uint32_t (&wd)[Fmt<Q
     wd[4 * i + 2] = v.z;
     wd[4 * i + 3] = v.w;
   }
-  wd[PD - 1] = reinterpret_cast<const uint32_t *>(p)[PD - 1];
+  wd[PD - 1] = ((g_u32 *)p)[PD - 1];
 }
 
 // fp32 value of a block's digit dot products I1 + I2/254 + I3/254^2.
@@ -693,30 +700,46 @@ __device__ __forceinline__ float group_sum(float v, int lanes) {
 }
 
 // Stage the token's digit planes ([3][H] bytes, contiguous) into an LDS digit
-// image, and the block scales: every global load is issued before the first
-// LDS store (one memory round trip).
+// image, and the block scales.  Split in two so that a caller can issue these
+// loads ahead of its weight loads and store them afterwards: every lane of a
+// used 256-piece round loads (indices past the end clamped to the last piece)
+// and stores (pieces past the end to the 16-byte dummyL), so the compiler
+// keeps the loads where they are issued.
 constexpr int kMaxTok16 = 6;  // 3 * 8192 / 16 / 256
-__device__ __forceinline__ void stage_token(const int8_t *__restrict__ q,
-                                            const float *__restrict__ sc, int H, uint8_t *qL,
-                                            float *scL) {
+struct TokStage {
+  u32x4 v[kMaxTok16];
+  float s;
+};
+__device__ __forceinline__ void stage_token_load(const int8_t *__restrict__ q,
+                                                 const float *__restrict__ sc, int H, TokStage &t) {
+  const int n16 = 3 * H / 16, nsc = H / 32;
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(q);
+#pragma unroll
+  for (int m = 0; m < kMaxTok16; ++m)
+    if (m * kThreads < n16) t.v[m] = src[min((int)threadIdx.x + m * kThreads, n16 - 1)];
+  t.s = sc[min((int)threadIdx.x, nsc - 1)];
+}
+__device__ __forceinline__ void stage_token_store(const TokStage &t, int H, uint8_t *qL, float *scL,
+                                                  uint8_t *dummyL) {
   const int n16 = 3 * H / 16, nsc = H / 32, per = H / 16, pb = plane_bytes(H);
-  const uint4 *src = reinterpret_cast<const uint4 *>(q);
-  uint4 v[kMaxTok16];
 #pragma unroll
   for (int m = 0; m < kMaxTok16; ++m) {
-    const int i = threadIdx.x + m * kThreads;
-    v[m] = i < n16 ? src[i] : make_uint4(0u, 0u, 0u, 0u);
-  }
-  const float s = (int)threadIdx.x < nsc ? sc[threadIdx.x] : 0.f;
-#pragma unroll
-  for (int m = 0; m < kMaxTok16; ++m) {
-    const int i = threadIdx.x + m * kThreads;
-    if (i < n16) {
+    if (m * kThreads < n16) {
+      const int i = threadIdx.x + m * kThreads;
       const int c = (i >= per) + (i >= 2 * per);
-      *reinterpret_cast<uint4 *>(qL + c * pb + pad_off(16 * (i - c * per))) = v[m];
+      uint8_t *dst = i < n16 ? qL + c * pb + pad_off(16 * (i - c * per)) : dummyL;
+      *reinterpret_cast<u32x4 *>(dst) = t.v[m];
     }
   }
-  if ((int)threadIdx.x < nsc) scL[threadIdx.x] = s;
+  float *dsc = (int)threadIdx.x < nsc ? scL + threadIdx.x : reinterpret_cast<float *>(dummyL);
+  *dsc = t.s;
+}
+__device__ __forceinline__ void stage_token(const int8_t *__restrict__ q,
+                                            const float *__restrict__ sc, int H, uint8_t *qL,
+                                            float *scL, uint8_t *dummyL) {
+  TokStage t;
+  stage_token_load(q, sc, H, t);
+  stage_token_store(t, H, qL, scL, dummyL);
 }
 
 // Digit sums of every 32-wide block of a staged digit image of n values
@@ -793,9 +816,10 @@ __device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I,
 // A block covers 256 / lanes >= 16 consecutive rows, so it also forms the
 // digits of its whole 16-wide blocks of h.  Block blk of the launch: expert
 // blk / bpe, rows from (blk % bpe) * (256 / lanes).
+// hit (nullable): per list position, 0 = skip this expert (its rows come from elsewhere).
 template <int QT>
-__device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertList &L, int blk,
-                                            uint8_t *smem8) {
+__device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertList &L,
+                                            const int32_t *hit, int blk, uint8_t *smem8) {
   constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kGateUpFlight;
   const int H = a.H, nb = H / 32, np = nb / 2, pb = plane_bytes(H);
   uint8_t *qL = smem8;                                     // digit image of the token
@@ -805,23 +829,36 @@ __device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertL
   const int upb = kThreads / a.lanes;
   const int bpe = (a.I + upb - 1) / upb;
   const int ei = blk / bpe;
-  if (ei >= L.n) return;  // uniform over the block
+  // the list's count, slot and position are read together (one round trip);
+  // ei < kMaxRouted always (the grid covers at most kMaxRouted experts)
+  const int n = L.n, pos = L.pos[ei], use = hit ? hit[ei] : 1;
+  const uint8_t *const payload = L.payload[ei];
+  // (the slot pointer is part of the test so that its load is issued with the count's)
+  if (ei >= n || !use || payload == nullptr) return;  // uniform over the block
   const int r0 = (blk - ei * bpe) * upb;
   const int r = r0 + (threadIdx.x >> a.lanes_log2);
   const int l = threadIdx.x & (a.lanes - 1);
   const bool active = r < a.I;
   const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
-  const uint8_t *gate = L.payload[ei] + (int64_t)r * rowb, *up = gate + mat;
+  const uint8_t *gate = payload + (int64_t)r * rowb, *up = gate + mat;
+  // the token's digits first, then the first round of weight pairs
+  // (unconditional: an idle slot reloads its row's first pair), then the
+  // digits into LDS while the weights are in flight
+  __shared__ __align__(16) uint8_t dummyL[16];
+  TokStage ts;
+  stage_token_load(a.xq, a.xsc, H, ts);
+  __builtin_amdgcn_sched_barrier(0);
+  const uint8_t *gatev = payload + (int64_t)min(r, a.I - 1) * rowb, *upv = gatev + mat;
   uint32_t wg[F][PD], wu[F][PD];
 #pragma unroll
   for (int m = 0; m < F; ++m) {
     const int p = l + m * a.lanes;
-    if (active && m < a.mpairs && p < np) {
-      load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
-      load_pair<QT>(up + (int64_t)p * 2 * BB, wu[m]);
-    }
+    const bool ok = active && m < a.mpairs && p < np;
+    load_pair<QT>(ok ? gate + (int64_t)p * 2 * BB : gatev, wg[m]);
+    load_pair<QT>(ok ? up + (int64_t)p * 2 * BB : upv, wu[m]);
   }
-  stage_token(a.xq, a.xsc, H, qL, scL);
+  __builtin_amdgcn_sched_barrier(0);
+  stage_token_store(ts, H, qL, scL, dummyL);
   __syncthreads();
   if constexpr (QT == 2) {
     digit_sums(qL, H, dsL);
@@ -857,13 +894,14 @@ __device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertL
   __syncthreads();
   // digits of the block's rows: one value per thread, 16-lane groups
   if ((int)threadIdx.x < upb)
-    store_h_digits<QT>(hL[threadIdx.x], L.pos[ei], r0 + threadIdx.x, a.I, a.k, a.hq, a.hsc, a.hds);
+    store_h_digits<QT>(hL[threadIdx.x], pos, r0 + threadIdx.x, a.I, a.k, a.hq, a.hsc, a.hds);
 }
 
-template <int QT>
+// DEV: the list is read from device memory (a.Ld), else from the arguments.
+template <int QT, bool DEV>
 __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
-  gateup_body<QT>(a, a.Ld ? *a.Ld : a.L, blockIdx.x, smem8);
+  gateup_body<QT>(a, DEV ? *a.Ld : a.L, nullptr, blockIdx.x, smem8);
 }
 
 // ---------------------------------------------------- copy + gate/up fused ---
@@ -892,10 +930,7 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
   extern __shared__ __align__(16) uint8_t smem8[];
   const WorkList &W = *a.W;
   if ((int)blockIdx.x >= a.copy_blocks) {  // gate/up of a hit expert
-    const int blk = blockIdx.x - a.copy_blocks;
-    const int upb = kThreads / a.g.lanes, bpe = (a.g.I + upb - 1) / upb, ei = blk / bpe;
-    if (ei >= W.list.n || !W.hit[ei]) return;
-    gateup_body<QT>(a.g, W.list, blk, smem8);
+    gateup_body<QT>(a.g, W.list, W.hit, blockIdx.x - a.copy_blocks, smem8);
     return;
   }
   const int n = W.n_copy;
@@ -918,7 +953,8 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
   const int n_units = n * upm;
   int u = blockIdx.x;
   if (u >= n_units) return;  // uniform
-  stage_token(a.g.xq, a.g.xsc, H, qL, scL);
+  __shared__ __align__(16) uint8_t dummyL[16];
+  stage_token(a.g.xq, a.g.xsc, H, qL, scL, dummyL);
   // the two spans of chunk c of unit u (source and slot), and whether it holds gate/up rows
   auto spans = [&](int uu, int c, const uint8_t *&s0, const uint8_t *&s1, uint8_t *&d0, uint8_t *&d1,
                    int &miss, int &g) -> bool {
@@ -1027,10 +1063,12 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
 constexpr int kMaxDig16 = 9;  // 3 * 12288 / 16 / 256
 constexpr int kMaxSc4 = 1;    // 12288 / 16 / 4 / 256
 constexpr int kMaxDs4 = 3;    // 3 * 12288 / 16 / 4 / 256
+// (16-byte pieces held as native vectors: HIP's uint4 / float4 structs are
+// copied through a stack object by the compiler)
 struct HStage {
-  uint4 d[kMaxDig16];
-  float4 s[kMaxSc4];
-  int4 q[kMaxDs4];
+  u32x4 d[kMaxDig16];
+  u32x4 s[kMaxSc4];
+  u32x4 q[kMaxDs4];
 };
 
 // Unit u of n groups of `per` units -> (group, index) by floor((u + 0.5) / per)
@@ -1042,68 +1080,82 @@ __device__ __forceinline__ int split_unit(int u, float rper, int per, int &j) {
   return g;
 }
 
+// posL: the listed experts' top-k positions (LDS, n of them).
 __device__ __forceinline__ void stage_h_load(const int8_t *__restrict__ hq,
                                              const float *__restrict__ hsc,
-                                             const int32_t *__restrict__ hds, const ExpertList &L,
+                                             const int32_t *__restrict__ hds, const int *posL, int n,
                                              int I, int k, bool sums, HStage &st) {
+  // Straight-line code: every lane loads (indices past the end are clamped to
+  // the last expert, so each address is inside the buffers) and only the
+  // in-range pieces are stored by stage_h_store.  Branch-free, the loads are
+  // issued back to back, with no wait between them.
   const int64_t KI = (int64_t)k * I;
-  const int n = L.n, u16 = I / 16, u64 = I / 64;
+  const int u16 = I / 16, u64 = I / 64;
   const float r16 = 1.f / (float)u16, r64 = 1.f / (float)u64;
+  const u32x4 *pd[kMaxDig16];
+  const u32x4 *ps[kMaxSc4];
+  const u32x4 *pq[kMaxDs4];
 #pragma unroll
   for (int m = 0; m < kMaxDig16; ++m) {
     const int u = threadIdx.x + m * kThreads;  // (expert, plane, unit)
     int j;
     const int ec = split_unit(u, r16, u16, j);
     const int e = min(ec / 3, n - 1), c = ec - 3 * (ec / 3);
-    st.d[m] = u < 3 * n * u16
-                  ? *reinterpret_cast<const uint4 *>(hq + c * KI + (int64_t)L.pos[e] * I + 16 * j)
-                  : make_uint4(0u, 0u, 0u, 0u);
+    pd[m] = reinterpret_cast<const u32x4 *>(hq + c * KI + (int64_t)posL[e] * I + 16 * j);
   }
 #pragma unroll
   for (int m = 0; m < kMaxSc4; ++m) {
     const int u = threadIdx.x + m * kThreads;  // (expert, 4 scales)
     int j;
     const int e = min(split_unit(u, r64, u64, j), n - 1);
-    st.s[m] = u < n * u64 ? *reinterpret_cast<const float4 *>(hsc + (int64_t)L.pos[e] * u16 + 4 * j)
-                          : make_float4(0.f, 0.f, 0.f, 0.f);
+    ps[m] = reinterpret_cast<const u32x4 *>(hsc + (int64_t)posL[e] * u16 + 4 * j);
   }
+#pragma unroll
+  for (int m = 0; m < kMaxDs4; ++m) {
+    const int u = threadIdx.x + m * kThreads;  // (expert, plane, 4 sums)
+    int j;
+    const int ec = split_unit(u, r64, u64, j);
+    const int e = min(ec / 3, n - 1), c = ec - 3 * (ec / 3);
+    pq[m] = reinterpret_cast<const u32x4 *>(hds + c * (KI / 16) + (int64_t)posL[e] * u16 + 4 * j);
+  }
+#pragma unroll
+  for (int m = 0; m < kMaxDig16; ++m) st.d[m] = *pd[m];
+#pragma unroll
+  for (int m = 0; m < kMaxSc4; ++m) st.s[m] = *ps[m];
   if (sums) {
 #pragma unroll
-    for (int m = 0; m < kMaxDs4; ++m) {
-      const int u = threadIdx.x + m * kThreads;  // (expert, plane, 4 sums)
-      int j;
-      const int ec = split_unit(u, r64, u64, j);
-      const int e = min(ec / 3, n - 1), c = ec - 3 * (ec / 3);
-      st.q[m] = u < 3 * n * u64 ? *reinterpret_cast<const int4 *>(hds + c * (KI / 16) +
-                                                                  (int64_t)L.pos[e] * u16 + 4 * j)
-                                : make_int4(0, 0, 0, 0);
-    }
+    for (int m = 0; m < kMaxDs4; ++m) st.q[m] = *pq[m];
   }
 }
 
+// Every lane stores each piece (no branches, so the compiler keeps the loads
+// where they were issued); pieces past the end go to the 16-byte dummyL.
 __device__ __forceinline__ void stage_h_store(const HStage &st, int n, int I, bool sums, uint8_t *qL,
-                                              float *scL, int *dsL) {
+                                              float *scL, int *dsL, uint8_t *dummyL) {
   const int u16 = I / 16, u64 = I / 64, pb = plane_bytes(I);
   const float r16 = 1.f / (float)u16;
 #pragma unroll
   for (int m = 0; m < kMaxDig16; ++m) {
     const int u = threadIdx.x + m * kThreads;
-    if (u < 3 * n * u16) {
-      int j;
-      const int ec = split_unit(u, r16, u16, j);
-      *reinterpret_cast<uint4 *>(qL + ec * pb + pad_off(16 * j)) = st.d[m];
-    }
+    int j;
+    const int ec = split_unit(u, r16, u16, j);
+    uint8_t *dst = u < 3 * n * u16 ? qL + ec * pb + pad_off(16 * j) : dummyL;
+    *reinterpret_cast<u32x4 *>(dst) = st.d[m];
   }
 #pragma unroll
   for (int m = 0; m < kMaxSc4; ++m) {
     const int u = threadIdx.x + m * kThreads;
-    if (u < n * u64) reinterpret_cast<float4 *>(scL)[u] = st.s[m];
+    u32x4 *dst = u < n * u64 ? reinterpret_cast<u32x4 *>(scL) + u
+                             : reinterpret_cast<u32x4 *>(dummyL);
+    *dst = st.s[m];
   }
   if (sums) {
 #pragma unroll
     for (int m = 0; m < kMaxDs4; ++m) {
       const int u = threadIdx.x + m * kThreads;
-      if (u < 3 * n * u64) reinterpret_cast<int4 *>(dsL)[u] = st.q[m];
+      u32x4 *dst = u < 3 * n * u64 ? reinterpret_cast<u32x4 *>(dsL) + u
+                                   : reinterpret_cast<u32x4 *>(dummyL);
+      *dst = st.q[m];
     }
   }
 }
@@ -1125,12 +1177,17 @@ struct DownParams {
 // One unit = (output row j, expert i), `lanes` lanes, lane l handling pairs
 // l, l+lanes, ... (F in flight).  grid: ceil(H / rows).
 // y[j] (+)= sum over the listed experts, in list order, of w[pos_i] (W_down,i h_i)_j.
-template <int QT>
-__global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
+// DEV: the list is read from device memory (a.Ld), else from the arguments.
+// Memory round trips: the list; then the activation digits, the routing
+// weights and the weight rows, all in flight together.
+template <int QT, bool DEV>
+__global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
+  __shared__ int posL[kMaxRouted];
+  __shared__ float wL[kMaxRouted];
+  __shared__ __align__(16) uint8_t dummyL[16];  // target of the idle lanes' staging stores
   constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kDownFlight;
-  const ExpertList &L = a.Ld ? *a.Ld : a.L;
-  if (L.n != a.L.n) return;  // a device list emptied by a routing error
+  const ExpertList &L = DEV ? *a.Ld : a.L;
   const int I = a.I, nb = I / 32, np = nb / 2, n = a.L.n, pb = plane_bytes(I);
   uint8_t *qL = smem8;                                         // n digit images
   float *scL = reinterpret_cast<float *>(smem8 + 3 * n * pb);  // [n][I/16]
@@ -1142,16 +1199,38 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
   const bool active = rr < a.rows && j < a.H;
   const int64_t rowb = (int64_t)nb * BB;
   const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
-  const uint8_t *row = L.payload[i] + 2 * mat + (int64_t)j * rowb;
+  // the list: count, this unit's slot, the positions (one round trip)
+  const int ndev = L.n;
+  const uint8_t *const payload = L.payload[i];
+  const int pos_t = (int)threadIdx.x < n ? L.pos[threadIdx.x] : 0;
+  if (ndev != n) return;  // a device list emptied by a routing error (uniform)
+  if ((int)threadIdx.x < n) posL[threadIdx.x] = pos_t;
+  __syncthreads();
+  const uint8_t *row = payload + 2 * mat + (int64_t)j * rowb;
+  const uint8_t *rowv = payload + 2 * mat + (int64_t)min(j, a.H - 1) * rowb;
   HStage st;
-  stage_h_load(a.hq, a.hsc, a.hds, L, I, a.k, QT == 2, st);  // ahead of the weights
+  stage_h_load(a.hq, a.hsc, a.hds, posL, n, I, a.k, QT == 2, st);  // ahead of the weights
+  // keeps the staging loads here, ahead of the weight loads (the compiler
+  // would otherwise sink each load to its LDS store and wait for it there)
+  __builtin_amdgcn_sched_barrier(0);
+  // unconditional loads at clamped (valid) indices, results selected after
+  const float w_t = a.w[posL[min((int)threadIdx.x, n - 1)]];
+  // the residual / accumulated output of row j0 + threadIdx.x (rows <= 256)
+  const int jt = j0 + (int)threadIdx.x;
+  const bool out_t = (int)threadIdx.x < a.rows && jt < a.H;
+  const float base_ld = (a.mode == 1 ? a.x : a.y)[min(jt, a.H - 1)];
+  const float base_t = a.mode == 0 ? 0.f : base_ld;
+  // first round of weight pairs, unconditional: an idle slot (inactive row,
+  // pair past the row's end) reloads the unit's first pair, which is valid
   uint32_t wd[F][PD];
 #pragma unroll
   for (int m = 0; m < F; ++m) {
     const int p = l + m * a.lanes;
-    if (active && m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
+    const bool ok = active && m < a.mpairs && p < np;
+    load_pair<QT>(ok ? row + (int64_t)p * 2 * BB : rowv, wd[m]);
   }
-  stage_h_store(st, n, I, QT == 2, qL, scL, dsL);
+  __builtin_amdgcn_sched_barrier(0);
+  stage_h_store(st, n, I, QT == 2, qL, scL, dsL, dummyL);
   __syncthreads();
   float acc = 0.f;
   for (int m0 = 0; m0 < a.mpairs; m0 += F) {
@@ -1175,13 +1254,12 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownParams a) {
   }
   acc = group_sum(acc, a.lanes);
   if (active && l == 0) res[rr * n + i] = acc;
+  if ((int)threadIdx.x < n) wL[threadIdx.x] = w_t;
   __syncthreads();
-  for (int t = threadIdx.x; t < a.rows; t += kThreads) {
-    const int jj = j0 + t;
-    if (jj >= a.H) continue;
-    float v = a.mode == 2 ? a.y[jj] : (a.mode == 1 ? a.x[jj] : 0.f);
-    for (int ii = 0; ii < n; ++ii) v = fmaf(a.w[L.pos[ii]], res[t * n + ii], v);
-    a.y[jj] = v;
+  if (out_t) {
+    float v = base_t;
+    for (int ii = 0; ii < n; ++ii) v = fmaf(wL[ii], res[threadIdx.x * n + ii], v);
+    a.y[jt] = v;
   }
 }
 
@@ -1721,10 +1799,15 @@ hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
   const int upb = kThreads / a.lanes;
   const size_t lds = 3 * (size_t)np * kPairPitch + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
   dim3 grid(L.n * ((I + upb - 1) / upb));
-  if (qtype == 8)
-    hipExtLaunchKernelGGL(gateup_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  if (L.n > kMaxRouted) return hipErrorInvalidValue;
+  if (qtype == 8 && Ld)
+    hipExtLaunchKernelGGL(gateup_kernel<8, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else if (qtype == 8)
+    hipExtLaunchKernelGGL(gateup_kernel<8, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else if (Ld)
+    hipExtLaunchKernelGGL(gateup_kernel<2, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
-    hipExtLaunchKernelGGL(gateup_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    hipExtLaunchKernelGGL(gateup_kernel<2, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 
@@ -1742,10 +1825,15 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
   const size_t lds = 3 * (size_t)L.n * np * kPairPitch + 4 * (size_t)L.n * (I / 16) * 4 +
                      4 * (size_t)a.rows * L.n;
   dim3 grid((H + a.rows - 1) / a.rows);
-  if (qtype == 8)
-    hipExtLaunchKernelGGL(down_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  if (L.n > kMaxRouted) return hipErrorInvalidValue;
+  if (qtype == 8 && Ld)
+    hipExtLaunchKernelGGL(down_kernel<8, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else if (qtype == 8)
+    hipExtLaunchKernelGGL(down_kernel<8, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else if (Ld)
+    hipExtLaunchKernelGGL(down_kernel<2, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
-    hipExtLaunchKernelGGL(down_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    hipExtLaunchKernelGGL(down_kernel<2, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 
