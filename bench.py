@@ -34,6 +34,7 @@ HBM_PEAK_GBS = 8000.0
 # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130 encoding / 8 bits
 PCIE_PEAK_GBS = 32.0 * 16 * 128 / 130 / 8
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+HBM_BYTES = 288 * 10**9    # MI355X HBM3E capacity
 
 
 def log(msg):
@@ -81,9 +82,18 @@ def main():
 
     import synth
     from paper_2607_09686_amd import (KIND_COPY, KIND_DOWN, KIND_GATEUP, KIND_ROUTER, HostBuffer,
-                                      MoeCache, probe_h2d)
+                                      MoeCache, plan_percent, probe_h2d)
 
     wl = synth.WORKLOADS[args.workload]
+    # slots per layer from the workload's cache percentage, by the library's static planner;
+    # the plan's lower bound (router weights + expert slots, no KV cache on this path) is
+    # checked against the GPU's HBM
+    model = {"n_layers": wl.n_layers, "n_experts": wl.n_experts, "top_k": wl.top_k,
+             "payload_bytes": wl.payload_bytes, "common_bytes": wl.n_layers * wl.hidden * wl.n_experts * 4,
+             "kv_bytes_per_token": 0, "overhead_bytes": 0, "target_bytes": HBM_BYTES}
+    plan = plan_percent(model, wl.cache_percent)
+    if plan["slots_per_layer"] != wl.budget_slots:
+        raise RuntimeError(f"planner gives {plan['slots_per_layer']} slots, workload {wl.budget_slots}")
     budget = args.budget or wl.budget_slots
     rho = wl.rho if args.rho is None else args.rho
     torch.cuda.set_device(0)
@@ -244,6 +254,7 @@ def main():
         "us_per_layer_call": 1e6 * dt / (tokens * wl.n_layers),
         "h2d_peak_gb_per_s": h2d_peak,
         "h2d_1gib_gb_per_s": h2d_big,
+        "static_plan": dict(plan, cache_percent=wl.cache_percent, target="HBM 288 GB"),
     }
     if timing and "copy" in stats:
         cp = stats["copy"]

@@ -13,11 +13,13 @@
  * Here the backing store is pinned host memory, the slots are HBM, and a
  * layer call does, in order:
  *   1. router logits z = x W_r, top-k by (-z, id), softmax over the chosen k;
- *   2. LRU slot-table lookup on the host with hit / miss / eviction counters;
- *   3. one host-to-device copy per miss into the chosen slot, on a side stream;
+ *   2. LRU slot-table lookup with hit / miss / eviction counters (decode: in
+ *      device memory, stepped by the router's last kernel; prefill and the
+ *      SIDE/SDMA copy modes: on the host);
+ *   3. the misses' copies host -> slot (decode: one copy kernel, fused with the
+ *      gate/up of every routed expert; or hipMemcpyAsync per miss);
  *   4. fused dequantise + SwiGLU gate/up, then down projection with the
- *      routing-weighted combine (and optional residual add); hit experts run
- *      while the misses are still being copied.
+ *      routing-weighted combine (and optional residual add).
  *
  * Conventions for every function below:
  *   - returns MOE_OK (0) or a negative MOE_E* code; moe_last_error() then
@@ -192,6 +194,56 @@ int moe_host_free(void *p);
  * HIP events from the first copy to the last.  *gb_per_s = bytes / time. */
 int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, int32_t n_streams,
                   double *gb_per_s);
+
+/* Static budget plan (no HIP dependency, no allocation).  The paper's Native
+ * Serving Path section derives the slot count of the routed layers from the
+ * requested cache bytes, the routed layer count, the bytes of one expert block,
+ * the active experts per token and the experts per layer; its Static Budget
+ * Check section bounds the serving footprint from below,
+ *   L(p, n) = C + E(p) + K(n)          F(p, n) = L(p, n) + O
+ * (C resident common tensors, E(p) the expert cache at cache percentage p,
+ * K(n) the KV cache at context n, O runtime overhead) and rejects a
+ * configuration whose L already exceeds the serving target.  Here every layer
+ * gets the same slot count s, clamped to [top_k, n_experts], so
+ * E = n_layers * s * payload_bytes, and K(n) = n * kv_bytes_per_token.
+ * All sizes in bytes.  Both functions return MOE_EINVAL (no message) on a bad
+ * argument or when a size overflows 64 bits, MOE_OK otherwise. */
+typedef struct {
+  int32_t n_layers;            /* routed MoE layers, >= 1 */
+  int32_t n_experts;           /* experts per layer, >= 1 */
+  int32_t top_k;               /* active experts per token, 1..n_experts: the fewest slots
+                                  a layer can work with */
+  int32_t pad;
+  uint64_t payload_bytes;      /* one expert block = one slot, >= 1 */
+  uint64_t common_bytes;       /* C */
+  uint64_t kv_bytes_per_token; /* K(n) / n */
+  uint64_t overhead_bytes;     /* O */
+  uint64_t target_bytes;       /* serving target the lower bound is checked against */
+} moe_plan_in;
+
+typedef struct {
+  int32_t slots_per_layer;     /* s */
+  int32_t clamped;             /* 1 if the budget asked for fewer than top_k or more than
+                                  n_experts slots and s was clamped */
+  uint64_t expert_cache_bytes; /* E = n_layers * s * payload_bytes */
+  uint64_t kv_bytes;           /* K(n) */
+  uint64_t lower_bound_bytes;  /* L = C + E + K(n) */
+  uint64_t footprint_bytes;    /* F = L + O */
+  int32_t feasible;            /* 1 if L <= target_bytes, 0 if the plan is rejected */
+  int32_t pad;
+} moe_plan_out;
+
+/* Cache as a percentage of each layer's experts, 0 < percent <= 100:
+ * s = nearest integer to percent/100 * n_experts, halves rounding up
+ * (computed in double as floor((2 * percent * n_experts + 100) / 200));
+ * 15, 35 and 75 % of 128 experts give 19, 45 and 96 slots. */
+int moe_plan_percent(const moe_plan_in *in, double percent, int64_t context_tokens,
+                     moe_plan_out *out);
+
+/* Cache as a byte budget for all routed layers: s = floor(cache_bytes /
+ * (n_layers * payload_bytes)). */
+int moe_plan_bytes(const moe_plan_in *in, uint64_t cache_bytes, int64_t context_tokens,
+                   moe_plan_out *out);
 
 /* The slot table alone, with no HIP dependency (used to check it on the CPU).
  * Same rule as inside moe_layer_forward: for one call with routed experts ids

@@ -15,10 +15,12 @@ What it computes, in plain fp64 numpy, one obviously-correct step at a time:
 * a whole MoE layer call and the residual stack   (``layer``)
 * the prefill variant that rounds weights, inputs and activations to bf16
   where the MFMA path does                        (``layer.moe_layer_bf16``)
+* the static budget planner: slots per layer from a cache budget and the
+  lower bound C + E(p) + K(n) against the serving target   (``planner``)
 
 The paper (its Native Serving Path section) fixes only the mechanism: per-layer
 slot tensors for routed experts, filled on a miss, with route-to-slot
 metadata.  Every finer point (eviction rule, hit granularity, tie-breaks, FFN
 form, block formats) is a stated reading; each function names the one it uses.
 """
-from . import numerics, quant, router, lru, ffn, layer  # noqa: F401
+from . import numerics, quant, router, lru, ffn, layer, planner  # noqa: F401

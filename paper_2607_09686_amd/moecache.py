@@ -60,6 +60,24 @@ class KernelStats(ctypes.Structure):
                 ("bytes", ctypes.c_uint64), ("flops", ctypes.c_uint64)]
 
 
+class PlanIn(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("payload_bytes", ctypes.c_uint64), ("common_bytes", ctypes.c_uint64),
+                ("kv_bytes_per_token", ctypes.c_uint64), ("overhead_bytes", ctypes.c_uint64),
+                ("target_bytes", ctypes.c_uint64)]
+
+
+class PlanOut(ctypes.Structure):
+    _fields_ = [("slots_per_layer", ctypes.c_int32), ("clamped", ctypes.c_int32),
+                ("expert_cache_bytes", ctypes.c_uint64), ("kv_bytes", ctypes.c_uint64),
+                ("lower_bound_bytes", ctypes.c_uint64), ("footprint_bytes", ctypes.c_uint64),
+                ("feasible", ctypes.c_int32), ("pad", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "pad"}
+
+
 _lib = None
 
 
@@ -110,6 +128,8 @@ def lib():
         "moe_lru_step": ([vp, P(i32), i32, P(StepRec), P(i32)], ctypes.c_int),
         "moe_lru_counters": ([vp, P(Counters)], ctypes.c_int),
         "moe_lru_destroy": ([vp], None),
+        "moe_plan_percent": ([P(PlanIn), ctypes.c_double, i64, P(PlanOut)], ctypes.c_int),
+        "moe_plan_bytes": ([P(PlanIn), u64, i64, P(PlanOut)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -294,3 +314,31 @@ class SlotTable:
             self.close()
         except Exception:
             pass
+
+
+def _plan_in(m):
+    return PlanIn(m["n_layers"], m["n_experts"], m["top_k"], 0, m["payload_bytes"],
+                  m.get("common_bytes", 0), m.get("kv_bytes_per_token", 0),
+                  m.get("overhead_bytes", 0), m.get("target_bytes", 0))
+
+
+def plan_percent(model, percent, context_tokens=0):
+    """Static budget plan for a cache percentage (moe_plan_percent); model is a dict with
+    n_layers, n_experts, top_k, payload_bytes and optionally common_bytes,
+    kv_bytes_per_token, overhead_bytes, target_bytes.  Returns the plan as a dict."""
+    out = PlanOut()
+    rc = lib().moe_plan_percent(ctypes.byref(_plan_in(model)), float(percent), int(context_tokens),
+                                ctypes.byref(out))
+    if rc != MOE_OK:
+        raise MoeError(rc, "moe_plan_percent: bad argument or size overflow")
+    return out.as_dict()
+
+
+def plan_bytes(model, cache_bytes, context_tokens=0):
+    """Static budget plan for a cache byte budget over all routed layers (moe_plan_bytes)."""
+    out = PlanOut()
+    rc = lib().moe_plan_bytes(ctypes.byref(_plan_in(model)), int(cache_bytes), int(context_tokens),
+                              ctypes.byref(out))
+    if rc != MOE_OK:
+        raise MoeError(rc, "moe_plan_bytes: bad argument or size overflow")
+    return out.as_dict()

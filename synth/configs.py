@@ -28,6 +28,7 @@ class Workload:
     mode: str = "decode"       # "decode" (one token per layer call) or "prefill" (whole chunk per call)
     sweep_slots: Tuple[int, ...] = field(default=())
     sweep_rhos: Tuple[float, ...] = field(default=())
+    cache_percent: float = 0.0  # the cache budget as a percentage of each layer's experts
 
     @property
     def block_bytes(self) -> int:
@@ -60,20 +61,21 @@ class Workload:
 
 TINY = Workload("tiny", n_layers=1, hidden=256, n_experts=16, top_k=2, inter=128,
                 qtype="q8_0", weight_sigma=0.02, router_sigma=0.1, n_tokens=64, rho=0.8,
-                budget_slots=4, model_seed=1, hidden_seed=1)
+                budget_slots=4, model_seed=1, hidden_seed=1, cache_percent=25)
 
 A3B_DECODE = Workload("a3b_decode", n_layers=48, hidden=2048, n_experts=128, top_k=8, inter=768,
                       qtype="q8_0", weight_sigma=0.02, router_sigma=0.05, n_tokens=96, rho=0.8,
-                      budget_slots=19, model_seed=2, hidden_seed=2)
+                      budget_slots=19, model_seed=2, hidden_seed=2, cache_percent=15)
 
 A3B_SWEEP = A3B_DECODE.with_(name="a3b_sweep", hidden_seed=3, sweep_slots=(19, 45, 96),
                              sweep_rhos=(0.3, 0.9))
 
 Q4_DECODE = Workload("q4_decode", n_layers=30, hidden=2816, n_experts=128, top_k=8, inter=1408,
                      qtype="q4_0", weight_sigma=0.02, router_sigma=0.05, n_tokens=96, rho=0.8,
-                     budget_slots=45, model_seed=4, hidden_seed=4)
+                     budget_slots=45, model_seed=4, hidden_seed=4, cache_percent=35)
 
 A3B_PREFILL = A3B_DECODE.with_(name="a3b_prefill", n_tokens=4096, rho=-1.0, budget_slots=45,
+                               cache_percent=35,
                                hidden_seed=5, mode="prefill")
 
 WORKLOADS = {w.name: w for w in (TINY, A3B_DECODE, A3B_SWEEP, Q4_DECODE, A3B_PREFILL)}
