@@ -63,10 +63,12 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 float *xsc, bool prenorm, const LruDev *lru, hipStream_t s,
                                 const Timing &t = {});
 
-// Prefill router: partial logits over router_slices() slices of H into
-// z [slices][T][E], then per token z = tscale[t] * (sum of slices) (tscale
+// Prefill router: partial logits over router_slices(T) slices of H into
+// z [slices][T][E] (router_zbuf_floats(T, E) floats cover any call of at most
+// T tokens), then per token z = tscale[t] * (sum of slices) (tscale
 // nullable) and top-k rows into idx/w [T][k].
-int router_slices();
+int router_slices(int T);
+int64_t router_zbuf_floats(int64_t T, int E);
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s);
 

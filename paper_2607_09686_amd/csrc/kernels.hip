@@ -427,14 +427,15 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
 
 // Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]:
 // a block owns 32 tokens, 128 expert columns (blockIdx.y) and one of
-// kPfSlices slices of H (blockIdx.z); thread (tt, cc) keeps a 4-token x
+// `slices` slices of H (blockIdx.z); thread (tt, cc) keeps a 4-token x
 // 4-expert tile of accumulators; K runs over the slice in 32-row steps
-// through LDS.  The top-k kernel adds the slices in order.
-constexpr int kPfTok = 32, kPfRows = 32, kPfCols = 128, kPfSlices = 4;
+// through LDS.  The top-k kernel adds the slices in order.  Few tokens get
+// many slices (a 5-token call would otherwise read all of W_r with 4 blocks).
+constexpr int kPfTok = 32, kPfRows = 32, kPfCols = 128;
 
 __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__restrict__ x,
                                                                  const float *__restrict__ wr,
-                                                                 int T, int H, int E,
+                                                                 int T, int H, int E, int slices,
                                                                  float *__restrict__ zp) {
   __shared__ float xs[kPfRows][kPfTok + 1];   // [k][token]
   __shared__ float ws[kPfRows][kPfCols + 4];  // [k][col]
@@ -446,7 +447,7 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-  const int per = (H / kPfSlices + kPfRows - 1) / kPfRows * kPfRows;
+  const int per = ((H + slices - 1) / slices + kPfRows - 1) / kPfRows * kPfRows;
   const int rbeg = blockIdx.z * per, rend = min(H, rbeg + per);
   for (int r0 = rbeg; r0 < rend; r0 += kPfRows) {
     for (int i = tid; i < kPfTok * kPfRows; i += kThreads) {
@@ -485,7 +486,7 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
 
 // z[t] = tscale[t] * sum of the slices in order; top-k of each token row.
 __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__restrict__ zp, int T,
-                                                             int E, int k,
+                                                             int E, int k, int slices,
                                                              const float *__restrict__ tscale,
                                                              int32_t *idx, float *w) {
   __shared__ float zs[kThreads / kWave][256];
@@ -495,7 +496,7 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__rest
   const float sc = tscale ? tscale[t] : 1.f;
   for (int e = lane; e < E; e += kWave) {
     float v = 0.f;
-    for (int sl = 0; sl < kPfSlices; ++sl) v += zp[((int64_t)sl * T + t) * E + e];
+    for (int sl = 0; sl < slices; ++sl) v += zp[((int64_t)sl * T + t) * E + e];
     zs[wave][e] = v * sc;
   }
   wave_topk(zs[wave], E, k, idx + (int64_t)t * k, w + (int64_t)t * k, nullptr, nullptr);
@@ -1778,14 +1779,15 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
 
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s) {
+  const int slices = router_slices(T);
   hipLaunchKernelGGL(router_logits_kernel,
-                     dim3((T + kPfTok - 1) / kPfTok, (E + kPfCols - 1) / kPfCols, kPfSlices),
-                     dim3(kThreads), 0, s, x, wr, T, H, E, z);
+                     dim3((T + kPfTok - 1) / kPfTok, (E + kPfCols - 1) / kPfCols, slices),
+                     dim3(kThreads), 0, s, x, wr, T, H, E, slices, z);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int wpb = kThreads / kWave;
   hipLaunchKernelGGL(topk_rows_kernel, dim3((T + wpb - 1) / wpb), dim3(kThreads), 0, s, z, T, E, k,
-                     tscale, idx, w);
+                     slices, tscale, idx, w);
   return hipGetLastError();
 }
 
@@ -1968,7 +1970,12 @@ hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, in
 }
 
 int pf_max_experts() { return kPfMaxExperts; }
-int router_slices() { return kPfSlices; }
+int router_slices(int T) { return T <= kPfTok ? 64 : (T <= 8 * kPfTok ? 16 : 4); }
+int64_t router_zbuf_floats(int64_t T, int E) {
+  // the most any call of at most T tokens needs (slices * tokens is not monotonic in T)
+  return (int64_t)E * std::max({64 * std::min<int64_t>(T, kPfTok), 16 * std::min<int64_t>(T, 8 * kPfTok),
+                                4 * T});
+}
 int max_copy() { return kMaxCopy; }
 
 }  // namespace moecache

@@ -275,7 +275,7 @@ int ensure_tokens(moe_cache *c, int64_t T) {
   const int64_t k = c->d.top_k, E = c->d.n_experts;
   if (hipMalloc(&c->topk_idx, T * k * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->topk_w, T * k * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->zbuf, router_slices() * T * E * sizeof(float)) != hipSuccess)
+      hipMalloc(&c->zbuf, router_zbuf_floats(T, (int)E) * sizeof(float)) != hipSuccess)
     return fail(MOE_ENOMEM, "cannot allocate routing buffers for %lld tokens", (long long)T);
   c->cap_tokens = T;
   return MOE_OK;
@@ -850,11 +850,13 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
   if (!rc) rc = check_dev_error(c);
   if (rc) return rc;
   *out = c->stats[kind];
-  if (c->dev_lru && kind == MOE_KIND_COPY) {  // the copy kernel counts its own work
+  if (c->dev_lru && kind == MOE_KIND_COPY) {
+    // decode copies are counted by the copy kernel itself (their spans carry no
+    // count); prefill copies by their spans
     uint64_t acc[2];
     HIP_TRY(c, hipMemcpy(acc, c->dl_copy_acc, 16, hipMemcpyDeviceToHost));
-    out->launches = acc[0];
-    out->bytes = acc[1];
+    out->launches += acc[0];
+    out->bytes += acc[1];
   }
   return MOE_OK;
 }

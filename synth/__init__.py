@@ -122,3 +122,19 @@ def hidden(wl: Workload, rho=None, n_tokens=None):
     if rc != 0:
         raise ValueError("synth_hidden rejected the shape")
     return out
+
+
+def acceptance(n_steps, horizon, q, seed):
+    """Verification outcomes [n_steps, horizon] (bool) of draft tokens: draft j of step s
+    passes when u < q, u the uniform in [0, 1) made of the top 53 bits of word j % 4 of
+    Philox4x64-10 at counter (s, j // 4, 0, 0) under key(5, seed, 0, 0, 0)."""
+    k0 = key(5, seed, 0, 0, 0)
+    out = np.zeros((n_steps, horizon), bool)
+    for s in range(n_steps):
+        for c in range((horizon + 3) // 4):
+            words = philox4x64((s, c, 0, 0), (k0, 0))
+            for i, wv in enumerate(words):
+                j = 4 * c + i
+                if j < horizon:
+                    out[s, j] = (wv >> 11) * (1.0 / (1 << 53)) < q
+    return out

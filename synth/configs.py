@@ -1,4 +1,4 @@
-"""The five synthetic workloads of the expert-slot-cache MoE FFN, by name.
+"""The synthetic workloads of the expert-slot-cache MoE FFN, by name.
 
 Shapes stand in for the paper's GGUF model profiles (its model-profile
 table): an "A3B"-shaped Q8_0 stack, a Q4_0 stack and a tiny one-layer case.
@@ -29,6 +29,8 @@ class Workload:
     sweep_slots: Tuple[int, ...] = field(default=())
     sweep_rhos: Tuple[float, ...] = field(default=())
     cache_percent: float = 0.0  # the cache budget as a percentage of each layer's experts
+    horizon: int = 0            # verify mode: draft tokens per verification window (window = 1 + horizon)
+    accept_q: float = 0.0       # verify mode: probability that a draft token passes verification
 
     @property
     def block_bytes(self) -> int:
@@ -78,4 +80,11 @@ A3B_PREFILL = A3B_DECODE.with_(name="a3b_prefill", n_tokens=4096, rho=-1.0, budg
                                cache_percent=35,
                                hidden_seed=5, mode="prefill")
 
-WORKLOADS = {w.name: w for w in (TINY, A3B_DECODE, A3B_SWEEP, Q4_DECODE, A3B_PREFILL)}
+# Speculative verification windows through the A3B stack: 1 + 4 tokens per layer call, each
+# draft accepted with probability 0.75 until the first rejection; 25 % cache (32 slots), the
+# paper's setting for its speculative comparison.  Same weights and hidden-state stream as
+# a3b_decode (the first 96 states are the decode workload's).
+A3B_VERIFY = A3B_DECODE.with_(name="a3b_verify", budget_slots=32, cache_percent=25, horizon=4,
+                              accept_q=0.75, mode="verify")
+
+WORKLOADS = {w.name: w for w in (TINY, A3B_DECODE, A3B_SWEEP, Q4_DECODE, A3B_PREFILL, A3B_VERIFY)}

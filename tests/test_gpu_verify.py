@@ -1,0 +1,104 @@
+"""GPU parity of speculative verification windows (1 + horizon tokens per layer call, the
+multi-token path) through a residual + pre-norm layer stack:
+
+* every route of every window token on every layer against the oracle router on the same
+  layer input (near-ties exempt);
+* the slot trace and counters bit-exact against the oracle LRU stepped once per window
+  and layer with the union of the window's routed experts;
+* layer outputs (all calls at the small shape, sampled calls at full size) against the
+  bf16-weight oracle (the multi-token path's numerics).
+
+Windows follow the verification schedule of the seeded draft outcomes."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, oracle_layer_y,
+                        replay_trace, store_buffer, torch_cuda)
+from oracle.verify import schedule, window_union
+
+pytestmark = pytest.mark.gpu
+
+
+def verify_chain(wl, budget, store, n_check, seed):
+    torch = torch_cuda()
+    keep, ptr, arr = store
+    W = wl.horizon + 1
+    R = synth.router(wl)
+    Rd = torch.from_numpy(R).cuda()
+    X = synth.hidden(wl, n_tokens=wl.n_tokens + wl.horizon)
+    steps = schedule(wl.n_tokens, wl.horizon,
+                     synth.acceptance(wl.n_tokens, wl.horizon, wl.accept_q, wl.hidden_seed))
+    log(f"{wl.name}: C={budget} W={W}: {len(steps)} windows x {wl.n_layers} layers")
+    cache = make_cache(wl, ptr, budget, trace=True, residual=True, prenorm=True)
+    L = wl.n_layers
+    inputs = np.empty((len(steps), L + 1, W, wl.hidden), np.float32)
+    idx = np.empty((len(steps), L, W, wl.top_k), np.int32)
+    wts = np.empty((len(steps), L, W, wl.top_k), np.float32)
+    h = torch.empty((W, wl.hidden), dtype=torch.float32, device="cuda")
+    y = torch.empty_like(h)
+    for s, (t, _, _) in enumerate(steps):
+        h.copy_(torch.from_numpy(np.ascontiguousarray(X[t:t + W])))
+        for l in range(L):
+            inputs[s, l] = h.cpu().numpy()
+            _, i_, w_ = cache.layer_forward(h, Rd[l], l, y, n_tokens=W, routes=True)
+            idx[s, l], wts[s, l] = i_, w_
+            h, y = y, h
+        inputs[s, L] = h.cpu().numpy()
+    assert np.all(np.isfinite(inputs))
+    flips = {}
+    for s in range(len(steps)):
+        for l in range(L):
+            io, wo, z, fl = check_routes(inputs[s, l], R[l], wl.top_k, idx[s, l], wts[s, l],
+                                         prenorm=True)
+            if fl:
+                flips[(s, l)] = (io, wo, z, fl)
+    log(f"  near-tie flips: {len(flips)}; checking trace")
+    calls = [[window_union(idx[s, l]) for s in range(len(steps))] for l in range(L)]
+    recs, cnt = replay_trace(calls, wl, budget)
+    assert sorted(cache.read_trace()) == sorted(recs)   # records carry (layer, step)
+    assert cache.counters().as_tuple() == cnt.as_tuple()
+    rng = np.random.default_rng(seed)
+    picks = {(0, 0), (len(steps) - 1, L - 1)}
+    all_calls = [(s, l) for s in range(len(steps)) for l in range(L)]
+    if n_check >= len(all_calls):
+        picks = set(all_calls)
+    while len(picks) < min(n_check, len(all_calls)):
+        picks.add((int(rng.integers(len(steps))), int(rng.integers(L))))
+    worst = 0.0
+    for s, l in sorted(picks):
+        xin = inputs[s, l]
+        ymoe = inputs[s, l + 1].astype(np.float64) - xin.astype(np.float64)
+        io, wo, z, fl = flips.get((s, l), (None, None, None, []))
+        if io is None:
+            io, wo, z, fl = check_routes(xin, R[l], wl.top_k, idx[s, l], wts[s, l], prenorm=True)
+        yo = oracle_layer_y(xin, R[l], arr, wl, l, io, wo, z, idx[s, l], fl, bf16=True,
+                            prenorm=True)
+        worst = max(worst, check_y(ymoe, yo, f"window {s} layer {l}"))
+    c = cache.counters()
+    log(f"  ok: {len(picks)} calls checked, worst err/rms {worst:.2e}; hit rate "
+        f"{c.hits / max(1, c.hits + c.misses):.3f}, mean union {(c.hits + c.misses) / len(all_calls):.2f}")
+    cache.close()
+    return c, steps
+
+
+@pytest.mark.parametrize("qtype,budget,q", [("q8_0", 4, 0.6), ("q4_0", 6, 0.9), ("q8_0", 16, 0.0)])
+def test_verify_small(qtype, budget, q):
+    wl = synth.WORKLOADS["tiny"].with_(name="tiny_verify", qtype=qtype, n_layers=3, n_tokens=24,
+                                       horizon=4, accept_q=q, mode="verify")
+    st = store_buffer(wl)
+    try:
+        verify_chain(wl, budget, st, 10 ** 9, 1)
+    finally:
+        st[0].free()
+
+
+def test_a3b_verify_full_size():
+    wl = synth.WORKLOADS["a3b_verify"]
+    st = store_buffer(wl)
+    try:
+        c, steps = verify_chain(wl, wl.budget_slots, st, 16, 5)
+        assert sum(g for _, _, g in steps) == wl.n_tokens
+        assert c.materialized_bytes == c.misses * wl.payload_bytes
+    finally:
+        st[0].free()
