@@ -245,6 +245,20 @@ int moe_plan_percent(const moe_plan_in *in, double percent, int64_t context_toke
 int moe_plan_bytes(const moe_plan_in *in, uint64_t cache_bytes, int64_t context_tokens,
                    moe_plan_out *out);
 
+/* Offline bound on misses (no HIP dependency): Belady's MIN for per-call expert
+ * sets.  For one layer's recorded calls -- call i routes ids[offsets[i] ..
+ * offsets[i+1]) (any order, duplicates allowed, each id in [0, n_experts);
+ * offsets[0] = 0, n_calls + 1 entries) -- *misses gets the fewest misses any
+ * slot policy with n_slots slots can have from a cold cache, each call's
+ * distinct experts being resident together: on a miss with every slot taken,
+ * evict the resident outside the call whose next use is farthest ahead.  The
+ * paper asks for a policy that minimises latency under a memory budget (its
+ * Discussion); with slots that do not compete with host memory the latency
+ * of a call follows the bytes it materialises, which this bounds.  MOE_EINVAL
+ * on a bad argument or a call routing more than n_slots distinct experts. */
+int moe_policy_min(const int32_t *ids, const int64_t *offsets, int64_t n_calls, int32_t n_experts,
+                   int32_t n_slots, uint64_t *misses);
+
 /* The slot table alone, with no HIP dependency (used to check it on the CPU).
  * Same rule as inside moe_layer_forward: for one call with routed experts ids
  * (any order, duplicates allowed), stamp the distinct ids in ascending order,

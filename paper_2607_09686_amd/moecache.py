@@ -130,6 +130,7 @@ def lib():
         "moe_lru_destroy": ([vp], None),
         "moe_plan_percent": ([P(PlanIn), ctypes.c_double, i64, P(PlanOut)], ctypes.c_int),
         "moe_plan_bytes": ([P(PlanIn), u64, i64, P(PlanOut)], ctypes.c_int),
+        "moe_policy_min": ([P(i32), P(i64), i64, i32, i32, P(u64)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -342,3 +343,20 @@ def plan_bytes(model, cache_bytes, context_tokens=0):
     if rc != MOE_OK:
         raise MoeError(rc, "moe_plan_bytes: bad argument or size overflow")
     return out.as_dict()
+
+
+def min_misses(calls, n_experts, n_slots):
+    """Fewest misses any slot policy can have on one layer's calls (moe_policy_min); calls is a
+    sequence of id arrays, one per layer call."""
+    calls = [np.asarray(c, np.int32).ravel() for c in calls]
+    off = np.zeros(len(calls) + 1, np.int64)
+    off[1:] = np.cumsum([c.size for c in calls])
+    ids = np.concatenate(calls) if calls else np.zeros(1, np.int32)
+    ids = np.ascontiguousarray(ids, np.int32)
+    m = ctypes.c_uint64()
+    rc = lib().moe_policy_min(ids.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                              off.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), len(calls),
+                              n_experts, n_slots, ctypes.byref(m))
+    if rc != MOE_OK:
+        raise MoeError(rc, "moe_policy_min: bad argument or a call with more experts than slots")
+    return m.value
