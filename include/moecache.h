@@ -68,6 +68,14 @@ extern "C" {
 #define MOE_F_SPLIT_COPY 64u /* decode, default copy mode: the copy kernel and gate/up as
                                 two launches instead of one launch that copies the misses
                                 and runs gate/up for every routed expert (results equal) */
+/* Slot policy (default: least recently used, the rule of moe_lru_step): */
+#define MOE_F_SCORE_EVICT 128u /* a miss with every slot taken evicts the resident, outside
+                                  the call, whose router logit for the call's token is lowest
+                                  (ties: the higher id): the expert the current token wants
+                                  least, as a guess at the next token's routes.  Decode with
+                                  the default copy modes only: moe_cache_create rejects it with
+                                  MOE_F_SIDE_COPY / MOE_F_SDMA_COPY, and a multi-token call on
+                                  such a handle returns MOE_EINVAL */
 
 typedef struct moe_cache moe_cache; /* opaque, owned by the library */
 
@@ -176,6 +184,12 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out);
 /* With MOE_F_TIMING, bracket only one layer call in every `every` (>= 1,
  * default 1) with events, so the timing itself barely perturbs the run. */
 int moe_cache_set_timing_stride(moe_cache *c, int32_t every);
+
+/* Router logits of the last one-token call, z [n_experts] fp32 (host), as the
+ * slot-table step saw them (scaled by the MOE_F_PRENORM factor when set; zeros
+ * before the first call).  Decode with the default copy modes only, else
+ * MOE_EINVAL.  Synchronises with the handle's streams first. */
+int moe_cache_last_logits(moe_cache *c, float *z);
 
 /* Waits for the handle's work, frees everything the library allocated. NULL-safe. */
 void moe_cache_destroy(moe_cache *c);

@@ -18,6 +18,11 @@ token of the call (one lookup per distinct expert per call).
 
 One record (layer, step, expert, hit, slot, evicted-or--1) is emitted per e in
 S, in ascending expert order.
+
+Policy "score" (an alternative for one-token calls, not the paper's): the victim
+of rule 3 is instead the resident outside S whose router logit for the call's
+token is lowest (ties: the higher id) -- the expert the current token wants
+least, as a guess at the next token's routes.
 """
 from dataclasses import dataclass, field
 from typing import List
@@ -44,6 +49,7 @@ class LayerLRU:
     n_slots: int
     payload_bytes: int
     layer: int = 0
+    policy: str = "lru"       # "lru", or "score": see step()
     slot_of: List[int] = field(default_factory=list)
     expert_in: List[int] = field(default_factory=list)
     stamp: List[int] = field(default_factory=list)
@@ -64,12 +70,20 @@ class LayerLRU:
         self.step_no = 0
         self.counters = Counters()
 
-    def step(self, routed):
+    def step(self, routed, z=None):
         """Apply one layer call whose tokens routed the experts in ``routed``.
+
+        With policy "score" (one-token calls), ``z`` holds the token's router logits
+        for every expert, and the victim of a miss with every slot taken is the
+        resident outside the call with the lowest logit (ties: the higher id) instead
+        of the least recently used one.  Stamps are kept either way.
 
         Returns the list of records (layer, step, expert, hit, slot, evicted).
         """
         S = sorted(set(int(e) for e in routed))
+        if self.policy == "score":
+            if z is None or len(S) > self.n_slots:
+                raise ValueError("the score policy needs the logits and at most n_slots experts")
         for e in S:
             if not (0 <= e < self.n_experts):
                 raise ValueError("expert id out of range")
@@ -90,6 +104,12 @@ class LayerLRU:
             free = [s for s in range(self.n_slots) if self.expert_in[s] < 0]
             if free:
                 s, victim = free[0], -1
+            elif self.policy == "score":
+                victim = min((v for v in self.expert_in if v not in S),
+                             key=lambda v: (_logit_key(z[v]), -v))
+                s = self.slot_of[victim]
+                self.slot_of[victim] = -1
+                self.counters.evictions += 1
             else:
                 victim = min((self.expert_in[s] for s in range(self.n_slots)),
                              key=lambda v: self.stamp[v])
@@ -102,6 +122,12 @@ class LayerLRU:
         out = [(self.layer, self.step_no, e, int(hit[e]), rec[e][0], rec[e][1]) for e in S]
         self.step_no += 1
         return out
+
+
+def _logit_key(v):
+    """A logit as an eviction key: NaN ranks below every number (evicted first)."""
+    v = float(v)
+    return float("-inf") if v != v else v
 
 
 def simulate(calls, n_experts, n_slots, payload_bytes, layer=0):

@@ -49,6 +49,8 @@ struct LruDev {
   WorkList *work;
   int64_t P;
   int32_t C, layer;
+  float *zlast;    // [E], nullable: the call's logits are written here
+  int32_t policy;  // 0 least recently used, 1 lowest logit (MOE_F_SCORE_EVICT)
 };
 
 // Decode router: one token, two launches.  partial: [grid * E + 1] fp32 scratch.

@@ -245,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
   __shared__ int32_t selL[kMaxRouted], vicL[kMaxRouted], vslL[kMaxRouted];
   __shared__ float zselL[kMaxRouted];
   __shared__ int32_t cntL[2][kThreads / kWave];
-  __shared__ int64_t keyL[256];
+  __shared__ uint64_t keyL[256];  // eviction key of each slot's resident (candidates only)
   __shared__ int32_t badL;
   const int tid = threadIdx.x;
   const int phases = kThreads / E;
@@ -286,6 +286,7 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     z *= inv;
     zs[tid] = z;
     keyZ[tid] = rank_key(z, tid);
+    if (lru.zlast) lru.zlast[tid] = z;
   }
   __syncthreads();
   // rank of expert c over the experts [ph E / phases, (ph+1) E / phases)
@@ -353,7 +354,7 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     cntL[0][wv] = __popcll(bS);
     cntL[1][wv] = __popcll(bM);
   }
-  for (int sl = tid; sl < lru.C; sl += kThreads) keyL[sl] = INT64_MAX;
+  for (int sl = tid; sl < lru.C; sl += kThreads) keyL[sl] = UINT64_MAX;
   __syncthreads();
   int rS = __popcll(bS & lt), rM = __popcll(bM & lt), nM = 0;
 #pragma unroll
@@ -364,14 +365,17 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     }
     nM += cntL[1][v];
   }
-  if (cand) keyL[so] = st;
+  // victims in ascending key: the stamp (least recently used first), or the
+  // logit's rank key (lowest logit first, the higher id on a tie); unique keys
+  const uint64_t vkey = !cand ? 0ull : lru.policy ? keyZ[tid] : (uint64_t)st;
+  if (cand) keyL[so] = vkey;
   const int nfree = lru.C - (int)used;
   const int nev = max(0, nM - nfree);
   __syncthreads();
   bool evicted = false;
   if (cand && nev > 0) {
-    int cr = 0;  // residents outside S with an older stamp (stamps are unique)
-    for (int sl = 0; sl < lru.C; ++sl) cr += keyL[sl] < st ? 1 : 0;
+    int cr = 0;  // residents outside S evicted before this one
+    for (int sl = 0; sl < lru.C; ++sl) cr += keyL[sl] < vkey ? 1 : 0;
     if (cr < nev) {
       evicted = true;
       vicL[cr] = tid;

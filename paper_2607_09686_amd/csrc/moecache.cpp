@@ -93,6 +93,7 @@ struct moe_cache {
   int32_t *dl_trace = nullptr;      // [dl_trace_cap][6]
   uint64_t *dl_trace_n = nullptr;
   int32_t *dl_err = nullptr;
+  float *dl_zlast = nullptr;  // [E] logits of the last decode call
   uint64_t *dl_copy_acc = nullptr;  // [2] copies and bytes of the timed copy launches
   WorkList *dl_work = nullptr;
   int64_t dl_trace_cap = 0, dl_trace_pending = 0;
@@ -210,6 +211,8 @@ int check_desc(const moe_model_desc *d, int32_t budget) {
     return fail(MOE_EINVAL, "budget_slots %d outside [top_k=%d, n_experts=%d]", budget, d->top_k,
                 d->n_experts);
   if (!d->host_store) return fail(MOE_EINVAL, "host_store is NULL");
+  if ((d->flags & MOE_F_SCORE_EVICT) && (d->flags & (MOE_F_SIDE_COPY | MOE_F_SDMA_COPY)))
+    return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT needs the default copy modes (device slot tables)");
   return MOE_OK;
 }
 
@@ -246,6 +249,7 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->dl_trace);
   (void)hipFree(c->dl_trace_n);
   (void)hipFree(c->dl_err);
+  (void)hipFree(c->dl_zlast);
   (void)hipFree(c->dl_copy_acc);
   (void)hipFree(c->dl_work);
   if (c->dl_stage) (void)hipHostFree(c->dl_stage);
@@ -297,6 +301,7 @@ int alloc_dev_tables(moe_cache *c) {
       hipMalloc(&c->dl_stamp, L * E * 8) != hipSuccess || hipMalloc(&c->dl_meta, L * 3 * 8) != hipSuccess ||
       hipMalloc(&c->dl_cnt, L * 4 * 8) != hipSuccess || hipMalloc(&c->dl_trace_n, 8) != hipSuccess ||
       hipMalloc(&c->dl_err, 4) != hipSuccess || hipMalloc(&c->dl_copy_acc, 16) != hipSuccess ||
+      hipMalloc(&c->dl_zlast, E * 4) != hipSuccess ||
       hipMalloc(&c->dl_work, sizeof(WorkList)) != hipSuccess ||
       hipHostMalloc(&c->dl_stage, table_bytes(c), hipHostMallocDefault) != hipSuccess) {
     (void)hipGetLastError();
@@ -322,6 +327,7 @@ int clear_dev_tables(moe_cache *c) {
   HIP_TRY(c, hipMemsetAsync(c->dl_cnt, 0, L * 4 * 8, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_trace_n, 0, 8, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_err, 0, 4, c->main));
+  HIP_TRY(c, hipMemsetAsync(c->dl_zlast, 0, E * 4, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_copy_acc, 0, 16, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_work, 0, sizeof(WorkList), c->main));
   c->dl_trace_pending = 0;
@@ -387,6 +393,8 @@ LruDev dev_table(moe_cache *c, int32_t layer) {
   L.P = c->P;
   L.C = (int32_t)C;
   L.layer = layer;
+  L.zlast = c->dl_zlast;
+  L.policy = (c->d.flags & MOE_F_SCORE_EVICT) ? 1 : 0;
   return L;
 }
 
@@ -766,6 +774,8 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
   if (xb < yb + bytes && yb < xb + bytes) return fail(MOE_EINVAL, "y overlaps x");
   if (hipSetDevice(c->device) != hipSuccess) return fail(MOE_EHIP, "hipSetDevice failed");
   if (n_tokens == 1) return forward_decode(c, x, router_w, layer, y, delta, topk_idx, topk_w);
+  if (c->d.flags & MOE_F_SCORE_EVICT)
+    return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
   return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
 }
 
@@ -858,6 +868,16 @@ int moe_cache_kernel_stats(moe_cache *c, int32_t kind, moe_kernel_stats *out) {
     out->launches += acc[0];
     out->bytes += acc[1];
   }
+  return MOE_OK;
+}
+
+int moe_cache_last_logits(moe_cache *c, float *z) {
+  if (!c || !z) return fail(MOE_EINVAL, "NULL argument");
+  if (!c->dev_lru) return fail(MOE_EINVAL, "logits are kept by the device slot tables only");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  int rc = sync_dev(c);
+  if (rc) return rc;
+  HIP_TRY(c, hipMemcpy(z, c->dl_zlast, (size_t)c->d.n_experts * 4, hipMemcpyDeviceToHost));
   return MOE_OK;
 }
 

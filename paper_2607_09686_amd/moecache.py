@@ -18,7 +18,7 @@ LIB_PATH = os.environ.get("MOECACHE_LIB") or os.path.join(_HERE, "libmoecache.so
 MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
 MOE_Q8_0, MOE_Q4_0 = 8, 2
 MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING, MOE_F_PRENORM = 1, 2, 4, 8
-MOE_F_SIDE_COPY, MOE_F_SDMA_COPY, MOE_F_SPLIT_COPY = 16, 32, 64
+MOE_F_SIDE_COPY, MOE_F_SDMA_COPY, MOE_F_SPLIT_COPY, MOE_F_SCORE_EVICT = 16, 32, 64, 128
 COPY_MODES = {"kernel": 0, "split": MOE_F_SPLIT_COPY, "side": MOE_F_SIDE_COPY, "sdma": MOE_F_SDMA_COPY}
 KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY = 0, 1, 2, 3
 KIND_NAMES = {KIND_ROUTER: "router", KIND_GATEUP: "gateup", KIND_DOWN: "down", KIND_COPY: "copy"}
@@ -120,6 +120,7 @@ def lib():
         "moe_cache_kernel_stats": ([vp, i32, P(KernelStats)], ctypes.c_int),
         "moe_cache_destroy": ([vp], None),
         "moe_cache_set_timing_stride": ([vp, i32], ctypes.c_int),
+        "moe_cache_last_logits": ([vp, vp], ctypes.c_int),
         "moe_last_error": ([], ctypes.c_char_p),
         "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
         "moe_host_free": ([vp], ctypes.c_int),
@@ -197,11 +198,11 @@ class MoeCache:
 
     def __init__(self, n_layers, n_experts, top_k, hidden, inter, qtype, store_ptr, store_bytes,
                  budget_slots, stream=None, residual=False, trace=False, timing=False,
-                 prenorm=False, copy_mode="kernel"):
+                 prenorm=False, copy_mode="kernel", score_evict=False):
         self.hidden, self.n_experts, self.top_k = hidden, n_experts, top_k
         flags = (MOE_F_RESIDUAL if residual else 0) | (MOE_F_TRACE if trace else 0) | \
                 (MOE_F_TIMING if timing else 0) | (MOE_F_PRENORM if prenorm else 0) | \
-                COPY_MODES[copy_mode]
+                COPY_MODES[copy_mode] | (MOE_F_SCORE_EVICT if score_evict else 0)
         q = QTYPES[qtype] if isinstance(qtype, str) else int(qtype)
         self._desc = ModelDesc(n_layers, n_experts, top_k, hidden, inter, q, store_ptr, store_bytes,
                                _stream_handle(stream), flags)
@@ -256,6 +257,12 @@ class MoeCache:
 
     def reset(self):
         _check(lib().moe_cache_reset(self.handle))
+
+    def last_logits(self):
+        """Router logits [n_experts] of the last one-token call (moe_cache_last_logits)."""
+        z = np.empty(self.n_experts, np.float32)
+        _check(lib().moe_cache_last_logits(self.handle, z.ctypes.data))
+        return z
 
     def set_timing_stride(self, every):
         _check(lib().moe_cache_set_timing_stride(self.handle, every))

@@ -175,3 +175,57 @@ def test_rejects_bad_sizes():
         LayerLRU(8, 9, 1)
     with pytest.raises(ValueError):
         LayerLRU(8, 2, 1).step([8])
+
+
+def test_score_policy_hand_worked():
+    """Score eviction (one-token calls): the victim is the resident outside the call with the
+    lowest logit, the higher id on a tie.  Worked by hand:
+      call 0 routes {0, 1, 2}: three misses into slots 0, 1, 2;
+      call 1 routes {3} with z = (0.5, -1, 2, 3, 0, 0): residents 0, 1, 2 have logits
+             0.5, -1, 2, so expert 1 leaves slot 1 (LRU would evict expert 0);
+      call 2 routes {0, 4} with z = (9, 0, 1, 1, 5, 0): 0 hits; 4 misses; residents outside
+             the call are 2 and 3, both at logit 1: the higher id, 3, leaves slot 1."""
+    lru = LayerLRU(6, 3, 10, 0, policy="score")
+    assert lru.step([0, 1, 2], np.zeros(6)) == [(0, 0, 0, 0, 0, -1), (0, 0, 1, 0, 1, -1),
+                                               (0, 0, 2, 0, 2, -1)]
+    assert lru.step([3], np.array([0.5, -1.0, 2.0, 3.0, 0.0, 0.0])) == [(0, 1, 3, 0, 1, 1)]
+    assert lru.step([0, 4], np.array([9.0, 0.0, 1.0, 1.0, 5.0, 0.0])) == [
+        (0, 2, 0, 1, 0, -1), (0, 2, 4, 0, 1, 3)]
+    assert lru.counters.as_tuple() == (1, 5, 2, 50)
+
+
+def test_score_policy_with_recency_logits_is_lru():
+    """Fed 'logits' that rank the residents by their last use (z[v] = a clock value taken by
+    v at its last use, calls in order and ascending ids within a call), the score rule picks
+    the least recently used resident: records equal the LRU table's."""
+    rng = np.random.default_rng(17)
+    for _ in range(200):
+        E, C = int(rng.integers(4, 24)), 0
+        k = int(rng.integers(1, 5))
+        C = int(rng.integers(max(k, 1), E + 1))
+        lru = LayerLRU(E, C, 3, 2)
+        sc = LayerLRU(E, C, 3, 2, policy="score")
+        last, clock = np.full(E, -1.0), 0
+        for _ in range(int(rng.integers(1, 40))):
+            S = rng.choice(E, size=k, replace=False)
+            assert sc.step(S, last.copy()) == lru.step(S)
+            for e in sorted(S.tolist()):
+                clock += 1
+                last[e] = clock
+        assert sc.counters.as_tuple() == lru.counters.as_tuple()
+
+
+def test_score_policy_bounds_and_nan():
+    """Misses never below the offline bound; a NaN logit ranks lowest (evicted first)."""
+    from oracle.policy import min_misses
+    rng = np.random.default_rng(18)
+    for _ in range(100):
+        E, C, k = 16, int(rng.integers(2, 10)), 2
+        calls = [rng.choice(E, size=k, replace=False) for _ in range(50)]
+        sc = LayerLRU(E, C, 1, 0, policy="score")
+        for S in calls:
+            sc.step(S, rng.normal(size=E))
+        assert sc.counters.misses >= min_misses(calls, E, C)
+    sc = LayerLRU(4, 2, 1, 0, policy="score")
+    sc.step([0, 1], np.zeros(4))
+    assert sc.step([2], np.array([np.nan, 5.0, 0.0, 0.0]))[0][5] == 0
