@@ -144,9 +144,12 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
  *   y        device, [n_tokens][hidden] fp32, written; must not overlap x
  *   delta    host, nullable: this call's counter increments
  * n_tokens == 1 takes the decode path (GEMV kernels on fp32 activations held
- * as three int8 digits per value); n_tokens > 1 the prefill path (bf16 MFMA
- * grouped GEMM: weights rounded to bf16, x and the SwiGLU activations carried
- * as two bf16 terms, fp32 accumulation).
+ * as three int8 digits per value).  n_tokens > 1: the routed experts of all
+ * tokens go through the slot table once; then a call of at most 8 tokens whose
+ * distinct experts fit the slots runs the decode GEMVs once per token (same
+ * numerics as decode), and any other call the prefill path (bf16 MFMA grouped
+ * GEMM: weights rounded to bf16, x and the SwiGLU activations carried as two
+ * bf16 terms, fp32 accumulation).
  * Work is queued on desc.hip_stream and y is ready when that stream passes
  * this call.  Decode with the default copy kernel does not block the host:
  * the layer's slot table lives in device memory and is stepped by the

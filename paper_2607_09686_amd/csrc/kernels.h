@@ -74,6 +74,12 @@ int64_t router_zbuf_floats(int64_t T, int E);
 hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, int E, int k,
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s);
 
+// The decode GEMVs' input form for T tokens: digits xq [T][3][H] and block
+// scales xsc [T][H/32] of x_t * s_t (s_t = 1/rms of x_t when prenorm, else 1),
+// formed exactly as the decode router forms one token's.
+hipError_t launch_token_digits(const float *x, int T, int H, bool prenorm, int8_t *xq, float *xsc,
+                               hipStream_t s);
+
 // Prefill.  inv[t] = 1/rms (or 1) and xb [2][T][H] = x * inv as bf16 hi and lo terms.
 hipError_t launch_prefill_prep(const float *x, int T, int H, bool prenorm, float *inv, __bf16 *xb,
                                hipStream_t s);

@@ -212,6 +212,52 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
   if (blockIdx.x == 0 && tid == 0) partial[(int64_t)gridDim.x * E] = inv;
 }
 
+// The decode GEMVs' input for each of T tokens: s = 1/sqrt(mean(x_t^2) + 1e-6)
+// (or 1), formed as in router_partial_kernel, and the digits of x_t * s in
+// 32-wide blocks: xq [T][3][H], xsc [T][H/32].  Block (bx, t): token t's
+// values [1024 bx, 1024 bx + 1024), one octet of lanes per 32-wide block.
+__global__ __launch_bounds__(kThreads) void token_digits_kernel(const float *__restrict__ x, int H,
+                                                                int prenorm, int8_t *__restrict__ xq,
+                                                                float *__restrict__ xsc) {
+  __shared__ float wsum[kThreads / kWave];
+  const int tid = threadIdx.x, t = blockIdx.y;
+  const int H4 = H / 4;
+  const float4 *x4 = reinterpret_cast<const float4 *>(x + (int64_t)t * H);
+  float4 xa[kMaxX4];
+#pragma unroll
+  for (int m = 0; m < kMaxX4; ++m) {
+    const int i = tid + m * kThreads;
+    xa[m] = prenorm && i < H4 ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  const int q = blockIdx.x * kThreads + tid;  // this lane's float4
+  const float4 mine = q < H4 ? x4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+  float ss = 0.f;
+#pragma unroll
+  for (int m = 0; m < kMaxX4; ++m) {
+    ss = fmaf(xa[m].x, xa[m].x, ss);
+    ss = fmaf(xa[m].y, xa[m].y, ss);
+    ss = fmaf(xa[m].z, xa[m].z, ss);
+    ss = fmaf(xa[m].w, xa[m].w, ss);
+  }
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
+  if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
+  const float inv = prenorm ? 1.f / sqrtf(tot / (float)H + 1e-6f) : 1.f;
+  const float4 v = make_float4(mine.x * inv, mine.y * inv, mine.z * inv, mine.w * inv);
+  uint32_t dw[3];
+  const float sc = octet_digits(v, dw);  // all lanes (an octet never straddles the end: H % 32 == 0)
+  if (q < H4) {
+    int8_t *row = xq + (int64_t)t * 3 * H;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) reinterpret_cast<uint32_t *>(row + (int64_t)p * H)[q] = dw[p];
+    if ((tid & 7) == 0) xsc[(int64_t)t * (H / 32) + q / 8] = sc;
+  }
+}
+
 // Decode router, second kernel (one block): z = s * (sum of the partials in
 // block order); top-k + softmax; with lru.slot_of set, the layer's slot-table
 // step.  Every global load is issued up front (the table state included).
@@ -1974,6 +2020,13 @@ hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, in
 }
 
 int pf_max_experts() { return kPfMaxExperts; }
+hipError_t launch_token_digits(const float *x, int T, int H, bool prenorm, int8_t *xq, float *xsc,
+                               hipStream_t s) {
+  if (H % 64 || H > 4 * kMaxX4 * kThreads) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(token_digits_kernel, dim3((H / 4 + kThreads - 1) / kThreads, T), dim3(kThreads), 0,
+                     s, x, H, (int)prenorm, xq, xsc);
+  return hipGetLastError();
+}
 int router_slices(int T) { return T <= kPfTok ? 64 : (T <= 8 * kPfTok ? 16 : 4); }
 int64_t router_zbuf_floats(int64_t T, int E) {
   // the most any call of at most T tokens needs (slices * tokens is not monotonic in T)

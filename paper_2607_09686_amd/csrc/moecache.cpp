@@ -42,6 +42,10 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr int kCopyGrid = 64;  // copy-kernel blocks: enough requests in flight to fill PCIe
+// Multi-token calls of at most this many tokens whose routed experts all fit the
+// slots run the decode GEMVs once per token instead of the MFMA grouped GEMMs
+// (whose 128-row tiles would hold a handful of rows).
+constexpr int kSmallTokens = 8;
 
 struct TimedSpan {
   int kind;
@@ -79,6 +83,10 @@ struct moe_cache {
   __bf16 *pf_ab = nullptr;      // [2][T*k][I] (hi, lo)
   float *pf_P = nullptr;        // [T*k][H]
   int32_t *pf_host_off = nullptr;  // pinned [E+1]
+  // multi-token calls small enough for the decode GEMVs (one token at a time)
+  int8_t *st_xq = nullptr;          // [kSmallTokens][3][H] digits of each token
+  float *st_xsc = nullptr;          // [kSmallTokens][H/32]
+  int32_t *st_host_idx = nullptr;   // pinned [kSmallTokens][top_k] routes
   std::vector<hipEvent_t> pf_ev;   // per-chunk events (copy done, compute done)
   int8_t *hq = nullptr;   // decode: digits of the SwiGLU activations [3][k*I]
   float *hsc = nullptr;   //   their 16-wide block scales [k*I/16]
@@ -238,6 +246,9 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->pf_ab);
   (void)hipFree(c->pf_P);
   if (c->pf_host_off) (void)hipHostFree(c->pf_host_off);
+  if (c->st_host_idx) (void)hipHostFree(c->st_host_idx);
+  (void)hipFree(c->st_xq);
+  (void)hipFree(c->st_xsc);
   for (auto e : c->pf_ev) (void)hipEventDestroy(e);
   (void)hipFree(c->xq);
   (void)hipFree(c->xsc);
@@ -733,6 +744,10 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
       hipMalloc(&c->hds, 3 * (size_t)desc->top_k * desc->inter / 16 * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->xq, 3 * (size_t)desc->hidden) != hipSuccess ||
       hipMalloc(&c->xsc, (size_t)desc->hidden / 32 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->st_xq, (size_t)kSmallTokens * 3 * desc->hidden) != hipSuccess ||
+      hipMalloc(&c->st_xsc, (size_t)kSmallTokens * desc->hidden / 32 * sizeof(float)) != hipSuccess ||
+      hipHostMalloc(&c->st_host_idx, (size_t)kSmallTokens * desc->top_k * sizeof(int32_t),
+                    hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc(&c->host_idx, kMaxRouted * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->host_w, kMaxRouted * sizeof(float), hipHostMallocCoherent) != hipSuccess) {
     (void)hipGetLastError();
@@ -965,6 +980,96 @@ int ensure_prefill(moe_cache *c, int64_t T) {
   return MOE_OK;
 }
 
+// End of a multi-token call: routes out (debug), trace records, counter delta.
+int finish_multi(moe_cache *c, int32_t T, int32_t layer, const moe_counters &before,
+                 moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  const int k = c->d.top_k;
+  if (dbg_idx || dbg_w) {
+    if (dbg_idx)
+      HIP_TRY(c, hipMemcpyAsync(dbg_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t),
+                                hipMemcpyDeviceToHost, c->main));
+    if (dbg_w)
+      HIP_TRY(c, hipMemcpyAsync(dbg_w, c->topk_w, (size_t)T * k * sizeof(float), hipMemcpyDeviceToHost,
+                                c->main));
+    HIP_TRY(c, hipStreamSynchronize(c->main));
+  }
+  if (c->d.flags & MOE_F_TRACE) c->trace.insert(c->trace.end(), c->recs.begin(), c->recs.end());
+  if (delta) {
+    const moe_counters &a = c->lru[layer].counters();
+    *delta = moe_counters{a.hits - before.hits, a.misses - before.misses, a.evictions - before.evictions,
+                          a.materialized_bytes - before.materialized_bytes};
+  }
+  return MOE_OK;
+}
+
+// The FFN of a multi-token call of at most kSmallTokens tokens whose routed
+// experts all hold slots after this call's table step (so no slot is reused
+// inside the call): the misses' copies, then per token the decode GEMVs over
+// its own top_k experts (the digits of every token formed by one kernel), all
+// on the caller's stream; each token's output row is written by its down
+// launch (with the residual when asked), so no combine is needed.
+int small_call_ffn(moe_cache *c, const float *x, int32_t T, int32_t layer, float *y) {
+  const moe_model_desc &d = c->d;
+  const int k = d.top_k, E = d.n_experts, H = d.hidden, I = d.inter;
+  std::vector<int32_t> slot_of(E, -1);
+  std::vector<int> miss;
+  for (size_t i = 0; i < c->recs.size(); ++i) {
+    slot_of[c->recs[i].expert] = c->recs[i].slot;
+    if (!c->recs[i].hit) miss.push_back((int)i);
+  }
+  const int copy_cap = max_copy();
+  for (size_t m0 = 0; m0 < miss.size(); m0 += copy_cap) {
+    const int n = (int)std::min<size_t>(copy_cap, miss.size() - m0);
+    const uint8_t *src[256];
+    uint8_t *dst[256];
+    for (int q = 0; q < n; ++q) {
+      const moe_step_rec &r = c->recs[miss[m0 + q]];
+      src[q] = c->store + ((int64_t)layer * E + r.expert) * c->P;
+      dst[q] = c->slot_ptr(layer, r.slot);
+    }
+    Span sp(c, c->main, MOE_KIND_COPY, n, (uint64_t)n * c->P, 0);
+    if (d.flags & (MOE_F_SDMA_COPY | MOE_F_SIDE_COPY)) {
+      sp.record_start();
+      for (int q = 0; q < n; ++q)
+        HIP_TRY(c, hipMemcpyAsync(dst[q], src[q], c->P, hipMemcpyDefault, c->main));
+      sp.record_stop();
+    } else {
+      HIP_TRY(c, launch_materialize(src, dst, n, c->P, kCopyGrid, c->main, sp.timing()));
+    }
+    sp.end();
+  }
+  HIP_TRY(c, launch_token_digits(x, T, H, (d.flags & MOE_F_PRENORM) != 0, c->st_xq, c->st_xsc, c->main));
+  const int mode = (d.flags & MOE_F_RESIDUAL) ? 1 : 0;
+  for (int32_t tk = 0; tk < T; ++tk) {
+    ExpertList L{};
+    for (int j = 0; j < k; ++j) {
+      const int32_t e = c->st_host_idx[tk * k + j];
+      if (e < 0 || e >= E || slot_of[e] < 0) {
+        c->poisoned = true;
+        return fail(MOE_EHIP, "routes of a multi-token call name expert %d outside the table step", e);
+      }
+      L.payload[j] = c->slot_ptr(layer, slot_of[e]);
+      L.pos[j] = j;
+    }
+    L.n = k;
+    DecodeScratch St = c->scratch();
+    St.xq = c->st_xq + (int64_t)tk * 3 * H;
+    St.xsc = c->st_xsc + (int64_t)tk * (H / 32);
+    {
+      Span sp(c, c->main, MOE_KIND_GATEUP, 1, (uint64_t)k * 2 * c->M, 4ull * k * H * I);
+      HIP_TRY(c, launch_gateup(d.qtype, St, H, I, k, L, nullptr, c->main, sp.timing()));
+      sp.end();
+    }
+    {
+      Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * H * I);
+      HIP_TRY(c, launch_down(d.qtype, St, H, I, k, L, nullptr, c->topk_w + (int64_t)tk * k,
+                             x + (int64_t)tk * H, y + (int64_t)tk * H, mode, c->main, sp.timing()));
+      sp.end();
+    }
+  }
+  return MOE_OK;
+}
+
 // A multi-token layer call.  The routed experts S of all tokens go through the
 // slot table once.  The experts are then processed in chunks: the copy kernel
 // of a chunk's misses runs on the caller's stream while the MFMA GEMMs of
@@ -994,6 +1099,9 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   }
   HIP_TRY(c, hipMemcpyAsync(c->pf_host_off, c->pf_off, (E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
                             c->main));
+  if (T <= kSmallTokens)
+    HIP_TRY(c, hipMemcpyAsync(c->st_host_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t),
+                              hipMemcpyDeviceToHost, c->main));
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
   HIP_TRY(c, hipEventSynchronize(c->ev_route));
   if (d.flags & MOE_F_TIMING) {
@@ -1017,6 +1125,11 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   const moe_counters before = t.counters();
   c->recs.clear();
   t.step(S.data(), (int32_t)S.size(), c->recs);
+  if (T <= kSmallTokens && (int)S.size() <= c->C) {
+    rc = small_call_ffn(c, x, T, layer, y);
+    if (rc) return rc;
+    return finish_multi(c, T, layer, before, delta, dbg_idx, dbg_w);
+  }
 
   // chunks of record indices: the hits first (no copy), then the misses in order
   struct Chunk {
@@ -1118,22 +1231,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   }
   if (!chunks.empty()) HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * chunks.size() - 1], 0));
   HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
-  if (dbg_idx || dbg_w) {
-    if (dbg_idx)
-      HIP_TRY(c, hipMemcpyAsync(dbg_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t),
-                                hipMemcpyDeviceToHost, c->main));
-    if (dbg_w)
-      HIP_TRY(c, hipMemcpyAsync(dbg_w, c->topk_w, (size_t)T * k * sizeof(float), hipMemcpyDeviceToHost,
-                                c->main));
-    HIP_TRY(c, hipStreamSynchronize(c->main));
-  }
-  if (d.flags & MOE_F_TRACE) c->trace.insert(c->trace.end(), c->recs.begin(), c->recs.end());
-  if (delta) {
-    const moe_counters &a = t.counters();
-    *delta = moe_counters{a.hits - before.hits, a.misses - before.misses, a.evictions - before.evictions,
-                          a.materialized_bytes - before.materialized_bytes};
-  }
-  return MOE_OK;
+  return finish_multi(c, T, layer, before, delta, dbg_idx, dbg_w);
 }
 
 // Prefill runs the layer's slot table on the host: with device tables, move

@@ -1,6 +1,7 @@
-"""GPU parity of the prefill path (many tokens per layer call): bf16 MFMA grouped
-GEMMs compared with the bf16-emulating oracle; routes, waves of slot reuse inside a
-call (more routed experts than slots), trace and counters exact."""
+"""GPU parity of the multi-token path (many tokens per layer call): bf16 MFMA grouped
+GEMMs compared with the bf16-weight oracle, and calls of at most 8 tokens whose routed
+experts fit the slots (decode GEMVs per token) with the exact oracle; routes, waves of
+slot reuse inside a call (more routed experts than slots), trace and counters exact."""
 import numpy as np
 import pytest
 
@@ -8,7 +9,7 @@ import synth
 from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, softmax_of, store_buffer,
                         torch_cuda)
 from oracle import router as oracle_router
-from oracle.layer import Shape, moe_layer_bf16, rms_normalize
+from oracle.layer import Shape, moe_layer, moe_layer_bf16, rms_normalize
 from oracle.lru import LayerLRU
 
 pytestmark = pytest.mark.gpu
@@ -20,8 +21,18 @@ def oracle_routes(x, wr, k, prenorm):
     return z, idx, w, gap
 
 
-def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens=None):
-    """Routes of every token, y of `tokens` (default all) against the bf16 oracle."""
+SMALL_TOKENS = 8  # calls this small whose routed experts fit the slots run the decode GEMVs
+
+
+def gemv_call(T, idx, budget):
+    """Whether a multi-token call takes the per-token decode GEMVs (fp32-accurate) instead of
+    the bf16 MFMA GEMMs."""
+    return T <= SMALL_TOKENS and len(np.unique(idx)) <= budget
+
+
+def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens=None, budget=None):
+    """Routes of every token, y of `tokens` (default all) against the oracle of the path the
+    call takes (bf16 weights for the MFMA GEMMs, exact for the decode GEMVs)."""
     z, idx, w, gap = oracle_routes(x, wr, wl.top_k, prenorm)
     flips = 0
     idx_use, w_use = idx.copy(), w.copy()
@@ -32,8 +43,10 @@ def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens
             w_use[t] = softmax_of(z[t], idx_g[t])
             flips += 1
     toks = list(range(x.shape[0])) if tokens is None else list(tokens)
-    yo = moe_layer_bf16(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
-                        prenorm=prenorm)["y"][toks]
+    exact = budget is not None and gemv_call(x.shape[0], idx_g, budget)
+    fn = moe_layer if exact else moe_layer_bf16
+    yo = fn(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
+            prenorm=prenorm)["y"][toks]
     yg = y_g[toks].astype(np.float64)
     if residual:
         yg = yg - x[toks].astype(np.float64)
@@ -60,7 +73,8 @@ def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=Non
             delta, idx, w = cache.layer_forward(x, torch.from_numpy(R[l]).cuda(), l, y,
                                                 n_tokens=T, routes=True)
             torch.cuda.synchronize()
-            flips, err = check_call(X, R[l], arr, wl, l, idx, w, y.cpu().numpy(), prenorm, residual)
+            flips, err = check_call(X, R[l], arr, wl, l, idx, w, y.cpu().numpy(), prenorm, residual,
+                                    budget=budget)
             worst = max(worst, err)
             want.extend(lrus[l].step(np.unique(idx)))
             assert delta.materialized_bytes == delta.misses * wl.payload_bytes
@@ -118,6 +132,18 @@ def test_prefill_and_decode_share_slot_tables():
 def test_prefill_small(qtype, T, budget):
     wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, name="tiny_pf")
     run_prefill(wl, max(budget, wl.top_k), T)
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("T,budget", [(3, 6), (5, 10), (8, 16), (8, 5), (9, 16)])
+def test_small_calls_both_paths(qtype, T, budget):
+    """Calls of up to 8 tokens whose experts fit the slots (decode GEMVs), and calls just past
+    either limit (MFMA): 8 tokens with 5 slots, 9 tokens."""
+    # (H, I as in the warm-cache test below: large enough that a bf16 rounding flip on the
+    # MFMA side stays far below the tolerance)
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, n_layers=2, hidden=1024, inter=384,
+                                       name="tiny_small")
+    run_prefill(wl, budget, T, calls=3, prenorm=True, residual=True, seed_shift=T)
 
 
 def test_prefill_warm_cache_prenorm_residual_multilayer():
@@ -181,7 +207,8 @@ def test_a3b_prefill_full_size():
     for l in sorted(check_layers):
         toks = sorted(rng.choice(T, size=6, replace=False).tolist())
         xin, idx, w = routes[l]
-        _, err = check_call(xin, R[l], arr, wl, l, idx, w, outputs[l], True, True, tokens=toks)
+        _, err = check_call(xin, R[l], arr, wl, l, idx, w, outputs[l], True, True, tokens=toks,
+                            budget=wl.budget_slots)
         worst = max(worst, err)
     log(f"  ok: worst err/rms {worst:.2e}; counters {cache.counters()}")
     cache.close()
