@@ -145,4 +145,13 @@ hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, in
 hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, uint64_t *acc,
                                    hipStream_t s, const Timing &t = {});
 
+// One layer's slot table to / from a pinned host staging buffer of
+// table_stage_bytes(E, C) bytes (stamp [E] i64 | meta [3] i64 | cnt [4] u64 |
+// err i32 | pad | slot_of [E] i32 | expert_in [C] i32), one kernel each way;
+// the pack also copies the device error word.
+size_t table_stage_bytes(int E, int C);
+hipError_t launch_table_pack(const LruDev &L, int E, int C, const int32_t *err, uint8_t *stage,
+                             hipStream_t s);
+hipError_t launch_table_unpack(const LruDev &L, int E, int C, const uint8_t *stage, hipStream_t s);
+
 }  // namespace moecache

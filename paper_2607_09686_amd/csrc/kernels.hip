@@ -546,7 +546,14 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float *__rest
   const float sc = tscale ? tscale[t] : 1.f;
   for (int e = lane; e < E; e += kWave) {
     float v = 0.f;
-    for (int sl = 0; sl < slices; ++sl) v += zp[((int64_t)sl * T + t) * E + e];
+    for (int s0 = 0; s0 < slices; s0 += 16) {  // 16 slices in flight, added in slice order
+      float p[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        p[j] = s0 + j < slices ? zp[((int64_t)(s0 + j) * T + t) * E + e] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v += p[j];
+    }
     zs[wave][e] = v * sc;
   }
   wave_topk(zs[wave], E, k, idx + (int64_t)t * k, w + (int64_t)t * k, nullptr, nullptr);

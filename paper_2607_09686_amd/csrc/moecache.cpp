@@ -106,6 +106,7 @@ struct moe_cache {
   WorkList *dl_work = nullptr;
   int64_t dl_trace_cap = 0, dl_trace_pending = 0;
   uint8_t *dl_stage = nullptr;      // pinned staging of one layer's table
+  bool table_pulled = false;        // a multi-token call holds the layer's table on the host
   int32_t *host_idx = nullptr;  // host mirrors [k] (decode)
   float *host_w = nullptr;
   hipEvent_t ev_route = nullptr, ev_copy = nullptr;
@@ -300,10 +301,6 @@ int ensure_tokens(moe_cache *c, int64_t T) {
 
 constexpr int64_t kTraceCap = 1 << 16;  // device trace records kept between drains
 
-size_t table_bytes(const moe_cache *c) {
-  const int64_t E = c->d.n_experts;
-  return (size_t)(4 * E + 4 * c->C + 8 * E + 8 * 3 + 8 * 4);
-}
 
 int alloc_dev_tables(moe_cache *c) {
   const int64_t L = c->d.n_layers, E = c->d.n_experts, C = c->C;
@@ -314,7 +311,8 @@ int alloc_dev_tables(moe_cache *c) {
       hipMalloc(&c->dl_err, 4) != hipSuccess || hipMalloc(&c->dl_copy_acc, 16) != hipSuccess ||
       hipMalloc(&c->dl_zlast, E * 4) != hipSuccess ||
       hipMalloc(&c->dl_work, sizeof(WorkList)) != hipSuccess ||
-      hipHostMalloc(&c->dl_stage, table_bytes(c), hipHostMallocDefault) != hipSuccess) {
+      hipHostMalloc(&c->dl_stage, table_stage_bytes((int)E, (int)C), hipHostMallocDefault) !=
+          hipSuccess) {
     (void)hipGetLastError();
     return fail(MOE_ENOMEM, "cannot allocate the device slot tables");
   }
@@ -409,24 +407,31 @@ LruDev dev_table(moe_cache *c, int32_t layer) {
   return L;
 }
 
-// Copy a layer's device table into the host table (synchronises first).
-int pull_table(moe_cache *c, int32_t layer) {
-  int rc = drain_dev_trace(c);
-  if (!rc) rc = sync_dev(c);
-  if (rc) return rc;
-  const LruDev L = dev_table(c, layer);
+// A multi-token call steps the layer's table on the host.  The pull is queued
+// behind the call's routing (one kernel writes the table and the device error
+// word into the pinned staging) and read once the routing has been waited for;
+// the push writes the staging and queues one kernel that copies it back.
+int pull_table_queue(moe_cache *c, int32_t layer) {
+  HIP_TRY(c, launch_table_pack(dev_table(c, layer), c->d.n_experts, c->C, c->dl_err, c->dl_stage,
+                               c->main));
+  return MOE_OK;
+}
+
+// After the caller's stream has passed the pack: the staging into the host table.
+int pull_table_load(moe_cache *c, int32_t layer) {
   const int64_t E = c->d.n_experts, C = c->C;
+  const uint8_t *p = c->dl_stage;
+  const int64_t *stamp = reinterpret_cast<const int64_t *>(p), *meta = stamp + E;
+  const uint64_t *cnt = reinterpret_cast<const uint64_t *>(meta + 3);
+  const int32_t *err = reinterpret_cast<const int32_t *>(cnt + 4), *so = err + 2, *ei = so + E;
+  if (*err) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "router produced expert id %d (non-finite logits?)", (int16_t)(*err - 1));
+  }
   SlotLru::State st;
-  st.slot_of.resize(E);
-  st.expert_in.resize(C);
-  std::vector<int64_t> stamp(E), meta(3);
-  std::vector<uint64_t> cnt(4);
-  HIP_TRY(c, hipMemcpy(st.slot_of.data(), L.slot_of, E * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(c, hipMemcpy(st.expert_in.data(), L.expert_in, C * 4, hipMemcpyDeviceToHost));
-  HIP_TRY(c, hipMemcpy(stamp.data(), L.stamp, E * 8, hipMemcpyDeviceToHost));
-  HIP_TRY(c, hipMemcpy(meta.data(), L.meta, 3 * 8, hipMemcpyDeviceToHost));
-  HIP_TRY(c, hipMemcpy(cnt.data(), L.cnt, 4 * 8, hipMemcpyDeviceToHost));
-  st.stamp.assign(stamp.begin(), stamp.end());
+  st.slot_of.assign(so, so + E);
+  st.expert_in.assign(ei, ei + C);
+  st.stamp.assign(stamp, stamp + E);
   st.clock = (uint64_t)meta[0];
   st.step = (int32_t)meta[1];
   st.used = (int32_t)meta[2];
@@ -435,18 +440,13 @@ int pull_table(moe_cache *c, int32_t layer) {
   return MOE_OK;
 }
 
-// Queue the host table of a layer back to the device (pinned staging; the
-// next pull synchronises before the staging is reused).
 int push_table(moe_cache *c, int32_t layer) {
-  const LruDev L = dev_table(c, layer);
   const int64_t E = c->d.n_experts, C = c->C;
   const SlotLru::State st = c->lru[layer].state();
   uint8_t *p = c->dl_stage;
-  int32_t *so = reinterpret_cast<int32_t *>(p), *ei = so + E;
-  int64_t *stamp = reinterpret_cast<int64_t *>(p + 4 * E + 4 * C), *meta = stamp + E;
+  int64_t *stamp = reinterpret_cast<int64_t *>(p), *meta = stamp + E;
   uint64_t *cnt = reinterpret_cast<uint64_t *>(meta + 3);
-  std::copy(st.slot_of.begin(), st.slot_of.end(), so);
-  std::copy(st.expert_in.begin(), st.expert_in.end(), ei);
+  int32_t *so = reinterpret_cast<int32_t *>(cnt + 4) + 2, *ei = so + E;
   for (int64_t e = 0; e < E; ++e) stamp[e] = (int64_t)st.stamp[e];
   meta[0] = (int64_t)st.clock;
   meta[1] = st.step;
@@ -455,11 +455,10 @@ int push_table(moe_cache *c, int32_t layer) {
   cnt[1] = st.cnt.misses;
   cnt[2] = st.cnt.evictions;
   cnt[3] = st.cnt.materialized_bytes;
-  HIP_TRY(c, hipMemcpyAsync(L.slot_of, so, E * 4, hipMemcpyHostToDevice, c->main));
-  HIP_TRY(c, hipMemcpyAsync(L.expert_in, ei, C * 4, hipMemcpyHostToDevice, c->main));
-  HIP_TRY(c, hipMemcpyAsync(L.stamp, stamp, E * 8, hipMemcpyHostToDevice, c->main));
-  HIP_TRY(c, hipMemcpyAsync(L.meta, meta, 3 * 8, hipMemcpyHostToDevice, c->main));
-  HIP_TRY(c, hipMemcpyAsync(L.cnt, cnt, 4 * 8, hipMemcpyHostToDevice, c->main));
+  std::copy(st.slot_of.begin(), st.slot_of.end(), so);
+  std::copy(st.expert_in.begin(), st.expert_in.end(), ei);
+  (void)C;
+  HIP_TRY(c, launch_table_unpack(dev_table(c, layer), (int)E, c->C, c->dl_stage, c->main));
   return MOE_OK;
 }
 
@@ -1102,8 +1101,13 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   if (T <= kSmallTokens)
     HIP_TRY(c, hipMemcpyAsync(c->st_host_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t),
                               hipMemcpyDeviceToHost, c->main));
+  if (c->dev_lru && (rc = pull_table_queue(c, layer))) return rc;
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
   HIP_TRY(c, hipEventSynchronize(c->ev_route));
+  if (c->dev_lru) {
+    if ((rc = pull_table_load(c, layer))) return rc;
+    c->table_pulled = true;
+  }
   if (d.flags & MOE_F_TIMING) {
     rc = drain_timing(c);
     if (rc) return rc;
@@ -1238,10 +1242,14 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
 // the table to the host for the call and queue it back afterwards.
 int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
                     moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
-  int rc = c->dev_lru ? pull_table(c, layer) : MOE_OK;
+  // the trace kept on the device is moved out before the host table adds records;
+  // the table itself is pulled behind the call's routing (forward_prefill_impl) and
+  // pushed back only if it was pulled
+  int rc = c->dev_lru ? drain_dev_trace(c) : MOE_OK;
   if (rc) return rc;
+  c->table_pulled = false;
   rc = forward_prefill_impl(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
-  if (c->dev_lru) {
+  if (c->dev_lru && c->table_pulled) {
     const int rc2 = push_table(c, layer);
     if (!rc) rc = rc2;
   }
