@@ -43,6 +43,7 @@ extern "C" {
 #define MOE_ENOMEM (-2) /* device or pinned-host allocation failed */
 #define MOE_EHIP (-3)   /* a HIP runtime call failed (text in moe_last_error) */
 #define MOE_ESTATE (-4) /* handle poisoned by an earlier MOE_EHIP */
+#define MOE_EIO (-5)    /* a file could not be opened, read or written */
 
 /* Block formats of the expert weights (GGUF-style, 32 weights per block).
  * Q8_0: 34 bytes = fp16 scale d (little-endian) + 32 int8 q; weight d*q.
@@ -275,6 +276,30 @@ int moe_plan_bytes(const moe_plan_in *in, uint64_t cache_bytes, int64_t context_
  * on a bad argument or a call routing more than n_slots distinct experts. */
 int moe_policy_min(const int32_t *ids, const int64_t *offsets, int64_t n_calls, int32_t n_experts,
                    int32_t n_slots, uint64_t *misses);
+
+/* Split-pack of a GGUF MoE model (no HIP dependency; the paper's Split-Pack
+ * Representation section): the routed expert tensors of every layer l,
+ * blk.l.ffn_{gate,up,down}_exps.weight (Q8_0 or Q4_0; dims (H, I, E), (H, I, E),
+ * (I, H, E), innermost first), are cut into one block per (layer, expert) and
+ * written to pack_path in the store layout of moe_model_desc.host_store:
+ * payload (l, e) at (l * n_experts + e) * P, [W_gate | W_up | W_down], bytes
+ * unchanged.  index_path gets one JSON line with the topology, one per block
+ * (layer, expert, offset and bytes in the pack, the source offset and bytes of
+ * each of the three matrices, an FNV-1a 64-bit digest of the block) and a last
+ * line with the block count, the pack size and a digest of the block digests.
+ * router_path (nullable) gets the routers, blk.l.ffn_gate_inp.weight (F32, F16
+ * or BF16, dims (H, E)), as fp32 [n_layers][hidden][n_experts], the router_w
+ * form of moe_layer_forward.  info gets the topology (top_k from the metadata
+ * key *.expert_used_count, 0 if absent).  GGUF versions 2 and 3.  MOE_EINVAL
+ * on a malformed file, missing or inconsistent tensors or another block type;
+ * MOE_EIO when a file cannot be opened, read or written. */
+typedef struct {
+  int32_t n_layers, n_experts, top_k, hidden, inter, qtype;
+  uint64_t payload_bytes; /* P */
+  uint64_t pack_bytes;    /* n_layers * n_experts * P */
+} moe_pack_info;
+int moe_pack_gguf(const char *gguf_path, const char *pack_path, const char *index_path,
+                  const char *router_path, moe_pack_info *info);
 
 /* The slot table alone, with no HIP dependency (used to check it on the CPU).
  * Same rule as inside moe_layer_forward: for one call with routed experts ids

@@ -28,8 +28,13 @@
 using namespace moecache;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
+
+// The message moe_last_error returns, set by the library's other translation units.
+void moecache_set_last_error(const char *msg) { g_err = msg; }
+
+namespace {
 
 int fail(int code, const char *fmt, ...) {
   char buf[512];

@@ -15,7 +15,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # MOECACHE_LIB: an alternative build of the library to load instead of the in-tree one
 LIB_PATH = os.environ.get("MOECACHE_LIB") or os.path.join(_HERE, "libmoecache.so")
 
-MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE = 0, -1, -2, -3, -4
+MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE, MOE_EIO = 0, -1, -2, -3, -4, -5
 MOE_Q8_0, MOE_Q4_0 = 8, 2
 MOE_F_RESIDUAL, MOE_F_TRACE, MOE_F_TIMING, MOE_F_PRENORM = 1, 2, 4, 8
 MOE_F_SIDE_COPY, MOE_F_SDMA_COPY, MOE_F_SPLIT_COPY, MOE_F_SCORE_EVICT = 16, 32, 64, 128
@@ -78,6 +78,13 @@ class PlanOut(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_ if f != "pad"}
 
 
+class PackInfo(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("qtype", ctypes.c_int32), ("payload_bytes", ctypes.c_uint64),
+                ("pack_bytes", ctypes.c_uint64)]
+
+
 _lib = None
 
 
@@ -132,6 +139,7 @@ def lib():
         "moe_plan_percent": ([P(PlanIn), ctypes.c_double, i64, P(PlanOut)], ctypes.c_int),
         "moe_plan_bytes": ([P(PlanIn), u64, i64, P(PlanOut)], ctypes.c_int),
         "moe_policy_min": ([P(i32), P(i64), i64, i32, i32, P(u64)], ctypes.c_int),
+        "moe_pack_gguf": ([ctypes.c_char_p] * 4 + [P(PackInfo)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -367,3 +375,12 @@ def min_misses(calls, n_experts, n_slots):
     if rc != MOE_OK:
         raise MoeError(rc, "moe_policy_min: bad argument or a call with more experts than slots")
     return m.value
+
+
+def pack_gguf(gguf_path, pack_path, index_path, router_path=None):
+    """Split-pack a GGUF MoE model (moe_pack_gguf).  Returns the topology as a dict."""
+    info = PackInfo()
+    enc = lambda p: None if p is None else os.fsencode(p)
+    _check(lib().moe_pack_gguf(enc(gguf_path), enc(pack_path), enc(index_path), enc(router_path),
+                               ctypes.byref(info)))
+    return {f: getattr(info, f) for f, _ in info._fields_}
