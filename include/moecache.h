@@ -150,7 +150,8 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
  * distinct experts fit the slots runs the decode GEMVs once per token (same
  * numerics as decode), and any other call the prefill path (bf16 MFMA grouped
  * GEMM: weights rounded to bf16, x and the SwiGLU activations carried as two
- * bf16 terms, fp32 accumulation).
+ * bf16 terms, fp32 accumulation); there n_tokens * max(hidden, top_k * inter)
+ * must be <= 2^34 (MOE_EINVAL otherwise).
  * Work is queued on desc.hip_stream and y is ready when that stream passes
  * this call.  Decode with the default copy kernel does not block the host:
  * the layer's slot table lives in device memory and is stepped by the

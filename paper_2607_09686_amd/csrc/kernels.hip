@@ -1568,54 +1568,70 @@ struct PfGateUpParams {
   int T, pairs, H, I, k;
 };
 
+// MFMA operand of v_mfma_f32_16x16x32_bf16 read straight from global memory:
+// lane l holds row l % 16 of a 16-row subtile and k = 8 * (l / 16) .. +7 of a
+// 32-wide k slice (16 bytes).  Activation rows are private to the wave that
+// multiplies them, so they skip LDS; only the dequantised weight tile, which
+// all four waves read, is staged there (37 KB, two blocks per CU).
+typedef __attribute__((address_space(1))) const bf16x8 g_bf16x8;
+
+// The K loop of both grouped GEMMs, two K steps of 64 per trip with a
+// one-step-ahead prefetch into registers (A: activation fragments, B: the
+// raw weight blocks of the next step) and a double-buffered LDS weight tile.
+// Loads are issued unconditionally (the last trip reloads step KT-1) so that
+// the wait counts the compiler places are exact; the scheduling barriers keep
+// the loads ahead of the MFMAs and the dequantisation after them.
+#define PF_K_LOOP(KT, GLOAD, MMA, DEQ)              \
+  do {                                              \
+    GLOAD(0, A0, B0);                               \
+    DEQ(B0, 0);                                     \
+    __syncthreads();                                \
+    int kt_ = 0;                                    \
+    for (; kt_ + 2 <= (KT); kt_ += 2) {             \
+      GLOAD(kt_ + 1, A1, B1);                       \
+      __builtin_amdgcn_sched_barrier(0);            \
+      MMA(A0, 0);                                   \
+      __builtin_amdgcn_sched_barrier(0);            \
+      DEQ(B1, 1);                                   \
+      __syncthreads();                              \
+      GLOAD(min(kt_ + 2, (KT) - 1), A0, B0);        \
+      __builtin_amdgcn_sched_barrier(0);            \
+      MMA(A1, 1);                                   \
+      __builtin_amdgcn_sched_barrier(0);            \
+      DEQ(B0, 0);                                   \
+      __syncthreads();                              \
+    }                                               \
+    if (kt_ < (KT)) MMA(A0, 0);                     \
+  } while (0)
+
 // grid: (M-tiles of the wave's experts, I / 64).  256 threads = 4 waves; wave w
-// owns tile rows [32w, 32w+32) (two 16-row MFMA tiles) and all 4+4 16-column
-// tiles of gate and up.  K loop over H in steps of 64 (one weight pair).
+// owns tile rows [32w, 32w+32) (two 16-row MFMA subtiles) and all 4+4
+// 16-column subtiles of gate and up.  K loop over H in steps of 64 (one
+// weight pair per row).  Rows past the expert's count read its last row and
+// are not stored.
 template <int QT>
-__global__ __launch_bounds__(kThreads) void pf_gateup_kernel(PfGateUpParams a) {
-  __shared__ __align__(16) __bf16 As[2][2][kPfBM][kPfLd];  // [buffer][hi, lo]
-  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];       // rows 0..63 gate, 64..127 up
+__global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a) {
+  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];  // rows 0..63 gate, 64..127 up
   constexpr int BB = Fmt<QT>::kBlockBytes;
   int j, m0;
   if (!pf_tile(a.X, blockIdx.x, j, m0)) return;
   const int n0 = blockIdx.y * 64;
   const int n = a.X.n[j], row0 = a.X.row0[j];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int nb = a.H / 32;
-  const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
-  const int64_t lo_off = (int64_t)a.T * a.H;
-  // A: 4 chunks of 16 bytes per thread per plane; B: one 32-weight block per thread
+  const int64_t rowb = (int64_t)(a.H / 32) * BB, mat = (int64_t)a.I * rowb;
   const int brow = tid >> 1, bhalf = tid & 1;
   const uint8_t *bptr = a.X.payload[j] + (brow >= 64 ? mat : 0) + (int64_t)(n0 + (brow & 63)) * rowb;
-  int arow_tok[4];
+  // activations in 16-byte units (the launch checks that 32 bits index them)
+  g_bf16x8 *xb = (g_bf16x8 *)a.xb;
+  const uint32_t lo16 = (uint32_t)((int64_t)a.T * a.H / 8);
+  uint32_t arow[2];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int ch = tid + c * kThreads, r = ch >> 3;
-    arow_tok[c] = m0 + r < n ? a.perm[row0 + m0 + r] / a.k : -1;
+  for (int i = 0; i < 2; ++i) {
+    const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
+    arow[i] = (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)(a.H / 8) + (lane >> 4);
   }
-  uint4 av[2][4];
-  uint32_t bv[9];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ch = tid + c * kThreads, c16 = ch & 7;
-      const int64_t o = (int64_t)arow_tok[c] * a.H + kt * kPfBK + 8 * c16;
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-        av[pl][c] = arow_tok[c] >= 0 ? *reinterpret_cast<const uint4 *>(a.xb + pl * lo_off + o)
-                                     : make_uint4(0, 0, 0, 0);
-    }
-    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, bv);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl) *reinterpret_cast<uint4 *>(&As[buf][pl][r][8 * c16]) = av[pl][c];
-    }
-    dequant_half<QT>(bv, bhalf, &Bs[buf][brow][32 * bhalf]);
-  };
+  bf16x8 A0[2][2][2], A1[2][2][2];  // [plane][i][ks]
+  uint32_t B0[9], B1[9];
   f32x4 accg[2][4], accu[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -1624,37 +1640,36 @@ __global__ __launch_bounds__(kThreads) void pf_gateup_kernel(PfGateUpParams a) {
       accg[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
       accu[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-  const int KT = a.H / kPfBK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+  auto gload = [&](int kt, bf16x8 (&A)[2][2][2], uint32_t (&Bv)[9]) {
+    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, Bv);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 bg[4], bu[4];
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          A[pl][i][ks] = xb[arow[i] + pl * lo16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+  };
+  // for each k slice and column subtile: hi then lo plane, both row subtiles
+  auto mma = [&](const bf16x8 (&A)[2][2][2], int buf) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        bg[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
-        bu[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][64 + 16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
-      }
+        const int c = 32 * ks + 8 * (lane >> 4);
+        const bf16x8 bg = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][c]);
+        const bf16x8 bu = *reinterpret_cast<const bf16x8 *>(&Bs[buf][64 + 16 * q + (lane & 15)][c]);
 #pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
+        for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
-              &As[buf][pl][32 * wv + 16 * i + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bg[q], accg[i][q], 0, 0, 0);
-            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bu[q], accu[i][q], 0, 0, 0);
+          for (int i = 0; i < 2; ++i) {
+            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bg, accg[i][q], 0, 0, 0);
+            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bu, accu[i][q], 0, 0, 0);
           }
-        }
-    }
-    if (kt + 1 < KT) lstore(buf ^ 1);
-    __syncthreads();
-  }
+      }
+  };
+  auto deq = [&](const uint32_t (&Bv)[9], int buf) { dequant_half<QT>(Bv, bhalf, &Bs[buf][brow][32 * bhalf]); };
+  PF_K_LOOP(a.H / kPfBK, gload, mma, deq);
   // C layout (16x16): lane holds rows 4*(lane/16) + r, column lane % 16
   const int64_t plane = (int64_t)a.pairs * a.I;
 #pragma unroll
@@ -1665,8 +1680,7 @@ __global__ __launch_bounds__(kThreads) void pf_gateup_kernel(PfGateUpParams a) {
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
         if (m < n) {
-          const float g = accg[i][q][r], u = accu[i][q][r];
-          const float v = silu(g) * u;
+          const float v = silu(accg[i][q][r]) * accu[i][q][r];
           const __bf16 hi = (__bf16)v;
           const int64_t o = (int64_t)(row0 + m) * a.I + n0 + 16 * q + (lane & 15);
           a.ab[o] = hi;
@@ -1684,11 +1698,12 @@ struct PfDownParams {
   int pairs, H, I;
 };
 
-// grid: (M-tiles, H / 128).  Wave w owns rows [32w, 32w+32) and the 8
-// 16-column tiles; K loop over I in steps of 64.
+// grid: (M-tiles, ceil(H / 128)).  Wave w owns rows [32w, 32w+32) and the 8
+// 16-column subtiles; K loop over I in steps of 64.  A last tile of 64
+// columns (H an odd multiple of 64) reads weight row H-1 for the missing
+// rows and stores only its first 64 columns.
 template <int QT>
-__global__ __launch_bounds__(kThreads) void pf_down_kernel(PfDownParams a) {
-  __shared__ __align__(16) __bf16 As[2][2][kPfBM][kPfLd];
+__global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
   __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];
   constexpr int BB = Fmt<QT>::kBlockBytes;
   int j, m0;
@@ -1696,84 +1711,77 @@ __global__ __launch_bounds__(kThreads) void pf_down_kernel(PfDownParams a) {
   const int n0 = blockIdx.y * 128;
   const int n = a.X.n[j], row0 = a.X.row0[j];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int nbI = a.I / 32;
-  const int64_t rowb = (int64_t)nbI * BB;
+  const int64_t rowb = (int64_t)(a.I / 32) * BB;
   const int64_t mat = (int64_t)a.I * ((int64_t)(a.H / 32) * BB);
-  const int64_t plane = (int64_t)a.pairs * a.I;
   const int brow = tid >> 1, bhalf = tid & 1;
-  const uint8_t *bptr = a.X.payload[j] + 2 * mat + (int64_t)(n0 + brow) * rowb;
-  bool arow_ok[4];
+  const uint8_t *bptr = a.X.payload[j] + 2 * mat + (int64_t)min(n0 + brow, a.H - 1) * rowb;
+  g_bf16x8 *ab = (g_bf16x8 *)a.ab;
+  const uint32_t pl16 = (uint32_t)((int64_t)a.pairs * a.I / 8);
+  uint32_t arow[2];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) arow_ok[c] = m0 + ((tid + c * kThreads) >> 3) < n;
-  uint4 av[2][4];
-  uint32_t bv[9];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
-      const int64_t o = (int64_t)(row0 + m0 + r) * a.I + kt * kPfBK + 8 * c16;
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-        av[pl][c] = arow_ok[c] ? *reinterpret_cast<const uint4 *>(a.ab + pl * plane + o)
-                               : make_uint4(0, 0, 0, 0);
-    }
-    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, bv);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ch = tid + c * kThreads, r = ch >> 3, c16 = ch & 7;
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl) *reinterpret_cast<uint4 *>(&As[buf][pl][r][8 * c16]) = av[pl][c];
-    }
-    dequant_half<QT>(bv, bhalf, &Bs[buf][brow][32 * bhalf]);
-  };
+  for (int i = 0; i < 2; ++i) {
+    const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
+    arow[i] = (uint32_t)(row0 + m) * (uint32_t)(a.I / 8) + (lane >> 4);
+  }
+  bf16x8 A0[2][2][2], A1[2][2][2];
+  uint32_t B0[9], B1[9];
   f32x4 acc[2][8];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int KT = a.I / kPfBK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+  auto gload = [&](int kt, bf16x8 (&A)[2][2][2], uint32_t (&Bv)[9]) {
+    load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, Bv);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 bf[8];
+    for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
-      for (int q = 0; q < 8; ++q)
-        bf[q] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
+        for (int ks = 0; ks < 2; ++ks)
+          A[pl][i][ks] = ab[arow[i] + pl * pl16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+  };
+  auto mma = [&](const bf16x8 (&A)[2][2][2], int buf) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
-              &As[buf][pl][32 * wv + 16 * i + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
-            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[q], acc[i][q], 0, 0, 0);
-        }
-    }
-    if (kt + 1 < KT) lstore(buf ^ 1);
-    __syncthreads();
-  }
+      for (int q = 0; q < 8; ++q) {
+        const bf16x8 bf =
+            *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bf, acc[i][q], 0, 0, 0);
+      }
+  };
+  auto deq = [&](const uint32_t (&Bv)[9], int buf) { dequant_half<QT>(Bv, bhalf, &Bs[buf][brow][32 * bhalf]); };
+  PF_K_LOOP(a.I / kPfBK, gload, mma, deq);
+  // the lane's 8 output rows: pair ids, then their weights (two round trips)
+  int pair[2][4];
+  float wt[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      pair[i][r] = a.perm[row0 + min(m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r, n - 1)];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wt[i][r] = a.w[pair[i][r]];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
       if (m < n) {
-        const int pair = a.perm[row0 + m];
-        const float wt = a.w[pair];
-        float *dst = a.P + (int64_t)pair * a.H + n0 + (lane & 15);
+        float *dst = a.P + (int64_t)pair[i][r] * a.H + n0 + (lane & 15);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) dst[16 * q] = wt * acc[i][q][r];
+        for (int q = 0; q < 8; ++q)
+          if (n0 + 16 * q < a.H) dst[16 * q] = wt[i][r] * acc[i][q][r];
       }
     }
 }
+#undef PF_K_LOOP
 
 // y[t] = (x[t] if residual) + sum_j P[t*k + j], j = 0..k-1 in rank order.
 __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__restrict__ P,
@@ -1984,6 +1992,8 @@ hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, con
   a.I = I;
   a.k = k;
   if (tiles == 0) return hipSuccess;
+  // the kernel indexes the activation planes in 16-byte units with 32 bits
+  if (2 * (int64_t)T * H / 8 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   dim3 grid(tiles, I / 64);
   if (qtype == 8)
     hipExtLaunchKernelGGL(pf_gateup_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
@@ -2012,7 +2022,8 @@ hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const
   a.H = H;
   a.I = I;
   if (tiles == 0) return hipSuccess;
-  dim3 grid(tiles, H / 128);
+  if (2 * (int64_t)pairs * I / 8 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  dim3 grid(tiles, (H + 127) / 128);
   if (qtype == 8)
     hipExtLaunchKernelGGL(pf_down_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
   else

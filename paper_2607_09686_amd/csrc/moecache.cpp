@@ -793,6 +793,9 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
   if (xb < yb + bytes && yb < xb + bytes) return fail(MOE_EINVAL, "y overlaps x");
   if (hipSetDevice(c->device) != hipSuccess) return fail(MOE_EHIP, "hipSetDevice failed");
   if (n_tokens == 1) return forward_decode(c, x, router_w, layer, y, delta, topk_idx, topk_w);
+  // the grouped GEMMs index their bf16 hi/lo activation planes in 16-byte units with 32 bits
+  if ((int64_t)n_tokens * std::max<int64_t>(c->d.hidden, (int64_t)c->d.top_k * c->d.inter) > (1ll << 34))
+    return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
   return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);

@@ -153,7 +153,9 @@ def test_prefill_warm_cache_prenorm_residual_multilayer():
     run_prefill(wl, 5, 200, calls=3, prenorm=True, residual=True)
 
 
-@pytest.mark.parametrize("shape", [(1024, 384, 40, 6, 9, 260), (768, 1408, 64, 8, 20, 96)])
+# 1088 = 17 x 64: the down GEMM's last 128-column tile holds 64 columns
+@pytest.mark.parametrize("shape", [(1024, 384, 40, 6, 9, 260), (768, 1408, 64, 8, 20, 96),
+                                   (1088, 320, 24, 4, 7, 180)])
 def test_prefill_other_shapes(shape):
     H, I, E, k, C, T = shape
     for qt in ("q8_0", "q4_0"):
