@@ -33,6 +33,25 @@ struct WorkList {
   ExpertList list;  // the k routed experts in rank order (n = 0 after a routing error)
 };
 
+// Work of a small multi-token call (T <= kMtTokens tokens whose routed
+// experts all fit the slots), written on the device by the slot-table step:
+// the misses' copies in ascending expert order and, per token, the slots of
+// its k experts in rank order.
+constexpr int kMtTokens = 8;
+constexpr int kMtMaxCopy = kMtTokens * kMaxRouted;
+constexpr int kMtParts = 16;  // router partial blocks per token of such a call
+struct MtWork {
+  int32_t n_copy, n_union;
+  const uint8_t *src[kMtMaxCopy];
+  uint8_t *dst[kMtMaxCopy];
+  ExpertList list[kMtTokens];
+  // the union's experts in ascending id: slot, the number of tokens routing
+  // to it and their positions q = t * k + j (token t, rank j), ascending t
+  const uint8_t *upay[kMtMaxCopy];
+  uint8_t unt[kMtMaxCopy];
+  uint8_t uq[kMtMaxCopy][kMtTokens];
+};
+
 // Device-resident slot table of one layer (the rule of slot_lru.h) and where
 // a call's results go.  trace: 6 int32 per record (moe_step_rec), nullable.
 struct LruDev {
@@ -64,6 +83,39 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 int32_t *idx, float *w, int32_t *host_idx, float *host_w, int8_t *xq,
                                 float *xsc, bool prenorm, const LruDev *lru, hipStream_t s,
                                 const Timing &t = {});
+
+// Router of a small multi-token call with the layer's table on the device
+// (lru.slot_of set, 1 <= T <= kMtTokens): per token, the decode router's
+// partials over at most kMtParts blocks of rows, s and digits (partial: T
+// regions of at most kMtParts * E + 1 floats; xq [T][3][H], xsc [T][H/32])
+// and routes idx / w [T][k]; then one
+// table step over the union of the routed experts, written to mw, unless
+// that union exceeds the slots.  flag[0] (host memory) becomes 0 (done), 1
+// (union too large: table untouched, mw empty) or 2 (routing failure);
+// flag[1] the union's size.
+hipError_t launch_router_small(const float *x, const float *wr, int T, int H, int E, int k, float *partial,
+                               int32_t *idx, float *w, int8_t *xq, float *xsc, bool prenorm,
+                               const LruDev &lru, MtWork *mw, int32_t *flag, hipStream_t s,
+                               const Timing &t = {});
+
+// The FFN of a small multi-token call from its work list, each union expert's
+// weights read once: gate/up for all the tokens routing to an expert
+// (activations at position q = t*k + j of hq [3][T*k*I], hsc [T*k*I/16], hds
+// [3][T*k*I/16]), down into R [T*k][H] (unweighted rows), then y_t =
+// (x_t if mode 1) + sum over j in rank order of w[t*k+j] R[t*k+j].  The
+// numerics are those of the decode GEMVs (launch_gateup / launch_down per
+// token).  umax: an upper bound on the union size (the grids); false from
+// mt_ffn_fits: a shape these kernels do not take.
+bool mt_ffn_fits(int H, int I, int T);
+size_t mt_gateup_lds(int H, int T);
+hipError_t launch_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc, int8_t *hq,
+                            float *hsc, int32_t *hds, int H, int I, int k, int T, int umax,
+                            hipStream_t s, const Timing &t = {});
+hipError_t launch_down_mt(int qtype, const MtWork *W, const int8_t *hq, const float *hsc,
+                          const int32_t *hds, float *R, int H, int I, int k, int T, int umax,
+                          hipStream_t s, const Timing &t = {});
+hipError_t launch_combine_mt(const float *R, const float *w, const float *x, float *y, int H, int k,
+                             int T, int mode, hipStream_t s, const Timing &t = {});
 
 // Prefill router: partial logits over router_slices(T) slices of H into
 // z [slices][T][E] (router_zbuf_floats(T, E) floats cover any call of at most
@@ -143,6 +195,8 @@ hipError_t launch_materialize(const uint8_t *const *src, uint8_t *const *dst, in
 // The copies a device work list names (n_copy of them); acc (nullable) gets
 // += copies, += bytes.
 hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, uint64_t *acc,
+                                   hipStream_t s, const Timing &t = {});
+hipError_t launch_materialize_list(const MtWork *w, int64_t bytes, int grid, uint64_t *acc,
                                    hipStream_t s, const Timing &t = {});
 
 // One layer's slot table to / from a pinned host staging buffer of

@@ -143,31 +143,44 @@ constexpr int kRouterRowsPerBlock = 32;
 
 constexpr int kMaxX4 = 8;  // H <= 8192
 
-// Decode router, first kernel: block b accumulates z over rows [32b, 32b+32)
+// Decode router, first kernel: block (b, t) accumulates token t's z over rows [rpb b, rpb b + rpb)
 // of W_r into partial[b][E] (no cross-block communication inside a launch:
 // on a multi-XCD GPU a device-scope fence costs more than a second launch).
 // Every block also forms s = 1/sqrt(mean(x^2) + 1e-6) (or 1) from the whole x,
 // in the same order, so all blocks hold the same s; block b writes the digits
 // of its 32-wide block of x * s, and block 0 writes s at partial[nb * E].
 __global__ __launch_bounds__(kThreads) void router_partial_kernel(
-    const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int prenorm,
+    const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int prenorm, int rpb,
     float *__restrict__ partial, int8_t *__restrict__ xq, float *__restrict__ xsc) {
   __shared__ float red[kThreads];
   __shared__ float wsum[kThreads / kWave];
+  {  // token blockIdx.y of a multi-token call: its own x row, partials, s and digits
+    const int t = blockIdx.y;
+    x += (int64_t)t * H;
+    partial += (int64_t)t * ((int64_t)gridDim.x * E + 1);
+    xq += (int64_t)t * 3 * H;
+    xsc += (int64_t)t * (H / 32);
+  }
   const int tid = threadIdx.x;
   const int phases = kThreads / E;  // E <= 256
   const int c = tid % E, ph = tid / E;
-  const int r0 = blockIdx.x * kRouterRowsPerBlock;
-  const int r1 = min(H, r0 + kRouterRowsPerBlock);
+  const int r0 = blockIdx.x * rpb;
+  const int r1 = min(H, r0 + rpb);
   const int H4 = H / 4;
   const float4 *x4 = reinterpret_cast<const float4 *>(x);
-  float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+  float acc = 0.f;
+  for (int q0 = r0; q0 < r1; q0 += kRouterRowsPerBlock) {  // 32-row pieces (one for decode)
+    const int q1 = min(r1, q0 + kRouterRowsPerBlock);
+    float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
 #pragma unroll
-  for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
-    const int r = r0 + ph + phases * j;
-    const bool ok = ph < phases && r < r1;
-    xv[j] = ok ? x[r] : 0.f;
-    wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
+    for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
+      const int r = q0 + ph + phases * j;
+      const bool ok = ph < phases && r < q1;
+      xv[j] = ok ? x[r] : 0.f;
+      wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
   }
   float4 xa[kMaxX4];
 #pragma unroll
@@ -175,10 +188,8 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
     const int i = tid + m * kThreads;
     xa[m] = prenorm && i < H4 ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  const float4 mine = tid < 8 ? x4[r0 / 4 + tid] : make_float4(0.f, 0.f, 0.f, 0.f);
-  float acc = 0.f;
-#pragma unroll
-  for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
+  const int oct = (r1 - r0) / 32;  // the block's 32-wide blocks of x, one octet of lanes each
+  const float4 mine = tid < 8 * oct ? x4[r0 / 4 + tid] : make_float4(0.f, 0.f, 0.f, 0.f);
   float ss = 0.f;
 #pragma unroll
   for (int m = 0; m < kMaxX4; ++m) {
@@ -201,13 +212,13 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
     for (int p = 0; p < phases; ++p) sum += red[p * E + tid];
     partial[blockIdx.x * E + tid] = sum;
   }
-  if (tid < 8) {  // one octet: the block's 32 values
+  if (tid < 8 * oct) {  // octet o: values r0 + 32 o .. + 31
     const float4 v = make_float4(mine.x * inv, mine.y * inv, mine.z * inv, mine.w * inv);
     uint32_t dw[3];
     const float sc = octet_digits(v, dw);
 #pragma unroll
     for (int p = 0; p < 3; ++p) reinterpret_cast<uint32_t *>(xq + (int64_t)p * H + r0)[tid] = dw[p];
-    if (tid == 0) xsc[blockIdx.x] = sc;
+    if ((tid & 7) == 0) xsc[r0 / 32 + tid / 8] = sc;
   }
   if (blockIdx.x == 0 && tid == 0) partial[(int64_t)gridDim.x * E] = inv;
 }
@@ -258,23 +269,9 @@ __global__ __launch_bounds__(kThreads) void token_digits_kernel(const float *__r
   }
 }
 
-// Decode router, second kernel (one block): z = s * (sum of the partials in
-// block order); top-k + softmax; with lru.slot_of set, the layer's slot-table
-// step.  Every global load is issued up front (the table state included).
-//
-// Top-k by rank: expert e is chosen iff fewer than k experts beat it in the
-// (logit descending, id ascending) order, and its rank is its position.  The
-// order is that of one 64-bit key per expert: the order-preserving bit image
-// of the logit (NaN taken as -inf, -0 as +0) above 255 - id.  A non-finite
-// chosen logit is a routing failure.
-//
-// Slot-table step (one thread per expert): the same rule as the host table
-// (stamp the routed set S in ascending order; a routed expert holding a slot
-// is a hit; misses in ascending order take the lowest free slot, else the
-// slot of the resident expert with the smallest stamp).  Stamps are unique
-// and all of S is stamped after every other resident, so the victims are the
-// oldest residents outside S, in stamp order, for the misses beyond the free
-// slots in expert order.
+// Order-preserving 64-bit rank key of expert e with logit z: the bit image of
+// z (NaN taken as -inf, -0 as +0) above 255 - e, so that a larger key means a
+// larger logit, then a lower id.
 __device__ __forceinline__ uint64_t rank_key(float z, int e) {
   z = z != z ? -INFINITY : z + 0.f;
   uint32_t u = __float_as_uint(z);
@@ -282,20 +279,219 @@ __device__ __forceinline__ uint64_t rank_key(float z, int e) {
   return ((uint64_t)u << 8) | (uint64_t)(255 - e);
 }
 
-__global__ __launch_bounds__(kThreads) void router_finish_kernel(
-    const float *__restrict__ partial, int nb, int E, int k, int32_t *idx, float *w,
-    int32_t *host_idx, float *host_w, LruDev lru) {
-  __shared__ float red[kThreads];
-  __shared__ float zs[256];
-  __shared__ uint64_t keyZ[256];
-  __shared__ int32_t selL[kMaxRouted], vicL[kMaxRouted], vslL[kMaxRouted];
-  __shared__ float zselL[kMaxRouted];
-  __shared__ int32_t cntL[2][kThreads / kWave];
-  __shared__ uint64_t keyL[256];  // eviction key of each slot's resident (candidates only)
-  __shared__ int32_t badL;
+// One token's routing inside a one-block finishing kernel (all threads; the
+// token's logits z = s * (sum of the partials in block order) with s at
+// partial[nb * E]).  Top-k by rank: expert e is chosen iff fewer than k
+// experts have a larger rank key, and its rank is its position.  Writes the
+// chosen ids and the softmax over their logits to idx / w [k] (and the
+// optional mirrors), the chosen ids to sel [k], keyZ [E] and zlast [E]
+// (nullable); returns the rank of expert tid (E for tid >= E) and sets *bad
+// when a chosen logit is not finite.
+struct RouteLds {
+  float red[kThreads];
+  float zs[256];
+  uint64_t keyZ[256];
+  float zsel[kMaxRouted];
+};
+__device__ __forceinline__ int route_sum(float sacc, float inv, int E, int k, int32_t *idx, float *w,
+                                         int32_t *host_idx, float *host_w, float *zlast, int32_t *sel,
+                                         int32_t *bad, RouteLds &sh) {
   const int tid = threadIdx.x;
   const int phases = kThreads / E;
   const int c = tid % E, ph = tid / E;
+  sh.red[tid] = sacc;
+  __syncthreads();
+  if (tid < E) {
+    float z = 0.f;
+    for (int p = 0; p < phases; ++p) z += sh.red[p * E + tid];
+    z *= inv;
+    sh.zs[tid] = z;
+    sh.keyZ[tid] = rank_key(z, tid);
+    if (zlast) zlast[tid] = z;
+  }
+  __syncthreads();
+  // rank of expert c over the experts [ph E / phases, (ph+1) E / phases)
+  {
+    int r = 0;
+    if (ph < phases) {
+      const uint64_t kc = sh.keyZ[c];
+      const int f0 = ph * E / phases, f1 = (ph + 1) * E / phases;
+      int f = f0;
+      for (; f + 8 <= f1; f += 8) {  // eight independent LDS reads per step
+        uint64_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = sh.keyZ[f + j];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r += v[j] > kc ? 1 : 0;
+      }
+      for (; f < f1; ++f) r += sh.keyZ[f] > kc ? 1 : 0;
+    }
+    __syncthreads();
+    sh.red[tid] = __int_as_float(r);
+  }
+  __syncthreads();
+  int rank = E;
+  if (tid < E) {
+    rank = 0;
+    for (int p = 0; p < phases; ++p) rank += __float_as_int(sh.red[p * E + tid]);
+    if (rank < k) {
+      sel[rank] = tid;
+      sh.zsel[rank] = sh.zs[tid];
+    }
+  }
+  __syncthreads();
+  if (tid < kWave) {  // softmax over the chosen logits (the first is the largest)
+    const bool ok = __ballot(tid < k && !isfinite(sh.zsel[tid < k ? tid : 0])) == 0;
+    const float ex = tid < k && ok ? expf(sh.zsel[tid] - sh.zsel[0]) : 0.f;
+    float sum = ex;
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+    if (tid < k) {
+      const int32_t id = ok ? sel[tid] : 0x7fffffff;
+      const float wi = ok ? ex / sum : 0.f;
+      idx[tid] = id;
+      w[tid] = wi;
+      if (host_idx) host_idx[tid] = id;
+      if (host_w) host_w[tid] = wi;
+    }
+    if (tid == 0 && !ok) *bad = 1;
+  }
+  return rank;
+}
+__device__ __forceinline__ int route_token(const float *__restrict__ partial, int nb, int E, int k,
+                                           int32_t *idx, float *w, int32_t *host_idx, float *host_w,
+                                           float *zlast, int32_t *sel, int32_t *bad, RouteLds &sh) {
+  const int tid = threadIdx.x;
+  const int phases = kThreads / E;
+  const int c = tid % E, ph = tid / E;
+  const float inv = partial[(int64_t)nb * E];
+  const int per = (nb + phases - 1) / phases;
+  float sacc = 0.f;
+  if (ph < phases) {
+    const int b0 = ph * per, b1 = min(nb, b0 + per);
+    for (int b = b0; b < b1; b += 48) {  // one round trip up to 48 partials per lane
+      float v[48];
+#pragma unroll
+      for (int j = 0; j < 48; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 48; ++j) sacc += v[j];
+    }
+  }
+  return route_sum(sacc, inv, E, k, idx, w, host_idx, host_w, zlast, sel, bad, sh);
+}
+
+// Slot-table step of one layer call inside a one-block kernel (all threads;
+// thread tid < E is expert tid, inS marks the call's routed set S).  The rule
+// of the host table: stamp S in ascending order; a routed expert holding a
+// slot is a hit; misses in ascending order take the lowest free slot, else
+// the slot of the resident outside S with the smallest eviction key (the
+// stamp: least recently used first; or, with lru.policy, the current rank key
+// zkey: lowest logit first, the higher id on a tie).  Stamps are unique and S
+// is stamped after every other resident, so the victims are the residents
+// outside S in key order, for the misses beyond the free slots in expert
+// order.  Writes the table, the counters, the clock and the trace records;
+// returns this expert's miss flag, final slot, rank among the misses and the
+// number of misses.  |S| <= C.
+struct StepLds {
+  int32_t cnt[2][kThreads / kWave];
+  uint64_t key[256];  // eviction key of each slot's resident (candidates only)
+  int32_t vic[256], vsl[256];
+};
+struct StepResult {
+  bool miss;
+  int fs, rS, rM, nM;
+};
+__device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool inS, int so, int64_t st,
+                                                 uint64_t zkey, int64_t clock0, int64_t step,
+                                                 int64_t used, uint64_t tn, StepLds &sh) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const bool miss = inS && so < 0;
+  const bool cand = tid < E && so >= 0 && !inS;
+  const uint64_t bS = __ballot(inS), bM = __ballot(miss), lt = (1ull << lane) - 1ull;
+  if (lane == 0) {
+    sh.cnt[0][wv] = __popcll(bS);
+    sh.cnt[1][wv] = __popcll(bM);
+  }
+  for (int sl = tid; sl < lru.C; sl += kThreads) sh.key[sl] = UINT64_MAX;
+  __syncthreads();
+  int rS = __popcll(bS & lt), rM = __popcll(bM & lt), nM = 0, nS = 0;
+#pragma unroll
+  for (int v = 0; v < kThreads / kWave; ++v) {
+    if (v < wv) {
+      rS += sh.cnt[0][v];
+      rM += sh.cnt[1][v];
+    }
+    nS += sh.cnt[0][v];
+    nM += sh.cnt[1][v];
+  }
+  const uint64_t vkey = !cand ? 0ull : lru.policy ? zkey : (uint64_t)st;
+  if (cand) sh.key[so] = vkey;
+  const int nfree = lru.C - (int)used;
+  const int nev = max(0, nM - nfree);
+  __syncthreads();
+  bool evicted = false;
+  if (cand && nev > 0) {
+    int cr = 0;  // residents outside S evicted before this one
+    for (int sl = 0; sl < lru.C; ++sl) cr += sh.key[sl] < vkey ? 1 : 0;
+    if (cr < nev) {
+      evicted = true;
+      sh.vic[cr] = tid;
+      sh.vsl[cr] = so;
+    }
+  }
+  __syncthreads();
+  int fs = so, fev = -1;
+  if (miss) {
+    if (rM < nfree) {
+      fs = (int)used + rM;
+    } else {
+      fs = sh.vsl[rM - nfree];
+      fev = sh.vic[rM - nfree];
+    }
+  }
+  if (evicted) lru.slot_of[tid] = -1;
+  if (inS) {
+    lru.stamp[tid] = clock0 + rS + 1;
+    if (miss) {
+      lru.slot_of[tid] = fs;
+      lru.expert_in[fs] = tid;
+    }
+    if (lru.trace) {
+      int32_t *r = lru.trace + 6 * (int64_t)(tn + rS);
+      r[0] = lru.layer;
+      r[1] = (int32_t)step;
+      r[2] = tid;
+      r[3] = miss ? 0 : 1;
+      r[4] = fs;
+      r[5] = fev;
+    }
+  }
+  if (tid == 0) {
+    lru.cnt[0] += (uint64_t)(nS - nM);
+    lru.cnt[1] += (uint64_t)nM;
+    lru.cnt[2] += (uint64_t)nev;
+    lru.cnt[3] += (uint64_t)nM * (uint64_t)lru.P;
+    lru.meta[0] = clock0 + nS;
+    lru.meta[1] = step + 1;
+    lru.meta[2] = used + min(nM, nfree);
+    if (lru.trace) *lru.trace_n = tn + (uint64_t)nS;
+  }
+  return StepResult{miss, fs, rS, rM, nM};
+}
+
+// Decode router, second kernel (one block): the token's routing (route_token)
+// and, with lru.slot_of set, the layer's slot-table step and the work list.
+// Every global load is issued up front (the table state included).  A
+// non-finite chosen logit is a routing failure: the error word is set and the
+// work list left empty.
+__global__ __launch_bounds__(kThreads) void router_finish_kernel(
+    const float *__restrict__ partial, int nb, int E, int k, int32_t *idx, float *w,
+    int32_t *host_idx, float *host_w, LruDev lru) {
+  __shared__ RouteLds rl;
+  __shared__ StepLds sl;
+  __shared__ int32_t selL[kMaxRouted];
+  __shared__ int32_t badL;
+  const int tid = threadIdx.x;
   const bool dev = lru.slot_of != nullptr;
   // the table state first: its latency hides behind the routing work
   int so = -1;
@@ -311,76 +507,8 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     used = lru.meta[2];
     if (lru.trace) tn = *lru.trace_n;
   }
-  const float inv = partial[(int64_t)nb * E];
-  const int per = (nb + phases - 1) / phases;
-  float sacc = 0.f;
-  if (ph < phases) {
-    const int b0 = ph * per, b1 = min(nb, b0 + per);
-    for (int b = b0; b < b1; b += 48) {  // one round trip up to 48 partials per lane
-      float v[48];
-#pragma unroll
-      for (int j = 0; j < 48; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
-#pragma unroll
-      for (int j = 0; j < 48; ++j) sacc += v[j];
-    }
-  }
-  red[tid] = sacc;
-  __syncthreads();
-  if (tid < E) {
-    float z = 0.f;
-    for (int p = 0; p < phases; ++p) z += red[p * E + tid];
-    z *= inv;
-    zs[tid] = z;
-    keyZ[tid] = rank_key(z, tid);
-    if (lru.zlast) lru.zlast[tid] = z;
-  }
-  __syncthreads();
-  // rank of expert c over the experts [ph E / phases, (ph+1) E / phases)
-  {
-    int r = 0;
-    if (ph < phases) {
-      const uint64_t kc = keyZ[c];
-      const int f0 = ph * E / phases, f1 = (ph + 1) * E / phases;
-      int f = f0;
-      for (; f + 8 <= f1; f += 8) {  // eight independent LDS reads per step
-        uint64_t v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = keyZ[f + j];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) r += v[j] > kc ? 1 : 0;
-      }
-      for (; f < f1; ++f) r += keyZ[f] > kc ? 1 : 0;
-    }
-    __syncthreads();
-    red[tid] = __int_as_float(r);
-  }
-  __syncthreads();
-  int rank = E;
-  if (tid < E) {
-    rank = 0;
-    for (int p = 0; p < phases; ++p) rank += __float_as_int(red[p * E + tid]);
-    if (rank < k) {
-      selL[rank] = tid;
-      zselL[rank] = zs[tid];
-    }
-  }
-  __syncthreads();
-  if (tid < kWave) {  // softmax over the chosen logits (the first is the largest)
-    const bool ok = __ballot(tid < k && !isfinite(zselL[tid < k ? tid : 0])) == 0;
-    const float ex = tid < k && ok ? expf(zselL[tid] - zselL[0]) : 0.f;
-    float sum = ex;
-#pragma unroll
-    for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
-    if (tid < k) {
-      const int32_t id = ok ? selL[tid] : 0x7fffffff;
-      const float wi = ok ? ex / sum : 0.f;
-      idx[tid] = id;
-      w[tid] = wi;
-      if (host_idx) host_idx[tid] = id;
-      if (host_w) host_w[tid] = wi;
-    }
-    if (tid == 0) badL = ok ? 0 : 1;
-  }
+  if (tid == 0) badL = 0;  // ordered before route_token's write by its barriers
+  const int rank = route_token(partial, nb, E, k, idx, w, host_idx, host_w, lru.zlast, selL, &badL, rl);
   if (!dev) return;  // uniform
   __syncthreads();
   if (badL) {  // no work for this call; reported at the next synchronisation
@@ -391,87 +519,127 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     }
     return;
   }
-  const int lane = tid & (kWave - 1), wv = tid / kWave;
   const bool inS = rank < k;
-  const bool miss = inS && so < 0;
-  const bool cand = tid < E && so >= 0 && !inS;
-  const uint64_t bS = __ballot(inS), bM = __ballot(miss), lt = (1ull << lane) - 1ull;
-  if (lane == 0) {
-    cntL[0][wv] = __popcll(bS);
-    cntL[1][wv] = __popcll(bM);
-  }
-  for (int sl = tid; sl < lru.C; sl += kThreads) keyL[sl] = UINT64_MAX;
-  __syncthreads();
-  int rS = __popcll(bS & lt), rM = __popcll(bM & lt), nM = 0;
-#pragma unroll
-  for (int v = 0; v < kThreads / kWave; ++v) {
-    if (v < wv) {
-      rS += cntL[0][v];
-      rM += cntL[1][v];
-    }
-    nM += cntL[1][v];
-  }
-  // victims in ascending key: the stamp (least recently used first), or the
-  // logit's rank key (lowest logit first, the higher id on a tie); unique keys
-  const uint64_t vkey = !cand ? 0ull : lru.policy ? keyZ[tid] : (uint64_t)st;
-  if (cand) keyL[so] = vkey;
-  const int nfree = lru.C - (int)used;
-  const int nev = max(0, nM - nfree);
-  __syncthreads();
-  bool evicted = false;
-  if (cand && nev > 0) {
-    int cr = 0;  // residents outside S evicted before this one
-    for (int sl = 0; sl < lru.C; ++sl) cr += keyL[sl] < vkey ? 1 : 0;
-    if (cr < nev) {
-      evicted = true;
-      vicL[cr] = tid;
-      vslL[cr] = so;
-    }
-  }
-  __syncthreads();
-  int fs = so, fev = -1;
-  if (miss) {
-    if (rM < nfree) {
-      fs = (int)used + rM;
-    } else {
-      fs = vslL[rM - nfree];
-      fev = vicL[rM - nfree];
-    }
-  }
-  if (evicted) lru.slot_of[tid] = -1;
+  const StepResult o =
+      table_step(lru, E, inS, so, st, tid < E ? rl.keyZ[tid] : 0ull, clock0, step, used, tn, sl);
   if (inS) {
-    lru.stamp[tid] = clock0 + rS + 1;
-    lru.work->hit[rank] = miss ? 0 : 1;
-    if (miss) {
-      lru.slot_of[tid] = fs;
-      lru.expert_in[fs] = tid;
-      lru.work->src[rM] = lru.store + (int64_t)tid * lru.P;
-      lru.work->dst[rM] = lru.slots + (int64_t)fs * lru.P;
-      lru.work->miss_pos[rM] = rank;
+    lru.work->hit[rank] = o.miss ? 0 : 1;
+    if (o.miss) {
+      lru.work->src[o.rM] = lru.store + (int64_t)tid * lru.P;
+      lru.work->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
+      lru.work->miss_pos[o.rM] = rank;
     }
-    lru.work->list.payload[rank] = lru.slots + (int64_t)fs * lru.P;
+    lru.work->list.payload[rank] = lru.slots + (int64_t)o.fs * lru.P;
     lru.work->list.pos[rank] = rank;
-    if (lru.trace) {
-      int32_t *r = lru.trace + 6 * (int64_t)(tn + rS);
-      r[0] = lru.layer;
-      r[1] = (int32_t)step;
-      r[2] = tid;
-      r[3] = miss ? 0 : 1;
-      r[4] = fs;
-      r[5] = fev;
-    }
   }
   if (tid == 0) {
     lru.work->list.n = k;
-    lru.work->n_copy = nM;
-    lru.cnt[0] += (uint64_t)(k - nM);
-    lru.cnt[1] += (uint64_t)nM;
-    lru.cnt[2] += (uint64_t)nev;
-    lru.cnt[3] += (uint64_t)nM * (uint64_t)lru.P;
-    lru.meta[0] = clock0 + k;
-    lru.meta[1] = step + 1;
-    lru.meta[2] = used + min(nM, nfree);
-    if (lru.trace) *lru.trace_n = tn + (uint64_t)k;
+    lru.work->n_copy = o.nM;
+  }
+}
+
+// Router of a small multi-token call (T <= kMtTokens), second kernel (one
+// block): each token's routing as in decode (route_token over its own
+// partials), then one slot-table step for the union S of the tokens' routed
+// experts, and a work list: the misses' copies and, per token, its k experts'
+// slots in rank order.  If |S| exceeds the slots (slots would be reused
+// inside the call) the table is left untouched and the work list empty;
+// flag (host memory) gets 0 (done), 1 (|S| > C) or 2 (routing failure, also
+// in the error word).
+__global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
+    const float *__restrict__ partial, int nb, int T, int E, int k, int32_t *idx, float *w, LruDev lru,
+    MtWork *mw, int32_t *flag) {
+  __shared__ RouteLds rl;
+  __shared__ StepLds sl;
+  __shared__ int32_t selL[kMtTokens][kMaxRouted];
+  __shared__ int32_t slotL[256];
+  __shared__ int32_t badL;
+  const int tid = threadIdx.x;
+  int so = -1;
+  int64_t st = 0;
+  if (tid < E) {
+    so = lru.slot_of[tid];
+    st = lru.stamp[tid];
+  }
+  const int64_t clock0 = lru.meta[0], step = lru.meta[1], used = lru.meta[2];
+  const uint64_t tn = lru.trace ? *lru.trace_n : 0;
+  if (tid == 0) badL = 0;
+  // every token's partials in one round trip (nb <= kMtParts): thread (c, ph)
+  // adds, per token, blocks [ph * per, ph * per + per) of expert c in block order
+  const int64_t pstride = (int64_t)nb * E + 1;
+  const int phases = kThreads / E;
+  const int c = tid % E, ph = tid / E;
+  const int per = (nb + phases - 1) / phases, b0 = ph * per, b1 = min(nb, b0 + per);
+  // (unconditional loads at clamped, valid addresses, selected afterwards: a
+  // guarded load becomes a branch with its own wait)
+  float v[kMtTokens][kMtParts], iv[kMtTokens];
+#pragma unroll
+  for (int t = 0; t < kMtTokens; ++t) {
+    const int64_t tb = (int64_t)min(t, T - 1) * pstride;
+#pragma unroll
+    for (int j = 0; j < kMtParts; ++j) v[t][j] = partial[tb + (int64_t)min(b0 + j, nb - 1) * E + c];
+    iv[t] = partial[tb + (int64_t)nb * E];
+  }
+  float sacc[kMtTokens], inv[kMtTokens];
+#pragma unroll
+  for (int t = 0; t < kMtTokens; ++t) {
+    float a = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMtParts; ++j) a += t < T && ph < phases && b0 + j < b1 ? v[t][j] : 0.f;
+    sacc[t] = a;
+    inv[t] = iv[t];
+  }
+  bool inS = false;
+#pragma unroll
+  for (int t = 0; t < kMtTokens; ++t) {
+    if (t < T) {  // uniform
+      const int rank = route_sum(sacc[t], inv[t], E, k, idx + t * k, w + t * k, nullptr, nullptr, nullptr,
+                                 selL[t], &badL, rl);
+      inS = inS || rank < k;
+      __syncthreads();  // rl is reused by the next token
+    }
+  }
+  const int nS = __syncthreads_count(inS);
+  if (badL || nS > lru.C) {  // uniform
+    if (tid < T) mw->list[tid].n = 0;
+    if (tid == 0) {
+      mw->n_copy = 0;
+      mw->n_union = 0;
+      if (badL) *lru.err = 1;
+      flag[1] = nS;
+      __threadfence_system();
+      flag[0] = badL ? 2 : 1;
+    }
+    return;
+  }
+  const StepResult o = table_step(lru, E, inS, so, st, 0ull, clock0, step, used, tn, sl);
+  if (inS) {
+    slotL[tid] = o.fs;
+    if (o.miss) {
+      mw->src[o.rM] = lru.store + (int64_t)tid * lru.P;
+      mw->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
+    }
+    // the union entry o.rS: slot and the (token, rank) positions routing here
+    mw->upay[o.rS] = lru.slots + (int64_t)o.fs * lru.P;
+    int nt = 0;
+    for (int t = 0; t < T; ++t)
+      for (int j = 0; j < k; ++j)
+        if (selL[t][j] == tid) mw->uq[o.rS][nt++] = (uint8_t)(t * k + j);
+    mw->unt[o.rS] = (uint8_t)nt;
+  }
+  __syncthreads();
+  for (int i = tid; i < T * k; i += kThreads) {
+    const int t = i / k, j = i - t * k;
+    mw->list[t].payload[j] = lru.slots + (int64_t)slotL[selL[t][j]] * lru.P;
+    mw->list[t].pos[j] = j;
+  }
+  if (tid < T) mw->list[tid].n = k;
+  if (tid == 0) {
+    mw->n_copy = o.nM;
+    mw->n_union = nS;
+    flag[1] = nS;
+    __threadfence_system();
+    flag[0] = 0;
   }
 }
 
@@ -962,6 +1130,7 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
   gateup_body<QT>(a, DEV ? *a.Ld : a.L, nullptr, blockIdx.x, smem8);
 }
 
+
 // ---------------------------------------------------- copy + gate/up fused ---
 //
 // Blocks [0, copy_blocks) move the misses' payloads in "chunks": two spans of
@@ -1325,6 +1494,228 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
 // the store into their slots: 16-byte loads and stores, four in flight per
 // thread, grid-strided over all misses' bytes.
 constexpr int kMaxCopy = 64;
+// ------------------------------------------- small multi-token calls ---
+//
+// The decode GEMVs over the union of a small call's experts: a block takes
+// one union expert's rows, holds each lane's weight pairs in registers and
+// forms the dot products with every token routing to that expert, in the
+// same lane, pair and summation order as the per-token kernels, so each
+// token's activations and output rows are those of gateup_kernel /
+// down_kernel.
+
+struct GateUpMtParams {
+  const MtWork *W;
+  const int8_t *xq;  // [T][3][H] token digits
+  const float *xsc;  // [T][H/32]
+  int8_t *hq;        // [3][T*k*I]
+  float *hsc;        // [T*k*I/16]
+  int32_t *hds;      // [3][T*k*I/16] (Q4_0)
+  int H, I, k, T;
+  int lanes, mpairs, lanes_log2;
+};
+
+// One token's LDS image for the gate/up GEMV: digit planes, block scales, digit sums.
+__device__ __forceinline__ int mt_image_bytes(int H) { return 3 * plane_bytes(H) + 16 * (H / 32); }
+
+// grid: umax * bpe blocks; block b: union expert b / bpe, rows from
+// (b % bpe) * (256 / lanes).  Dynamic LDS: T images, then [kMtTokens][256 / lanes] floats.
+template <int QT>
+__global__ __launch_bounds__(kThreads) void gateup_mt_kernel(GateUpMtParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  __shared__ __align__(16) uint8_t dummyL[16];
+  __shared__ int qL[kMtTokens];
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kGateUpFlight;
+  const int H = a.H, nb = H / 32, np = nb / 2, pb = plane_bytes(H), img = mt_image_bytes(H);
+  const int upb = kThreads / a.lanes;
+  const int bpe = (a.I + upb - 1) / upb;
+  const int u = blockIdx.x / bpe;  // < kMtMaxCopy (the launch bounds the grid)
+  // the union's size, this expert's slot, token count and positions (one round trip)
+  const int nu = a.W->n_union;
+  const uint8_t *const payload = a.W->upay[u];
+  const int nt = a.W->unt[u];
+  const int q_t = (int)threadIdx.x < kMtTokens ? a.W->uq[u][threadIdx.x] : 0;
+  if (u >= nu || payload == nullptr) return;  // uniform over the block
+  if ((int)threadIdx.x < kMtTokens) qL[threadIdx.x] = q_t;
+  const int r0 = (blockIdx.x - u * bpe) * upb;
+  const int r = r0 + (threadIdx.x >> a.lanes_log2);
+  const int l = threadIdx.x & (a.lanes - 1);
+  const bool active = r < a.I;
+  const int64_t rowb = (int64_t)nb * BB, mat = (int64_t)a.I * rowb;
+  const uint8_t *gate = payload + (int64_t)r * rowb, *up = gate + mat;
+  const uint8_t *gatev = payload + (int64_t)min(r, a.I - 1) * rowb, *upv = gatev + mat;
+  uint32_t wg[F][PD], wu[F][PD];
+#pragma unroll
+  for (int m = 0; m < F; ++m) {
+    const int p = l + m * a.lanes;
+    const bool ok = active && m < a.mpairs && p < np;
+    load_pair<QT>(ok ? gate + (int64_t)p * 2 * BB : gatev, wg[m]);
+    load_pair<QT>(ok ? up + (int64_t)p * 2 * BB : upv, wu[m]);
+  }
+  __syncthreads();
+  // the digits of the tokens routing here while the weights are in flight
+  for (int i = 0; i < nt; ++i) {
+    const int t = qL[i] / a.k;
+    uint8_t *im = smem8 + i * img;
+    stage_token(a.xq + (int64_t)t * 3 * H, a.xsc + (int64_t)t * nb, H, im,
+                reinterpret_cast<float *>(im + 3 * pb), dummyL);
+  }
+  __syncthreads();
+  if constexpr (QT == 2) {
+    for (int i = 0; i < nt; ++i) {
+      uint8_t *im = smem8 + i * img;
+      digit_sums(im, H, reinterpret_cast<int *>(im + 3 * pb + 4 * nb));
+    }
+    __syncthreads();
+  }
+  float g[kMtTokens], v[kMtTokens];
+#pragma unroll
+  for (int i = 0; i < kMtTokens; ++i) g[i] = v[i] = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < F; ++m) {
+        const int p = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && p < np) {
+          load_pair<QT>(gate + (int64_t)p * 2 * BB, wg[m]);
+          load_pair<QT>(up + (int64_t)p * 2 * BB, wu[m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < F; ++m) {
+      const int p = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && p < np) {
+#pragma unroll
+        for (int i = 0; i < kMtTokens; ++i) {
+          if (i < nt) {
+            const uint8_t *im = smem8 + i * img;
+            const float *scL = reinterpret_cast<const float *>(im + 3 * pb);
+            const int *dsL = reinterpret_cast<const int *>(im + 3 * pb + 4 * nb);
+            uint32_t D[48];
+            load_digits(im, pb, p, D);
+            const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
+            g[i] += pair_dot<QT>(wg[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+            v[i] += pair_dot<QT>(wu[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+          }
+        }
+      }
+    }
+  }
+  float *hL = reinterpret_cast<float *>(smem8 + a.T * img);  // [kMtTokens][upb]
+#pragma unroll
+  for (int i = 0; i < kMtTokens; ++i) {
+    if (i < nt) {  // uniform
+      const float gs = group_sum(g[i], a.lanes), us = group_sum(v[i], a.lanes);
+      if (l == 0) hL[i * upb + (threadIdx.x >> a.lanes_log2)] = active ? silu(gs) * us : 0.f;
+    }
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < upb)
+    for (int i = 0; i < nt; ++i)
+      store_h_digits<QT>(hL[i * upb + threadIdx.x], qL[i], r0 + threadIdx.x, a.I, a.T * a.k, a.hq,
+                         a.hsc, a.hds);
+}
+
+struct DownMtParams {
+  const MtWork *W;
+  const int8_t *hq;  // [3][T*k*I]
+  const float *hsc;
+  const int32_t *hds;
+  float *R;  // [T*k][H]
+  int H, I, k, T;
+  int lanes, mpairs, lanes_log2, rows;  // rows = 256 / lanes
+};
+
+// grid: umax * ceil(H / rows) blocks; block b: union expert b / bpe, output
+// rows from (b % bpe) * rows.  Dynamic LDS: the h digit images of T positions.
+template <int QT>
+__global__ __launch_bounds__(kThreads) void down_mt_kernel(DownMtParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  __shared__ int posL[kMtTokens];
+  __shared__ __align__(16) uint8_t dummyL[16];
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kDownFlight;
+  const int I = a.I, nb = I / 32, np = nb / 2, pb = plane_bytes(I);
+  const int bpe = (a.H + a.rows - 1) / a.rows;
+  const int u = blockIdx.x / bpe;
+  const int nu = a.W->n_union;
+  const uint8_t *const payload = a.W->upay[u];
+  const int nt = a.W->unt[u];
+  const int q_t = (int)threadIdx.x < kMtTokens ? a.W->uq[u][threadIdx.x] : 0;
+  if (u >= nu || payload == nullptr) return;  // uniform
+  if ((int)threadIdx.x < kMtTokens) posL[threadIdx.x] = q_t;
+  __syncthreads();
+  uint8_t *qL = smem8;                                          // nt digit images
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * a.T * pb);  // [nt][I/16]
+  int *dsL = reinterpret_cast<int *>(scL + a.T * (I / 16));      // [nt][3][I/16]
+  const int j = (blockIdx.x - u * bpe) * a.rows + (threadIdx.x >> a.lanes_log2);
+  const int l = threadIdx.x & (a.lanes - 1);
+  const bool active = j < a.H;
+  const int64_t rowb = (int64_t)nb * BB;
+  const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
+  const uint8_t *row = payload + 2 * mat + (int64_t)j * rowb;
+  const uint8_t *rowv = payload + 2 * mat + (int64_t)min(j, a.H - 1) * rowb;
+  HStage st;
+  stage_h_load(a.hq, a.hsc, a.hds, posL, nt, I, a.T * a.k, QT == 2, st);  // ahead of the weights
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t wd[F][PD];
+#pragma unroll
+  for (int m = 0; m < F; ++m) {
+    const int p = l + m * a.lanes;
+    const bool ok = active && m < a.mpairs && p < np;
+    load_pair<QT>(ok ? row + (int64_t)p * 2 * BB : rowv, wd[m]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  stage_h_store(st, nt, I, QT == 2, qL, scL, dsL, dummyL);
+  __syncthreads();
+  float acc[kMtTokens];
+#pragma unroll
+  for (int i = 0; i < kMtTokens; ++i) acc[i] = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < F; ++m) {
+        const int p = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && p < np) load_pair<QT>(row + (int64_t)p * 2 * BB, wd[m]);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < F; ++m) {
+      const int p = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && p < np) {
+#pragma unroll
+        for (int i = 0; i < kMtTokens; ++i) {
+          if (i < nt) {
+            uint32_t D[48];
+            load_digits(qL + 3 * i * pb, pb, p, D);
+            acc[i] += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p, dsL + 3 * i * (I / 16) + 4 * p,
+                                     I / 16);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kMtTokens; ++i) {
+    if (i < nt) {  // uniform
+      const float s = group_sum(acc[i], a.lanes);
+      if (active && l == 0) a.R[(int64_t)posL[i] * a.H + j] = s;
+    }
+  }
+}
+
+// y_t[j] = (x_t[j] if mode 1) + sum over ranks r of w[t*k+r] R[t*k+r][j], in rank order.
+__global__ __launch_bounds__(kThreads) void combine_mt_kernel(const float *__restrict__ R,
+                                                              const float *__restrict__ w,
+                                                              const float *__restrict__ x,
+                                                              float *__restrict__ y, int H, int k,
+                                                              int mode) {
+  const int t = blockIdx.y, j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= H) return;
+  float v = mode == 1 ? x[(int64_t)t * H + j] : 0.f;
+  for (int r = 0; r < k; ++r) v = fmaf(w[t * k + r], R[((int64_t)t * k + r) * H + j], v);
+  y[(int64_t)t * H + j] = v;
+}
+
 struct CopyParams {
   const uint4 *src[kMaxCopy];
   uint4 *dst[kMaxCopy];
@@ -1356,7 +1747,8 @@ __global__ __launch_bounds__(kThreads) void materialize_kernel(CopyParams a) {
 }
 
 // The same copy for the misses a device work list names.
-__global__ __launch_bounds__(kThreads) void materialize_list_kernel(const WorkList *w, int64_t p16,
+template <class Work>
+__global__ __launch_bounds__(kThreads) void materialize_list_kernel(const Work *w, int64_t p16,
                                                                     uint64_t *acc) {
   const int n = w->n_copy;
   if (acc && blockIdx.x == 0 && threadIdx.x == 0) {
@@ -1834,11 +2226,30 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
   const LruDev none{};
   const int nb = router_decode_grid(H);
   hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
-                        wr, H, E, (int)prenorm, partial, xq, xsc);
+                        wr, H, E, (int)prenorm, kRouterRowsPerBlock, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0, partial,
                         nb, E, k, idx, w, host_idx, host_w, lru ? *lru : none);
+  return hipGetLastError();
+}
+
+hipError_t launch_router_small(const float *x, const float *wr, int T, int H, int E, int k, float *partial,
+                               int32_t *idx, float *w, int8_t *xq, float *xsc, bool prenorm,
+                               const LruDev &lru, MtWork *mw, int32_t *flag, hipStream_t s,
+                               const Timing &t) {
+  if (T < 1 || T > kMtTokens || !lru.slot_of) return hipErrorInvalidValue;
+  // at most kMtParts blocks per token, so the finishing block loads every
+  // token's partials in one round trip
+  const int pieces = (H + kRouterRowsPerBlock - 1) / kRouterRowsPerBlock;
+  const int rpb = kRouterRowsPerBlock * ((pieces + kMtParts - 1) / kMtParts);
+  const int nb = (H + rpb - 1) / rpb;
+  hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb, T), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
+                        wr, H, E, (int)prenorm, rpb, partial, xq, xsc);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(router_finish_mt_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0,
+                        partial, nb, T, E, k, idx, w, lru, mw, flag);
   return hipGetLastError();
 }
 
@@ -1904,6 +2315,60 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
   return hipGetLastError();
 }
 
+size_t mt_gateup_lds(int H, int T) {
+  return (size_t)T * (3 * (size_t)(H / 64) * kPairPitch + 16 * (size_t)(H / 32)) +
+         (size_t)kMtTokens * kThreads * sizeof(float);
+}
+static size_t mt_down_lds(int I, int T) { return (size_t)T * (3 * (size_t)(I / 64) * kPairPitch + I); }
+
+bool mt_ffn_fits(int H, int I, int T) {
+  return T >= 1 && T <= kMtTokens && 3 * T * I / 16 <= kMaxDig16 * kThreads &&
+         mt_gateup_lds(H, T) <= 64 * 1024 && mt_down_lds(I, T) <= 64 * 1024;
+}
+
+hipError_t launch_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc, int8_t *hq,
+                            float *hsc, int32_t *hds, int H, int I, int k, int T, int umax,
+                            hipStream_t s, const Timing &t) {
+  if (!mt_ffn_fits(H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
+  GateUpMtParams a{W, xq, xsc, hq, hsc, hds, H, I, k, T, 0, 0, 0};
+  pick_lanes(H / 64, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes, a.lanes,
+             a.mpairs);
+  while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
+  const int upb = kThreads / a.lanes;
+  dim3 grid(umax * ((I + upb - 1) / upb));
+  const size_t lds = mt_gateup_lds(H, T);
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(gateup_mt_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(gateup_mt_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_mt(int qtype, const MtWork *W, const int8_t *hq, const float *hsc,
+                          const int32_t *hds, float *R, int H, int I, int k, int T, int umax,
+                          hipStream_t s, const Timing &t) {
+  if (!mt_ffn_fits(H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
+  DownMtParams a{W, hq, hsc, hds, R, H, I, k, T, 0, 0, 0, 0};
+  pick_lanes(I / 64, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
+             a.mpairs);
+  while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
+  a.rows = kThreads / a.lanes;
+  dim3 grid(umax * ((H + a.rows - 1) / a.rows));
+  const size_t lds = mt_down_lds(I, T);
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(down_mt_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(down_mt_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_mt(const float *R, const float *w, const float *x, float *y, int H, int k,
+                             int T, int mode, hipStream_t s, const Timing &t) {
+  hipExtLaunchKernelGGL(combine_mt_kernel, dim3((H + kThreads - 1) / kThreads, T), dim3(kThreads), 0, s,
+                        t.start, t.stop, 0, R, w, x, y, H, k, mode);
+  return hipGetLastError();
+}
+
 bool fusable_copy_gateup(int qtype, int H, int I) {
   const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
   return 2 * 4 * rowb <= (int64_t)kChunkSlots * kThreads * 16 && I % 32 == 0;
@@ -1938,8 +2403,15 @@ hipError_t launch_copy_gateup(int qtype, const DecodeScratch &S, int H, int I, i
 
 hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, uint64_t *acc,
                                    hipStream_t s, const Timing &t) {
-  hipExtLaunchKernelGGL(materialize_list_kernel, dim3(grid), dim3(kThreads), 0, s, t.start, t.stop, 0,
-                        w, bytes / 16, acc);
+  hipExtLaunchKernelGGL(materialize_list_kernel<WorkList>, dim3(grid), dim3(kThreads), 0, s, t.start,
+                        t.stop, 0, w, bytes / 16, acc);
+  return hipGetLastError();
+}
+
+hipError_t launch_materialize_list(const MtWork *w, int64_t bytes, int grid, uint64_t *acc,
+                                   hipStream_t s, const Timing &t) {
+  hipExtLaunchKernelGGL(materialize_list_kernel<MtWork>, dim3(grid), dim3(kThreads), 0, s, t.start,
+                        t.stop, 0, w, bytes / 16, acc);
   return hipGetLastError();
 }
 

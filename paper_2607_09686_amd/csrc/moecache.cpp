@@ -50,7 +50,7 @@ constexpr int kCopyGrid = 64;  // copy-kernel blocks: enough requests in flight 
 // Multi-token calls of at most this many tokens whose routed experts all fit the
 // slots run the decode GEMVs once per token instead of the MFMA grouped GEMMs
 // (whose 128-row tiles would hold a handful of rows).
-constexpr int kSmallTokens = 8;
+constexpr int kSmallTokens = kMtTokens;
 
 struct TimedSpan {
   int kind;
@@ -109,6 +109,15 @@ struct moe_cache {
   float *dl_zlast = nullptr;  // [E] logits of the last decode call
   uint64_t *dl_copy_acc = nullptr;  // [2] copies and bytes of the timed copy launches
   WorkList *dl_work = nullptr;
+  // small multi-token calls stepped on the device
+  float *mt_partial = nullptr;  // [kMtTokens][router grid * E + 1]
+  MtWork *mt_work = nullptr;
+  int32_t *mt_flag = nullptr;   // pinned [2]: verdict (0 done, 1 union exceeds the slots, 2
+                                //   routing failure), union size
+  int8_t *mt_hq = nullptr;      // [3][kMtTokens * k * I] activation digits by (token, rank)
+  float *mt_hsc = nullptr;      // [kMtTokens * k * I / 16]
+  int32_t *mt_hds = nullptr;    // [3][kMtTokens * k * I / 16]
+  float *mt_R = nullptr;        // [kMtTokens * k][H] unweighted down rows
   int64_t dl_trace_cap = 0, dl_trace_pending = 0;
   uint8_t *dl_stage = nullptr;      // pinned staging of one layer's table
   bool table_pulled = false;        // a multi-token call holds the layer's table on the host
@@ -207,6 +216,13 @@ struct Span {
     if (on) c->pending.push_back(sp);
     on = false;
   }
+  void discard() {  // not kept: the events go back to the pool
+    if (on) {
+      c->ev_pool.push_back(sp.start);
+      c->ev_pool.push_back(sp.stop);
+    }
+    on = false;
+  }
 };
 
 int check_desc(const moe_model_desc *d, int32_t budget) {
@@ -269,6 +285,13 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->dl_zlast);
   (void)hipFree(c->dl_copy_acc);
   (void)hipFree(c->dl_work);
+  (void)hipFree(c->mt_partial);
+  (void)hipFree(c->mt_work);
+  (void)hipFree(c->mt_hq);
+  (void)hipFree(c->mt_hsc);
+  (void)hipFree(c->mt_hds);
+  (void)hipFree(c->mt_R);
+  if (c->mt_flag) (void)hipHostFree(c->mt_flag);
   if (c->dl_stage) (void)hipHostFree(c->dl_stage);
   if (c->host_idx) (void)hipHostFree(c->host_idx);
   if (c->host_w) (void)hipHostFree(c->host_w);
@@ -309,6 +332,7 @@ constexpr int64_t kTraceCap = 1 << 16;  // device trace records kept between dra
 
 int alloc_dev_tables(moe_cache *c) {
   const int64_t L = c->d.n_layers, E = c->d.n_experts, C = c->C;
+  const size_t mtKI = (size_t)kMtTokens * c->d.top_k * c->d.inter;
   if (hipMalloc(&c->dl_slot_of, L * E * 4) != hipSuccess ||
       hipMalloc(&c->dl_expert_in, L * C * 4) != hipSuccess ||
       hipMalloc(&c->dl_stamp, L * E * 8) != hipSuccess || hipMalloc(&c->dl_meta, L * 3 * 8) != hipSuccess ||
@@ -316,6 +340,14 @@ int alloc_dev_tables(moe_cache *c) {
       hipMalloc(&c->dl_err, 4) != hipSuccess || hipMalloc(&c->dl_copy_acc, 16) != hipSuccess ||
       hipMalloc(&c->dl_zlast, E * 4) != hipSuccess ||
       hipMalloc(&c->dl_work, sizeof(WorkList)) != hipSuccess ||
+      hipMalloc(&c->mt_partial, ((size_t)router_decode_grid(c->d.hidden) * E + 1) * kMtTokens *
+                                    sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->mt_work, sizeof(MtWork)) != hipSuccess ||
+      hipMalloc(&c->mt_hq, 3 * mtKI) != hipSuccess ||
+      hipMalloc(&c->mt_hsc, mtKI / 16 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->mt_hds, 3 * mtKI / 16 * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->mt_R, (size_t)kMtTokens * c->d.top_k * c->d.hidden * sizeof(float)) != hipSuccess ||
+      hipHostMalloc(&c->mt_flag, 2 * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->dl_stage, table_stage_bytes((int)E, (int)C), hipHostMallocDefault) !=
           hipSuccess) {
     (void)hipGetLastError();
@@ -344,6 +376,7 @@ int clear_dev_tables(moe_cache *c) {
   HIP_TRY(c, hipMemsetAsync(c->dl_zlast, 0, E * 4, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_copy_acc, 0, 16, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_work, 0, sizeof(WorkList), c->main));
+  HIP_TRY(c, hipMemsetAsync(c->mt_work, 0, sizeof(MtWork), c->main));
   c->dl_trace_pending = 0;
   return MOE_OK;
 }
@@ -682,6 +715,127 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
 int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer,
                     float *y, moe_counters *delta, int32_t *dbg_idx, float *dbg_w);
 
+// A multi-token call of at most kMtTokens tokens with the layer's table on
+// the device: per token the decode router's partials and digits, then one
+// block routes every token, steps the table over the union of their experts
+// and writes the work list (two launches); the misses' copies from that list
+// and per token the decode GEMVs over its own experts follow, all queued on
+// the caller's stream.  The host then waits for the table step only to learn
+// whether the union fit the slots: if not, the table was left untouched, the
+// queued copies and GEMVs find an empty list, and the call is run by the
+// multi-token path with the table on the host (which reuses slots inside the
+// call).
+int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
+                      moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+  const moe_model_desc &d = c->d;
+  const int k = d.top_k, E = d.n_experts, H = d.hidden, I = d.inter;
+  int rc = ensure_tokens(c, T);
+  if (rc) return rc;
+  c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
+  uint64_t before[4] = {0, 0, 0, 0};
+  if (delta) {
+    if ((rc = sync_dev(c))) return rc;
+    HIP_TRY(c, hipMemcpy(before, c->dl_cnt + 4 * layer, 32, hipMemcpyDeviceToHost));
+  }
+  if (c->dl_trace && c->dl_trace_pending + (int64_t)T * k > c->dl_trace_cap && (rc = drain_dev_trace(c)))
+    return rc;
+  const LruDev L = dev_table(c, layer);
+  volatile int32_t *flag = c->mt_flag;
+  flag[0] = -1;
+  {
+    Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)H * E * 4 + (uint64_t)T * H * 4,
+            2ull * T * H * E);
+    HIP_TRY(c, launch_router_small(x, wr, T, H, E, k, c->mt_partial, c->topk_idx, c->topk_w, c->st_xq,
+                                   c->st_xsc, (d.flags & MOE_F_PRENORM) != 0, L, c->mt_work, c->mt_flag,
+                                   c->main, sp.timing()));
+    sp.end();
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
+  if (c->dl_trace) c->dl_trace_pending += (int64_t)T * k;
+  {
+    Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
+    HIP_TRY(c, launch_materialize_list(c->mt_work, c->P, kCopyGrid,
+                                       c->timing_now ? c->dl_copy_acc : nullptr, c->main, sp.timing()));
+    sp.end();
+  }
+  const int mode = (d.flags & MOE_F_RESIDUAL) ? 1 : 0;
+  // the union's GEMVs (each expert's weights read once; their byte counts are
+  // set once the union's size is known) or, for shapes those kernels do not
+  // take, the decode GEMVs once per token
+  const bool union_ffn = mt_ffn_fits(H, I, T);
+  Span gu(c, c->main, MOE_KIND_GATEUP, 1, 0, 4ull * T * k * H * I);
+  Span dn(c, c->main, MOE_KIND_DOWN, 1, 0, 2ull * T * k * H * I);
+  if (union_ffn) {
+    const int umax = std::min(T * k, (int)c->C);
+    HIP_TRY(c, launch_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc, c->mt_hds,
+                                H, I, k, T, umax, c->main, gu.timing()));
+    HIP_TRY(c, launch_down_mt(d.qtype, c->mt_work, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H, I, k, T,
+                              umax, c->main, dn.timing()));
+    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->main));
+  } else {
+    ExpertList shape{};
+    shape.n = k;
+    for (int32_t tk = 0; tk < T; ++tk) {
+      DecodeScratch St = c->scratch();
+      St.xq = c->st_xq + (int64_t)tk * 3 * H;
+      St.xsc = c->st_xsc + (int64_t)tk * (H / 32);
+      {
+        Span sp(c, c->main, MOE_KIND_GATEUP, 1, (uint64_t)k * 2 * c->M, 4ull * k * H * I);
+        HIP_TRY(c, launch_gateup(d.qtype, St, H, I, k, shape, &c->mt_work->list[tk], c->main, sp.timing()));
+        sp.end();
+      }
+      {
+        Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * H * I);
+        HIP_TRY(c, launch_down(d.qtype, St, H, I, k, shape, &c->mt_work->list[tk],
+                               c->topk_w + (int64_t)tk * k, x + (int64_t)tk * H, y + (int64_t)tk * H, mode,
+                               c->main, sp.timing()));
+        sp.end();
+      }
+    }
+  }
+  // the table step's verdict: spin on the flag the finishing block writes to
+  // host memory; now and then ask the event, which also reports a failed launch
+  for (long spin = 0; flag[0] < 0; ++spin) {
+    if ((spin & 0xfff) == 0xfff && hipEventQuery(c->ev_route) != hipErrorNotReady) {
+      HIP_TRY(c, hipEventSynchronize(c->ev_route));
+      break;
+    }
+  }
+  const int32_t verdict = flag[0];
+  if (union_ffn && verdict == 0) {
+    gu.sp.bytes = (uint64_t)flag[1] * 2 * c->M;
+    dn.sp.bytes = (uint64_t)flag[1] * c->M;
+    gu.end();
+    dn.end();
+  } else {
+    gu.discard();
+    dn.discard();
+  }
+  if (verdict == 2) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "router of a multi-token call produced non-finite logits");
+  }
+  if (verdict != 0 && verdict != 1) {
+    c->poisoned = true;
+    return fail(MOE_EHIP, "multi-token table step did not report (flag %d)", verdict);
+  }
+  if ((d.flags & MOE_F_TIMING) && (rc = drain_timing(c))) return rc;
+  if (verdict == 1) return forward_prefill(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
+  if (delta || dbg_idx || dbg_w) {
+    if ((rc = sync_dev(c))) return rc;
+    if (dbg_idx)
+      HIP_TRY(c, hipMemcpy(dbg_idx, c->topk_idx, (size_t)T * k * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (dbg_w) HIP_TRY(c, hipMemcpy(dbg_w, c->topk_w, (size_t)T * k * sizeof(float), hipMemcpyDeviceToHost));
+    if (delta) {
+      uint64_t after[4];
+      HIP_TRY(c, hipMemcpy(after, c->dl_cnt + 4 * layer, 32, hipMemcpyDeviceToHost));
+      *delta = moe_counters{after[0] - before[0], after[1] - before[1], after[2] - before[2],
+                            after[3] - before[3]};
+    }
+  }
+  return MOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -798,6 +952,8 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
     return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
+  if (c->dev_lru && n_tokens <= kSmallTokens)
+    return forward_small_dev(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
   return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
 }
 

@@ -146,6 +146,15 @@ def test_small_calls_both_paths(qtype, T, budget):
     run_prefill(wl, budget, T, calls=3, prenorm=True, residual=True, seed_shift=T)
 
 
+@pytest.mark.parametrize("T", [3, 5])
+def test_small_calls_wide_hidden(T):
+    """Hidden 4096: 3 tokens run the union GEMVs (each routed expert's weights read once for
+    all its tokens), 5 tokens the decode GEMVs once per token (five tokens' digit images
+    exceed the union kernel's LDS budget)."""
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=2, hidden=4096, inter=256, name="tiny_wide")
+    run_prefill(wl, 10, T, calls=3, prenorm=True, residual=True, seed_shift=T)
+
+
 def test_prefill_warm_cache_prenorm_residual_multilayer():
     # (H, I large enough that one bf16 rounding flip of an input, ~4e-3 of its value,
     # stays far below the tolerance; at H 256 a single flip moves y by ~2e-3 x RMS)
