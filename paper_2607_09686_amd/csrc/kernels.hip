@@ -538,23 +538,64 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
   }
 }
 
+// Top-k of one token by one wave over the rank keys kz[0..E) (E <= 256, k <=
+// 16): k rounds of a wave-wide maximum (a key names its expert), then the
+// softmax over the chosen logits z as in route_sum.  Lanes < k return their
+// chosen id and weight (id 0x7fffffff and weight 0 if a chosen logit is not
+// finite, which *bad records).
+__device__ __forceinline__ void wave_topk_keys(const uint64_t *kz, const float *z, int E, int k,
+                                               int32_t &id, float &wt, int32_t *bad) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint64_t kv[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) kv[j] = lane + kWave * j < E ? kz[lane + kWave * j] : 0ull;
+  int my_id = 0, first = 0;
+  for (int r = 0; r < k; ++r) {
+    uint64_t best = kv[0];
+#pragma unroll
+    for (int j = 1; j < 4; ++j) best = kv[j] > best ? kv[j] : best;
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+      const uint64_t o = __shfl_xor(best, off, kWave);
+      best = o > best ? o : best;
+    }
+    const int e = 255 - (int)(best & 0xffu);
+    if (lane == (e & (kWave - 1))) kv[e / kWave] = 0ull;  // taken
+    if (lane == r) my_id = e;
+    if (r == 0) first = e;
+  }
+  const float z0 = z[first], zl = lane < k ? z[my_id] : 0.f;
+  const bool ok = __ballot(lane < k && !isfinite(zl)) == 0;
+  const float ex = lane < k && ok ? expf(zl - z0) : 0.f;
+  float sum = ex;
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+  id = ok ? my_id : 0x7fffffff;
+  wt = ok ? ex / sum : 0.f;
+  if (lane == 0 && !ok) *bad = 1;
+}
+
 // Router of a small multi-token call (T <= kMtTokens), second kernel (one
-// block): each token's routing as in decode (route_token over its own
-// partials), then one slot-table step for the union S of the tokens' routed
-// experts, and a work list: the misses' copies and, per token, its k experts'
-// slots in rank order.  If |S| exceeds the slots (slots would be reused
-// inside the call) the table is left untouched and the work list empty;
-// flag (host memory) gets 0 (done), 1 (|S| > C) or 2 (routing failure, also
-// in the error word).
+// block): every token's logits (the decode router's sums), top-k and softmax
+// by one wave per token, then one slot-table step for the union S of the
+// tokens' routed experts, and a work list: the misses' copies, per token its
+// k experts' slots in rank order, and per union expert its tokens.  If |S|
+// exceeds the slots (slots would be reused inside the call) the table is
+// left untouched and the work list empty; flag[0] (host memory) gets 0
+// (done), 1 (|S| > C) or 2 (routing failure, also in the error word) and
+// flag[1] the union's size.
 __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     const float *__restrict__ partial, int nb, int T, int E, int k, int32_t *idx, float *w, LruDev lru,
     MtWork *mw, int32_t *flag) {
-  __shared__ RouteLds rl;
+  __shared__ float redL[kThreads * kMtTokens];  // [phase][token][expert] partial sums (phases * E <= 256)
+  __shared__ float zL[kMtTokens][256];
+  __shared__ uint64_t keyL[kMtTokens][256];
   __shared__ StepLds sl;
   __shared__ int32_t selL[kMtTokens][kMaxRouted];
-  __shared__ int32_t slotL[256];
+  __shared__ uint32_t tokL[256];   // bit t: token t routes the expert
+  __shared__ int32_t slotL[256], uL[256];
   __shared__ int32_t badL;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
   int so = -1;
   int64_t st = 0;
   if (tid < E) {
@@ -564,14 +605,15 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   const int64_t clock0 = lru.meta[0], step = lru.meta[1], used = lru.meta[2];
   const uint64_t tn = lru.trace ? *lru.trace_n : 0;
   if (tid == 0) badL = 0;
+  tokL[tid] = 0u;
   // every token's partials in one round trip (nb <= kMtParts): thread (c, ph)
-  // adds, per token, blocks [ph * per, ph * per + per) of expert c in block order
+  // adds, per token, blocks [ph * per, ph * per + per) of expert c in block
+  // order (unconditional loads at clamped, valid addresses, selected
+  // afterwards: a guarded load becomes a branch with its own wait)
   const int64_t pstride = (int64_t)nb * E + 1;
   const int phases = kThreads / E;
   const int c = tid % E, ph = tid / E;
   const int per = (nb + phases - 1) / phases, b0 = ph * per, b1 = min(nb, b0 + per);
-  // (unconditional loads at clamped, valid addresses, selected afterwards: a
-  // guarded load becomes a branch with its own wait)
   float v[kMtTokens][kMtParts], iv[kMtTokens];
 #pragma unroll
   for (int t = 0; t < kMtTokens; ++t) {
@@ -580,25 +622,41 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     for (int j = 0; j < kMtParts; ++j) v[t][j] = partial[tb + (int64_t)min(b0 + j, nb - 1) * E + c];
     iv[t] = partial[tb + (int64_t)nb * E];
   }
-  float sacc[kMtTokens], inv[kMtTokens];
 #pragma unroll
   for (int t = 0; t < kMtTokens; ++t) {
     float a = 0.f;
 #pragma unroll
     for (int j = 0; j < kMtParts; ++j) a += t < T && ph < phases && b0 + j < b1 ? v[t][j] : 0.f;
-    sacc[t] = a;
-    inv[t] = iv[t];
+    if (t < T && ph < phases) redL[(ph * kMtTokens + t) * E + c] = a;
   }
-  bool inS = false;
+  __syncthreads();
+  // z = s * (sum over the phases in order), as route_sum forms it
+  if (tid < E) {
 #pragma unroll
-  for (int t = 0; t < kMtTokens; ++t) {
-    if (t < T) {  // uniform
-      const int rank = route_sum(sacc[t], inv[t], E, k, idx + t * k, w + t * k, nullptr, nullptr, nullptr,
-                                 selL[t], &badL, rl);
-      inS = inS || rank < k;
-      __syncthreads();  // rl is reused by the next token
+    for (int t = 0; t < kMtTokens; ++t) {
+      if (t < T) {
+        float z = 0.f;
+        for (int p = 0; p < phases; ++p) z += redL[(p * kMtTokens + t) * E + tid];
+        z *= iv[t];
+        zL[t][tid] = z;
+        keyL[t][tid] = rank_key(z, tid);
+      }
     }
   }
+  __syncthreads();
+  for (int t = wv; t < T; t += kThreads / kWave) {
+    int32_t id;
+    float wt;
+    wave_topk_keys(keyL[t], zL[t], E, k, id, wt, &badL);
+    if (lane < k) {
+      idx[t * k + lane] = id;
+      w[t * k + lane] = wt;
+      selL[t][lane] = id;
+      if (id >= 0 && id < E) atomicOr(&tokL[id], 1u << t);
+    }
+  }
+  __syncthreads();
+  const bool inS = tid < E && tokL[tid] != 0u;
   const int nS = __syncthreads_count(inS);
   if (badL || nS > lru.C) {  // uniform
     if (tid < T) mw->list[tid].n = 0;
@@ -615,23 +673,22 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   const StepResult o = table_step(lru, E, inS, so, st, 0ull, clock0, step, used, tn, sl);
   if (inS) {
     slotL[tid] = o.fs;
+    uL[tid] = o.rS;
     if (o.miss) {
       mw->src[o.rM] = lru.store + (int64_t)tid * lru.P;
       mw->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
     }
-    // the union entry o.rS: slot and the (token, rank) positions routing here
     mw->upay[o.rS] = lru.slots + (int64_t)o.fs * lru.P;
-    int nt = 0;
-    for (int t = 0; t < T; ++t)
-      for (int j = 0; j < k; ++j)
-        if (selL[t][j] == tid) mw->uq[o.rS][nt++] = (uint8_t)(t * k + j);
-    mw->unt[o.rS] = (uint8_t)nt;
+    mw->unt[o.rS] = (uint8_t)__popc(tokL[tid]);
   }
   __syncthreads();
+  // (token t, rank j): its expert's slot, and its place among the expert's tokens
   for (int i = tid; i < T * k; i += kThreads) {
     const int t = i / k, j = i - t * k;
-    mw->list[t].payload[j] = lru.slots + (int64_t)slotL[selL[t][j]] * lru.P;
+    const int e = selL[t][j];
+    mw->list[t].payload[j] = lru.slots + (int64_t)slotL[e] * lru.P;
     mw->list[t].pos[j] = j;
+    mw->uq[uL[e]][__popc(tokL[e] & ((1u << t) - 1u))] = (uint8_t)i;
   }
   if (tid < T) mw->list[tid].n = k;
   if (tid == 0) {
