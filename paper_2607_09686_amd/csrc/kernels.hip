@@ -23,6 +23,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWave = 64;
 
+// MFMA operand and accumulator vectors.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ float half_bits_to_float(uint32_t bits16) {
   _Float16 h;
   uint16_t b = (uint16_t)bits16;
@@ -700,63 +704,110 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   }
 }
 
-// Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]:
-// a block owns 32 tokens, 128 expert columns (blockIdx.y) and one of
-// `slices` slices of H (blockIdx.z); thread (tt, cc) keeps a 4-token x
-// 4-expert tile of accumulators; K runs over the slice in 32-row steps
-// through LDS.  The top-k kernel adds the slices in order.  Few tokens get
-// many slices (a 5-token call would otherwise read all of W_r with 4 blocks).
-constexpr int kPfTok = 32, kPfRows = 32, kPfCols = 128;
+// Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]
+// on the fp32 matrix cores (v_mfma_f32_16x16x4_f32, fp32 products and sums):
+// a block owns 64 tokens, 128 expert columns (blockIdx.y) and one of `slices`
+// slices of H (blockIdx.z); wave w owns tokens 32 (w & 1) .. +31 (two 16-row
+// subtiles) and experts 64 (w >> 1) .. +63 (four 16-column subtiles).  K runs
+// over the slice in 32-row chunks staged through LDS (x as float4, W_r as
+// coalesced scalars: E need not be a multiple of 4), the next chunk loaded
+// into registers while the current one is multiplied.  The top-k kernel adds
+// the slices in order.  Few tokens get many slices (a 5-token call would
+// otherwise read all of W_r with 4 blocks).
+constexpr int kPfTok = 32;  // token granularity of router_slices
+constexpr int kRtTok = 64, kRtCols = 128, kRtK = 32;
+constexpr int kRtXPitch = 34;   // floats: 16 rows x 2 k of one read on distinct banks
+constexpr int kRtWPitch = 144;  // floats: consecutive k rows 16 banks apart
 
 __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__restrict__ x,
                                                                  const float *__restrict__ wr,
                                                                  int T, int H, int E, int slices,
                                                                  float *__restrict__ zp) {
-  __shared__ float xs[kPfRows][kPfTok + 1];   // [k][token]
-  __shared__ float ws[kPfRows][kPfCols + 4];  // [k][col]
-  const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * kPfTok, c0 = blockIdx.y * kPfCols;
-  const int tt = (tid / 32) * 4, cc = (tid % 32) * 4;  // 8 x 32 threads, 4 x 4 each
-  float acc[4][4];
+  __shared__ __align__(16) float xs[2][kRtTok][kRtXPitch];
+  __shared__ __align__(16) float ws[2][kRtK][kRtWPitch];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int t0 = blockIdx.x * kRtTok, c0 = blockIdx.y * kRtCols;
+  const int per = ((H + slices - 1) / slices + kRtK - 1) / kRtK * kRtK;
+  const int rbeg = blockIdx.z * per, rend = min(H, rbeg + per);  // multiples of 32
+  // loads of one chunk: x rows as float4 (i = tid + 256 m: row i / 8, k 4 (i % 8)),
+  // W_r elements (i = tid + 256 m: k i / 128, column i % 128); clamped, selected on store
+  float4 xv[2];
+  float wvv[16];
+  auto gload = [&](int r0) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-  const int per = ((H + slices - 1) / slices + kPfRows - 1) / kPfRows * kPfRows;
-  const int rbeg = blockIdx.z * per, rend = min(H, rbeg + per);
-  for (int r0 = rbeg; r0 < rend; r0 += kPfRows) {
-    for (int i = tid; i < kPfTok * kPfRows; i += kThreads) {
-      const int t = i / kPfRows, rr = i % kPfRows;
-      xs[rr][t] = (t0 + t < T && r0 + rr < rend) ? x[(int64_t)(t0 + t) * H + r0 + rr] : 0.f;
+    for (int m = 0; m < 2; ++m) {
+      const int i = tid + m * kThreads, row = i >> 3, k4 = (i & 7) * 4;
+      const int t = min(t0 + row, T - 1);
+      xv[m] = *reinterpret_cast<const float4 *>(x + (int64_t)t * H + r0 + k4);
     }
-    for (int i = tid; i < kPfRows * kPfCols; i += kThreads) {
-      const int rr = i / kPfCols, col = i % kPfCols;
-      ws[rr][col] = (r0 + rr < rend && c0 + col < E) ? wr[(int64_t)(r0 + rr) * E + c0 + col] : 0.f;
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const int i = tid + m * kThreads, kk = i >> 7, col = i & (kRtCols - 1);
+      wvv[m] = wr[(int64_t)(r0 + kk) * E + min(c0 + col, E - 1)];
     }
-    __syncthreads();
-#pragma unroll 8
-    for (int rr = 0; rr < kPfRows; ++rr) {
-      float xv[4], wv[4];
+  };
+  auto lstore = [&](int buf) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) xv[i] = xs[rr][tt + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) wv[j] = ws[rr][cc + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(xv[i], wv[j], acc[i][j]);
+    for (int m = 0; m < 2; ++m) {
+      const int i = tid + m * kThreads, row = i >> 3, k4 = (i & 7) * 4;
+      const bool ok = t0 + row < T;
+      float2 *d = reinterpret_cast<float2 *>(&xs[buf][row][k4]);
+      d[0] = ok ? make_float2(xv[m].x, xv[m].y) : make_float2(0.f, 0.f);
+      d[1] = ok ? make_float2(xv[m].z, xv[m].w) : make_float2(0.f, 0.f);
     }
-    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const int i = tid + m * kThreads, kk = i >> 7, col = i & (kRtCols - 1);
+      ws[buf][kk][col] = c0 + col < E ? wvv[m] : 0.f;
+    }
+  };
+  f32x4 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int wrow = 32 * (wv & 1), wcol = 64 * (wv >> 1);
+  int buf = 0;
+  if (rbeg < rend) {
+    gload(rbeg);
+    lstore(0);
   }
+  __syncthreads();
+  for (int r0 = rbeg; r0 < rend; r0 += kRtK) {
+    const bool more = r0 + kRtK < rend;  // uniform
+    if (more) gload(r0 + kRtK);
+#pragma unroll
+    for (int s4 = 0; s4 < kRtK / 4; ++s4) {
+      const int kk = 4 * s4 + (lane >> 4);
+      float av[2], bv[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) av[i] = xs[buf][wrow + 16 * i + (lane & 15)][kk];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bv[q] = ws[buf][kk][wcol + 16 * q + (lane & 15)];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[q], acc[i][q], 0, 0, 0);
+    }
+    if (more) lstore(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+  // C layout (16x16): lane holds rows 4 (lane / 16) + r, column lane % 16
   float *z = zp + (int64_t)blockIdx.z * T * E;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = t0 + tt + i;
-    if (t >= T) continue;
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (c0 + cc + j < E) z[(int64_t)t * E + c0 + cc + j] = acc[i][j];
-  }
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + wrow + 16 * i + 4 * (lane >> 4) + r;
+      if (t >= T) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = c0 + wcol + 16 * q + (lane & 15);
+        if (col < E) z[(int64_t)t * E + col] = acc[i][q][r];
+      }
+    }
 }
 
 // z[t] = tscale[t] * sum of the slices in order; top-k of each token row.
@@ -1849,8 +1900,6 @@ __global__ __launch_bounds__(kThreads) void materialize_list_kernel(const Work *
 //   down:     P[pair] = w_pair * (A_e W_down^T)[row]     [n_e, H]
 // and finally y[t] = (x[t] +) sum over the token's k pairs, in rank order.
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // inv[t] = 1/sqrt(mean(x_t^2) + 1e-6) (or 1); v = x_t * inv[t] as
 // xb[t] = bf16(v) and xb[T*H + t] = bf16(v - bf16(v)).
@@ -1881,60 +1930,129 @@ __global__ __launch_bounds__(kThreads) void prefill_prep_kernel(const float *__r
   }
 }
 
-// counts[e] = number of pairs routed to e (one block per expert).
+// Grouping of the (token, rank) pairs by expert (a stable counting sort).
+// The pair ids are read as 16-byte groups of four; npairs % 4 trailing pairs
+// are read one by one.  Loads are unconditional at clamped, valid addresses
+// and selected afterwards (a guarded load becomes a branch with its own wait).
+constexpr int kGroupBatch = 32;  // 16-byte loads in flight per thread
+
+// counts[e] = number of pairs routed to e; block e scans every pair, its
+// threads taking the 16-byte groups tid, tid + 256, ...
 __global__ __launch_bounds__(kThreads) void group_count_kernel(const int32_t *__restrict__ idx,
                                                                int npairs,
                                                                int32_t *__restrict__ counts) {
   __shared__ int wsum[kThreads / kWave];
-  const int e = blockIdx.x;
+  const int e = blockIdx.x, tid = threadIdx.x;
+  const int n4 = npairs / 4;
+  const int4 *v4 = reinterpret_cast<const int4 *>(idx);
   int c = 0;
-  for (int i = threadIdx.x; i < npairs; i += kThreads) c += idx[i] == e;
+  for (int base = 0; base < n4; base += kThreads * kGroupBatch) {
+    int4 q[kGroupBatch];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(base + tid + m * kThreads, n4 - 1)];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m)
+      if (base + tid + m * kThreads < n4)
+        c += (q[m].x == e) + (q[m].y == e) + (q[m].z == e) + (q[m].w == e);
+  }
+  if (tid < npairs - 4 * n4) c += idx[4 * n4 + tid] == e;
 #pragma unroll
   for (int off = kWave / 2; off >= 1; off >>= 1) c += __shfl_xor(c, off, kWave);
-  if ((threadIdx.x & (kWave - 1)) == 0) wsum[threadIdx.x / kWave] = c;
+  if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = c;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     int tot = 0;
     for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
     counts[e] = tot;
   }
 }
 
+// Exclusive prefix sum of v over the block's threads (all threads call it).
+__device__ __forceinline__ int block_exclusive_scan(int v, int *wsum, int &total) {
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  int inc = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(inc, off, kWave);
+    if (lane >= off) inc += o;
+  }
+  if (lane == kWave - 1) wsum[wv] = inc;
+  __syncthreads();
+  int before = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / kWave; ++w) {
+    if (w < wv) before += wsum[w];
+    total += wsum[w];
+  }
+  return before + inc - v;
+}
+
 // perm[offsets[e] + r] = the r-th pair (in pair order) routed to e;
-// offsets[e] = sum of counts below e, offsets[E] = npairs (block 0 writes it).
+// offsets[e] = sum of counts below e, offsets[E] = npairs (block E-1 writes
+// it).  Thread tid takes a contiguous run of 16-byte groups (the trailing
+// pairs go to the last thread), so one block-wide scan of the threads' hit
+// counts orders the pairs: a first pass counts, a second writes.
 __global__ __launch_bounds__(kThreads) void group_scatter_kernel(const int32_t *__restrict__ idx,
                                                                  int npairs, int E,
                                                                  const int32_t *__restrict__ counts,
                                                                  int32_t *__restrict__ offsets,
                                                                  int32_t *__restrict__ perm) {
-  __shared__ int wcnt[kThreads / kWave];
-  __shared__ int base_s;
-  const int e = blockIdx.x;
-  if (threadIdx.x == 0) {
-    int off = 0;
-    for (int i = 0; i < e; ++i) off += counts[i];
-    base_s = off;
-    offsets[e] = off;
-    if (e == E - 1) offsets[E] = off + counts[e];
-  }
+  __shared__ int wsum[kThreads / kWave];
+  __shared__ int wsum2[kThreads / kWave];
+  const int e = blockIdx.x, tid = threadIdx.x;
+  // offset of e: the counts of the experts below it (E <= 256)
+  int total = 0;
+  const int below = block_exclusive_scan(tid < E ? counts[tid] : 0, wsum, total);
+  __shared__ int off_s;
+  if (tid == e) off_s = below;
   __syncthreads();
-  int base = base_s;
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  for (int i0 = 0; i0 < npairs; i0 += kThreads) {
-    const int i = i0 + threadIdx.x;
-    const bool hit = i < npairs && idx[i] == e;
-    const uint64_t mask = __ballot(hit);
-    const int before = __popcll(mask & ((1ull << lane) - 1ull));
-    if (lane == 0) wcnt[wv] = __popcll(mask);
-    __syncthreads();
-    int woff = 0;
-    for (int w = 0; w < wv; ++w) woff += wcnt[w];
-    int tot = 0;
-    for (int w = 0; w < kThreads / kWave; ++w) tot += wcnt[w];
-    if (hit) perm[base + woff + before] = i;
-    base += tot;
-    __syncthreads();
+  const int off = off_s;
+  if (tid == 0) {
+    offsets[e] = off;
+    if (e == E - 1) offsets[E] = total;
   }
+  const int n4 = npairs / 4, tail = npairs - 4 * n4;
+  const int seg = (n4 + kThreads - 1) / kThreads;  // 16-byte groups per thread
+  const int g0 = min(n4, tid * seg), g1 = min(n4, g0 + seg);
+  const int4 *v4 = reinterpret_cast<const int4 *>(idx);
+  auto hits4 = [&](const int4 &q) {
+    return (q.x == e) + (q.y == e) + (q.z == e) + (q.w == e);
+  };
+  int c = 0;
+  for (int g = g0; g < g1; g += kGroupBatch) {
+    int4 q[kGroupBatch];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(g + m, max(n4 - 1, 0))];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m)
+      if (g + m < g1) c += hits4(q[m]);
+  }
+  const bool last = tid == kThreads - 1;
+  if (last)
+    for (int i = 4 * n4; i < npairs; ++i) c += idx[i] == e;
+  int dummy = 0;
+  int pos = off + block_exclusive_scan(c, wsum2, dummy);
+  if (c == 0) return;  // (no barrier follows)
+  for (int g = g0; g < g1; g += kGroupBatch) {
+    int4 q[kGroupBatch];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(g + m, max(n4 - 1, 0))];
+#pragma unroll
+    for (int m = 0; m < kGroupBatch; ++m) {
+      if (g + m < g1) {
+        const int i = 4 * (g + m);
+        if (q[m].x == e) perm[pos++] = i;
+        if (q[m].y == e) perm[pos++] = i + 1;
+        if (q[m].z == e) perm[pos++] = i + 2;
+        if (q[m].w == e) perm[pos++] = i + 3;
+      }
+    }
+  }
+  if (last)
+    for (int i = 4 * n4; i < npairs; ++i)
+      if (idx[i] == e) perm[pos++] = i;
+  (void)tail;
 }
 
 // One wave's experts for the grouped GEMMs (kernel argument).
@@ -2314,7 +2432,7 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
                                  const float *tscale, float *z, int32_t *idx, float *w, hipStream_t s) {
   const int slices = router_slices(T);
   hipLaunchKernelGGL(router_logits_kernel,
-                     dim3((T + kPfTok - 1) / kPfTok, (E + kPfCols - 1) / kPfCols, slices),
+                     dim3((T + kRtTok - 1) / kRtTok, (E + kRtCols - 1) / kRtCols, slices),
                      dim3(kThreads), 0, s, x, wr, T, H, E, slices, z);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
