@@ -153,6 +153,9 @@ constexpr int kMaxX4 = 8;  // H <= 8192
 // Every block also forms s = 1/sqrt(mean(x^2) + 1e-6) (or 1) from the whole x,
 // in the same order, so all blocks hold the same s; block b writes the digits
 // of its 32-wide block of x * s, and block 0 writes s at partial[nb * E].
+// MULTI: blocks of rpb rows (a multiple of 32) for multi-token calls; else 32 rows
+// (decode: all of the block's loads issued before the first use).
+template <bool MULTI>
 __global__ __launch_bounds__(kThreads) void router_partial_kernel(
     const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int prenorm, int rpb,
     float *__restrict__ partial, int8_t *__restrict__ xq, float *__restrict__ xsc) {
@@ -168,23 +171,34 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
   const int tid = threadIdx.x;
   const int phases = kThreads / E;  // E <= 256
   const int c = tid % E, ph = tid / E;
-  const int r0 = blockIdx.x * rpb;
-  const int r1 = min(H, r0 + rpb);
+  const int rows = MULTI ? rpb : kRouterRowsPerBlock;
+  const int r0 = blockIdx.x * rows;
+  const int r1 = min(H, r0 + rows);
   const int H4 = H / 4;
   const float4 *x4 = reinterpret_cast<const float4 *>(x);
   float acc = 0.f;
-  for (int q0 = r0; q0 < r1; q0 += kRouterRowsPerBlock) {  // 32-row pieces (one for decode)
-    const int q1 = min(r1, q0 + kRouterRowsPerBlock);
-    float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+  float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+  if constexpr (MULTI) {
+    for (int q0 = r0; q0 < r1; q0 += kRouterRowsPerBlock) {  // 32-row pieces
+      const int q1 = min(r1, q0 + kRouterRowsPerBlock);
+#pragma unroll
+      for (int j = 0; j < kRouterRowsPerBlock; ++j) {
+        const int r = q0 + ph + phases * j;
+        const bool ok = ph < phases && r < q1;
+        xv[j] = ok ? x[r] : 0.f;
+        wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
+    }
+  } else {
 #pragma unroll
     for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
-      const int r = q0 + ph + phases * j;
-      const bool ok = ph < phases && r < q1;
+      const int r = r0 + ph + phases * j;
+      const bool ok = ph < phases && r < r1;
       xv[j] = ok ? x[r] : 0.f;
       wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
     }
-#pragma unroll
-    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
   }
   float4 xa[kMaxX4];
 #pragma unroll
@@ -192,8 +206,12 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
     const int i = tid + m * kThreads;
     xa[m] = prenorm && i < H4 ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  const int oct = (r1 - r0) / 32;  // the block's 32-wide blocks of x, one octet of lanes each
+  const int oct = MULTI ? (r1 - r0) / 32 : 1;  // the block's 32-wide blocks of x, an octet of lanes each
   const float4 mine = tid < 8 * oct ? x4[r0 / 4 + tid] : make_float4(0.f, 0.f, 0.f, 0.f);
+  if constexpr (!MULTI) {
+#pragma unroll
+    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
+  }
   float ss = 0.f;
 #pragma unroll
   for (int m = 0; m < kMaxX4; ++m) {
@@ -634,7 +652,7 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     if (t < T && ph < phases) redL[(ph * kMtTokens + t) * E + c] = a;
   }
   __syncthreads();
-  // z = s * (sum over the phases in order), as route_sum forms it
+  // z = s * (sum over the phases in order), as the decode router forms it
   if (tid < E) {
 #pragma unroll
     for (int t = 0; t < kMtTokens; ++t) {
@@ -2400,7 +2418,7 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 const Timing &t) {
   const LruDev none{};
   const int nb = router_decode_grid(H);
-  hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
+  hipExtLaunchKernelGGL(router_partial_kernel<false>, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
                         wr, H, E, (int)prenorm, kRouterRowsPerBlock, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2419,8 +2437,8 @@ hipError_t launch_router_small(const float *x, const float *wr, int T, int H, in
   const int pieces = (H + kRouterRowsPerBlock - 1) / kRouterRowsPerBlock;
   const int rpb = kRouterRowsPerBlock * ((pieces + kMtParts - 1) / kMtParts);
   const int nb = (H + rpb - 1) / rpb;
-  hipExtLaunchKernelGGL(router_partial_kernel, dim3(nb, T), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
-                        wr, H, E, (int)prenorm, rpb, partial, xq, xsc);
+  hipExtLaunchKernelGGL(router_partial_kernel<true>, dim3(nb, T), dim3(kThreads), 0, s, t.start, nullptr, 0,
+                        x, wr, H, E, (int)prenorm, rpb, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(router_finish_mt_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0,
