@@ -2369,15 +2369,34 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
 #undef PF_K_LOOP
 
 // y[t] = (x[t] if residual) + sum_j P[t*k + j], j = 0..k-1 in rank order.
+// One block per token, four values per thread and step (H % 4 == 0), the k
+// rows' loads all issued before the sums.
 __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__restrict__ P,
                                                               const float *__restrict__ x,
                                                               float *__restrict__ y, int H, int k,
                                                               int residual) {
   const int t = blockIdx.x;
-  for (int i = threadIdx.x; i < H; i += kThreads) {
-    float v = residual ? x[(int64_t)t * H + i] : 0.f;
-    for (int jj = 0; jj < k; ++jj) v += P[((int64_t)t * k + jj) * H + i];
-    y[(int64_t)t * H + i] = v;
+  const int H4 = H / 4;
+  const float4 *x4 = reinterpret_cast<const float4 *>(x + (int64_t)t * H);
+  const float4 *P4 = reinterpret_cast<const float4 *>(P + (int64_t)t * k * H);
+  float4 *y4 = reinterpret_cast<float4 *>(y + (int64_t)t * H);
+  for (int i = threadIdx.x; i < H4; i += kThreads) {
+    float4 v = residual ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j0 = 0; j0 < k; j0 += 8) {  // eight rows in flight (clamped to the last row)
+      float4 p[8];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) p[jj] = P4[(int64_t)min(j0 + jj, k - 1) * H4 + i];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (j0 + jj < k) {
+          v.x += p[jj].x;
+          v.y += p[jj].y;
+          v.z += p[jj].z;
+          v.w += p[jj].w;
+        }
+      }
+    }
+    y4[i] = v;
   }
 }
 
