@@ -107,3 +107,36 @@ def test_a3b_verify_full_size():
         assert c.materialized_bytes == c.misses * wl.payload_bytes
     finally:
         st[0].free()
+
+
+@pytest.mark.parametrize("qtype,H,I", [("q8_0", 512, 256), ("q4_0", 256, 384)])
+def test_window_equals_decode_bitwise(qtype, H, I):
+    """A window call of 5 tokens computes each token exactly as a decode call does: at hidden
+    <= 512 the window router uses the decode router's 32-row partial blocks, so routes and
+    weights match bit for bit, and the union GEMVs and the rank-order combine reproduce the
+    decode GEMVs' outputs bit for bit (the slot tables differ: one step for the union against
+    one per token, which changes where experts live, not what is computed)."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, hidden=H, inter=I, n_experts=32, top_k=4,
+                                       n_layers=2, name=f"win_eq_{qtype}")
+    keep, ptr, arr = store_buffer(wl)
+    R = synth.router(wl)
+    Rd = torch.from_numpy(R).cuda()
+    X = np.ascontiguousarray(synth.hidden(wl, n_tokens=5))
+    win = make_cache(wl, ptr, 24, residual=True, prenorm=True)
+    dec = make_cache(wl, ptr, 24, residual=True, prenorm=True)
+    for l in range(wl.n_layers):
+        x = torch.from_numpy(X).cuda()
+        y = torch.empty_like(x)
+        _, iw, ww = win.layer_forward(x, Rd[l], l, y, n_tokens=5, routes=True)
+        yw = y.cpu().numpy()
+        for t in range(5):
+            xt = torch.from_numpy(np.ascontiguousarray(X[t:t + 1])).cuda()
+            yt = torch.empty_like(xt)
+            _, it, wt = dec.layer_forward(xt, Rd[l], l, yt, n_tokens=1, routes=True)
+            assert np.array_equal(it.reshape(-1), iw[t]), (l, t)
+            assert np.array_equal(wt.reshape(-1).view(np.uint32), ww[t].view(np.uint32)), (l, t)
+            assert np.array_equal(yt.cpu().numpy()[0].view(np.uint32), yw[t].view(np.uint32)), (l, t)
+        X = yw
+    win.close()
+    dec.close()
