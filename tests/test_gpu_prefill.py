@@ -54,13 +54,16 @@ def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens
     return flips, err
 
 
-def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=None, seed_shift=0):
+def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=None, seed_shift=0,
+                copy_mode="kernel"):
     torch = torch_cuda()
     log(f"prefill {wl.qtype} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
-        f"L={wl.n_layers} C={budget} T={T} calls={calls} prenorm={prenorm} residual={residual}")
+        f"L={wl.n_layers} C={budget} T={T} calls={calls} prenorm={prenorm} residual={residual} "
+        f"copy_mode={copy_mode}")
     keep, ptr, arr = store if store is not None else store_buffer(wl)
     R = synth.router(wl)
-    cache = make_cache(wl, ptr, budget, trace=True, residual=residual, prenorm=prenorm)
+    cache = make_cache(wl, ptr, budget, trace=True, residual=residual, prenorm=prenorm,
+                       copy_mode=copy_mode)
     lrus = [LayerLRU(wl.n_experts, budget, wl.payload_bytes, l) for l in range(wl.n_layers)]
     want = []
     worst = 0.0
@@ -144,6 +147,17 @@ def test_small_calls_both_paths(qtype, T, budget):
     wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, n_layers=2, hidden=1024, inter=384,
                                        name="tiny_small")
     run_prefill(wl, budget, T, calls=3, prenorm=True, residual=True, seed_shift=T)
+
+
+@pytest.mark.parametrize("copy_mode", ["side", "sdma"])
+@pytest.mark.parametrize("T,budget", [(5, 10), (8, 5)])
+def test_small_calls_host_table(copy_mode, T, budget):
+    """The copy modes that keep the slot tables on the host: calls of up to 8 tokens whose
+    experts fit the slots run the decode GEMVs once per token after the host's table step
+    (5 tokens), others the MFMA GEMMs (8 tokens with 5 slots)."""
+    wl = synth.WORKLOADS["tiny"].with_(n_layers=2, hidden=1024, inter=384, name="tiny_small_host")
+    run_prefill(wl, budget, T, calls=2, prenorm=True, residual=True, seed_shift=T,
+                copy_mode=copy_mode)
 
 
 @pytest.mark.parametrize("T", [3, 5])
