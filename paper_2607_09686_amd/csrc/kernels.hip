@@ -2157,36 +2157,42 @@ struct PfGateUpParams {
 // lane l holds row l % 16 of a 16-row subtile and k = 8 * (l / 16) .. +7 of a
 // 32-wide k slice (16 bytes).  Activation rows are private to the wave that
 // multiplies them, so they skip LDS; only the dequantised weight tile, which
-// all four waves read, is staged there (37 KB, two blocks per CU).
+// all four waves read, is staged there (three 18 KB buffers, two blocks per CU).
 typedef __attribute__((address_space(1))) const bf16x8 g_bf16x8;
 
-// The K loop of both grouped GEMMs, two K steps of 64 per trip with a
-// one-step-ahead prefetch into registers (A: activation fragments, B: the
-// raw weight blocks of the next step) and a double-buffered LDS weight tile.
-// Loads are issued unconditionally (the last trip reloads step KT-1) so that
-// the wait counts the compiler places are exact; the scheduling barriers keep
-// the loads ahead of the MFMAs and the dequantisation after them.
-#define PF_K_LOOP(KT, GLOAD, MMA, DEQ)              \
-  do {                                              \
-    GLOAD(0, A0, B0);                               \
-    DEQ(B0, 0);                                     \
-    __syncthreads();                                \
-    int kt_ = 0;                                    \
-    for (; kt_ + 2 <= (KT); kt_ += 2) {             \
-      GLOAD(kt_ + 1, A1, B1);                       \
-      __builtin_amdgcn_sched_barrier(0);            \
-      MMA(A0, 0);                                   \
-      __builtin_amdgcn_sched_barrier(0);            \
-      DEQ(B1, 1);                                   \
-      __syncthreads();                              \
-      GLOAD(min(kt_ + 2, (KT) - 1), A0, B0);        \
-      __builtin_amdgcn_sched_barrier(0);            \
-      MMA(A1, 1);                                   \
-      __builtin_amdgcn_sched_barrier(0);            \
-      DEQ(B0, 0);                                   \
-      __syncthreads();                              \
-    }                                               \
-    if (kt_ < (KT)) MMA(A0, 0);                     \
+// The K loop of both grouped GEMMs (K steps of 64) with two steps of
+// prefetch: three register sets (A: activation fragments, B: the raw weight
+// blocks of a step) rotate with three LDS weight buffers.  Step kt multiplies
+// set kt % 3 from Bs[kt % 3], dequantises the weights of step kt + 1 into
+// Bs[(kt + 1) % 3] and loads step kt + 2 (clamped to KT - 1) into set
+// (kt + 2) % 3.  Loads are issued unconditionally so that the wait counts the
+// compiler places are exact; the scheduling barriers keep the loads ahead of
+// the MFMAs and the dequantisation after them.  Two steps in flight cover the
+// global loads' latency also while the host-copy kernel runs beside the GEMMs
+// (which inflates it): there the one-step loop took 1.3-1.9x as long.
+#define PF_STEP(S, KT, kt, GLOAD, MMA, DEQ)                             \
+  do {                                                                  \
+    GLOAD(min((kt) + 2, (KT) - 1), A[((S) + 2) % 3], B[((S) + 2) % 3]); \
+    __builtin_amdgcn_sched_barrier(0);                                  \
+    MMA(A[(S)], (S));                                                   \
+    __builtin_amdgcn_sched_barrier(0);                                  \
+    DEQ(B[((S) + 1) % 3], ((S) + 1) % 3);                               \
+    __syncthreads();                                                    \
+  } while (0)
+#define PF_K_LOOP(KT, GLOAD, MMA, DEQ)                                  \
+  do {                                                                  \
+    GLOAD(0, A[0], B[0]);                                               \
+    GLOAD(min(1, (KT) - 1), A[1], B[1]);                                \
+    DEQ(B[0], 0);                                                       \
+    __syncthreads();                                                    \
+    int kt_ = 0;                                                        \
+    for (; kt_ + 3 <= (KT); kt_ += 3) {                                 \
+      PF_STEP(0, KT, kt_, GLOAD, MMA, DEQ);                             \
+      PF_STEP(1, KT, kt_ + 1, GLOAD, MMA, DEQ);                         \
+      PF_STEP(2, KT, kt_ + 2, GLOAD, MMA, DEQ);                         \
+    }                                                                   \
+    if (kt_ < (KT)) PF_STEP(0, KT, kt_, GLOAD, MMA, DEQ);               \
+    if (kt_ + 1 < (KT)) PF_STEP(1, KT, kt_ + 1, GLOAD, MMA, DEQ);       \
   } while (0)
 
 // grid: (M-tiles of the wave's experts, I / 64).  256 threads = 4 waves; wave w
@@ -2196,7 +2202,7 @@ typedef __attribute__((address_space(1))) const bf16x8 g_bf16x8;
 // are not stored.
 template <int QT>
 __global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a) {
-  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];  // rows 0..63 gate, 64..127 up
+  __shared__ __align__(16) __bf16 Bs[3][128][kPfLd];  // rows 0..63 gate, 64..127 up
   constexpr int BB = Fmt<QT>::kBlockBytes;
   int j, m0;
   if (!pf_tile(a.X, blockIdx.x, j, m0)) return;
@@ -2215,8 +2221,8 @@ __global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a
     const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
     arow[i] = (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)(a.H / 8) + (lane >> 4);
   }
-  bf16x8 A0[2][2][2], A1[2][2][2];  // [plane][i][ks]
-  uint32_t B0[9], B1[9];
+  bf16x8 A[3][2][2][2];  // [set][plane][i][ks]
+  uint32_t B[3][9];
   f32x4 accg[2][4], accu[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -2225,7 +2231,7 @@ __global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a
       accg[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
       accu[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-  auto gload = [&](int kt, bf16x8 (&A)[2][2][2], uint32_t (&Bv)[9]) {
+  auto gload = [&](int kt, bf16x8 (&Ar)[2][2][2], uint32_t (&Bv)[9]) {
     load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, Bv);
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
@@ -2233,10 +2239,10 @@ __global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
-          A[pl][i][ks] = xb[arow[i] + pl * lo16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+          Ar[pl][i][ks] = xb[arow[i] + pl * lo16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
   };
   // for each k slice and column subtile: hi then lo plane, both row subtiles
-  auto mma = [&](const bf16x8 (&A)[2][2][2], int buf) {
+  auto mma = [&](const bf16x8 (&Ar)[2][2][2], int buf) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -2248,8 +2254,8 @@ __global__ __launch_bounds__(kThreads, 2) void pf_gateup_kernel(PfGateUpParams a
         for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
-            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bg, accg[i][q], 0, 0, 0);
-            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bu, accu[i][q], 0, 0, 0);
+            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bg, accg[i][q], 0, 0, 0);
+            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bu, accu[i][q], 0, 0, 0);
           }
       }
   };
@@ -2289,7 +2295,7 @@ struct PfDownParams {
 // rows and stores only its first 64 columns.
 template <int QT>
 __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
-  __shared__ __align__(16) __bf16 Bs[2][128][kPfLd];
+  __shared__ __align__(16) __bf16 Bs[3][128][kPfLd];
   constexpr int BB = Fmt<QT>::kBlockBytes;
   int j, m0;
   if (!pf_tile(a.X, blockIdx.x, j, m0)) return;
@@ -2308,14 +2314,14 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
     const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
     arow[i] = (uint32_t)(row0 + m) * (uint32_t)(a.I / 8) + (lane >> 4);
   }
-  bf16x8 A0[2][2][2], A1[2][2][2];
-  uint32_t B0[9], B1[9];
+  bf16x8 A[3][2][2][2];
+  uint32_t B[3][9];
   f32x4 acc[2][8];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto gload = [&](int kt, bf16x8 (&A)[2][2][2], uint32_t (&Bv)[9]) {
+  auto gload = [&](int kt, bf16x8 (&Ar)[2][2][2], uint32_t (&Bv)[9]) {
     load_half<QT>(bptr + (int64_t)kt * 2 * BB, bhalf, Bv);
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
@@ -2323,9 +2329,9 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
-          A[pl][i][ks] = ab[arow[i] + pl * pl16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+          Ar[pl][i][ks] = ab[arow[i] + pl * pl16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
   };
-  auto mma = [&](const bf16x8 (&A)[2][2][2], int buf) {
+  auto mma = [&](const bf16x8 (&Ar)[2][2][2], int buf) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -2336,7 +2342,7 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
         for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
           for (int i = 0; i < 2; ++i)
-            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[pl][i][ks], bf, acc[i][q], 0, 0, 0);
+            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bf, acc[i][q], 0, 0, 0);
       }
   };
   auto deq = [&](const uint32_t (&Bv)[9], int buf) { dequant_half<QT>(Bv, bhalf, &Bs[buf][brow][32 * bhalf]); };
@@ -2367,6 +2373,7 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
     }
 }
 #undef PF_K_LOOP
+#undef PF_STEP
 
 // y[t] = (x[t] if residual) + sum_j P[t*k + j], j = 0..k-1 in rank order.
 // One block per token, four values per thread and step (H % 4 == 0), the k
