@@ -179,12 +179,12 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
   float acc = 0.f;
   float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
   if constexpr (MULTI) {
-    for (int q0 = r0; q0 < r1; q0 += kRouterRowsPerBlock) {  // 32-row pieces
-      const int q1 = min(r1, q0 + kRouterRowsPerBlock);
+    // the block's rows r0 + ph + phases * j, 32 of them per round trip
+    for (int j0 = 0; j0 * phases < rows; j0 += kRouterRowsPerBlock) {
 #pragma unroll
       for (int j = 0; j < kRouterRowsPerBlock; ++j) {
-        const int r = q0 + ph + phases * j;
-        const bool ok = ph < phases && r < q1;
+        const int r = r0 + ph + phases * (j0 + j);
+        const bool ok = ph < phases && r < r1;
         xv[j] = ok ? x[r] : 0.f;
         wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
       }
