@@ -50,6 +50,8 @@ struct MtWork {
   const uint8_t *upay[kMtMaxCopy];
   uint8_t unt[kMtMaxCopy];
   uint8_t uq[kMtMaxCopy][kMtTokens];
+  uint8_t uhit[kMtMaxCopy];  // 1: the expert was resident before the call
+  uint8_t mu[kMtMaxCopy];    // per miss (copy order): its index in the union
 };
 
 // Device-resident slot table of one layer (the rule of slot_lru.h) and where
@@ -187,6 +189,17 @@ bool fusable_copy_gateup(int qtype, int H, int I);
 hipError_t launch_copy_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
                               const WorkList *w, int64_t payload_bytes, int copy_blocks,
                               uint64_t *acc, hipStream_t s, const Timing &t = {});
+
+// The same for a small multi-token call (device work list MtWork): the
+// misses' copies with their tokens' activations formed from the copied
+// rows, and gate/up of the union's hit experts alongside.  Writes the same
+// activation digits as launch_gateup_mt.  Returns hipErrorInvalidValue for a
+// shape it does not take (fusable_copy_gateup_mt false).
+bool fusable_copy_gateup_mt(int qtype, int H, int I, int T);
+hipError_t launch_copy_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc,
+                                 int8_t *hq, float *hsc, int32_t *hds, int H, int I, int k, int T,
+                                 int umax, int64_t payload_bytes, int copy_blocks, uint64_t *acc,
+                                 hipStream_t s, const Timing &t = {});
 
 // Copy n <= max_copy() payloads of `bytes` (multiple of 16, 16-byte aligned)
 // src[i] -> dst[i] with a copy kernel of `grid` blocks (host-pinned or device sources).

@@ -699,9 +699,11 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     if (o.miss) {
       mw->src[o.rM] = lru.store + (int64_t)tid * lru.P;
       mw->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
+      mw->mu[o.rM] = (uint8_t)o.rS;
     }
     mw->upay[o.rS] = lru.slots + (int64_t)o.fs * lru.P;
     mw->unt[o.rS] = (uint8_t)__popc(tokL[tid]);
+    mw->uhit[o.rS] = (uint8_t)!o.miss;
   }
   __syncthreads();
   // (token t, rank j): its expert's slot, and its place among the expert's tokens
@@ -1643,26 +1645,27 @@ struct GateUpMtParams {
 // One token's LDS image for the gate/up GEMV: digit planes, block scales, digit sums.
 __device__ __forceinline__ int mt_image_bytes(int H) { return 3 * plane_bytes(H) + 16 * (H / 32); }
 
-// grid: umax * bpe blocks; block b: union expert b / bpe, rows from
-// (b % bpe) * (256 / lanes).  Dynamic LDS: T images, then [kMtTokens][256 / lanes] floats.
+// Block blk: union expert blk / bpe, rows from (blk % bpe) * (256 / lanes).
+// Dynamic LDS: T images, then [kMtTokens][256 / lanes] floats.  hits_only:
+// the experts copied in by the same launch are left to its copy blocks.
 template <int QT>
-__global__ __launch_bounds__(kThreads) void gateup_mt_kernel(GateUpMtParams a) {
-  extern __shared__ __align__(16) uint8_t smem8[];
+__device__ __forceinline__ void gateup_mt_body(const GateUpMtParams &a, bool hits_only, int blk,
+                                               uint8_t *smem8) {
   __shared__ __align__(16) uint8_t dummyL[16];
   __shared__ int qL[kMtTokens];
   constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords, F = Fmt<QT>::kGateUpFlight;
   const int H = a.H, nb = H / 32, np = nb / 2, pb = plane_bytes(H), img = mt_image_bytes(H);
   const int upb = kThreads / a.lanes;
   const int bpe = (a.I + upb - 1) / upb;
-  const int u = blockIdx.x / bpe;  // < kMtMaxCopy (the launch bounds the grid)
+  const int u = blk / bpe;  // < kMtMaxCopy (the launch bounds the grid)
   // the union's size, this expert's slot, token count and positions (one round trip)
   const int nu = a.W->n_union;
   const uint8_t *const payload = a.W->upay[u];
-  const int nt = a.W->unt[u];
+  const int nt = a.W->unt[u], hit = a.W->uhit[u];
   const int q_t = (int)threadIdx.x < kMtTokens ? a.W->uq[u][threadIdx.x] : 0;
-  if (u >= nu || payload == nullptr) return;  // uniform over the block
+  if (u >= nu || payload == nullptr || (hits_only && !hit)) return;  // uniform over the block
   if ((int)threadIdx.x < kMtTokens) qL[threadIdx.x] = q_t;
-  const int r0 = (blockIdx.x - u * bpe) * upb;
+  const int r0 = (blk - u * bpe) * upb;
   const int r = r0 + (threadIdx.x >> a.lanes_log2);
   const int l = threadIdx.x & (a.lanes - 1);
   const bool active = r < a.I;
@@ -1740,6 +1743,177 @@ __global__ __launch_bounds__(kThreads) void gateup_mt_kernel(GateUpMtParams a) {
     for (int i = 0; i < nt; ++i)
       store_h_digits<QT>(hL[i * upb + threadIdx.x], qL[i], r0 + threadIdx.x, a.I, a.T * a.k, a.hq,
                          a.hsc, a.hds);
+}
+
+// grid: umax * bpe blocks (gateup_mt_body).
+template <int QT>
+__global__ __launch_bounds__(kThreads) void gateup_mt_kernel(GateUpMtParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  gateup_mt_body<QT>(a, false, blockIdx.x, smem8);
+}
+
+// Copy + gate/up of a small multi-token call in one launch, as
+// copy_gateup_kernel does for one token: blocks [0, copy_blocks) move the
+// misses' payloads in chunks of R rows of W_gate and W_up (then the down
+// matrix) and form, from the rows in LDS, the activations of every token
+// routing to the copied expert; the blocks after them run gateup_mt_body for
+// the union's hit experts.  Per (token, row) the lanes, pair order and sums
+// are gateup_mt_body's, so the activations are bit-identical to its result.
+struct CopyGateUpMtParams {
+  GateUpMtParams g;  // token digits, activation outputs, shape, hit-block lanes
+  int64_t P;
+  int copy_blocks, R;  // rows per chunk (R divides 16 and 256 / lanes)
+  uint64_t *acc;       // nullable: += copies, += bytes
+};
+
+// Dynamic LDS: the T token images, hL [kMtTokens][16] floats, one chunk (2 R
+// rows); at least what gateup_mt_body takes.
+template <int QT>
+__global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  const MtWork &W = *a.g.W;
+  if ((int)blockIdx.x >= a.copy_blocks) {  // gate/up of a hit expert
+    gateup_mt_body<QT>(a.g, true, blockIdx.x - a.copy_blocks, smem8);
+    return;
+  }
+  const int n = W.n_copy;
+  if (n == 0) return;
+  if (a.acc && blockIdx.x == 0 && threadIdx.x == 0) {
+    atomicAdd(reinterpret_cast<unsigned long long *>(a.acc), (unsigned long long)n);
+    atomicAdd(reinterpret_cast<unsigned long long *>(a.acc + 1), (unsigned long long)(n * a.P));
+  }
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
+  const int H = a.g.H, I = a.g.I, T = a.g.T, k = a.g.k;
+  const int nb = H / 32, np = nb / 2, pb = plane_bytes(H), img = mt_image_bytes(H);
+  float *hL = reinterpret_cast<float *>(smem8 + T * img);  // [kMtTokens][16]
+  uint8_t *cL = reinterpret_cast<uint8_t *>(hL + kMtTokens * 16);
+  __shared__ int qL[kMtTokens];  // positions of the tokens of the chunk's expert
+  const int R = a.R, cpu = 16 / R;
+  const int64_t rowb = (int64_t)nb * BB, M = (int64_t)I * rowb, half = R * rowb;
+  const int h16 = (int)(half / 16), c16 = 2 * h16;
+  const int upm = I / 16 + I / 32;
+  const int n_units = n * upm;
+  int u = blockIdx.x;
+  if (u >= n_units) return;  // uniform
+  __shared__ __align__(16) uint8_t dummyL[16];
+  for (int t = 0; t < T; ++t) {
+    uint8_t *im = smem8 + t * img;
+    stage_token(a.g.xq + (int64_t)t * 3 * H, a.g.xsc + (int64_t)t * nb, H, im,
+                reinterpret_cast<float *>(im + 3 * pb), dummyL);
+  }
+  // chunk c of unit uu: its two spans, the miss's union index, token count
+  // and (threads < kMtTokens) token positions
+  auto spans = [&](int uu, int c, const uint8_t *&s0, const uint8_t *&s1, uint8_t *&d0, uint8_t *&d1,
+                   int &g, int &nt, int &q) -> bool {
+    const int miss = uu / upm;
+    const int j = uu - miss * upm;
+    int64_t o0, o1;
+    const bool gu = j < I / 16;
+    if (gu) {
+      g = j;
+      o0 = (int64_t)(16 * j + c * R) * rowb;
+      o1 = M + o0;
+    } else {
+      g = -1;
+      o0 = 2 * M + ((int64_t)(j - I / 16) * cpu + c) * 2 * half;
+      o1 = o0 + half;
+    }
+    s0 = W.src[miss] + o0;
+    s1 = W.src[miss] + o1;
+    d0 = W.dst[miss] + o0;
+    d1 = W.dst[miss] + o1;
+    const int um = W.mu[miss];
+    nt = W.unt[um];
+    q = W.uq[um][threadIdx.x & (kMtTokens - 1)];
+    return gu;
+  };
+  uint4 buf[kChunkSlots];
+  auto load_chunk = [&](const uint8_t *s0, const uint8_t *s1) {
+#pragma unroll
+    for (int m = 0; m < kChunkSlots; ++m) {
+      const int q = threadIdx.x + m * kThreads;
+      const uint8_t *p = q < h16 ? s0 + 16 * (int64_t)q : s1 + 16 * (int64_t)(q - h16);
+      buf[m] = q < c16 ? *reinterpret_cast<const uint4 *>(p) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  const uint8_t *s0, *s1;
+  uint8_t *d0, *d1;
+  int g, nt, q, c = 0;
+  bool gu = spans(u, 0, s0, s1, d0, d1, g, nt, q);
+  load_chunk(s0, s1);
+  if constexpr (QT == 2) {
+    __syncthreads();
+    for (int t = 0; t < T; ++t) {
+      uint8_t *im = smem8 + t * img;
+      digit_sums(im, H, reinterpret_cast<int *>(im + 3 * pb + 4 * nb));
+    }
+  }
+  const int L = a.g.lanes, rr = threadIdx.x >> a.g.lanes_log2, l = threadIdx.x & (L - 1);
+  const int tpp = (kThreads / L) / R;  // tokens per pass: row slot rr -> token rr / R, row rr % R
+  const int ri = rr % R;
+  for (;;) {
+#pragma unroll
+    for (int m = 0; m < kChunkSlots; ++m) {
+      const int qq = threadIdx.x + m * kThreads;
+      if (qq < c16) {
+        uint8_t *p = qq < h16 ? d0 + 16 * (int64_t)qq : d1 + 16 * (int64_t)(qq - h16);
+        *reinterpret_cast<uint4 *>(p) = buf[m];
+        if (gu) reinterpret_cast<uint4 *>(cL)[qq] = buf[m];
+      }
+    }
+    if (gu && (int)threadIdx.x < kMtTokens) qL[threadIdx.x] = q;
+    const bool cur_gu = gu;
+    const int cur_c = c, cur_g = g, cur_nt = nt;
+    if (++c == cpu) {
+      c = 0;
+      u += a.copy_blocks;
+    }
+    const bool more = u < n_units;
+    if (more) {
+      gu = spans(u, c, s0, s1, d0, d1, g, nt, q);
+      load_chunk(s0, s1);
+    }
+    __syncthreads();  // chunk and positions in LDS
+    if (cur_gu) {
+      const uint8_t *grow = cL + (int64_t)ri * rowb, *urow = grow + half;
+      for (int i0 = 0; i0 < cur_nt; i0 += tpp) {
+        const int i = i0 + rr / R;
+        const bool act = i < cur_nt;
+        const uint8_t *im = smem8 + (act ? qL[i] / k : 0) * img;
+        const float *scL = reinterpret_cast<const float *>(im + 3 * pb);
+        const int *dsL = reinterpret_cast<const int *>(im + 3 * pb + 4 * nb);
+        float gs = 0.f, us = 0.f;
+        for (int p = act ? l : np; p < np; p += L) {
+          uint32_t wg[PD], wu[PD];
+          const uint32_t *gp = reinterpret_cast<const uint32_t *>(grow + (int64_t)p * 2 * BB);
+          const uint32_t *up = reinterpret_cast<const uint32_t *>(urow + (int64_t)p * 2 * BB);
+#pragma unroll
+          for (int e = 0; e < PD; ++e) {
+            wg[e] = gp[e];
+            wu[e] = up[e];
+          }
+          uint32_t D[48];
+          load_digits(im, pb, p, D);
+          const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
+          gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+          us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+        }
+        gs = group_sum(gs, L);
+        us = group_sum(us, L);
+        if (l == 0 && act) hL[i * 16 + cur_c * R + ri] = silu(gs) * us;
+      }
+      if (cur_c == cpu - 1) {
+        __syncthreads();
+        if ((int)threadIdx.x < 16 * cur_nt) {
+          const int i = threadIdx.x >> 4, row = threadIdx.x & 15;
+          store_h_digits<QT>(hL[threadIdx.x], qL[i], 16 * cur_g + row, I, T * k, a.g.hq, a.g.hsc,
+                             a.g.hds);
+        }
+      }
+    }
+    __syncthreads();  // LDS free for the next chunk
+    if (!more) break;
+  }
 }
 
 struct DownMtParams {
@@ -2617,6 +2791,61 @@ hipError_t launch_copy_gateup(int qtype, const DecodeScratch &S, int H, int I, i
     hipExtLaunchKernelGGL(copy_gateup_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   else
     hipExtLaunchKernelGGL(copy_gateup_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  return hipGetLastError();
+}
+
+constexpr size_t kMtCopyLds = 160 * 1024;  // LDS one workgroup may take on gfx950
+
+// Rows per chunk of the multi-token fused launch: the largest of 8, 4, 2
+// whose chunk fits the copy slots and whose LDS (T images, hL, the chunk)
+// fits a workgroup; 0 if none does.
+static int mt_copy_rows(int qtype, int H, int I, int T, size_t *lds) {
+  if (!mt_ffn_fits(H, I, T) || I % 32 != 0) return 0;
+  const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
+  const size_t images = (size_t)T * (3 * (size_t)(H / 64) * kPairPitch + 16 * (size_t)(H / 32));
+  for (int R = 8; R >= 2; R /= 2) {
+    const size_t need = images + kMtTokens * 16 * sizeof(float) + 2 * (size_t)R * rowb;
+    if (2 * R * rowb <= (int64_t)kChunkSlots * kThreads * 16 && need <= kMtCopyLds) {
+      if (lds) *lds = std::max(need, mt_gateup_lds(H, T));
+      return R;
+    }
+  }
+  return 0;
+}
+
+bool fusable_copy_gateup_mt(int qtype, int H, int I, int T) {
+  return mt_copy_rows(qtype, H, I, T, nullptr) > 0;
+}
+
+hipError_t launch_copy_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc,
+                                 int8_t *hq, float *hsc, int32_t *hds, int H, int I, int k, int T,
+                                 int umax, int64_t payload_bytes, int copy_blocks, uint64_t *acc,
+                                 hipStream_t s, const Timing &t) {
+  size_t lds = 0;
+  const int R = mt_copy_rows(qtype, H, I, T, &lds);
+  if (R == 0 || copy_blocks < 1 || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
+  CopyGateUpMtParams a{};
+  a.g = GateUpMtParams{W, xq, xsc, hq, hsc, hds, H, I, k, T, 0, 0, 0};
+  pick_lanes(H / 64, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes,
+             a.g.lanes, a.g.mpairs);
+  while ((1 << a.g.lanes_log2) < a.g.lanes) ++a.g.lanes_log2;
+  const int upb = kThreads / a.g.lanes;
+  if (upb % R != 0) return hipErrorInvalidValue;  // a pass covers whole tokens of R rows
+  a.P = payload_bytes;
+  a.copy_blocks = copy_blocks;
+  a.R = R;
+  a.acc = acc;
+  dim3 grid(copy_blocks + umax * ((I + upb - 1) / upb));
+  const void *fn = qtype == 8 ? reinterpret_cast<const void *>(&copy_gateup_mt_kernel<8>)
+                              : reinterpret_cast<const void *>(&copy_gateup_mt_kernel<2>);
+  if (lds > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  if (qtype == 8)
+    hipExtLaunchKernelGGL(copy_gateup_mt_kernel<8>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(copy_gateup_mt_kernel<2>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
   return hipGetLastError();
 }
 

@@ -752,23 +752,32 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
   if (c->dl_trace) c->dl_trace_pending += (int64_t)T * k;
+  // the union's GEMVs (each expert's weights read once; their byte counts are
+  // set once the union's size is known) or, for shapes those kernels do not
+  // take, the decode GEMVs once per token.  By default the union's gate/up
+  // runs inside the copy launch (misses from the rows being copied, hits
+  // alongside), as in decode.
+  const bool union_ffn = mt_ffn_fits(H, I, T);
+  const bool fused = union_ffn && !(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup_mt(d.qtype, H, I, T);
+  const int umax = std::min(T * k, (int)c->C);
+  uint64_t *acc = c->timing_now ? c->dl_copy_acc : nullptr;
   {
     Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
-    HIP_TRY(c, launch_materialize_list(c->mt_work, c->P, kCopyGrid,
-                                       c->timing_now ? c->dl_copy_acc : nullptr, c->main, sp.timing()));
+    if (fused)
+      HIP_TRY(c, launch_copy_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc,
+                                       c->mt_hds, H, I, k, T, umax, c->P, kCopyGrid, acc, c->main,
+                                       sp.timing()));
+    else
+      HIP_TRY(c, launch_materialize_list(c->mt_work, c->P, kCopyGrid, acc, c->main, sp.timing()));
     sp.end();
   }
   const int mode = (d.flags & MOE_F_RESIDUAL) ? 1 : 0;
-  // the union's GEMVs (each expert's weights read once; their byte counts are
-  // set once the union's size is known) or, for shapes those kernels do not
-  // take, the decode GEMVs once per token
-  const bool union_ffn = mt_ffn_fits(H, I, T);
   Span gu(c, c->main, MOE_KIND_GATEUP, 1, 0, 4ull * T * k * H * I);
   Span dn(c, c->main, MOE_KIND_DOWN, 1, 0, 2ull * T * k * H * I);
   if (union_ffn) {
-    const int umax = std::min(T * k, (int)c->C);
-    HIP_TRY(c, launch_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc, c->mt_hds,
-                                H, I, k, T, umax, c->main, gu.timing()));
+    if (!fused)
+      HIP_TRY(c, launch_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc,
+                                  c->mt_hds, H, I, k, T, umax, c->main, gu.timing()));
     HIP_TRY(c, launch_down_mt(d.qtype, c->mt_work, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H, I, k, T,
                               umax, c->main, dn.timing()));
     HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->main));
@@ -805,7 +814,10 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   if (union_ffn && verdict == 0) {
     gu.sp.bytes = (uint64_t)flag[1] * 2 * c->M;
     dn.sp.bytes = (uint64_t)flag[1] * c->M;
-    gu.end();
+    if (fused)
+      gu.discard();  // timed with the copies
+    else
+      gu.end();
     dn.end();
   } else {
     gu.discard();

@@ -140,3 +140,37 @@ def test_window_equals_decode_bitwise(qtype, H, I):
         X = yw
     win.close()
     dec.close()
+
+
+@pytest.mark.parametrize("qtype,H,I,T", [("q8_0", 512, 256, 5), ("q8_0", 1024, 384, 8),
+                                         ("q4_0", 256, 384, 2), ("q4_0", 768, 256, 7)])
+def test_window_fused_copy_equals_split_bitwise(qtype, H, I, T):
+    """The default copy mode runs a window's gate/up inside the copy launch (copied experts
+    from the rows in flight, resident ones alongside); the split mode copies first and then
+    runs the union gate/up kernel.  Over a run of warm-cache windows both give the same routes,
+    outputs and slot trace bit for bit."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, hidden=H, inter=I, n_experts=32, top_k=4,
+                                       n_layers=2, name=f"win_fuse_{qtype}")
+    log(f"fused vs split window: {qtype} H={H} I={I} T={T}")
+    keep, ptr, arr = store_buffer(wl)
+    R = synth.router(wl)
+    Rd = torch.from_numpy(R).cuda()
+    X = np.ascontiguousarray(synth.hidden(wl, n_tokens=4 * T))
+    caches = [make_cache(wl, ptr, 4 * T, residual=True, prenorm=True, trace=True, copy_mode=m)
+              for m in ("kernel", "split")]
+    for call in range(4):
+        xs = np.ascontiguousarray(X[call * T:(call + 1) * T])
+        for l in range(wl.n_layers):
+            outs = []
+            for c in caches:
+                x = torch.from_numpy(xs).cuda()
+                y = torch.empty_like(x)
+                d, idx, w = c.layer_forward(x, Rd[l], l, y, n_tokens=T, routes=True)
+                outs.append((d.as_tuple(), idx, w.view(np.uint32), y.cpu().numpy().view(np.uint32)))
+            (d0, i0, w0, y0), (d1, i1, w1, y1) = outs
+            assert d0 == d1 and np.array_equal(i0, i1) and np.array_equal(w0, w1), (call, l)
+            assert np.array_equal(y0, y1), (call, l)
+    assert caches[0].read_trace() == caches[1].read_trace()
+    for c in caches:
+        c.close()
