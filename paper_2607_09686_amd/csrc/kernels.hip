@@ -1272,6 +1272,80 @@ __global__ __launch_bounds__(kThreads) void gateup_kernel(GateUpParams a) {
 // the hit experts (gateup_body); those of missed positions exit.
 constexpr int kChunkSlots = 9;  // 16-byte loads per lane per chunk: 2 * R * rowb <= 9 * 4096
 
+// Payload byte offsets of the two spans of chunk c of unit j of a miss:
+// gate/up units (j < I/16) hold rows 16 j + c R .. +R-1 of W_gate and of
+// W_up; the down matrix follows in pieces of the same size.  True for a
+// gate/up unit.
+__device__ __forceinline__ bool chunk_spans(int j, int c, int I, int R, int64_t rowb, int64_t &o0,
+                                            int64_t &o1) {
+  const int64_t M = (int64_t)I * rowb, half = R * rowb;
+  if (j < I / 16) {
+    o0 = (int64_t)(16 * j + c * R) * rowb;
+    o1 = M + o0;
+    return true;
+  }
+  o0 = 2 * M + ((int64_t)(j - I / 16) * (16 / R) + c) * 2 * half;
+  o1 = o0 + half;
+  return false;
+}
+
+// One chunk (h16 16-byte pieces of each span) into registers: piece
+// threadIdx.x + 256 m; pieces past the chunk read as zero.
+__device__ __forceinline__ void load_chunk(const uint8_t *s0, const uint8_t *s1, int h16,
+                                           uint4 (&buf)[kChunkSlots]) {
+#pragma unroll
+  for (int m = 0; m < kChunkSlots; ++m) {
+    const int q = threadIdx.x + m * kThreads;
+    const uint8_t *p = q < h16 ? s0 + 16 * (int64_t)q : s1 + 16 * (int64_t)(q - h16);
+    buf[m] = q < 2 * h16 ? *reinterpret_cast<const uint4 *>(p) : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+// The chunk in registers to its slot and, with to_lds, to the LDS chunk image cL.
+__device__ __forceinline__ void store_chunk(const uint4 (&buf)[kChunkSlots], uint8_t *d0, uint8_t *d1,
+                                            int h16, bool to_lds, uint8_t *cL) {
+#pragma unroll
+  for (int m = 0; m < kChunkSlots; ++m) {
+    const int q = threadIdx.x + m * kThreads;
+    if (q < 2 * h16) {
+      uint8_t *p = q < h16 ? d0 + 16 * (int64_t)q : d1 + 16 * (int64_t)(q - h16);
+      *reinterpret_cast<uint4 *>(p) = buf[m];
+      if (to_lds) reinterpret_cast<uint4 *>(cL)[q] = buf[m];
+    }
+  }
+}
+
+// This lane's share of the gate and up dot products of chunk row ri (cL: R
+// rows of W_gate, then R of W_up, `half` bytes apart) with a staged token
+// image: pairs l, l + L, ... in order, none if !act (the gate/up kernels'
+// lanes and order, so the group sums equal theirs bit for bit).
+template <int QT>
+__device__ __forceinline__ void chunk_row_dots(const uint8_t *cL, int ri, int64_t rowb, int64_t half,
+                                               const uint8_t *qL, int pb, const float *scL,
+                                               const int *dsL, int nb, int l, int L, bool act,
+                                               float &gs, float &us) {
+  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
+  const int np = nb / 2;
+  const uint8_t *grow = cL + (int64_t)ri * rowb, *urow = grow + half;
+  gs = 0.f;
+  us = 0.f;
+  for (int p = act ? l : np; p < np; p += L) {
+    uint32_t wg[PD], wu[PD];
+    const uint32_t *gp = reinterpret_cast<const uint32_t *>(grow + (int64_t)p * 2 * BB);
+    const uint32_t *up = reinterpret_cast<const uint32_t *>(urow + (int64_t)p * 2 * BB);
+#pragma unroll
+    for (int e = 0; e < PD; ++e) {
+      wg[e] = gp[e];
+      wu[e] = up[e];
+    }
+    uint32_t D[48];
+    load_digits(qL, pb, p, D);
+    const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
+    gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+    us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+  }
+}
+
 struct CopyGateUpParams {
   GateUpParams g;     // token digits, activation outputs, shape, hit-block lanes
   const WorkList *W;
@@ -1294,16 +1368,16 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
     atomicAdd(reinterpret_cast<unsigned long long *>(a.acc), (unsigned long long)n);
     atomicAdd(reinterpret_cast<unsigned long long *>(a.acc + 1), (unsigned long long)(n * a.P));
   }
-  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
-  const int H = a.g.H, I = a.g.I, nb = H / 32, np = nb / 2, pb = plane_bytes(H);
+  constexpr int BB = Fmt<QT>::kBlockBytes;
+  const int H = a.g.H, I = a.g.I, nb = H / 32, pb = plane_bytes(H);
   uint8_t *qL = smem8;
   float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);
   int *dsL = reinterpret_cast<int *>(scL + nb);
   float *hL = reinterpret_cast<float *>(dsL + 3 * nb);  // [16]
   uint8_t *cL = reinterpret_cast<uint8_t *>(hL + 16);    // one chunk: 2 spans
   const int R = a.R, cpu = 16 / R;                        // chunks per unit
-  const int64_t rowb = (int64_t)nb * BB, M = (int64_t)I * rowb, half = R * rowb;
-  const int h16 = (int)(half / 16), c16 = 2 * h16;        // 16-byte pieces per span / chunk
+  const int64_t rowb = (int64_t)nb * BB, half = R * rowb;
+  const int h16 = (int)(half / 16);                       // 16-byte pieces per span
   const int upm = I / 16 + I / 32;                         // units per miss
   const int n_units = n * upm;
   int u = blockIdx.x;
@@ -1316,16 +1390,8 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
     miss = uu / upm;
     const int j = uu - miss * upm;
     int64_t o0, o1;
-    const bool gu = j < I / 16;
-    if (gu) {
-      g = j;
-      o0 = (int64_t)(16 * j + c * R) * rowb;
-      o1 = M + o0;
-    } else {
-      g = -1;
-      o0 = 2 * M + ((int64_t)(j - I / 16) * cpu + c) * 2 * half;
-      o1 = o0 + half;
-    }
+    const bool gu = chunk_spans(j, c, I, R, rowb, o0, o1);
+    g = gu ? j : -1;
     s0 = W.src[miss] + o0;
     s1 = W.src[miss] + o1;
     d0 = W.dst[miss] + o0;
@@ -1333,19 +1399,11 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
     return gu;
   };
   uint4 buf[kChunkSlots];
-  auto load_chunk = [&](const uint8_t *s0, const uint8_t *s1) {
-#pragma unroll
-    for (int m = 0; m < kChunkSlots; ++m) {
-      const int q = threadIdx.x + m * kThreads;
-      const uint8_t *p = q < h16 ? s0 + 16 * (int64_t)q : s1 + 16 * (int64_t)(q - h16);
-      buf[m] = q < c16 ? *reinterpret_cast<const uint4 *>(p) : make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
   const uint8_t *s0, *s1;
   uint8_t *d0, *d1;
   int miss, g, c = 0;
   bool gu = spans(u, 0, s0, s1, d0, d1, miss, g);
-  load_chunk(s0, s1);
+  load_chunk(s0, s1, h16, buf);
   if constexpr (QT == 2) {
     __syncthreads();
     digit_sums(qL, H, dsL);
@@ -1353,16 +1411,7 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
   // the gate/up kernel's lanes and pair order, so h is bit-identical to its result
   const int L = a.g.lanes, rr = threadIdx.x >> a.g.lanes_log2, l = threadIdx.x & (L - 1);
   for (;;) {
-    // the chunk in buf: to its slot, and (gate/up rows) to LDS
-#pragma unroll
-    for (int m = 0; m < kChunkSlots; ++m) {
-      const int q = threadIdx.x + m * kThreads;
-      if (q < c16) {
-        uint8_t *p = q < h16 ? d0 + 16 * (int64_t)q : d1 + 16 * (int64_t)(q - h16);
-        *reinterpret_cast<uint4 *>(p) = buf[m];
-        if (gu) reinterpret_cast<uint4 *>(cL)[q] = buf[m];
-      }
-    }
+    store_chunk(buf, d0, d1, h16, gu, cL);  // to its slot, and (gate/up rows) to LDS
     const bool cur_gu = gu;
     const int cur_c = c, cur_miss = miss, cur_g = g;
     // next chunk of this block, loads issued before the compute below
@@ -1373,29 +1422,13 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
     const bool more = u < n_units;
     if (more) {
       gu = spans(u, c, s0, s1, d0, d1, miss, g);
-      load_chunk(s0, s1);
+      load_chunk(s0, s1, h16, buf);
     }
     __syncthreads();  // chunk in LDS
     if (cur_gu) {
-      // R rows of h from the chunk: L lanes per row, pairs l, l+L, ...
-      float gs = 0.f, us = 0.f;
-      const int rrc = rr < R ? rr : 0;
-      const uint8_t *grow = cL + (int64_t)rrc * rowb, *urow = grow + half;
-      for (int p = rr < R ? l : np; p < np; p += L) {
-        uint32_t wg[PD], wu[PD];
-        const uint32_t *gp = reinterpret_cast<const uint32_t *>(grow + (int64_t)p * 2 * BB);
-        const uint32_t *up = reinterpret_cast<const uint32_t *>(urow + (int64_t)p * 2 * BB);
-#pragma unroll
-        for (int i = 0; i < PD; ++i) {
-          wg[i] = gp[i];
-          wu[i] = up[i];
-        }
-        uint32_t D[48];
-        load_digits(qL, pb, p, D);
-        const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
-        gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-        us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-      }
+      // R rows of h from the chunk: L lanes per row
+      float gs, us;
+      chunk_row_dots<QT>(cL, rr < R ? rr : 0, rowb, half, qL, pb, scL, dsL, nb, l, L, rr < R, gs, us);
       gs = group_sum(gs, L);
       us = group_sum(us, L);
       if (l == 0 && rr < R) hL[cur_c * R + rr] = silu(gs) * us;
@@ -1782,15 +1815,15 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
     atomicAdd(reinterpret_cast<unsigned long long *>(a.acc), (unsigned long long)n);
     atomicAdd(reinterpret_cast<unsigned long long *>(a.acc + 1), (unsigned long long)(n * a.P));
   }
-  constexpr int BB = Fmt<QT>::kBlockBytes, PD = Fmt<QT>::kPairDwords;
+  constexpr int BB = Fmt<QT>::kBlockBytes;
   const int H = a.g.H, I = a.g.I, T = a.g.T, k = a.g.k;
-  const int nb = H / 32, np = nb / 2, pb = plane_bytes(H), img = mt_image_bytes(H);
+  const int nb = H / 32, pb = plane_bytes(H), img = mt_image_bytes(H);
   float *hL = reinterpret_cast<float *>(smem8 + T * img);  // [kMtTokens][16]
   uint8_t *cL = reinterpret_cast<uint8_t *>(hL + kMtTokens * 16);
   __shared__ int qL[kMtTokens];  // positions of the tokens of the chunk's expert
   const int R = a.R, cpu = 16 / R;
-  const int64_t rowb = (int64_t)nb * BB, M = (int64_t)I * rowb, half = R * rowb;
-  const int h16 = (int)(half / 16), c16 = 2 * h16;
+  const int64_t rowb = (int64_t)nb * BB, half = R * rowb;
+  const int h16 = (int)(half / 16);
   const int upm = I / 16 + I / 32;
   const int n_units = n * upm;
   int u = blockIdx.x;
@@ -1808,16 +1841,8 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
     const int miss = uu / upm;
     const int j = uu - miss * upm;
     int64_t o0, o1;
-    const bool gu = j < I / 16;
-    if (gu) {
-      g = j;
-      o0 = (int64_t)(16 * j + c * R) * rowb;
-      o1 = M + o0;
-    } else {
-      g = -1;
-      o0 = 2 * M + ((int64_t)(j - I / 16) * cpu + c) * 2 * half;
-      o1 = o0 + half;
-    }
+    const bool gu = chunk_spans(j, c, I, R, rowb, o0, o1);
+    g = gu ? j : -1;
     s0 = W.src[miss] + o0;
     s1 = W.src[miss] + o1;
     d0 = W.dst[miss] + o0;
@@ -1828,19 +1853,11 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
     return gu;
   };
   uint4 buf[kChunkSlots];
-  auto load_chunk = [&](const uint8_t *s0, const uint8_t *s1) {
-#pragma unroll
-    for (int m = 0; m < kChunkSlots; ++m) {
-      const int q = threadIdx.x + m * kThreads;
-      const uint8_t *p = q < h16 ? s0 + 16 * (int64_t)q : s1 + 16 * (int64_t)(q - h16);
-      buf[m] = q < c16 ? *reinterpret_cast<const uint4 *>(p) : make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
   const uint8_t *s0, *s1;
   uint8_t *d0, *d1;
   int g, nt, q, c = 0;
   bool gu = spans(u, 0, s0, s1, d0, d1, g, nt, q);
-  load_chunk(s0, s1);
+  load_chunk(s0, s1, h16, buf);
   if constexpr (QT == 2) {
     __syncthreads();
     for (int t = 0; t < T; ++t) {
@@ -1852,15 +1869,7 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
   const int tpp = (kThreads / L) / R;  // tokens per pass: row slot rr -> token rr / R, row rr % R
   const int ri = rr % R;
   for (;;) {
-#pragma unroll
-    for (int m = 0; m < kChunkSlots; ++m) {
-      const int qq = threadIdx.x + m * kThreads;
-      if (qq < c16) {
-        uint8_t *p = qq < h16 ? d0 + 16 * (int64_t)qq : d1 + 16 * (int64_t)(qq - h16);
-        *reinterpret_cast<uint4 *>(p) = buf[m];
-        if (gu) reinterpret_cast<uint4 *>(cL)[qq] = buf[m];
-      }
-    }
+    store_chunk(buf, d0, d1, h16, gu, cL);
     if (gu && (int)threadIdx.x < kMtTokens) qL[threadIdx.x] = q;
     const bool cur_gu = gu;
     const int cur_c = c, cur_g = g, cur_nt = nt;
@@ -1871,33 +1880,17 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
     const bool more = u < n_units;
     if (more) {
       gu = spans(u, c, s0, s1, d0, d1, g, nt, q);
-      load_chunk(s0, s1);
+      load_chunk(s0, s1, h16, buf);
     }
     __syncthreads();  // chunk and positions in LDS
     if (cur_gu) {
-      const uint8_t *grow = cL + (int64_t)ri * rowb, *urow = grow + half;
       for (int i0 = 0; i0 < cur_nt; i0 += tpp) {
         const int i = i0 + rr / R;
         const bool act = i < cur_nt;
         const uint8_t *im = smem8 + (act ? qL[i] / k : 0) * img;
-        const float *scL = reinterpret_cast<const float *>(im + 3 * pb);
-        const int *dsL = reinterpret_cast<const int *>(im + 3 * pb + 4 * nb);
-        float gs = 0.f, us = 0.f;
-        for (int p = act ? l : np; p < np; p += L) {
-          uint32_t wg[PD], wu[PD];
-          const uint32_t *gp = reinterpret_cast<const uint32_t *>(grow + (int64_t)p * 2 * BB);
-          const uint32_t *up = reinterpret_cast<const uint32_t *>(urow + (int64_t)p * 2 * BB);
-#pragma unroll
-          for (int e = 0; e < PD; ++e) {
-            wg[e] = gp[e];
-            wu[e] = up[e];
-          }
-          uint32_t D[48];
-          load_digits(im, pb, p, D);
-          const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
-          gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-          us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-        }
+        float gs, us;
+        chunk_row_dots<QT>(cL, ri, rowb, half, im, pb, reinterpret_cast<const float *>(im + 3 * pb),
+                           reinterpret_cast<const int *>(im + 3 * pb + 4 * nb), nb, l, L, act, gs, us);
         gs = group_sum(gs, L);
         us = group_sum(us, L);
         if (l == 0 && act) hL[i * 16 + cur_c * R + ri] = silu(gs) * us;
