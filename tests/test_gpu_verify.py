@@ -142,22 +142,27 @@ def test_window_equals_decode_bitwise(qtype, H, I):
     dec.close()
 
 
-@pytest.mark.parametrize("qtype,H,I,T", [("q8_0", 512, 256, 5), ("q8_0", 1024, 384, 8),
-                                         ("q4_0", 256, 384, 2), ("q4_0", 768, 256, 7)])
-def test_window_fused_copy_equals_split_bitwise(qtype, H, I, T):
+@pytest.mark.parametrize("qtype,H,I,T,E,k,C", [
+    ("q8_0", 512, 256, 5, 32, 4, 20), ("q8_0", 1024, 384, 8, 32, 4, 32),
+    ("q4_0", 256, 384, 2, 32, 4, 8), ("q4_0", 768, 256, 7, 32, 4, 28),
+    # 8 tokens x 16 experts: the union lists at their 128-entry capacity
+    ("q8_0", 512, 192, 8, 256, 16, 128),
+    # fewer slots than some windows' unions: those calls take the host-table path in both modes
+    ("q4_0", 512, 256, 6, 64, 8, 30)])
+def test_window_fused_copy_equals_split_bitwise(qtype, H, I, T, E, k, C):
     """The default copy mode runs a window's gate/up inside the copy launch (copied experts
     from the rows in flight, resident ones alongside); the split mode copies first and then
     runs the union gate/up kernel.  Over a run of warm-cache windows both give the same routes,
     outputs and slot trace bit for bit."""
     torch = torch_cuda()
-    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, hidden=H, inter=I, n_experts=32, top_k=4,
-                                       n_layers=2, name=f"win_fuse_{qtype}")
-    log(f"fused vs split window: {qtype} H={H} I={I} T={T}")
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, hidden=H, inter=I, n_experts=E, top_k=k,
+                                       n_layers=2, name=f"win_fuse_{qtype}_{E}")
+    log(f"fused vs split window: {qtype} H={H} I={I} T={T} E={E} k={k} C={C}")
     keep, ptr, arr = store_buffer(wl)
     R = synth.router(wl)
     Rd = torch.from_numpy(R).cuda()
     X = np.ascontiguousarray(synth.hidden(wl, n_tokens=4 * T))
-    caches = [make_cache(wl, ptr, 4 * T, residual=True, prenorm=True, trace=True, copy_mode=m)
+    caches = [make_cache(wl, ptr, C, residual=True, prenorm=True, trace=True, copy_mode=m)
               for m in ("kernel", "split")]
     for call in range(4):
         xs = np.ascontiguousarray(X[call * T:(call + 1) * T])
