@@ -214,6 +214,20 @@ int moe_host_free(void *p);
 int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, int32_t n_streams,
                   double *gb_per_s);
 
+/* Reference durations for the short HBM-bound kernels (the decode down
+ * GEMV reads 13 MB per launch, where a launch's fixed cost is a large part of
+ * its duration): *read_us = the average duration of a plain streaming read of
+ * `bytes` (multiple of 16, at most 1 GiB) from device memory in one launch,
+ * best of three grid sizes, each launch reading a different region of a
+ * buffer at least four times the last-level cache so that its bytes come from
+ * HBM; *empty_us = the same for an empty kernel.  Durations come from the
+ * runtime's kernel start/end stamps, as the library's own span timings do;
+ * `iters` launches per measurement (1..10000).  The probe allocates and frees
+ * its own buffer (max(1 GiB, 4 * bytes)) and stream on the current device.
+ * MOE_EINVAL on a bad argument, MOE_ENOMEM if the buffer cannot be had,
+ * MOE_EHIP on a HIP failure. */
+int moe_probe_hbm_read(uint64_t bytes, int32_t iters, double *read_us, double *empty_us);
+
 /* Static budget plan (no HIP dependency, no allocation).  The paper's Native
  * Serving Path section derives the slot count of the routed layers from the
  * requested cache bytes, the routed layer count, the bytes of one expert block,

@@ -5,4 +5,5 @@ The library is ``libmoecache.so`` (``include/moecache.h``), built in-tree by
 """
 from .moecache import (HostBuffer, MoeCache, MoeError, SlotTable, Counters,  # noqa: F401
                        KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY, KIND_NAMES, lib,
-                       min_misses, pack_gguf, plan_bytes, plan_percent, probe_h2d)
+                       min_misses, pack_gguf, plan_bytes, plan_percent, probe_h2d,
+                       probe_hbm_read)

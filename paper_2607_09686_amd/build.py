@@ -6,7 +6,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmoecache.so")
-SOURCES = ["kernels.hip", "tables.hip", "moecache.cpp", "slot_lru.cpp", "planner.cpp", "policy.cpp", "pack.cpp"]
+SOURCES = ["kernels.hip", "tables.hip", "probe.hip", "moecache.cpp", "slot_lru.cpp", "planner.cpp", "policy.cpp", "pack.cpp"]
 ARCH = os.environ.get("MOECACHE_ARCH", "gfx950")
 # packed fp32 instructions are disabled: the compiler must not emit them
 HIPFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",

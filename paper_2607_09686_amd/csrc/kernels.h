@@ -212,6 +212,12 @@ hipError_t launch_materialize_list(const WorkList *w, int64_t bytes, int grid, u
 hipError_t launch_materialize_list(const MtWork *w, int64_t bytes, int grid, uint64_t *acc,
                                    hipStream_t s, const Timing &t = {});
 
+// Reference launch (probe.hip): a plain streaming read of `bytes` (multiple of
+// 16) from device memory src by `grid` blocks of 256 threads, one word per
+// block to out [grid]; bytes == 0 launches an empty kernel instead.
+hipError_t launch_read_probe(const uint8_t *src, int64_t bytes, int grid, uint32_t *out, hipStream_t s,
+                             const Timing &t = {});
+
 // One layer's slot table to / from a pinned host staging buffer of
 // table_stage_bytes(E, C) bytes (stamp [E] i64 | meta [3] i64 | cnt [4] u64 |
 // err i32 | pad | slot_of [E] i32 | expert_in [C] i32), one kernel each way;

@@ -1123,6 +1123,63 @@ int moe_probe_h2d(const void *host_src, uint64_t chunk_bytes, int32_t n_chunks, 
   return rc;
 }
 
+int moe_probe_hbm_read(uint64_t bytes, int32_t iters, double *read_us, double *empty_us) {
+  if (!read_us || !empty_us || bytes == 0 || bytes % 16 || bytes > (1ull << 30) || iters < 1 ||
+      iters > 10000)
+    return fail(MOE_EINVAL, "moe_probe_hbm_read: bad arguments");
+  // read consecutive regions of a buffer four times the size of the 256 MiB
+  // last-level cache (or of 4 regions), so that no launch finds its bytes cached
+  const uint64_t span = std::max<uint64_t>(1ull << 30, 4 * bytes);
+  const uint64_t regions = span / bytes;
+  constexpr int kGrids[] = {256, 512, 2048};
+  uint8_t *buf = nullptr;
+  uint32_t *out = nullptr;
+  hipEvent_t start = nullptr, stop = nullptr;
+  hipStream_t s = nullptr;
+  auto cleanup = [&]() {
+    if (s) (void)hipStreamDestroy(s);
+    if (start) (void)hipEventDestroy(start);
+    if (stop) (void)hipEventDestroy(stop);
+    (void)hipFree(buf);
+    (void)hipFree(out);
+  };
+  if (hipMalloc(&buf, span) != hipSuccess || hipMalloc(&out, 2048 * sizeof(uint32_t)) != hipSuccess) {
+    cleanup();
+    return fail(MOE_ENOMEM, "moe_probe_hbm_read: %llu-byte buffer", (unsigned long long)span);
+  }
+  bool ok = hipEventCreate(&start) == hipSuccess && hipEventCreate(&stop) == hipSuccess &&
+            hipStreamCreateWithFlags(&s, hipStreamNonBlocking) == hipSuccess &&
+            hipMemsetAsync(buf, 0x5a, span, s) == hipSuccess && hipStreamSynchronize(s) == hipSuccess;
+  // average duration of `n` single launches, each timed by its own kernel events
+  auto time = [&](uint64_t nbytes, int grid, int n, uint64_t &region, double &avg_us) {
+    double tot = 0.0;
+    for (int j = -2; ok && j < n; ++j) {  // two untimed warm-up launches
+      const uint8_t *src = buf + (region++ % regions) * nbytes;
+      float ms = 0.f;
+      ok = launch_read_probe(src, (int64_t)nbytes, grid, out, s, Timing{start, stop}) == hipSuccess &&
+           hipEventSynchronize(stop) == hipSuccess && hipEventElapsedTime(&ms, start, stop) == hipSuccess;
+      if (j >= 0) tot += ms;
+    }
+    avg_us = 1e3 * tot / n;
+  };
+  uint64_t region = 0;
+  double best = 0.0, empty = 0.0;
+  for (int g : kGrids) {
+    double us = 0.0;
+    time(bytes, g, iters, region, us);
+    if (ok && (best == 0.0 || us < best)) best = us;
+  }
+  time(0, kGrids[0], iters, region, empty);
+  if (!ok) {
+    cleanup();
+    return fail(MOE_EHIP, "moe_probe_hbm_read: HIP call failed");
+  }
+  *read_us = best;
+  *empty_us = empty;
+  cleanup();
+  return MOE_OK;
+}
+
 }  // extern "C"
 
 namespace {

@@ -132,6 +132,7 @@ def lib():
         "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
         "moe_host_free": ([vp], ctypes.c_int),
         "moe_probe_h2d": ([vp, u64, i32, i32, P(ctypes.c_double)], ctypes.c_int),
+        "moe_probe_hbm_read": ([u64, i32, P(ctypes.c_double), P(ctypes.c_double)], ctypes.c_int),
         "moe_lru_create": ([i32, i32, u64, i32, P(vp)], ctypes.c_int),
         "moe_lru_step": ([vp, P(i32), i32, P(StepRec), P(i32)], ctypes.c_int),
         "moe_lru_counters": ([vp, P(Counters)], ctypes.c_int),
@@ -290,6 +291,14 @@ class MoeCache:
             self.close()
         except Exception:
             pass
+
+
+def probe_hbm_read(nbytes, iters=50):
+    """(read_us, empty_us): one plain streaming read of nbytes from HBM per launch, and an empty
+    launch, average kernel durations (moe_probe_hbm_read)."""
+    r, e = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(lib().moe_probe_hbm_read(nbytes, iters, ctypes.byref(r), ctypes.byref(e)))
+    return r.value, e.value
 
 
 def probe_h2d(host_ptr, chunk_bytes, n_chunks, n_streams=1):

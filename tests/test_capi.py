@@ -103,3 +103,13 @@ def test_null_handle_calls_fail_cleanly(mc):
     assert L.moe_cache_counters(None, -1, ctypes.byref(c)) == mc.MOE_EINVAL
     assert L.moe_cache_reset(None) == mc.MOE_EINVAL
     assert L.moe_layer_forward(None, None, 1, None, 0, None, None) == mc.MOE_EINVAL
+
+
+def test_probes_reject_bad_arguments_before_touching_hip(mc):
+    L = mc.lib()
+    r, e = ctypes.c_double(), ctypes.c_double()
+    for nbytes, iters in ((0, 10), (1000, 10), (16 << 30, 10), (1 << 20, 0), (1 << 20, 20000)):
+        assert L.moe_probe_hbm_read(nbytes, iters, ctypes.byref(r), ctypes.byref(e)) == mc.MOE_EINVAL
+    assert L.moe_probe_hbm_read(1 << 20, 10, None, ctypes.byref(e)) == mc.MOE_EINVAL
+    g = ctypes.c_double()
+    assert L.moe_probe_h2d(None, 1 << 20, 1, 1, ctypes.byref(g)) == mc.MOE_EINVAL

@@ -291,3 +291,16 @@ def test_argument_errors():
     assert e.value.code == moecache.MOE_EINVAL
     with pytest.raises(MoeError):
         make_cache(wl, ptr, 17)
+
+
+def test_hbm_read_probe():
+    """The reference launches: a plain read of 13 MB and of 256 MB takes longer than an empty
+    launch, and neither is faster than the HBM peak (the loads are not dropped)."""
+    torch_cuda()
+    from paper_2607_09686_amd import probe_hbm_read
+    for nbytes, iters in ((13369344, 20), (256 << 20, 5)):
+        read_us, empty_us = probe_hbm_read(nbytes, iters)
+        log(f"plain read of {nbytes} B: {read_us:.2f} us ({nbytes / read_us / 1e3:.0f} GB/s); "
+            f"empty launch {empty_us:.2f} us")
+        assert 0.0 < empty_us < read_us
+        assert nbytes / read_us / 1e3 < 8000.0
