@@ -283,6 +283,13 @@ def test_argument_errors():
     assert e.value.code == moecache.MOE_EINVAL
     with pytest.raises(MoeError):
         cache.layer_forward(x[:wl.hidden], R, 0, x[wl.hidden // 2: wl.hidden // 2 + wl.hidden])
+    # an empty call is an argument error and leaves the table alone
+    with pytest.raises(MoeError) as e:
+        cache.layer_forward(x[:0], R, 0, y[:0], n_tokens=0)
+    assert e.value.code == moecache.MOE_EINVAL
+    assert moecache.lib().moe_layer_forward(cache.handle, x.data_ptr(), -1, R.data_ptr(), 0,
+                                            y.data_ptr(), None) == moecache.MOE_EINVAL
+    assert cache.counters().as_tuple() == (0, 0, 0, 0)
     cache.layer_forward(x[:wl.hidden], R, 0, y)     # still usable after argument errors
     cache.close()
     pageable = np.zeros(wl.store_bytes, np.uint8)
