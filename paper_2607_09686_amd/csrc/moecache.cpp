@@ -118,6 +118,9 @@ struct moe_cache {
   float *mt_hsc = nullptr;      // [kMtTokens * k * I / 16]
   int32_t *mt_hds = nullptr;    // [3][kMtTokens * k * I / 16]
   float *mt_R = nullptr;        // [kMtTokens * k][H] unweighted down rows
+  // per-chunk work lists of small calls on the host-table path (device, pinned staging)
+  MtWork *pf_mt_dev = nullptr, *pf_mt_host = nullptr;
+  int pf_mt_cap = 0;
   int64_t dl_trace_cap = 0, dl_trace_pending = 0;
   uint8_t *dl_stage = nullptr;      // pinned staging of one layer's table
   bool table_pulled = false;        // a multi-token call holds the layer's table on the host
@@ -291,6 +294,8 @@ void free_all(moe_cache *c) {
   (void)hipFree(c->mt_hsc);
   (void)hipFree(c->mt_hds);
   (void)hipFree(c->mt_R);
+  (void)hipFree(c->pf_mt_dev);
+  if (c->pf_mt_host) (void)hipHostFree(c->pf_mt_host);
   if (c->mt_flag) (void)hipHostFree(c->mt_flag);
   if (c->dl_stage) (void)hipHostFree(c->dl_stage);
   if (c->host_idx) (void)hipHostFree(c->host_idx);
@@ -330,9 +335,22 @@ int ensure_tokens(moe_cache *c, int64_t T) {
 constexpr int64_t kTraceCap = 1 << 16;  // device trace records kept between drains
 
 
+// The union GEMVs' activations and down rows for calls of up to kMtTokens
+// tokens (every copy mode: the host-table path uses them too).
+int alloc_mt_buffers(moe_cache *c) {
+  const size_t mtKI = (size_t)kMtTokens * c->d.top_k * c->d.inter;
+  if (hipMalloc(&c->mt_hq, 3 * mtKI) != hipSuccess ||
+      hipMalloc(&c->mt_hsc, mtKI / 16 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->mt_hds, 3 * mtKI / 16 * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->mt_R, (size_t)kMtTokens * c->d.top_k * c->d.hidden * sizeof(float)) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MOE_ENOMEM, "cannot allocate the multi-token activation buffers");
+  }
+  return MOE_OK;
+}
+
 int alloc_dev_tables(moe_cache *c) {
   const int64_t L = c->d.n_layers, E = c->d.n_experts, C = c->C;
-  const size_t mtKI = (size_t)kMtTokens * c->d.top_k * c->d.inter;
   if (hipMalloc(&c->dl_slot_of, L * E * 4) != hipSuccess ||
       hipMalloc(&c->dl_expert_in, L * C * 4) != hipSuccess ||
       hipMalloc(&c->dl_stamp, L * E * 8) != hipSuccess || hipMalloc(&c->dl_meta, L * 3 * 8) != hipSuccess ||
@@ -343,10 +361,6 @@ int alloc_dev_tables(moe_cache *c) {
       hipMalloc(&c->mt_partial, ((size_t)router_decode_grid(c->d.hidden) * E + 1) * kMtTokens *
                                     sizeof(float)) != hipSuccess ||
       hipMalloc(&c->mt_work, sizeof(MtWork)) != hipSuccess ||
-      hipMalloc(&c->mt_hq, 3 * mtKI) != hipSuccess ||
-      hipMalloc(&c->mt_hsc, mtKI / 16 * sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->mt_hds, 3 * mtKI / 16 * sizeof(int32_t)) != hipSuccess ||
-      hipMalloc(&c->mt_R, (size_t)kMtTokens * c->d.top_k * c->d.hidden * sizeof(float)) != hipSuccess ||
       hipHostMalloc(&c->mt_flag, 2 * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->dl_stage, table_stage_bytes((int)E, (int)C), hipHostMallocDefault) !=
           hipSuccess) {
@@ -931,6 +945,7 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
     return fail(MOE_EHIP, "HIP setup failed");
   }
   rc = ensure_tokens(c, 1);
+  if (!rc) rc = alloc_mt_buffers(c);
   c->dev_lru = !(desc->flags & (MOE_F_SIDE_COPY | MOE_F_SDMA_COPY));
   if (!rc && c->dev_lru) {
     rc = alloc_dev_tables(c);
@@ -1309,6 +1324,23 @@ int small_call_ffn(moe_cache *c, const float *x, int32_t T, int32_t layer, float
 // the expert that held it (if it is routed in this call) has been computed:
 // the copy stream waits for that expert's chunk, and a chunk is closed early
 // when one of its own experts would be evicted by the next miss.
+// Room for n per-chunk work lists.  Called after the call's routing has been
+// waited for, so no earlier call's copies of these lists are still pending.
+int ensure_mt_chunks(moe_cache *c, int n) {
+  if (n <= c->pf_mt_cap) return MOE_OK;
+  (void)hipFree(c->pf_mt_dev);
+  if (c->pf_mt_host) (void)hipHostFree(c->pf_mt_host);
+  c->pf_mt_dev = c->pf_mt_host = nullptr;
+  c->pf_mt_cap = 0;
+  if (hipMalloc(&c->pf_mt_dev, (size_t)n * sizeof(MtWork)) != hipSuccess ||
+      hipHostMalloc(&c->pf_mt_host, (size_t)n * sizeof(MtWork), hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MOE_ENOMEM, "cannot allocate %d chunk work lists", n);
+  }
+  c->pf_mt_cap = n;
+  return MOE_OK;
+}
+
 int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer,
                          float *y, moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
@@ -1406,6 +1438,17 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   }
   // chunk i: pf_ev[2i] = its copies done (caller's stream), pf_ev[2i+1] = computed (side)
   HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_route, 0));
+  // a call of at most kMtTokens tokens (here: more routed experts than slots)
+  // runs each chunk's experts through the union GEMVs, fp32-accurate like the
+  // decode path, instead of the bf16 GEMMs sized for many tokens: the token
+  // digits once, then per chunk a work list naming its experts, their slots
+  // and the (token, rank) positions routed to each
+  const bool mt = T <= kSmallTokens && mt_ffn_fits(H, I, T);
+  if (mt) {
+    if ((rc = ensure_mt_chunks(c, (int)chunks.size()))) return rc;
+    HIP_TRY(c, launch_token_digits(x, T, H, prenorm, c->st_xq, c->st_xsc, c->side));
+  }
+  int mt_positions = 0;
   const int copy_cap = max_copy();
   const uint64_t M = (uint64_t)c->M;
   int waited = -1;
@@ -1442,6 +1485,39 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
       HIP_TRY(c, hipEventRecord(c->pf_ev[2 * ci], c->main));
       HIP_TRY(c, hipStreamWaitEvent(c->side, c->pf_ev[2 * ci], 0));
     }
+    if (mt) {
+      MtWork &h = c->pf_mt_host[ci];
+      h.n_copy = 0;
+      h.n_union = (int32_t)ch.recs.size();
+      uint64_t pos = 0;
+      for (size_t u = 0; u < ch.recs.size(); ++u) {
+        const moe_step_rec &r = c->recs[ch.recs[u]];
+        h.upay[u] = c->slot_ptr(layer, r.slot);
+        h.uhit[u] = 1;
+        int n = 0;
+        for (int q = 0; q < T * k; ++q)
+          if (c->st_host_idx[q] == r.expert && n < kMtTokens) h.uq[u][n++] = (uint8_t)q;
+        h.unt[u] = (uint8_t)n;
+        pos += n;
+      }
+      mt_positions += (int)pos;
+      HIP_TRY(c, hipMemcpyAsync(c->pf_mt_dev + ci, &h, sizeof(MtWork), hipMemcpyHostToDevice, c->side));
+      const int umax = h.n_union;
+      {
+        Span sp(c, c->side, MOE_KIND_GATEUP, 1, umax * 2 * M, pos * 4ull * H * I);
+        HIP_TRY(c, launch_gateup_mt(d.qtype, c->pf_mt_dev + ci, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc,
+                                    c->mt_hds, H, I, k, T, umax, c->side, sp.timing()));
+        sp.end();
+      }
+      {
+        Span sp(c, c->side, MOE_KIND_DOWN, 1, umax * M, pos * 2ull * H * I);
+        HIP_TRY(c, launch_down_mt(d.qtype, c->pf_mt_dev + ci, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H,
+                                  I, k, T, umax, c->side, sp.timing()));
+        sp.end();
+      }
+      HIP_TRY(c, hipEventRecord(c->pf_ev[2 * ci + 1], c->side));
+      continue;
+    }
     PfWave W{};
     uint64_t rows = 0;
     for (int q : ch.recs) {
@@ -1467,7 +1543,16 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
     HIP_TRY(c, hipEventRecord(c->pf_ev[2 * ci + 1], c->side));
   }
   if (!chunks.empty()) HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * chunks.size() - 1], 0));
-  HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
+  if (mt) {
+    if (mt_positions != T * k) {  // every (token, rank) belongs to one routed expert
+      c->poisoned = true;
+      return fail(MOE_EHIP, "routes of a multi-token call do not match its grouping");
+    }
+    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, (d.flags & MOE_F_RESIDUAL) ? 1 : 0,
+                                 c->main));
+  } else {
+    HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
+  }
   return finish_multi(c, T, layer, before, delta, dbg_idx, dbg_w);
 }
 

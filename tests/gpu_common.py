@@ -99,6 +99,22 @@ def replay_trace(calls_by_layer, wl, budget):
     return recs, cnt
 
 
+def union_gemv_fits(H, I, T):
+    """Whether the library's union GEMVs take a call of T tokens at this shape (their token
+    images and activation digits fit the LDS budgets): mirrors mt_ffn_fits in kernels.hip."""
+    pair_pitch = 80
+    gateup_lds = T * (3 * (H // 64) * pair_pitch + 16 * (H // 32)) + 8 * 256 * 4
+    down_lds = T * (3 * (I // 64) * pair_pitch + I)
+    return 1 <= T <= 8 and 3 * T * I // 16 <= 9 * 256 and gateup_lds <= 65536 and down_lds <= 65536
+
+
+def small_call_exact(T, H, I, n_union, budget):
+    """Whether a multi-token call runs the fp32-accurate GEMVs (exact oracle) rather than the
+    bf16 MFMA GEMMs: at most 8 tokens, and either the routed experts fit the slots (decode or
+    union GEMVs) or the union GEMVs take the shape (run per chunk of the host-table path)."""
+    return T <= 8 and (n_union <= budget or union_gemv_fits(H, I, T))
+
+
 def oracle_layer_y(x, wr, store, wl, layer, idx_or, w_or, z, idx_gpu, flipped, bf16=False,
                    tokens=None, prenorm=False):
     """Oracle y of one layer call; for tokens whose top-k flipped at a near-tie the
@@ -139,4 +155,5 @@ def decode_chain(cache, wl, X, routers_dev, record_inputs=True):
 
 
 __all__ = ["log", "store_buffer", "make_cache", "check_routes", "check_y", "replay_trace",
-           "softmax_of", "decode_chain", "oracle_layer_y", "Shape", "moe_layer", "moe_layer_bf16", "TIE_GAP", "Y_TOL"]
+           "softmax_of", "decode_chain", "oracle_layer_y", "union_gemv_fits", "small_call_exact",
+           "Shape", "moe_layer", "moe_layer_bf16", "TIE_GAP", "Y_TOL"]

@@ -1,13 +1,13 @@
 """GPU parity of the multi-token path (many tokens per layer call): bf16 MFMA grouped
-GEMMs compared with the bf16-weight oracle, and calls of at most 8 tokens whose routed
-experts fit the slots (decode GEMVs per token) with the exact oracle; routes, waves of
-slot reuse inside a call (more routed experts than slots), trace and counters exact."""
+GEMMs compared with the bf16-weight oracle, and calls of at most 8 tokens (GEMVs) with the
+exact oracle; routes, waves of slot reuse inside a call (more routed experts than slots),
+trace and counters exact."""
 import numpy as np
 import pytest
 
 import synth
-from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, softmax_of, store_buffer,
-                        torch_cuda)
+from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, small_call_exact, softmax_of,
+                        store_buffer, torch_cuda)
 from oracle import router as oracle_router
 from oracle.layer import Shape, moe_layer, moe_layer_bf16, rms_normalize
 from oracle.lru import LayerLRU
@@ -21,13 +21,10 @@ def oracle_routes(x, wr, k, prenorm):
     return z, idx, w, gap
 
 
-SMALL_TOKENS = 8  # calls this small whose routed experts fit the slots run the decode GEMVs
-
-
-def gemv_call(T, idx, budget):
-    """Whether a multi-token call takes the per-token decode GEMVs (fp32-accurate) instead of
-    the bf16 MFMA GEMMs."""
-    return T <= SMALL_TOKENS and len(np.unique(idx)) <= budget
+def gemv_call(T, idx, budget, H, I):
+    """Whether a multi-token call takes the GEMVs (fp32-accurate) instead of the bf16 MFMA
+    GEMMs."""
+    return small_call_exact(T, H, I, len(np.unique(idx)), budget)
 
 
 def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens=None, budget=None):
@@ -43,7 +40,7 @@ def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens
             w_use[t] = softmax_of(z[t], idx_g[t])
             flips += 1
     toks = list(range(x.shape[0])) if tokens is None else list(tokens)
-    exact = budget is not None and gemv_call(x.shape[0], idx_g, budget)
+    exact = budget is not None and gemv_call(x.shape[0], idx_g, budget, wl.hidden, wl.inter)
     fn = moe_layer if exact else moe_layer_bf16
     yo = fn(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
             prenorm=prenorm)["y"][toks]
@@ -140,8 +137,9 @@ def test_prefill_small(qtype, T, budget):
 @pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
 @pytest.mark.parametrize("T,budget", [(3, 6), (5, 10), (8, 16), (8, 5), (9, 16)])
 def test_small_calls_both_paths(qtype, T, budget):
-    """Calls of up to 8 tokens whose experts fit the slots (decode GEMVs), and calls just past
-    either limit (MFMA): 8 tokens with 5 slots, 9 tokens."""
+    """Calls of up to 8 tokens whose experts fit the slots (union GEMVs), 8 tokens with 5
+    slots (host-table path, slots reused inside the call, the union GEMVs per chunk) and 9
+    tokens (MFMA GEMMs)."""
     # (H, I as in the warm-cache test below: large enough that a bf16 rounding flip on the
     # MFMA side stays far below the tolerance)
     wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, n_layers=2, hidden=1024, inter=384,
@@ -154,7 +152,8 @@ def test_small_calls_both_paths(qtype, T, budget):
 def test_small_calls_host_table(copy_mode, T, budget):
     """The copy modes that keep the slot tables on the host: calls of up to 8 tokens whose
     experts fit the slots run the decode GEMVs once per token after the host's table step
-    (5 tokens), others the MFMA GEMMs (8 tokens with 5 slots)."""
+    (5 tokens), those with more experts than slots the union GEMVs per chunk (8 tokens with
+    5 slots)."""
     wl = synth.WORKLOADS["tiny"].with_(n_layers=2, hidden=1024, inter=384, name="tiny_small_host")
     run_prefill(wl, budget, T, calls=2, prenorm=True, residual=True, seed_shift=T,
                 copy_mode=copy_mode)

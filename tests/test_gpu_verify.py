@@ -6,8 +6,9 @@ multi-token path) through a residual + pre-norm layer stack:
 * the slot trace and counters bit-exact against the oracle LRU stepped once per window
   and layer with the union of the window's routed experts;
 * layer outputs (all calls at the small shape, sampled calls at full size) against the
-  oracle of the path each call takes: exact for windows whose experts fit the slots (decode
-  GEMVs per token), bf16 weights otherwise (MFMA GEMMs).
+  oracle of the path each call takes: exact for the GEMVs (windows whose experts fit the
+  slots, and the host-table path's chunks where the union GEMVs take the shape), bf16
+  weights otherwise (MFMA GEMMs).
 
 Windows follow the verification schedule of the seeded draft outcomes."""
 import numpy as np
@@ -15,7 +16,7 @@ import pytest
 
 import synth
 from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, oracle_layer_y,
-                        replay_trace, store_buffer, torch_cuda)
+                        replay_trace, small_call_exact, store_buffer, torch_cuda)
 from oracle.verify import schedule, window_union
 
 pytestmark = pytest.mark.gpu
@@ -73,9 +74,10 @@ def verify_chain(wl, budget, store, n_check, seed):
         io, wo, z, fl = flips.get((s, l), (None, None, None, []))
         if io is None:
             io, wo, z, fl = check_routes(xin, R[l], wl.top_k, idx[s, l], wts[s, l], prenorm=True)
-        # windows whose experts fit the slots run the decode GEMVs (exact oracle), others the
-        # bf16 MFMA GEMMs (bf16-weight oracle)
-        gemv = W <= 8 and len(window_union(idx[s, l])) <= budget
+        # windows of at most 8 tokens run GEMVs (exact oracle): the union GEMVs, or with more
+        # experts than slots the union GEMVs per chunk of the host-table path when the shape
+        # fits them; others the bf16 MFMA GEMMs (bf16-weight oracle)
+        gemv = small_call_exact(W, wl.hidden, wl.inter, len(window_union(idx[s, l])), budget)
         n_gemv += gemv
         yo = oracle_layer_y(xin, R[l], arr, wl, l, io, wo, z, idx[s, l], fl, bf16=not gemv,
                             prenorm=True)
