@@ -129,6 +129,9 @@ struct moe_cache {
   hipEvent_t ev_route = nullptr, ev_copy = nullptr;
 
   std::vector<SlotLru> lru;
+  // per layer: the last call of at most kSmallTokens tokens routed more experts
+  // than the slots (the next such call goes straight to the host-table path)
+  std::vector<uint8_t> small_overflow;
   std::vector<moe_step_rec> trace;
   size_t trace_head = 0;
   std::vector<moe_step_rec> recs;  // scratch for one call
@@ -846,7 +849,10 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
     return fail(MOE_EHIP, "multi-token table step did not report (flag %d)", verdict);
   }
   if ((d.flags & MOE_F_TIMING) && (rc = drain_timing(c))) return rc;
-  if (verdict == 1) return forward_prefill(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
+  if (verdict == 1) {
+    c->small_overflow[layer] = 1;
+    return forward_prefill(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
+  }
   if (delta || dbg_idx || dbg_w) {
     if ((rc = sync_dev(c))) return rc;
     if (dbg_idx)
@@ -914,6 +920,7 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
     return fail(MOE_EHIP, "no HIP device");
   }
   for (int32_t l = 0; l < desc->n_layers; ++l) c->lru.emplace_back(desc->n_experts, budget_slots, c->P, l);
+  c->small_overflow.assign(desc->n_layers, 0);
 
   const int64_t slot_bytes = (int64_t)desc->n_layers * budget_slots * c->P;
   if (hipMalloc(&c->slots, slot_bytes) != hipSuccess) {
@@ -979,7 +986,10 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
     return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
-  if (c->dev_lru && n_tokens <= kSmallTokens)
+  // a small call tries the device path unless the layer's last small call did
+  // not fit the slots (then the device step would only report that again); the
+  // two paths step the table by the same rule
+  if (c->dev_lru && n_tokens <= kSmallTokens && !c->small_overflow[layer])
     return forward_small_dev(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
   return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
 }
@@ -1044,6 +1054,7 @@ int moe_cache_reset(moe_cache *c) {
   if (!rc) rc = check_dev_error(c);
   if (rc) return rc;
   for (auto &t : c->lru) t.reset();
+  std::fill(c->small_overflow.begin(), c->small_overflow.end(), 0);
   if (c->dev_lru) {
     rc = clear_dev_tables(c);
     if (rc) return rc;
@@ -1394,6 +1405,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   const moe_counters before = t.counters();
   c->recs.clear();
   t.step(S.data(), (int32_t)S.size(), c->recs);
+  if (T <= kSmallTokens) c->small_overflow[layer] = (int)S.size() > c->C;
   if (T <= kSmallTokens && (int)S.size() <= c->C) {
     rc = small_call_ffn(c, x, T, layer, y);
     if (rc) return rc;
