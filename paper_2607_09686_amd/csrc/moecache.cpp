@@ -1452,15 +1452,38 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_route, 0));
   // a call of at most kMtTokens tokens (here: more routed experts than slots)
   // runs each chunk's experts through the union GEMVs, fp32-accurate like the
-  // decode path, instead of the bf16 GEMMs sized for many tokens: the token
-  // digits once, then per chunk a work list naming its experts, their slots
-  // and the (token, rank) positions routed to each
+  // decode path, instead of the bf16 GEMMs sized for many tokens: one work
+  // list per chunk (its experts, their slots and the (token, rank) positions
+  // routed to each), all uploaded at once, and the token digits once
   const bool mt = T <= kSmallTokens && mt_ffn_fits(H, I, T);
+  int mt_positions = 0;
   if (mt) {
     if ((rc = ensure_mt_chunks(c, (int)chunks.size()))) return rc;
+    for (size_t ci = 0; ci < chunks.size(); ++ci) {
+      const Chunk &ch = chunks[ci];
+      MtWork &h = c->pf_mt_host[ci];
+      h.n_copy = 0;
+      h.n_union = (int32_t)ch.recs.size();
+      for (size_t u = 0; u < ch.recs.size(); ++u) {
+        const moe_step_rec &r = c->recs[ch.recs[u]];
+        h.upay[u] = c->slot_ptr(layer, r.slot);
+        h.uhit[u] = 1;
+        int n = 0;
+        for (int q = 0; q < T * k; ++q)
+          if (c->st_host_idx[q] == r.expert && n < kMtTokens) h.uq[u][n++] = (uint8_t)q;
+        h.unt[u] = (uint8_t)n;
+        mt_positions += n;
+      }
+    }
+    // every (token, rank) belongs to one routed expert
+    if (mt_positions != T * k) {
+      c->poisoned = true;
+      return fail(MOE_EHIP, "routes of a multi-token call do not match its grouping");
+    }
+    HIP_TRY(c, hipMemcpyAsync(c->pf_mt_dev, c->pf_mt_host, chunks.size() * sizeof(MtWork),
+                              hipMemcpyHostToDevice, c->side));
     HIP_TRY(c, launch_token_digits(x, T, H, prenorm, c->st_xq, c->st_xsc, c->side));
   }
-  int mt_positions = 0;
   const int copy_cap = max_copy();
   const uint64_t M = (uint64_t)c->M;
   int waited = -1;
@@ -1498,22 +1521,9 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
       HIP_TRY(c, hipStreamWaitEvent(c->side, c->pf_ev[2 * ci], 0));
     }
     if (mt) {
-      MtWork &h = c->pf_mt_host[ci];
-      h.n_copy = 0;
-      h.n_union = (int32_t)ch.recs.size();
+      const MtWork &h = c->pf_mt_host[ci];
       uint64_t pos = 0;
-      for (size_t u = 0; u < ch.recs.size(); ++u) {
-        const moe_step_rec &r = c->recs[ch.recs[u]];
-        h.upay[u] = c->slot_ptr(layer, r.slot);
-        h.uhit[u] = 1;
-        int n = 0;
-        for (int q = 0; q < T * k; ++q)
-          if (c->st_host_idx[q] == r.expert && n < kMtTokens) h.uq[u][n++] = (uint8_t)q;
-        h.unt[u] = (uint8_t)n;
-        pos += n;
-      }
-      mt_positions += (int)pos;
-      HIP_TRY(c, hipMemcpyAsync(c->pf_mt_dev + ci, &h, sizeof(MtWork), hipMemcpyHostToDevice, c->side));
+      for (int u = 0; u < h.n_union; ++u) pos += h.unt[u];
       const int umax = h.n_union;
       {
         Span sp(c, c->side, MOE_KIND_GATEUP, 1, umax * 2 * M, pos * 4ull * H * I);
@@ -1556,10 +1566,6 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   }
   if (!chunks.empty()) HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * chunks.size() - 1], 0));
   if (mt) {
-    if (mt_positions != T * k) {  // every (token, rank) belongs to one routed expert
-      c->poisoned = true;
-      return fail(MOE_EHIP, "routes of a multi-token call do not match its grouping");
-    }
     HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, (d.flags & MOE_F_RESIDUAL) ? 1 : 0,
                                  c->main));
   } else {
