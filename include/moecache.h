@@ -6,7 +6,7 @@
  * the full set of routed-expert weights stays in a large backing store; each
  * MoE layer owns a fixed number of slots for expert weight blocks; the router
  * decides which experts a token needs; a needed expert that holds no slot is
- * copied ("materialised") into one, and the route-to-slot metadata is updated
+ * copied ("materialised") into one, and the expert-to-slot map is updated
  * (the paper's Native Serving Path section; the store layout follows its
  * Split-Pack section: one block of bytes per layer and expert).
  *

@@ -19,8 +19,8 @@ What it computes, in plain fp64 numpy, one obviously-correct step at a time:
   lower bound C + E(p) + K(n) against the serving target   (``planner``)
 
 The paper (its Native Serving Path section) fixes only the mechanism: per-layer
-slot tensors for routed experts, filled on a miss, with route-to-slot
-metadata.  Every finer point (eviction rule, hit granularity, tie-breaks, FFN
+slot tensors for routed experts, filled on a miss, with a map from experts
+to slots.  Every finer point (eviction rule, hit granularity, tie-breaks, FFN
 form, block formats) is a stated reading; each function names the one it uses.
 """
 from . import numerics, quant, router, lru, ffn, layer, planner  # noqa: F401

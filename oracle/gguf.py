@@ -1,7 +1,7 @@
 """GGUF reader and the expected split-pack of a GGUF MoE model (oracle; test infrastructure only).
 
-The paper's Split-Pack Representation section: routed expert tensors are split into
-deterministic per-layer, per-expert blocks.  Here the expected pack is built by the
+The paper's Split-Pack Representation section: routed expert tensors are cut, in a
+fixed order, into one block per layer and expert.  Here the expected pack is built by the
 plainest route: read the whole file, find each expert's three matrices as slices of the
 layer's three expert tensors, and concatenate them per (layer, expert).
 

@@ -1,9 +1,9 @@
 """Per-layer LRU expert-slot table with hit / miss accounting (oracle; test infrastructure only).
 
 The paper's Native Serving Path section: each layer owns a fixed number of
-slots for routed experts; on a miss the runtime materialises the expert's
-block into an available slot and updates the route-to-slot metadata.  The
-paper states no eviction rule; this build uses least-recently-used, with
+slots for routed experts; a miss copies the expert's block into a free slot
+and records which slot now holds that expert.  The paper states no eviction
+rule; this build uses least-recently-used, with
 these readings (listed in the design notes):
 
 For one layer call, S is the ascending set of distinct experts routed by any

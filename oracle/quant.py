@@ -9,7 +9,7 @@ this build's stand-in for its 4-bit profile):
 * Q4_0, 18 bytes per 32 weights: bytes 0-1 scale d; byte 2+j (j < 16) holds
   n_j in its low nibble and n_{j+16} in its high nibble.  Weight is d*(n-8).
 
-Expert payload (the paper's Split-Pack section: per-layer, per-expert blocks;
+Expert payload (the paper's Split-Pack section: one block per layer and expert;
 its Native Serving Path section: separate gate, up and down tensors): one
 contiguous byte range per (layer l, expert e) at offset (l*E + e)*P, laid out
 as [W_gate (inter x hidden) | W_up (inter x hidden) | W_down (hidden x inter)].

@@ -2,9 +2,9 @@
 // tensors are cut into one block per (layer, expert) and written in the
 // expert-store layout the cache reads, with an index of the blocks and the
 // routers in the cache's [hidden][n_experts] fp32 form.  This is the paper's
-// Split-Pack Representation step: expert tensors split into deterministic
-// per-layer, per-expert blocks, each recorded with its kind, layer, expert,
-// source offsets, byte counts, topology and a digest.
+// Split-Pack Representation step: each expert tensor cut, in a fixed order,
+// into one block per layer and expert, and a record per block of its kind,
+// layer, expert, source offsets, byte counts, topology and a digest.
 //
 // GGUF (version 2 or 3): magic "GGUF", version, tensor count, metadata count,
 // the metadata (key string, value type, value), the tensor infos (name, dims,

@@ -1,7 +1,7 @@
 // Per-layer LRU expert-slot table (no HIP dependency).
 //
 // Each MoE layer owns n_slots slots; the table maps expert ids to slots (the
-// route-to-slot metadata of the paper's Native Serving Path section) and picks
+// expert-to-slot map of the paper's Native Serving Path section) and picks
 // the slot a missed expert is materialised into.  Rule for one layer call with
 // routed set S (distinct ids, ascending):
 //   1. stamp[e] = ++clock for every e in S, ascending;
