@@ -18,8 +18,8 @@ What it computes, in plain fp64 numpy, one obviously-correct step at a time:
 * the static budget planner: slots per layer from a cache budget and the
   lower bound C + E(p) + K(n) against the serving target   (``planner``)
 
-The paper (its Native Serving Path section) fixes only the mechanism: per-layer
-slot tensors for routed experts, filled on a miss, with a map from experts
+The paper (its Native Serving Path section) fixes only the mechanism: a fixed
+set of slots per layer for the routed experts, filled on a miss, with a map from experts
 to slots.  Every finer point (eviction rule, hit granularity, tie-breaks, FFN
 form, block formats) is a stated reading; each function names the one it uses.
 """
