@@ -1,8 +1,8 @@
 """GGUF-style block formats and the expert payload layout (oracle; test infrastructure only).
 
 Block formats (GGUF, the llama.cpp model format the paper serves from; the
-paper names the types through its Q8_0 model profiles, the Q4_0 variant is
-this build's stand-in for its 4-bit profile):
+paper names the types through its Q8_0 model profiles; Q4_0 stands in here
+for its 4-bit profile):
 
 * Q8_0, 34 bytes per 32 weights: bytes 0-1 scale d (binary16, little-endian),
   bytes 2-33 signed 8-bit q_j.  Weight j is d * q_j.
