@@ -4,7 +4,7 @@ The paper's Native Serving Path section: each layer owns a fixed number of
 slots for routed experts; a miss copies the expert's block into a free slot
 and records which slot now holds that expert.  The paper states no eviction
 rule; least-recently-used is used here, with these
-readings (listed in the design notes):
+readings:
 
 For one layer call, S is the ascending set of distinct experts routed by any
 token of the call (one lookup per distinct expert per call).

@@ -2,7 +2,7 @@
 
 The paper's introduction and Native Serving Path section say only that the
 router selects each token's routed experts, and that this selection is what
-drives materialisation.  Readings used here (the design notes list them):
+drives materialisation.  Readings used here:
 
 * logits z = x W_r with W_r stored [hidden, n_experts] row-major, fp32 inputs,
   evaluated exactly in fp64;
