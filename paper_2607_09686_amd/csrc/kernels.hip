@@ -1582,14 +1582,17 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
   int *dsL = reinterpret_cast<int *>(scL + n * (I / 16));      // [n][3][I/16]
   float *res = reinterpret_cast<float *>(dsL + 3 * n * (I / 16));  // [rows][n]
   const int j0 = blockIdx.x * a.rows;
+  // consecutive units take consecutive rows of one expert, so the lanes of a
+  // wave that handle the same pair read the same activation digits from LDS
+  // (one broadcast read instead of one per expert); ic: i clamped to the list
   const int unit = threadIdx.x >> a.lanes_log2, l = threadIdx.x & (a.lanes - 1);
-  const int i = unit % n, rr = unit / n, j = j0 + rr;
-  const bool active = rr < a.rows && j < a.H;
+  const int i = unit / a.rows, rr = unit - i * a.rows, j = j0 + rr, ic = min(i, n - 1);
+  const bool active = i < n && j < a.H;
   const int64_t rowb = (int64_t)nb * BB;
   const int64_t mat = (int64_t)I * ((int64_t)(a.H / 32) * BB);
   // the list: count, this unit's slot, the positions (one round trip)
   const int ndev = L.n;
-  const uint8_t *const payload = L.payload[i];
+  const uint8_t *const payload = L.payload[ic];
   const int pos_t = (int)threadIdx.x < n ? L.pos[threadIdx.x] : 0;
   if (ndev != n) return;  // a device list emptied by a routing error (uniform)
   if ((int)threadIdx.x < n) posL[threadIdx.x] = pos_t;
