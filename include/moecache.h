@@ -132,7 +132,9 @@ typedef struct {
 #define MOE_KIND_COUNT 4
 
 /* Create a cache with budget_slots slots per layer (top_k <= budget_slots <=
- * n_experts), all empty.  Allocates n_layers*budget_slots*P bytes of HBM for
+ * n_experts), all empty: the fixed per-layer slot tensors of the paper's
+ * Native Serving Path section, one slot holding one expert's whole block
+ * (gate, up and down), sized once from the budget and never grown.  Allocates n_layers*budget_slots*P bytes of HBM for
  * the slots plus small scratch, on the current HIP device.  MOE_EINVAL on a
  * bad descriptor, MOE_ENOMEM if the slots do not fit. */
 int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache **out);
@@ -171,16 +173,33 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
                           int32_t layer, float *y, moe_counters *delta, int32_t *topk_idx,
                           float *topk_w);
 
-/* Counters since creation or the last reset: one layer, or layer = -1 for the sum. */
+/* Counters since creation or the last reset: one layer, or layer = -1 for the sum.
+ * These are the cache figures the paper's serving telemetry reports (hit rate
+ * and materialised expert bytes; its Native Serving Path and Measurements
+ * sections): hit rate = hits / (hits + misses), one lookup per distinct routed
+ * expert of a layer call. */
 int moe_cache_counters(const moe_cache *c, int32_t layer, moe_counters *out);
 
 /* Move up to cap kept records (MOE_F_TRACE) into buf, oldest first; *n_out
- * gets the number moved.  Records not moved stay for the next read. */
+ * gets the number moved.  Records not moved stay for the next read.  A record
+ * is one decision of the route-to-slot update the paper's Native Serving Path
+ * section describes (hit, or the slot a miss was copied into and the expert it
+ * displaced), so a run's cache behaviour can be replayed and checked. */
 int moe_cache_read_trace(moe_cache *c, moe_step_rec *buf, int64_t cap, int64_t *n_out);
 
-/* Empty every slot, zero counters, drop the trace and timing totals.
- * Synchronises with the handle's streams first. */
+/* Empty every slot, zero counters, drop the trace and timing totals: the cold
+ * cache every run of the paper's validation matrix starts from (its
+ * Experimental Method section).  Synchronises with the handle's streams first. */
 int moe_cache_reset(moe_cache *c);
+
+/* Overwrite every byte of every slot of every layer with `byte` (0..255),
+ * leaving the slot tables as they are.  For tests: after moe_cache_reset (all
+ * slots empty) with byte 0xFF, every block scale in a slot reads as a NaN
+ * until the slot's expert has been copied in, so a kernel that reads a slot
+ * before its copy has landed, or a slot it was not given, shows up as a
+ * non-finite output.  Synchronises with the handle's streams first.
+ * MOE_EINVAL for byte outside 0..255. */
+int moe_cache_fill_slots(moe_cache *c, int32_t byte);
 
 /* Totals of one MOE_KIND_* since creation or reset (needs MOE_F_TIMING).
  * Synchronises with the handle's streams first. */
@@ -316,7 +335,9 @@ typedef struct {
 int moe_pack_gguf(const char *gguf_path, const char *pack_path, const char *index_path,
                   const char *router_path, moe_pack_info *info);
 
-/* The slot table alone, with no HIP dependency (used to check it on the CPU).
+/* The slot table alone, with no HIP dependency (used to check it on the CPU):
+ * the route-to-slot map of the paper's Native Serving Path section, whose
+ * eviction choice the paper leaves open (here least recently used per layer).
  * Same rule as inside moe_layer_forward: for one call with routed experts ids
  * (any order, duplicates allowed), stamp the distinct ids in ascending order,
  * count hits, then give each miss (ascending) the lowest free slot or the slot

@@ -106,7 +106,8 @@ hipError_t launch_router_small(const float *x, const float *wr, int T, int H, in
 // [3][T*k*I/16]), down into R [T*k][H] (unweighted rows), then y_t =
 // (x_t if mode 1) + sum over j in rank order of w[t*k+j] R[t*k+j].  The
 // numerics are those of the decode GEMVs (launch_gateup / launch_down per
-// token).  umax: an upper bound on the union size (the grids); false from
+// token); combine does nothing when W (nullable) is a device list left empty
+// by the table step.  umax: an upper bound on the union size (the grids); false from
 // mt_ffn_fits: a shape these kernels do not take.
 bool mt_ffn_fits(int H, int I, int T);
 size_t mt_gateup_lds(int H, int T);
@@ -117,7 +118,7 @@ hipError_t launch_down_mt(int qtype, const MtWork *W, const int8_t *hq, const fl
                           const int32_t *hds, float *R, int H, int I, int k, int T, int umax,
                           hipStream_t s, const Timing &t = {});
 hipError_t launch_combine_mt(const float *R, const float *w, const float *x, float *y, int H, int k,
-                             int T, int mode, hipStream_t s, const Timing &t = {});
+                             int T, int mode, const MtWork *W, hipStream_t s, const Timing &t = {});
 
 // Prefill router: partial logits over router_slices(T) slices of H into
 // z [slices][T][E] (router_zbuf_floats(T, E) floats cover any call of at most

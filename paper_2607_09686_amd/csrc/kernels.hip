@@ -1648,9 +1648,11 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
   if ((int)threadIdx.x < n) wL[threadIdx.x] = w_t;
   __syncthreads();
   if (out_t) {
-    float v = base_t;
+    // the weighted rows first, then the residual / earlier sum in one addition,
+    // so that a small MoE output on a large residual is rounded once
+    float v = 0.f;
     for (int ii = 0; ii < n; ++ii) v = fmaf(wL[ii], res[threadIdx.x * n + ii], v);
-    a.y[jt] = v;
+    a.y[jt] = base_t + v;
   }
 }
 
@@ -2000,16 +2002,18 @@ __global__ __launch_bounds__(kThreads) void down_mt_kernel(DownMtParams a) {
 }
 
 // y_t[j] = (x_t[j] if mode 1) + sum over ranks r of w[t*k+r] R[t*k+r][j], in rank order.
+// W (nullable): the device work list of the call; an empty one (the union
+// did not fit the slots, or routing failed) leaves y untouched.
 __global__ __launch_bounds__(kThreads) void combine_mt_kernel(const float *__restrict__ R,
                                                               const float *__restrict__ w,
                                                               const float *__restrict__ x,
                                                               float *__restrict__ y, int H, int k,
-                                                              int mode) {
+                                                              int mode, const MtWork *W) {
   const int t = blockIdx.y, j = blockIdx.x * kThreads + threadIdx.x;
-  if (j >= H) return;
-  float v = mode == 1 ? x[(int64_t)t * H + j] : 0.f;
+  if (j >= H || (W && W->n_union == 0)) return;
+  float v = 0.f;  // rows first, then the residual (one rounding at its scale)
   for (int r = 0; r < k; ++r) v = fmaf(w[t * k + r], R[((int64_t)t * k + r) * H + j], v);
-  y[(int64_t)t * H + j] = v;
+  y[(int64_t)t * H + j] = mode == 1 ? x[(int64_t)t * H + j] + v : v;
 }
 
 struct CopyParams {
@@ -2545,7 +2549,7 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
 #undef PF_K_LOOP
 #undef PF_STEP
 
-// y[t] = (x[t] if residual) + sum_j P[t*k + j], j = 0..k-1 in rank order.
+// y[t] = (x[t] if residual) + (sum_j P[t*k + j], j = 0..k-1 in rank order).
 // One block per token, four values per thread and step (H % 4 == 0), the k
 // rows' loads all issued before the sums.
 __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__restrict__ P,
@@ -2558,7 +2562,7 @@ __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__res
   const float4 *P4 = reinterpret_cast<const float4 *>(P + (int64_t)t * k * H);
   float4 *y4 = reinterpret_cast<float4 *>(y + (int64_t)t * H);
   for (int i = threadIdx.x; i < H4; i += kThreads) {
-    float4 v = residual ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);  // rows first, then the residual
     for (int j0 = 0; j0 < k; j0 += 8) {  // eight rows in flight (clamped to the last row)
       float4 p[8];
 #pragma unroll
@@ -2572,6 +2576,10 @@ __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__res
           v.w += p[jj].w;
         }
       }
+    }
+    if (residual) {
+      const float4 r = x4[i];
+      v = make_float4(r.x + v.x, r.y + v.y, r.z + v.z, r.w + v.w);
     }
     y4[i] = v;
   }
@@ -2752,9 +2760,9 @@ hipError_t launch_down_mt(int qtype, const MtWork *W, const int8_t *hq, const fl
 }
 
 hipError_t launch_combine_mt(const float *R, const float *w, const float *x, float *y, int H, int k,
-                             int T, int mode, hipStream_t s, const Timing &t) {
+                             int T, int mode, const MtWork *W, hipStream_t s, const Timing &t) {
   hipExtLaunchKernelGGL(combine_mt_kernel, dim3((H + kThreads - 1) / kThreads, T), dim3(kThreads), 0, s,
-                        t.start, t.stop, 0, R, w, x, y, H, k, mode);
+                        t.start, t.stop, 0, R, w, x, y, H, k, mode, W);
   return hipGetLastError();
 }
 

@@ -797,7 +797,7 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
                                   c->mt_hds, H, I, k, T, umax, c->main, gu.timing()));
     HIP_TRY(c, launch_down_mt(d.qtype, c->mt_work, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H, I, k, T,
                               umax, c->main, dn.timing()));
-    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->main));
+    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->mt_work, c->main));
   } else {
     ExpertList shape{};
     shape.n = k;
@@ -851,6 +851,8 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   if ((d.flags & MOE_F_TIMING) && (rc = drain_timing(c))) return rc;
   if (verdict == 1) {
     c->small_overflow[layer] = 1;
+    // one API call: the host-table path counts it again for the timing stride
+    if (d.flags & MOE_F_TIMING) --c->n_calls;
     return forward_prefill(c, x, T, wr, layer, y, delta, dbg_idx, dbg_w);
   }
   if (delta || dbg_idx || dbg_w) {
@@ -1064,6 +1066,17 @@ int moe_cache_reset(moe_cache *c) {
   c->trace.clear();
   c->trace_head = 0;
   for (auto &s : c->stats) s = moe_kernel_stats{};
+  return MOE_OK;
+}
+
+int moe_cache_fill_slots(moe_cache *c, int32_t byte) {
+  if (!c || byte < 0 || byte > 255) return fail(MOE_EINVAL, "bad arguments");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  HIP_TRY(c, hipStreamSynchronize(c->side));
+  HIP_TRY(c, hipStreamSynchronize(c->main));
+  const size_t bytes = (size_t)c->d.n_layers * c->C * c->P;
+  HIP_TRY(c, hipMemsetAsync(c->slots, byte, bytes, c->main));
+  HIP_TRY(c, hipStreamSynchronize(c->main));
   return MOE_OK;
 }
 
@@ -1567,7 +1580,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   if (!chunks.empty()) HIP_TRY(c, hipStreamWaitEvent(c->main, c->pf_ev[2 * chunks.size() - 1], 0));
   if (mt) {
     HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, (d.flags & MOE_F_RESIDUAL) ? 1 : 0,
-                                 c->main));
+                                 nullptr, c->main));
   } else {
     HIP_TRY(c, launch_pf_combine(c->pf_P, x, y, T, H, k, (d.flags & MOE_F_RESIDUAL) != 0, c->main));
   }

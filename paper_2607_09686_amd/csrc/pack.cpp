@@ -69,7 +69,7 @@ struct Reader {
     return s;
   }
   void skip(uint64_t n) {
-    if (std::fseek(f, (long)n, SEEK_CUR) != 0) ok = false;
+    if (n > (uint64_t)INT64_MAX || fseeko(f, (off_t)n, SEEK_CUR) != 0) ok = false;
   }
 };
 
@@ -99,7 +99,9 @@ bool read_value(Reader &r, uint32_t type, int64_t *ival) {
     } else if (et == 9 || scalar_size(et) == 0) {
       return false;  // nested arrays are not used by the models this reads
     } else {
-      r.skip(n * scalar_size(et));
+      uint64_t bytes = 0;
+      if (__builtin_mul_overflow(n, scalar_size(et), &bytes)) return false;
+      r.skip(bytes);
     }
     return r.ok;
   }
@@ -148,7 +150,8 @@ float half_to_float(uint16_t h) {
 }
 
 bool read_at(std::FILE *f, uint64_t off, void *dst, size_t n) {
-  return std::fseek(f, (long)off, SEEK_SET) == 0 && std::fread(dst, 1, n, f) == n;
+  return off <= (uint64_t)INT64_MAX && fseeko(f, (off_t)off, SEEK_SET) == 0 &&
+         std::fread(dst, 1, n, f) == n;
 }
 
 struct Closer {

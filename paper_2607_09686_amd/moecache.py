@@ -128,6 +128,7 @@ def lib():
         "moe_cache_destroy": ([vp], None),
         "moe_cache_set_timing_stride": ([vp, i32], ctypes.c_int),
         "moe_cache_last_logits": ([vp, vp], ctypes.c_int),
+        "moe_cache_fill_slots": ([vp, i32], ctypes.c_int),
         "moe_last_error": ([], ctypes.c_char_p),
         "moe_host_alloc": ([u64, P(vp)], ctypes.c_int),
         "moe_host_free": ([vp], ctypes.c_int),
@@ -266,6 +267,10 @@ class MoeCache:
 
     def reset(self):
         _check(lib().moe_cache_reset(self.handle))
+
+    def fill_slots(self, byte):
+        """Overwrite every slot byte with `byte` (moe_cache_fill_slots; tests)."""
+        _check(lib().moe_cache_fill_slots(self.handle, byte))
 
     def last_logits(self):
         """Router logits [n_experts] of the last one-token call (moe_cache_last_logits)."""

@@ -80,12 +80,26 @@ def check_routes(x, wr, k, idx_gpu, w_gpu, prenorm=False):
     return idx, w, z, flipped
 
 
-def check_y(y_gpu, y_ref, what=""):
+def check_y(y_gpu, y_ref, what="", slack=None):
+    """max |y_gpu - y_ref| <= 2e-3 * RMS(y_ref).  slack (nullable, per element): what the
+    output format itself cannot hold, added to the bound -- with the residual flag the GPU
+    returns fp32(x + y), whose rounding is not the MoE output's error."""
     y_ref = np.asarray(y_ref, np.float64)
     rms = float(np.sqrt(np.mean(y_ref ** 2)))
-    err = float(np.max(np.abs(np.asarray(y_gpu, np.float64) - y_ref)))
+    diff = np.abs(np.asarray(y_gpu, np.float64) - y_ref)
+    if slack is not None:
+        diff = np.maximum(diff - np.asarray(slack, np.float64), 0.0)
+    err = float(np.max(diff))
     assert err <= Y_TOL * rms, f"{what}: max err {err:.3e} > {Y_TOL} * rms {rms:.3e}"
     return err / rms if rms > 0 else 0.0
+
+
+def residual_slack(y_stored):
+    """One fp32 ulp of each stored output value: the kernels add the residual (or an earlier
+    launch's sum) to the MoE sum in one fp32 addition, at most two such roundings per call
+    (the host-table copy modes run the hit and the missed experts in two launches)."""
+    y = np.abs(np.asarray(y_stored, np.float32))
+    return np.spacing(y).astype(np.float64)
 
 
 def replay_trace(calls_by_layer, wl, budget):
@@ -154,6 +168,7 @@ def decode_chain(cache, wl, X, routers_dev, record_inputs=True):
     return out, inputs, idx_all, w_all
 
 
-__all__ = ["log", "store_buffer", "make_cache", "check_routes", "check_y", "replay_trace",
+__all__ = ["log", "store_buffer", "make_cache", "check_routes", "check_y", "residual_slack",
+           "replay_trace",
            "softmax_of", "decode_chain", "oracle_layer_y", "union_gemv_fits", "small_call_exact",
            "Shape", "moe_layer", "moe_layer_bf16", "TIE_GAP", "Y_TOL"]

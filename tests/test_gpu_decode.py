@@ -5,13 +5,13 @@ import pytest
 
 import synth
 from gpu_common import (check_routes, check_y, log, make_cache, oracle_layer_y, replay_trace,
-                        store_buffer, torch_cuda)
+                        residual_slack, store_buffer, torch_cuda)
 
 pytestmark = pytest.mark.gpu
 
 
 def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, store=None,
-               timing=False, prenorm=False, copy_mode="kernel"):
+               timing=False, prenorm=False, copy_mode="kernel", X=None, poison=False):
     torch = torch_cuda()
     n_tokens = wl.n_tokens if n_tokens is None else n_tokens
     log(f"decode {wl.name} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
@@ -19,10 +19,12 @@ def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, st
         f"copy={copy_mode}")
     keep, ptr, arr = store if store is not None else store_buffer(wl, device=device_store)
     R = synth.router(wl)
-    X = synth.hidden(wl, n_tokens=n_tokens)
+    X = synth.hidden(wl, n_tokens=n_tokens) if X is None else X
     Rd = torch.from_numpy(R).cuda()
     cache = make_cache(wl, ptr, budget, trace=True, residual=residual, timing=timing,
                        prenorm=prenorm, copy_mode=copy_mode)
+    if poison:
+        cache.fill_slots(0xFF)   # every slot scale reads NaN until its expert is copied in
     calls = [[] for _ in range(wl.n_layers)]
     worst = 0.0
     y = torch.empty(wl.hidden, dtype=torch.float32, device="cuda")
@@ -32,13 +34,16 @@ def run_decode(wl, budget, residual=False, device_store=False, n_tokens=None, st
             x = torch.from_numpy(xh).cuda()
             delta, idx, w = cache.layer_forward(x, Rd[l], l, y, routes=True)
             torch.cuda.synchronize()
-            yg = y.cpu().numpy().astype(np.float64)
+            ys = y.cpu().numpy()
+            yg = ys.astype(np.float64)
+            slack = None
             if residual:
                 yg = yg - xh.astype(np.float64)
+                slack = residual_slack(ys)[None]
             idx_or, w_or, z, flipped = check_routes(xh[None], R[l], wl.top_k, idx, w, prenorm)
             yo = oracle_layer_y(xh[None], R[l], arr, wl, l, idx_or, w_or, z, idx, flipped,
                                 prenorm=prenorm)
-            worst = max(worst, check_y(yg[None], yo, f"token {t} layer {l}"))
+            worst = max(worst, check_y(yg[None], yo, f"token {t} layer {l}", slack=slack))
             calls[l].append(idx[0])
             assert delta.hits + delta.misses == len(set(idx[0].tolist()))
             assert delta.materialized_bytes == delta.misses * wl.payload_bytes

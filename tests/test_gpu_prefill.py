@@ -6,8 +6,8 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, small_call_exact, softmax_of,
-                        store_buffer, torch_cuda)
+from gpu_common import (TIE_GAP, check_routes, check_y, log, make_cache, residual_slack,
+                        small_call_exact, softmax_of, store_buffer, torch_cuda)
 from oracle import router as oracle_router
 from oracle.layer import Shape, moe_layer, moe_layer_bf16, rms_normalize
 from oracle.lru import LayerLRU
@@ -45,14 +45,16 @@ def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens
     yo = fn(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
             prenorm=prenorm)["y"][toks]
     yg = y_g[toks].astype(np.float64)
+    slack = None
     if residual:
         yg = yg - x[toks].astype(np.float64)
-    err = check_y(yg, yo, f"layer {layer}")
+        slack = residual_slack(y_g[toks])
+    err = check_y(yg, yo, f"layer {layer}", slack=slack)
     return flips, err
 
 
 def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=None, seed_shift=0,
-                copy_mode="kernel"):
+                copy_mode="kernel", xs=None, poison=False):
     torch = torch_cuda()
     log(f"prefill {wl.qtype} E={wl.n_experts} k={wl.top_k} H={wl.hidden} I={wl.inter} "
         f"L={wl.n_layers} C={budget} T={T} calls={calls} prenorm={prenorm} residual={residual} "
@@ -61,12 +63,14 @@ def run_prefill(wl, budget, T, calls=1, prenorm=False, residual=False, store=Non
     R = synth.router(wl)
     cache = make_cache(wl, ptr, budget, trace=True, residual=residual, prenorm=prenorm,
                        copy_mode=copy_mode)
+    if poison:
+        cache.fill_slots(0xFF)   # every slot scale reads NaN until its expert is copied in
     lrus = [LayerLRU(wl.n_experts, budget, wl.payload_bytes, l) for l in range(wl.n_layers)]
     want = []
     worst = 0.0
     for c in range(calls):
         X = synth.hidden(wl.with_(hidden_seed=wl.hidden_seed + 7 * c + seed_shift), rho=-1.0,
-                         n_tokens=T)
+                         n_tokens=T) if xs is None else xs[c]
         for l in range(wl.n_layers):
             x = torch.from_numpy(X).cuda()
             y = torch.empty_like(x)

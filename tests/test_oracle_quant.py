@@ -28,7 +28,7 @@ def _golden_blocks():
     return rows
 
 
-@pytest.mark.parametrize("row", range(7))
+@pytest.mark.parametrize("row", range(12))
 def test_hand_blocks(row):
     kind, raw, want = _golden_blocks()[row]
     got = quant.dequant_q8_0(raw) if kind == "q8" else quant.dequant_q4_0(raw)
@@ -36,7 +36,7 @@ def test_hand_blocks(row):
 
 
 def test_golden_file_has_all_rows():
-    assert len(_golden_blocks()) == 7
+    assert len(_golden_blocks()) == 12
 
 
 def test_multi_block_rows_and_matrix_layout():
