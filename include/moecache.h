@@ -167,6 +167,25 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
 int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
                       int32_t layer, float *y, moe_counters *delta);
 
+/* For callers that cannot allocate device memory during a call (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * moe_layer_forward for one token (n_tokens must be 1; MOE_EINVAL otherwise)
+ * with the same arguments, results, counters and trace, whose per-call
+ * scratch -- router partials, routes, the token's and the activations' digit
+ * staging, the call's work list -- lives in a static device array of the
+ * library (1 MiB per GPU, held until the process ends) instead of the
+ * handle's buffers.  It calls no hipMalloc, hipFree or other allocating
+ * routine; with delta NULL it queues its kernels on desc.hip_stream and
+ * returns without waiting.  Needs the device slot tables (the default copy
+ * modes: MOE_EINVAL with MOE_F_SIDE_COPY / MOE_F_SDMA_COPY) and a shape whose
+ * scratch fits the array (MOE_EINVAL otherwise; every shape moe_cache_create
+ * accepts does).  Every call on one GPU shares that GPU's array, whichever
+ * handle and stream it comes from: calls that overlap in time on one GPU race
+ * (the array keeps the last call's contents; nothing in it needs clearing,
+ * each call writes what it reads first). */
+int moe_layer_forward_static(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                             int32_t layer, float *y, moe_counters *delta);
+
 /* As moe_layer_forward, also copying the routes out (host, nullable):
  * topk_idx [n_tokens][top_k] int32 in rank order, topk_w [n_tokens][top_k] fp32. */
 int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,

@@ -17,6 +17,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -26,6 +27,14 @@
 #include "slot_lru.h"
 
 using namespace moecache;
+
+// Per-call scratch of moe_layer_forward_static (router partials, routes, digit
+// staging, work list of one decode call), held by every GPU the library runs on
+// until the process ends.  Host code never uses this name as an address: each
+// device's copy is reached through the pointer hipGetSymbolAddress returns for
+// it (static_scratch_ptr).
+constexpr size_t kStaticScratchBytes = size_t(1) << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
 
 namespace {
 thread_local std::string g_err;
@@ -143,6 +152,8 @@ struct moe_cache {
   int32_t timing_every = 1;
   uint64_t n_calls = 0;
   bool timing_now = false;  // this call is bracketed
+
+  uint8_t *static_scratch = nullptr;  // this device's copy of `scratch` (moe_layer_forward_static)
 
   uint8_t *slot_ptr(int32_t layer, int32_t s) const { return slots + ((int64_t)layer * C + s) * P; }
   DecodeScratch scratch() const { return DecodeScratch{xq, xsc, hq, hsc, hds}; }
@@ -462,6 +473,68 @@ LruDev dev_table(moe_cache *c, int32_t layer) {
   return L;
 }
 
+// Where one decode call keeps its per-call scratch (router partials, routes,
+// digit staging, work list): the handle's own buffers, or the library's static
+// per-device array (moe_layer_forward_static).
+struct DecodeBufs {
+  float *partial;
+  int32_t *idx;
+  float *w;
+  DecodeScratch s;
+  WorkList *work;
+};
+
+DecodeBufs handle_bufs(moe_cache *c) {
+  return DecodeBufs{c->partial, c->topk_idx, c->topk_w, c->scratch(), c->dl_work};
+}
+
+// The address of `scratch` on each device, resolved once per device with that
+// device current.
+std::mutex g_static_mu;
+std::vector<uint8_t *> g_static_ptr;
+
+int static_scratch_ptr(int device, uint8_t **out) {
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (device < 0) return fail(MOE_EINVAL, "bad device %d", device);
+  if ((int)g_static_ptr.size() <= device) g_static_ptr.resize(device + 1, nullptr);
+  if (!g_static_ptr[device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(MOE_EHIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    g_static_ptr[device] = static_cast<uint8_t *>(p);
+  }
+  *out = g_static_ptr[device];
+  return MOE_OK;
+}
+
+// One decode call's buffers carved out of the static array (each 256-byte
+// aligned); *bytes gets the total.  Nothing in it needs to start at zero: each
+// call's router writes the partials, routes, digits and the whole work list
+// (count included) before any kernel of the call reads them.
+DecodeBufs static_bufs(const moe_cache *c, uint8_t *base, size_t *bytes) {
+  const moe_model_desc &d = c->d;
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    uint8_t *p = base + off;
+    off += (n + 255) / 256 * 256;
+    return p;
+  };
+  const size_t kI = (size_t)d.top_k * d.inter;
+  DecodeBufs b{};
+  b.partial = reinterpret_cast<float *>(take(((size_t)router_decode_grid(d.hidden) * d.n_experts + 1) * 4));
+  b.idx = reinterpret_cast<int32_t *>(take((size_t)d.top_k * 4));
+  b.w = reinterpret_cast<float *>(take((size_t)d.top_k * 4));
+  b.s.xq = reinterpret_cast<int8_t *>(take(3 * (size_t)d.hidden));
+  b.s.xsc = reinterpret_cast<float *>(take((size_t)d.hidden / 32 * 4));
+  b.s.hq = reinterpret_cast<int8_t *>(take(3 * kI));
+  b.s.hsc = reinterpret_cast<float *>(take(kI / 16 * 4));
+  b.s.hds = reinterpret_cast<int32_t *>(take(3 * kI / 16 * 4));
+  b.work = reinterpret_cast<WorkList *>(take(sizeof(WorkList)));
+  *bytes = off;
+  return b;
+}
+
 // A multi-token call steps the layer's table on the host.  The pull is queued
 // behind the call's routing (one kernel writes the table and the device error
 // word into the pinned staging) and read once the routing has been waited for;
@@ -520,7 +593,7 @@ int push_table(moe_cache *c, int32_t layer) {
 // Decode call with the slot table on the device: four launches, no host wait
 // (unless the caller asks for the counter delta or the routes).
 int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t layer, float *y,
-                       moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
+                       moe_counters *delta, int32_t *dbg_idx, float *dbg_w, const DecodeBufs &b) {
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
   c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
@@ -532,12 +605,13 @@ int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t la
   }
   if (c->dl_trace && c->dl_trace_pending + k > c->dl_trace_cap && (rc = drain_dev_trace(c)))
     return rc;
-  const LruDev L = dev_table(c, layer);
+  LruDev L = dev_table(c, layer);
+  L.work = b.work;
   {
     Span sp(c, c->main, MOE_KIND_ROUTER, 1, (uint64_t)d.hidden * d.n_experts * 4 + d.hidden * 4,
             2ull * d.hidden * d.n_experts);
-    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, c->partial, c->topk_idx,
-                                    c->topk_w, nullptr, nullptr, c->xq, c->xsc,
+    HIP_TRY(c, launch_router_decode(x, wr, d.hidden, d.n_experts, k, b.partial, b.idx, b.w,
+                                    nullptr, nullptr, b.s.xq, b.s.xsc,
                                     (d.flags & MOE_F_PRENORM) != 0, &L, c->main, sp.timing()));
     sp.end();
   }
@@ -548,31 +622,31 @@ int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t la
   if (!(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup(d.qtype, d.hidden, d.inter)) {
     // one launch: the misses' copies, their gate/up on the fly, the hits' gate/up alongside
     Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
-    HIP_TRY(c, launch_copy_gateup(d.qtype, c->scratch(), d.hidden, d.inter, k, c->dl_work, c->P,
+    HIP_TRY(c, launch_copy_gateup(d.qtype, b.s, d.hidden, d.inter, k, b.work, c->P,
                                   kCopyGrid, acc, c->main, sp.timing()));
     sp.end();
   } else {
     {
       Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);
-      HIP_TRY(c, launch_materialize_list(c->dl_work, c->P, kCopyGrid, acc, c->main, sp.timing()));
+      HIP_TRY(c, launch_materialize_list(b.work, c->P, kCopyGrid, acc, c->main, sp.timing()));
       sp.end();
     }
     Span sp(c, c->main, MOE_KIND_GATEUP, 1, (uint64_t)k * 2 * c->M, 4ull * k * d.hidden * d.inter);
-    HIP_TRY(c, launch_gateup(d.qtype, c->scratch(), d.hidden, d.inter, k, shape, &c->dl_work->list,
+    HIP_TRY(c, launch_gateup(d.qtype, b.s, d.hidden, d.inter, k, shape, &b.work->list,
                              c->main, sp.timing()));
     sp.end();
   }
   {
     Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * d.hidden * d.inter);
-    HIP_TRY(c, launch_down(d.qtype, c->scratch(), d.hidden, d.inter, k, shape, &c->dl_work->list,
-                           c->topk_w, x, y, (d.flags & MOE_F_RESIDUAL) ? 1 : 0, c->main, sp.timing()));
+    HIP_TRY(c, launch_down(d.qtype, b.s, d.hidden, d.inter, k, shape, &b.work->list,
+                           b.w, x, y, (d.flags & MOE_F_RESIDUAL) ? 1 : 0, c->main, sp.timing()));
     sp.end();
   }
   if ((d.flags & MOE_F_TIMING) && (rc = drain_timing(c))) return rc;
   if (delta || dbg_idx || dbg_w) {
     if ((rc = sync_dev(c))) return rc;
-    if (dbg_idx) HIP_TRY(c, hipMemcpy(dbg_idx, c->topk_idx, k * sizeof(int32_t), hipMemcpyDeviceToHost));
-    if (dbg_w) HIP_TRY(c, hipMemcpy(dbg_w, c->topk_w, k * sizeof(float), hipMemcpyDeviceToHost));
+    if (dbg_idx) HIP_TRY(c, hipMemcpy(dbg_idx, b.idx, k * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (dbg_w) HIP_TRY(c, hipMemcpy(dbg_w, b.w, k * sizeof(float), hipMemcpyDeviceToHost));
     if (delta) {
       uint64_t after[4];
       HIP_TRY(c, hipMemcpy(after, c->dl_cnt + 4 * layer, 32, hipMemcpyDeviceToHost));
@@ -585,7 +659,7 @@ int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t la
 
 int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer, float *y,
                    moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
-  if (c->dev_lru) return forward_decode_dev(c, x, wr, layer, y, delta, dbg_idx, dbg_w);
+  if (c->dev_lru) return forward_decode_dev(c, x, wr, layer, y, delta, dbg_idx, dbg_w, handle_bufs(c));
   const moe_model_desc &d = c->d;
   const int k = d.top_k;
   c->timing_now = (d.flags & MOE_F_TIMING) && c->n_calls++ % c->timing_every == 0;
@@ -921,6 +995,10 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
     delete c;
     return fail(MOE_EHIP, "no HIP device");
   }
+  if ((rc = static_scratch_ptr(c->device, &c->static_scratch))) {
+    delete c;
+    return rc;
+  }
   for (int32_t l = 0; l < desc->n_layers; ++l) c->lru.emplace_back(desc->n_experts, budget_slots, c->P, l);
   c->small_overflow.assign(desc->n_layers, 0);
 
@@ -999,6 +1077,29 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
 int moe_layer_forward(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
                       int32_t layer, float *y, moe_counters *delta) {
   return moe_layer_forward_dbg(c, x, n_tokens, router_w, layer, y, delta, nullptr, nullptr);
+}
+
+int moe_layer_forward_static(moe_cache *c, const float *x, int32_t n_tokens, const float *router_w,
+                             int32_t layer, float *y, moe_counters *delta) {
+  if (!c) return fail(MOE_EINVAL, "handle is NULL");
+  if (c->poisoned) return fail(MOE_ESTATE, "handle poisoned by an earlier HIP error");
+  if (!x || !router_w || !y) return fail(MOE_EINVAL, "x, router_w and y must be non-NULL");
+  if (n_tokens != 1) return fail(MOE_EINVAL, "moe_layer_forward_static takes one token (n_tokens = 1)");
+  if (layer < 0 || layer >= c->d.n_layers)
+    return fail(MOE_EINVAL, "layer %d outside [0, %d)", layer, c->d.n_layers);
+  if (!c->dev_lru)
+    return fail(MOE_EINVAL, "moe_layer_forward_static needs the device slot tables (not the "
+                "MOE_F_SIDE_COPY / MOE_F_SDMA_COPY modes)");
+  const int64_t bytes = (int64_t)c->d.hidden * 4;
+  const char *xb = (const char *)x, *yb = (const char *)y;
+  if (xb < yb + bytes && yb < xb + bytes) return fail(MOE_EINVAL, "y overlaps x");
+  size_t need = 0;
+  const DecodeBufs b = static_bufs(c, c->static_scratch, &need);
+  if (need > kStaticScratchBytes)
+    return fail(MOE_EINVAL, "this shape needs %zu bytes of call scratch, more than the static %zu",
+                need, kStaticScratchBytes);
+  if (hipSetDevice(c->device) != hipSuccess) return fail(MOE_EHIP, "hipSetDevice failed");
+  return forward_decode_dev(c, x, router_w, layer, y, delta, nullptr, nullptr, b);
 }
 
 int moe_cache_counters(const moe_cache *cc, int32_t layer, moe_counters *out) {

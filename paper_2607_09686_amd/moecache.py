@@ -121,6 +121,7 @@ def lib():
         "moe_cache_create": ([P(ModelDesc), i32, P(vp)], ctypes.c_int),
         "moe_layer_forward": ([vp, vp, i32, vp, i32, vp, P(Counters)], ctypes.c_int),
         "moe_layer_forward_dbg": ([vp, vp, i32, vp, i32, vp, P(Counters), vp, vp], ctypes.c_int),
+        "moe_layer_forward_static": ([vp, vp, i32, vp, i32, vp, P(Counters)], ctypes.c_int),
         "moe_cache_counters": ([vp, i32, P(Counters)], ctypes.c_int),
         "moe_cache_read_trace": ([vp, P(StepRec), i64, P(i64)], ctypes.c_int),
         "moe_cache_reset": ([vp], ctypes.c_int),
@@ -247,6 +248,17 @@ class MoeCache:
         _check(lib().moe_layer_forward_dbg(self.handle, xp, T, wp, layer, yp, ctypes.byref(delta),
                                            idx.ctypes.data, w.ctypes.data))
         return delta, idx, w
+
+    def layer_forward_static(self, x, router_w, layer, y, counters=False):
+        """One-token call through moe_layer_forward_static (scratch in the library's static
+        device array, no allocation).  Returns the counter delta if counters=True."""
+        xp = _dev_ptr(x, "float32", self.hidden, "x")
+        wp = _dev_ptr(router_w, "float32", self.hidden * self.n_experts, "router_w")
+        yp = _dev_ptr(y, "float32", self.hidden, "y")
+        delta = Counters()
+        _check(lib().moe_layer_forward_static(self.handle, xp, 1, wp, layer, yp,
+                                              ctypes.byref(delta) if counters else None))
+        return delta if counters else None
 
     def counters(self, layer=-1):
         c = Counters()
