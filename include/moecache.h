@@ -45,12 +45,31 @@ extern "C" {
 #define MOE_ESTATE (-4) /* handle poisoned by an earlier MOE_EHIP */
 #define MOE_EIO (-5)    /* a file could not be opened, read or written */
 
-/* Block formats of the expert weights (GGUF-style, 32 weights per block).
- * Q8_0: 34 bytes = fp16 scale d (little-endian) + 32 int8 q; weight d*q.
- * Q4_0: 18 bytes = fp16 scale d + 16 bytes, byte j holding element j in its
- *       low nibble and element j+16 in its high nibble; weight d*(n-8). */
+/* Block formats of the expert weights (GGUF; the paper's model profiles are
+ * Q8_0 and Q4_K_M GGUF files, its Model Profiles section).
+ * Q8_0: 34 bytes per 32 weights = fp16 scale d (little-endian) + 32 int8 q;
+ *       weight d*q.
+ * Q4_0: 18 bytes per 32 weights = fp16 scale d + 16 bytes, byte j holding
+ *       element j in its low nibble and element j+16 in its high nibble;
+ *       weight d*(n-8).
+ * Q4_K: 144 bytes per super-block of 256 weights = fp16 d, fp16 dmin, 12
+ *       bytes of eight 6-bit sub-block scales sc_j and mins m_j, 128 bytes of
+ *       4-bit q (chunk c of 64 weights: 32 bytes, low nibbles sub-block 2c,
+ *       high nibbles 2c+1); weight d*sc_j*q - dmin*m_j.
+ * Q6_K: 210 bytes per super-block of 256 weights = 128 bytes of low 4 bits,
+ *       64 bytes of high 2 bits, 16 int8 scales (one per 16 weights), fp16 d;
+ *       weight d*scale*(q-32).
+ * desc.qtype names the format of W_gate and W_up in its low byte and that of
+ * W_down in the next byte, 0 meaning the same (MOE_QTYPE_MIX).  The K-quant
+ * formats need hidden (their gate/up rows) or inter (their down rows) to be a
+ * multiple of 256. */
 #define MOE_Q8_0 8
 #define MOE_Q4_0 2
+#define MOE_Q4_K 12
+#define MOE_Q6_K 14
+#define MOE_QTYPE_MIX(gate_up, down) ((gate_up) | ((down) << 8))
+/* the paper's 4-bit profile as stored here: Q4_K gate/up, Q6_K down */
+#define MOE_Q4_K_M MOE_QTYPE_MIX(MOE_Q4_K, MOE_Q6_K)
 
 /* desc.flags */
 #define MOE_F_RESIDUAL 1u /* y = x + moe(x) instead of y = moe(x) */
@@ -332,7 +351,8 @@ int moe_policy_min(const int32_t *ids, const int64_t *offsets, int64_t n_calls, 
 
 /* Split-pack of a GGUF MoE model (no HIP dependency; the paper's Split-Pack
  * Representation section): the routed expert tensors of every layer l,
- * blk.l.ffn_{gate,up,down}_exps.weight (Q8_0 or Q4_0; dims (H, I, E), (H, I, E),
+ * blk.l.ffn_{gate,up,down}_exps.weight (Q8_0, Q4_0, Q4_K or Q6_K, gate and up of
+ * one type and down of one type in every layer; dims (H, I, E), (H, I, E),
  * (I, H, E), innermost first), are cut into one block per (layer, expert) and
  * written to pack_path in the store layout of moe_model_desc.host_store:
  * payload (l, e) at (l * n_experts + e) * P, [W_gate | W_up | W_down], bytes
@@ -340,12 +360,15 @@ int moe_policy_min(const int32_t *ids, const int64_t *offsets, int64_t n_calls, 
  * (layer, expert, offset and bytes in the pack, the source offset and bytes of
  * each of the three matrices, an FNV-1a 64-bit digest of the block) and a last
  * line with the block count, the pack size and a digest of the block digests.
- * router_path (nullable) gets the routers, blk.l.ffn_gate_inp.weight (F32, F16
+ * info->qtype is the desc.qtype of the pack (MOE_QTYPE_MIX when the down type
+ * differs).  router_path (nullable) gets the routers, blk.l.ffn_gate_inp.weight (F32, F16
  * or BF16, dims (H, E)), as fp32 [n_layers][hidden][n_experts], the router_w
  * form of moe_layer_forward.  info gets the topology (top_k from the metadata
  * key *.expert_used_count, 0 if absent).  GGUF versions 2 and 3.  MOE_EINVAL
- * on a malformed file, missing or inconsistent tensors or another block type;
- * MOE_EIO when a file cannot be opened, read or written. */
+ * on a malformed file, missing or inconsistent tensors, another block type, a
+ * block type that changes between layers, or widths above 65536; MOE_EIO when
+ * a file cannot be opened, read or written; MOE_ENOMEM when host memory runs
+ * out. */
 typedef struct {
   int32_t n_layers, n_experts, top_k, hidden, inter, qtype;
   uint64_t payload_bytes; /* P */

@@ -18,9 +18,12 @@ import numpy as np
 
 SCALAR = {0: "<B", 1: "<b", 2: "<H", 3: "<h", 4: "<I", 5: "<i", 6: "<f", 7: "<?", 10: "<Q",
           11: "<q", 12: "<d"}
-# bytes per 32 elements for the block types, per element for the float types
-BLOCK = {8: 34, 2: 18}
+# (bytes, elements) per block of the block types (ggml type codes: Q8_0 8, Q4_0 2, Q4_K 12,
+# Q6_K 14); bytes per element of the float types
+BLOCK = {8: (34, 32), 2: (18, 32), 12: (144, 256), 14: (210, 256)}
 ELEM = {0: 4, 1: 2, 30: 2}
+# the pack's qtype code for a (gate/up type, down type) pair: the type alone when both
+# matrices share it, else gate/up | down << 8
 
 
 class _Cursor:
@@ -50,7 +53,8 @@ class _Cursor:
 def tensor_bytes(dims, ggml_type):
     n = int(np.prod(dims, dtype=np.int64))
     if ggml_type in BLOCK:
-        return n // 32 * BLOCK[ggml_type]
+        bb, wpb = BLOCK[ggml_type]
+        return n // wpb * bb
     return n * ELEM[ggml_type]
 
 
@@ -97,22 +101,25 @@ def expected_pack(path):
     while f"blk.{L}.ffn_gate_exps.weight" in tensors:
         L += 1
     (H, I, E), qt, _, _ = tensors["blk.0.ffn_gate_exps.weight"]
-    M = I * H // 32 * BLOCK[qt]
+    qd = tensors["blk.0.ffn_down_exps.weight"][1]
+    M = tensor_bytes([H, I], qt)       # one expert's gate (or up) matrix
+    Md = tensor_bytes([I, H], qd)      # one expert's down matrix
     blocks, routers = [], np.empty((L, H, E), np.float32)
     for l in range(L):
         mats = []
-        for kind in ("gate", "up", "down"):
+        for kind, want_t, m in (("gate", qt, M), ("up", qt, M), ("down", qd, Md)):
             d, t, off, nb = tensors[f"blk.{l}.ffn_{kind}_exps.weight"]
-            assert t == qt and nb == E * M
-            mats.append(np.frombuffer(buf, np.uint8, count=nb, offset=off).reshape(E, M))
+            assert t == want_t and nb == E * m
+            mats.append(np.frombuffer(buf, np.uint8, count=nb, offset=off).reshape(E, m))
         for e in range(E):
             blocks.append(np.concatenate([mats[0][e], mats[1][e], mats[2][e]]))
         d, t, off, nb = tensors[f"blk.{l}.ffn_gate_inp.weight"]
         w = _f32(buf[off:off + nb], t).reshape(E, H)   # E rows of H
         routers[l] = w.T
     used = [v for k, v in meta.items() if k.endswith(".expert_used_count")]
-    topo = {"n_layers": L, "n_experts": E, "hidden": H, "inter": I, "qtype": qt,
-            "top_k": used[0] if used else 0, "payload_bytes": 3 * M}
+    topo = {"n_layers": L, "n_experts": E, "hidden": H, "inter": I,
+            "qtype": qt if qd == qt else qt | (qd << 8),
+            "top_k": used[0] if used else 0, "payload_bytes": 2 * M + Md}
     return np.concatenate(blocks), routers, topo
 
 

@@ -21,7 +21,9 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <exception>
 #include <map>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -41,7 +43,22 @@ int perr(int code, const char *fmt, ...) {
   return code;
 }
 
-enum : uint32_t { kF32 = 0, kF16 = 1, kQ4_0 = 2, kQ8_0 = 8, kBF16 = 30 };
+enum : uint32_t { kF32 = 0, kF16 = 1, kQ4_0 = 2, kQ8_0 = 8, kQ4_K = 12, kQ6_K = 14, kBF16 = 30 };
+
+// Bytes and weights per block of the expert block types read here (0: another type).
+uint64_t block_bytes(uint32_t t, uint64_t *weights) {
+  switch (t) {
+    case kQ8_0: *weights = 32; return 34;
+    case kQ4_0: *weights = 32; return 18;
+    case kQ4_K: *weights = 256; return 144;
+    case kQ6_K: *weights = 256; return 210;
+    default: *weights = 0; return 0;
+  }
+}
+
+// Largest hidden / intermediate width and expert count taken from a file (far above any
+// model this path serves; keeps every size below 2^63).
+constexpr uint64_t kMaxWidth = 1u << 16, kMaxExperts = 1u << 16;
 
 struct Tensor {
   std::vector<uint64_t> dims;
@@ -161,12 +178,8 @@ struct Closer {
   }
 };
 
-}  // namespace
-
-extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const char *index_path,
-                             const char *router_path, moe_pack_info *info) {
-  if (!gguf_path || !pack_path || !index_path || !info)
-    return perr(MOE_EINVAL, "moe_pack_gguf: NULL argument");
+int pack_gguf(const char *gguf_path, const char *pack_path, const char *index_path,
+              const char *router_path, moe_pack_info *info) {
   std::memset(info, 0, sizeof *info);
   Reader r;
   r.f = std::fopen(gguf_path, "rb");
@@ -186,7 +199,8 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
     if (!read_value(r, type, &v)) return perr(MOE_EINVAL, "bad GGUF metadata value for %s", key.c_str());
     if (key == "general.alignment" && v > 0) alignment = v;
     const std::string suffix = ".expert_used_count";
-    if (key.size() > suffix.size() && key.compare(key.size() - suffix.size(), suffix.size(), suffix) == 0 && v > 0)
+    if (key.size() > suffix.size() && key.compare(key.size() - suffix.size(), suffix.size(), suffix) == 0 &&
+        v > 0 && v <= (int64_t)kMaxExperts)
       used = v;
   }
   std::map<std::string, Tensor> tensors;
@@ -201,11 +215,19 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
     if (!r.ok) return perr(MOE_EINVAL, "truncated GGUF tensor info");
     tensors[name] = t;
   }
-  long pos = std::ftell(r.f);
-  if (pos < 0 || alignment <= 0 || (alignment & (alignment - 1)))
+  const off_t pos = ftello(r.f);
+  if (pos < 0 || alignment <= 0 || alignment > (1 << 20) || (alignment & (alignment - 1)))
     return perr(MOE_EINVAL, "bad GGUF alignment %" PRId64, alignment);
+  if (fseeko(r.f, 0, SEEK_END) != 0) return perr(MOE_EIO, "cannot seek in %s", gguf_path);
+  const off_t fend = ftello(r.f);
+  if (fend < pos) return perr(MOE_EIO, "cannot size %s", gguf_path);
+  const uint64_t file_bytes = (uint64_t)fend;
   const uint64_t data0 = ((uint64_t)pos + alignment - 1) / alignment * alignment;
-  for (auto &kv : tensors) kv.second.offset += data0;
+  for (auto &kv : tensors) {
+    if (kv.second.offset > file_bytes) return perr(MOE_EINVAL, "tensor %s starts past the end of the file",
+                                                  kv.first.c_str());
+    kv.second.offset += data0;
+  }
 
   // the routed-expert layers: consecutive from 0
   int32_t L = 0;
@@ -215,21 +237,43 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
   const Tensor &g0 = tensors[name(0, "ffn_gate_exps")];
   if (g0.dims.size() != 3) return perr(MOE_EINVAL, "expert tensors must have 3 dims");
   const uint64_t H = g0.dims[0], I = g0.dims[1], E = g0.dims[2];
+  // gate and up share one block type, down may have another (the Q4_K_M mix); each is the
+  // same in every layer, so that every slot holds P bytes
   const uint32_t qt = g0.type;
-  if (qt != kQ8_0 && qt != kQ4_0)
-    return perr(MOE_EINVAL, "expert tensors of ggml type %u: only Q8_0 (8) and Q4_0 (2) are read", qt);
-  if (H % 32 || I % 32 || E < 1 || E > 65536) return perr(MOE_EINVAL, "bad expert shape");
-  const uint64_t bb = qt == kQ8_0 ? 34 : 18;
-  const uint64_t M = I * (H / 32) * bb, P = 3 * M;
+  uint64_t wgu = 0, wdn = 0;
+  const uint64_t bgu = block_bytes(qt, &wgu);
+  if (!bgu)
+    return perr(MOE_EINVAL, "expert tensors of ggml type %u: only Q8_0 (8), Q4_0 (2), Q4_K (12) and "
+                "Q6_K (14) are read", qt);
+  auto d0 = tensors.find(name(0, "ffn_down_exps"));
+  if (d0 == tensors.end()) return perr(MOE_EINVAL, "missing %s", name(0, "ffn_down_exps").c_str());
+  const uint32_t qd = d0->second.type;
+  const uint64_t bdn = block_bytes(qd, &wdn);
+  if (!bdn)
+    return perr(MOE_EINVAL, "down expert tensors of ggml type %u: only Q8_0 (8), Q4_0 (2), Q4_K (12) "
+                "and Q6_K (14) are read", qd);
+  if (H == 0 || I == 0 || H > kMaxWidth || I > kMaxWidth || H % wgu || I % wdn || E < 1 || E > kMaxExperts)
+    return perr(MOE_EINVAL, "bad expert shape (hidden %" PRIu64 ", inter %" PRIu64 ", experts %" PRIu64 ")",
+                H, I, E);
+  // sizes below 2^16 * 2^16 * 2 bytes per matrix, 2^34 * 3 per payload: no overflow
+  const uint64_t M = I * (H / wgu) * bgu, Md = H * (I / wdn) * bdn, P = 2 * M + Md;
+  uint64_t pack_total = 0;
+  if (__builtin_mul_overflow(P, E * (uint64_t)L, &pack_total))
+    return perr(MOE_EINVAL, "the pack would exceed 2^64 bytes");
   for (int32_t l = 0; l < L; ++l) {
     const char *kinds[3] = {"ffn_gate_exps", "ffn_up_exps", "ffn_down_exps"};
     for (int m = 0; m < 3; ++m) {
       auto it = tensors.find(name(l, kinds[m]));
       if (it == tensors.end()) return perr(MOE_EINVAL, "missing %s", name(l, kinds[m]).c_str());
       const Tensor &t = it->second;
-      const bool ok = t.dims.size() == 3 && t.type == qt && t.dims[2] == E &&
+      const bool ok = t.dims.size() == 3 && t.type == (m < 2 ? qt : qd) && t.dims[2] == E &&
                       (m < 2 ? (t.dims[0] == H && t.dims[1] == I) : (t.dims[0] == I && t.dims[1] == H));
-      if (!ok) return perr(MOE_EINVAL, "%s does not match blk.0's experts", name(l, kinds[m]).c_str());
+      if (!ok)
+        return perr(MOE_EINVAL, "%s does not match blk.0's experts (shape, or a block type that "
+                    "differs between layers)", name(l, kinds[m]).c_str());
+      const uint64_t bytes = E * (m < 2 ? M : Md);  // <= 2^16 * 2^34
+      if (t.offset > file_bytes || bytes > file_bytes - t.offset)
+        return perr(MOE_EINVAL, "%s runs past the end of the file", name(l, kinds[m]).c_str());
     }
     if (router_path) {
       auto it = tensors.find(name(l, "ffn_gate_inp"));
@@ -238,6 +282,9 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
           (it->second.type != kF32 && it->second.type != kF16 && it->second.type != kBF16))
         return perr(MOE_EINVAL, "router %s missing or not an F32 / F16 / BF16 (H, E) tensor",
                     name(l, "ffn_gate_inp").c_str());
+      const uint64_t rbytes = H * E * (it->second.type == kF32 ? 4 : 2);
+      if (it->second.offset > file_bytes || rbytes > file_bytes - it->second.offset)
+        return perr(MOE_EINVAL, "router %s runs past the end of the file", name(l, "ffn_gate_inp").c_str());
     }
   }
 
@@ -255,16 +302,17 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
   std::fprintf(fi, "{\"format\": \"moecache expert pack\", \"source\": \"%s\", \"n_layers\": %d, "
                "\"n_experts\": %" PRIu64 ", \"top_k\": %" PRId64 ", \"hidden\": %" PRIu64
                ", \"inter\": %" PRIu64 ", \"qtype\": %u, \"payload_bytes\": %" PRIu64 "}\n",
-               src_json.c_str(), L, E, used, H, I, qt == kQ8_0 ? 8u : 2u, P);
+               src_json.c_str(), L, E, used, H, I, qt == qd ? qt : qt | (qd << 8), P);
   std::vector<uint8_t> buf(P);
   uint64_t out = 0, digest_all = 0xcbf29ce484222325ull;
   for (int32_t l = 0; l < L; ++l) {
     const Tensor &tg = tensors[name(l, "ffn_gate_exps")], &tu = tensors[name(l, "ffn_up_exps")],
                  &td = tensors[name(l, "ffn_down_exps")];
     for (uint64_t e = 0; e < E; ++e) {
-      const uint64_t src[3] = {tg.offset + e * M, tu.offset + e * M, td.offset + e * M};
+      const uint64_t src[3] = {tg.offset + e * M, tu.offset + e * M, td.offset + e * Md};
+      const uint64_t len[3] = {M, M, Md};
       for (int m = 0; m < 3; ++m)
-        if (!read_at(r.f, src[m], buf.data() + m * M, M))
+        if (!read_at(r.f, src[m], buf.data() + m * M, len[m]))
           return perr(MOE_EIO, "short read in %s (layer %d expert %" PRIu64 ")", gguf_path, l, e);
       if (std::fwrite(buf.data(), 1, P, fp) != P) return perr(MOE_EIO, "short write to %s", pack_path);
       const uint64_t dg = fnv1a(buf.data(), P);
@@ -272,7 +320,7 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
       std::fprintf(fi, "{\"layer\": %d, \"expert\": %" PRIu64 ", \"offset\": %" PRIu64 ", \"bytes\": %" PRIu64
                    ", \"gate\": [%" PRIu64 ", %" PRIu64 "], \"up\": [%" PRIu64 ", %" PRIu64
                    "], \"down\": [%" PRIu64 ", %" PRIu64 "], \"fnv1a64\": \"%016" PRIx64 "\"}\n",
-                   l, e, out, P, src[0], M, src[1], M, src[2], M, dg);
+                   l, e, out, P, src[0], M, src[1], M, src[2], Md, dg);
       out += P;
     }
   }
@@ -317,8 +365,23 @@ extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const
   info->top_k = (int32_t)used;
   info->hidden = (int32_t)H;
   info->inter = (int32_t)I;
-  info->qtype = qt == kQ8_0 ? MOE_Q8_0 : MOE_Q4_0;
+  info->qtype = (int32_t)(qt == qd ? qt : qt | (qd << 8));
   info->payload_bytes = P;
   info->pack_bytes = out;
   return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_pack_gguf(const char *gguf_path, const char *pack_path, const char *index_path,
+                             const char *router_path, moe_pack_info *info) {
+  if (!gguf_path || !pack_path || !index_path || !info)
+    return perr(MOE_EINVAL, "moe_pack_gguf: NULL argument");
+  try {
+    return pack_gguf(gguf_path, pack_path, index_path, router_path, info);
+  } catch (const std::bad_alloc &) {
+    return perr(MOE_ENOMEM, "moe_pack_gguf: out of host memory");
+  } catch (const std::exception &ex) {
+    return perr(MOE_EINVAL, "moe_pack_gguf: %s", ex.what());
+  }
 }

@@ -67,12 +67,14 @@ def f32_to_f16_bits(x):
 
 
 def encode_blocks(qcode, w):
-    """Encode fp32 weights (length multiple of 32) into Q8_0 (8) / Q4_0 (2) blocks."""
+    """Encode fp32 weights into blocks of format code qcode: Q8_0 (8) / Q4_0 (2), 32 weights
+    per block, or Q4_K (12) / Q6_K (14), 256 weights per super-block."""
+    from .configs import FORMATS
+    bb, wpb = {code: (b, n) for b, n, code in FORMATS.values()}[qcode]
     w = np.ascontiguousarray(w, np.float32).ravel()
-    assert w.size % 32 == 0
-    bb = 34 if qcode == 8 else 18
-    out = np.empty(w.size // 32 * bb, np.uint8)
-    _lib().synth_encode_blocks(qcode, w.ctypes.data, w.size // 32, out.ctypes.data)
+    assert w.size % wpb == 0
+    out = np.empty(w.size // wpb * bb, np.uint8)
+    _lib().synth_encode_blocks(qcode, w.ctypes.data, w.size // wpb, out.ctypes.data)
     return out
 
 

@@ -1,6 +1,7 @@
 /*
  * Seeded synthetic inputs for the expert-slot-cache MoE FFN: expert weights
- * (quantised to GGUF-style Q8_0 / Q4_0 blocks), router matrices and hidden
+ * (quantised to GGUF-style Q8_0 / Q4_0 blocks or Q4_K / Q6_K super-blocks),
+ * router matrices and hidden
  * states.  This module holds none of the MoE layer's arithmetic: it only
  * draws numbers and encodes them into the block format the store uses.
  *
@@ -202,11 +203,118 @@ static void encode_q4_0(const float *w, int64_t n_blocks, uint8_t *dst) {
   }
 }
 
-/* Encode n_blocks*32 fp32 weights (consecutive 32-weight blocks) as qtype
- * 8 (Q8_0, 34-byte blocks) or 2 (Q4_0, 18-byte blocks). */
-void synth_encode_blocks(int32_t qtype, const float *w, int64_t n_blocks, uint8_t *dst) {
-  if (qtype == 8) encode_q8_0(w, n_blocks, dst);
-  else encode_q4_0(w, n_blocks, dst);
+static float clampf(float v, float lo, float hi) { return v < lo ? lo : v > hi ? hi : v; }
+
+/* Q4_K (generation only): per 32-weight sub-block j an offset o_j = max(0, -min w)
+ * and a step s_j = (max w + o_j) / 15, so w ~ s_j q - o_j with q in 0..15; the
+ * super-block scales d = fp16(max s_j / 63), dmin = fp16(max o_j / 63); the 6-bit
+ * sc_j = rint(s_j / d), m_j = rint(o_j / dmin); q = clamp(rint((w + dmin m_j) /
+ * (d sc_j)), 0, 15).  Packed as the format prescribes: d, dmin, the 12 scale
+ * bytes (sc_0..3 and m_0..3 in the low 6 bits of bytes 0..7, their top two bits
+ * holding the high bits of sc_4..7 / m_4..7, whose low nibbles fill bytes
+ * 8..11), then chunk c's 32 bytes with sub-block 2c in the low nibbles and 2c+1
+ * in the high ones. */
+static void encode_q4_k(const float *w, int64_t n_blocks, uint8_t *dst) {
+  for (int64_t blk = 0; blk < n_blocks; ++blk, w += 256, dst += 144) {
+    float step[8], off[8], smax = 0.f, omax = 0.f;
+    for (int j = 0; j < 8; ++j) {
+      float mn = w[32 * j], mx = w[32 * j];
+      for (int l = 1; l < 32; ++l) {
+        mn = w[32 * j + l] < mn ? w[32 * j + l] : mn;
+        mx = w[32 * j + l] > mx ? w[32 * j + l] : mx;
+      }
+      off[j] = mn < 0.f ? -mn : 0.f;
+      step[j] = (mx + off[j]) / 15.f;
+      smax = step[j] > smax ? step[j] : smax;
+      omax = off[j] > omax ? off[j] : omax;
+    }
+    const uint16_t dh = synth_f32_to_f16(smax / 63.f), mh = synth_f32_to_f16(omax / 63.f);
+    const float d = synth_f16_to_f32(dh), dmin = synth_f16_to_f32(mh);
+    int sc[8], m[8];
+    for (int j = 0; j < 8; ++j) {
+      sc[j] = d > 0.f ? (int)clampf(__builtin_rintf(step[j] / d), 0.f, 63.f) : 0;
+      m[j] = dmin > 0.f ? (int)clampf(__builtin_rintf(off[j] / dmin), 0.f, 63.f) : 0;
+    }
+    dst[0] = (uint8_t)(dh & 0xff);
+    dst[1] = (uint8_t)(dh >> 8);
+    dst[2] = (uint8_t)(mh & 0xff);
+    dst[3] = (uint8_t)(mh >> 8);
+    for (int j = 0; j < 4; ++j) {
+      dst[4 + j] = (uint8_t)(sc[j] | ((sc[j + 4] >> 4) << 6));
+      dst[8 + j] = (uint8_t)(m[j] | ((m[j + 4] >> 4) << 6));
+      dst[12 + j] = (uint8_t)((sc[j + 4] & 15) | ((m[j + 4] & 15) << 4));
+    }
+    for (int c = 0; c < 4; ++c)
+      for (int l = 0; l < 32; ++l) {
+        int q2[2];
+        for (int h = 0; h < 2; ++h) {
+          const int j = 2 * c + h;
+          const float st = d * (float)sc[j], o = dmin * (float)m[j];
+          q2[h] = st > 0.f ? (int)clampf(__builtin_rintf((w[32 * j + l] + o) / st), 0.f, 15.f) : 0;
+        }
+        dst[16 + 32 * c + l] = (uint8_t)(q2[0] | (q2[1] << 4));
+      }
+  }
+}
+
+/* Q6_K (generation only): per 16-weight group i a step t_i = (max |w|) / 31 with
+ * the sign of the group's extreme; d = fp16(max |t_i| / 127), scale_i =
+ * rint(t_i / d) (signed 8-bit), q = clamp(rint(w / (d scale_i)) + 32, 0, 63).
+ * Packed as the format prescribes: weight 32g + l of half h keeps its low 4 bits
+ * in ql[64h + 32(g mod 2) + l] (low nibble for g < 2, high for g >= 2) and its
+ * high 2 bits in bits 2g, 2g+1 of qh[32h + l]; then the 16 scales and d. */
+static void encode_q6_k(const float *w, int64_t n_blocks, uint8_t *dst) {
+  for (int64_t blk = 0; blk < n_blocks; ++blk, w += 256, dst += 210) {
+    float t[16], tmax = 0.f;
+    for (int i = 0; i < 16; ++i) {
+      float ext = 0.f;
+      for (int l = 0; l < 16; ++l) {
+        const float v = w[16 * i + l], a = v < 0.f ? -v : v, ea = ext < 0.f ? -ext : ext;
+        ext = a > ea ? v : ext;
+      }
+      t[i] = ext / -32.f;  /* q = 0 carries the extreme: |q - 32| reaches 32 on its side */
+      const float at = t[i] < 0.f ? -t[i] : t[i];
+      tmax = at > tmax ? at : tmax;
+    }
+    const uint16_t dh = synth_f32_to_f16(tmax / 127.f);
+    const float d = synth_f16_to_f32(dh);
+    int8_t scale[16];
+    for (int i = 0; i < 16; ++i)
+      scale[i] = d > 0.f ? (int8_t)clampf(__builtin_rintf(t[i] / d), -127.f, 127.f) : 0;
+    memset(dst, 0, 192);
+    for (int n = 0; n < 256; ++n) {
+      const float st = d * (float)scale[n / 16];
+      const int q = st != 0.f ? (int)clampf(__builtin_rintf(w[n] / st) + 32.f, 0.f, 63.f) : 32;
+      const int h = n / 128, g = (n % 128) / 32, l = n % 32;
+      uint8_t *lo = dst + 64 * h + 32 * (g % 2) + l;
+      *lo |= (uint8_t)((q & 15) << (g < 2 ? 0 : 4));
+      dst[128 + 32 * h + l] |= (uint8_t)((q >> 4) << (2 * g));
+    }
+    memcpy(dst + 192, scale, 16);
+    dst[208] = (uint8_t)(dh & 0xff);
+    dst[209] = (uint8_t)(dh >> 8);
+  }
+}
+
+/* Bytes and weights per block of a format code: 8 Q8_0, 2 Q4_0, 12 Q4_K, 14 Q6_K. */
+static int format_of(int32_t fmt, int64_t *bytes, int64_t *weights) {
+  switch (fmt) {
+    case 8: *bytes = 34; *weights = 32; return 0;
+    case 2: *bytes = 18; *weights = 32; return 0;
+    case 12: *bytes = 144; *weights = 256; return 0;
+    case 14: *bytes = 210; *weights = 256; return 0;
+    default: return -1;
+  }
+}
+
+/* Encode n_blocks blocks of fp32 weights (consecutive) in format fmt: 8 (Q8_0,
+ * 34-byte blocks of 32), 2 (Q4_0, 18 of 32), 12 (Q4_K, 144 of 256), 14 (Q6_K,
+ * 210 of 256). */
+void synth_encode_blocks(int32_t fmt, const float *w, int64_t n_blocks, uint8_t *dst) {
+  if (fmt == 8) encode_q8_0(w, n_blocks, dst);
+  else if (fmt == 2) encode_q4_0(w, n_blocks, dst);
+  else if (fmt == 12) encode_q4_k(w, n_blocks, dst);
+  else if (fmt == 14) encode_q6_k(w, n_blocks, dst);
 }
 
 /* Stream key for one tensor: kind (1 expert, 2 router, 3 hidden), model
@@ -220,17 +328,23 @@ uint64_t synth_key(uint32_t kind, uint32_t seed, uint32_t l, uint32_t e, uint32_
  * Fill the expert store for layers layer0 .. layer0+n_layers-1 (store points
  * at layer layer0).  Per (layer l, expert e) a contiguous payload
  * [gate (inter x hidden) | up (inter x hidden) | down (hidden x inter)], each
- * matrix row-major with every row split into 32-weight blocks along the
- * input dimension.  Weights ~ N(0, sigma) from key (1, seed, l, e, m), drawn
- * in row-major element order.  Returns 0, or -1 on bad arguments.
+ * matrix row-major with every row split into blocks along the input
+ * dimension.  qtype: the format of gate and up in its low byte and that of
+ * down in the next byte (0: the same).  Weights ~ N(0, sigma) from key
+ * (1, seed, l, e, m), drawn in row-major element order.  Returns 0, or -1 on
+ * bad arguments.
  */
 int synth_expert_store(int32_t qtype, int32_t layer0, int32_t n_layers, int32_t n_experts,
                        int32_t hidden, int32_t inter, float sigma, uint32_t seed,
                        uint8_t *store, int32_t n_threads) {
-  if ((qtype != 8 && qtype != 2) || hidden % 32 || inter % 32 || n_layers < 0) return -1;
-  const int64_t bb = qtype == 8 ? 34 : 18;
-  const int64_t mat_bytes = (int64_t)inter * hidden / 32 * bb;
-  const int64_t payload = 3 * mat_bytes;
+  const int32_t fgu = qtype & 0xff, fdn = (qtype >> 8) & 0xff ? (qtype >> 8) & 0xff : qtype & 0xff;
+  int64_t bgu, wgu, bdn, wdn;
+  if (format_of(fgu, &bgu, &wgu) || format_of(fdn, &bdn, &wdn) || hidden % wgu || inter % wdn ||
+      n_layers < 0)
+    return -1;
+  const int64_t gu_bytes = (int64_t)inter * hidden / wgu * bgu;
+  const int64_t dn_bytes = (int64_t)inter * hidden / wdn * bdn;
+  const int64_t payload = 2 * gu_bytes + dn_bytes;
   const int64_t n_mats = (int64_t)n_layers * n_experts * 3;
 #ifdef _OPENMP
   if (n_threads > 0) omp_set_num_threads(n_threads);
@@ -244,12 +358,14 @@ int synth_expert_store(int32_t qtype, int32_t layer0, int32_t n_layers, int32_t 
       int32_t m = (int32_t)(mi % 3);
       int32_t l = (int32_t)(le / n_experts), e = (int32_t)(le % n_experts);
       uint64_t k0 = synth_key(1, seed, (uint32_t)(layer0 + l), (uint32_t)e, (uint32_t)m);
-      uint8_t *dst = store + le * payload + m * mat_bytes;
+      uint8_t *dst = store + le * payload + m * gu_bytes;
+      const int32_t f = m < 2 ? fgu : fdn;
+      const int64_t bb = m < 2 ? bgu : bdn, wpb = m < 2 ? wgu : wdn;
       const int64_t n_w = (int64_t)inter * hidden;
-      for (int64_t s = 0; s < n_w; s += 4096) {
+      for (int64_t s = 0; s < n_w; s += 4096) {  /* 4096 is a whole number of blocks */
         int64_t n = n_w - s < 4096 ? n_w - s : 4096;
         synth_normal_f32(k0, 0, (uint64_t)s, (uint64_t)n, sigma, buf);
-        synth_encode_blocks(qtype, buf, n / 32, dst + s / 32 * bb);
+        synth_encode_blocks(f, buf, n / wpb, dst + s / wpb * bb);
       }
     }
   }

@@ -44,8 +44,9 @@ def write(path, metadata, tensors, alignment=32, version=3):
 
 def moe_model(path, n_layers, n_experts, hidden, inter, qcode, top_k, seed, router_type=0,
               alignment=32):
-    """A GGUF MoE model with random expert blocks (Q8_0 / Q4_0 by synth's encoders), routers of
-    the given float type, and a few other tensors and metadata entries around them."""
+    """A GGUF MoE model with random expert blocks (by synth's encoders), routers of the given
+    float type, and a few other tensors and metadata entries around them.  qcode: the block
+    type of every expert tensor (8 Q8_0, 2 Q4_0, 12 Q4_K, 14 Q6_K), or gate/up | down << 8."""
     import synth
     rng = np.random.default_rng(seed)
     meta = [("general.architecture", 8, "testmoe"), ("general.name", 8, "tiny test moe"),
@@ -59,11 +60,13 @@ def moe_model(path, n_layers, n_experts, hidden, inter, qcode, top_k, seed, rout
     for l in range(n_layers):
         tensors.append((f"blk.{l}.attn_norm.weight", [hidden], 0,
                         rng.normal(size=hidden).astype("<f4").tobytes()))
-        for kind, dims in (("gate", [hidden, inter, n_experts]), ("up", [hidden, inter, n_experts]),
-                           ("down", [inter, hidden, n_experts])):
+        gu, dn = qcode & 0xFF, (qcode >> 8) or (qcode & 0xFF)
+        for kind, dims, code in (("gate", [hidden, inter, n_experts], gu),
+                                 ("up", [hidden, inter, n_experts], gu),
+                                 ("down", [inter, hidden, n_experts], dn)):
             w = (rng.normal(size=int(np.prod(dims))) * 0.02).astype(np.float32)
-            tensors.append((f"blk.{l}.ffn_{kind}_exps.weight", dims, qcode,
-                            synth.encode_blocks(qcode, w).tobytes()))
+            tensors.append((f"blk.{l}.ffn_{kind}_exps.weight", dims, code,
+                            synth.encode_blocks(code, w).tobytes()))
         r = rng.normal(size=n_experts * hidden) * 0.1
         raw = {0: r.astype("<f4").tobytes(), 1: r.astype("<f2").tobytes(),
                30: (r.astype(np.float32).view(np.uint32) >> 16).astype("<u2").tobytes()}[router_type]

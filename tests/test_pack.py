@@ -49,10 +49,13 @@ def test_fnv1a_reference_values():
     assert gguf.fnv1a64(b"foobar") == 0x85944171f73967e8
 
 
-@pytest.mark.parametrize("qcode,router_type,alignment", [(8, 0, 32), (2, 1, 64), (8, 30, 128)])
+@pytest.mark.parametrize("qcode,router_type,alignment", [(8, 0, 32), (2, 1, 64), (8, 30, 128),
+                                                        (12, 0, 32), (14, 1, 32),
+                                                        (12 | 14 << 8, 30, 64)])
 def test_pack_matches_oracle(mc, tmp_path, qcode, router_type, alignment):
     src = tmp_path / "m.gguf"
-    gguf_writer.moe_model(src, n_layers=3, n_experts=8, hidden=256, inter=128, qcode=qcode,
+    gguf_writer.moe_model(src, n_layers=3, n_experts=8, hidden=256,
+                          inter=128 if qcode in (8, 2) else 256, qcode=qcode,
                           top_k=2, seed=qcode + router_type, router_type=router_type,
                           alignment=alignment)
     info = mc.pack_gguf(src, tmp_path / "e.pack", tmp_path / "e.index", tmp_path / "r.bin")
@@ -76,10 +79,11 @@ def test_pack_matches_oracle(mc, tmp_path, qcode, router_type, alignment):
     for i, b in enumerate(blocks):
         assert (b["layer"], b["expert"], b["offset"], b["bytes"]) == (i // 8, i % 8, i * P, P)
         assert int(b["fnv1a64"], 16) == gguf.fnv1a64(want[i * P:(i + 1) * P].tobytes())
-        for kind, part in (("gate", 0), ("up", 1), ("down", 2)):
+        m_gu = tensors["blk.0.ffn_gate_exps.weight"][3] // 8
+        for kind, start in (("gate", 0), ("up", m_gu), ("down", 2 * m_gu)):
             off, nb = b[kind]
-            assert nb == P // 3
-            assert bytes(buf[off:off + nb]) == want[i * P + part * nb:i * P + (part + 1) * nb].tobytes()
+            assert nb == (m_gu if kind != "down" else P - 2 * m_gu)
+            assert bytes(buf[off:off + nb]) == want[i * P + start:i * P + start + nb].tobytes()
             _, _, toff, tnb = tensors[f"blk.{b['layer']}.ffn_{kind}_exps.weight"]
             assert toff + b["expert"] * nb == off
 
@@ -118,3 +122,48 @@ def test_rejects_bad_files(mc, tmp_path):
     with pytest.raises(mc.MoeError) as e:
         mc.pack_gguf(src, tmp_path / "x.pack", tmp_path / "x.index")
     assert e.value.code == mc.MOE_EINVAL and "blk.1.ffn_down_exps" in str(e.value)
+
+
+def test_rejects_types_that_change_between_layers(mc, tmp_path):
+    """Every slot holds P bytes, so the down matrices must share one block type in all
+    layers (a file mixing Q6_K and Q4_K down tensors is refused)."""
+    src = tmp_path / "mixed_layers.gguf"
+    gguf_writer.moe_model(src, 2, 4, 256, 256, 12 | 14 << 8, 2, 1)
+    _, tensors, buf = gguf.read(src)
+    items = []
+    rng = np.random.default_rng(2)
+    for name, (dims, t, off, nb) in tensors.items():
+        raw = bytes(buf[off:off + nb])
+        if name == "blk.1.ffn_down_exps.weight":
+            import synth
+            t = 12
+            raw = synth.encode_blocks(12, (rng.normal(size=int(np.prod(dims))) * 0.02)
+                                      .astype(np.float32)).tobytes()
+        items.append((name, dims, t, raw))
+    gguf_writer.write(src, [], items)
+    with pytest.raises(mc.MoeError) as e:
+        mc.pack_gguf(src, tmp_path / "x.pack", tmp_path / "x.index")
+    assert e.value.code == mc.MOE_EINVAL and "blk.1.ffn_down_exps" in str(e.value)
+
+
+@pytest.mark.skipif(__import__("shutil").which("g++") is None, reason="g++ not available")
+def test_packer_under_sanitizers_on_damaged_files(tmp_path):
+    """The GGUF reader and packer built with AddressSanitizer + UndefinedBehaviorSanitizer
+    (g++, host code only) on truncated, bit-flipped and field-overwritten copies of valid
+    files: every call returns a code of the interface, nothing faults or overflows."""
+    import subprocess
+    from conftest import ROOT
+    seeds = []
+    for i, (qcode, inter) in enumerate(((8, 128), (12 | 14 << 8, 256))):
+        p = tmp_path / f"seed{i}.gguf"
+        gguf_writer.moe_model(p, 2, 4, 256, inter, qcode, 2, i, router_type=i)
+        seeds.append(str(p))
+    exe = tmp_path / "pack_fuzz"
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", os.path.join(ROOT, "tests", "pack_fuzz.cpp"),
+           os.path.join(ROOT, "paper_2607_09686_amd", "csrc", "pack.cpp"), "-o", str(exe)]
+    subprocess.run(cmd, check=True)
+    r = subprocess.run([str(exe), str(tmp_path), *seeds], capture_output=True, text=True,
+                       timeout=600)
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-4000:]
+    assert r.stdout.startswith("ok"), r.stdout

@@ -92,6 +92,23 @@ def test_hidden_ar1_and_iid():
 def test_workload_sizes(name):
     wl = synth.WORKLOADS[name]
     expect_p = {"tiny": 104448, "a3b_decode": 5013504, "a3b_sweep": 5013504,
-                "q4_decode": 6690816, "a3b_prefill": 5013504, "a3b_verify": 5013504}[name]
+                "q4_decode": 6690816, "a3b_prefill": 5013504, "a3b_verify": 5013504,
+                "q4km_decode": 3059712}[name]
     assert wl.payload_bytes == expect_p
     assert wl.payload_bytes % 16 == 0
+
+
+@pytest.mark.parametrize("qtype", ["q4_k", "q6_k", "q4_k_m"])
+def test_kquant_store_decodes_near_the_drawn_weights(qtype):
+    """The K-quant encoders (generation only) keep the drawn N(0, 0.02) weights: the oracle's
+    decoding of the store is within the formats' quantisation error of them."""
+    from oracle import quant
+    wl = synth.WORKLOADS["tiny"].with_(qtype=qtype, inter=256)
+    arr = synth.expert_store(wl)
+    assert arr.size == wl.store_bytes
+    gu, dn = wl.formats
+    for m, fmt in enumerate((gu, gu, dn)):
+        w = quant.expert_weights(arr, qtype, wl.n_experts, wl.hidden, wl.inter, 0, 5)[m]
+        drawn = synth.normal_f32(synth.key(1, wl.model_seed, 0, 5, m), 0, w.size, wl.weight_sigma)
+        rel = np.sqrt(np.mean((w.ravel() - drawn) ** 2)) / np.sqrt(np.mean(drawn.astype(np.float64) ** 2))
+        assert rel < {"q4_k": 0.1, "q6_k": 0.03}[fmt], (m, fmt, rel)
