@@ -106,13 +106,17 @@ typedef struct {
   int32_t hidden;    /* H, model width, multiple of 64, <= 8192 */
   int32_t inter;     /* I, expert intermediate width, multiple of 64, <= 8192;
                         top_k * inter <= 12288 (decode activations live in LDS) */
-  int32_t qtype;     /* MOE_Q8_0 or MOE_Q4_0 */
+  int32_t qtype;     /* MOE_Q8_0, MOE_Q4_0, MOE_Q4_K, MOE_Q6_K, or MOE_QTYPE_MIX of the two
+                        K-quant formats (MOE_Q4_K_M); K-quants: hidden (gate/up) and inter
+                        (down) multiples of 256 */
   /* Expert store, caller-owned, must outlive the handle and stay unchanged.
    * Layout: for layer l and expert e a payload of P bytes at offset
-   * (l*n_experts + e)*P, P = 3*M with M = inter*(hidden/32)*block_bytes:
+   * (l*n_experts + e)*P, P = 2*M + Md with M = inter*(hidden/w)*block_bytes
+   * and Md = hidden*(inter/w_d)*block_bytes_d (w = 32 or 256 weights per block
+   * of the matrix's format):
    *   [W_gate: inter rows x hidden | W_up: inter x hidden | W_down: hidden x inter]
    * each row-major, one row per output, a row = its inputs as consecutive
-   * 32-weight blocks.  Must be pinned host memory from hipHostMalloc (e.g.
+   * blocks (or super-blocks).  Must be pinned host memory from hipHostMalloc (e.g.
    * moe_host_alloc); device memory is accepted too.  Pageable memory is
    * rejected with MOE_EINVAL. */
   const void *host_store;

@@ -10,6 +10,22 @@ namespace moecache {
 
 constexpr int kMaxRouted = 16;  // experts per FFN launch (top_k <= 16 in decode)
 
+// Model type codes (desc.qtype): the format of W_gate / W_up in the low byte,
+// that of W_down in the next byte (0: the same).  Formats: 8 Q8_0, 2 Q4_0
+// (32 weights per block), 12 Q4_K, 14 Q6_K (256 per super-block).
+inline int fmt_gate_up(int qtype) { return qtype & 0xff; }
+inline int fmt_down(int qtype) { return (qtype >> 8) & 0xff ? (qtype >> 8) & 0xff : qtype & 0xff; }
+inline bool fmt_known(int f) { return f == 8 || f == 2 || f == 12 || f == 14; }
+inline bool fmt_kquant(int f) { return f == 12 || f == 14; }
+inline int fmt_block_bytes(int f) { return f == 8 ? 34 : f == 2 ? 18 : f == 12 ? 144 : f == 14 ? 210 : 0; }
+inline int fmt_block_weights(int f) { return fmt_kquant(f) ? 256 : 32; }
+// the activations' digit sums are needed by down formats with an offset (Q4_0) or a min (Q4_K)
+inline bool fmt_needs_sums(int f) { return f == 2 || f == 12; }
+// bytes of a rows x cols matrix (rows of cols inputs) in format f
+inline int64_t fmt_matrix_bytes(int f, int64_t rows, int64_t cols) {
+  return rows * (cols / fmt_block_weights(f)) * fmt_block_bytes(f);
+}
+
 // Optional events recorded by the runtime right at the start of the first
 // kernel and the end of the last kernel of a launch wrapper (null: none).
 struct Timing {
@@ -109,7 +125,7 @@ hipError_t launch_router_small(const float *x, const float *wr, int T, int H, in
 // token); combine does nothing when W (nullable) is a device list left empty
 // by the table step.  umax: an upper bound on the union size (the grids); false from
 // mt_ffn_fits: a shape these kernels do not take.
-bool mt_ffn_fits(int H, int I, int T);
+bool mt_ffn_fits(int qtype, int H, int I, int T);
 size_t mt_gateup_lds(int H, int T);
 hipError_t launch_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc, int8_t *hq,
                             float *hsc, int32_t *hds, int H, int I, int k, int T, int umax,

@@ -1124,16 +1124,18 @@ struct GateUpParams {
   float *hsc;        // their 16-wide block scales [k*I/16]
   int32_t *hds;      // their digit sums [3][k*I/16] (Q4_0)
   int H, I, k;
-  int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs per lane
+  int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs (K-quants: items) per lane
   int lanes_log2;
+  int h_sums;  // K-quant gate/up: also write the activations' digit sums (down format Q4_0 / Q4_K)
 };
 
 // Digits of SwiGLU activations in 16-wide blocks, called by 16 consecutive
 // lanes holding the values of rows row0 .. row0+15 of the expert at top-k
 // position pos (one value each, lane l has row row0 + l).
-template <int QT>
-__device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I, int k, int8_t *hq,
-                                               float *hsc, int32_t *hds) {
+// sums: also the blocks' digit sums (the down formats with an offset or a
+// min term, Q4_0 and Q4_K, need them).  Uniform over the 16 lanes.
+__device__ __forceinline__ void store_h_digits_rt(float v, int pos, int row, int I, int k, int8_t *hq,
+                                                  float *hsc, int32_t *hds, bool sums) {
   float m = fabsf(v);
 #pragma unroll
   for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
@@ -1141,7 +1143,7 @@ __device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I,
   int d1, d2, d3;
   digits_of(v, rs, d1, d2, d3);
   int t1 = d1, t2 = d2, t3 = d3;
-  if constexpr (QT == 2) {
+  if (sums) {
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
       t1 += __shfl_xor(t1, off, kWave);
@@ -1156,13 +1158,18 @@ __device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I,
     hq[2 * KI + i] = (int8_t)d3;
     if ((row & 15) == 0) {
       hsc[i / 16] = m * (1.f / 127.f);
-      if constexpr (QT == 2) {
+      if (sums) {
         hds[i / 16] = t1;
         hds[KI / 16 + i / 16] = t2;
         hds[2 * (KI / 16) + i / 16] = t3;
       }
     }
   }
+}
+template <int QT>
+__device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I, int k, int8_t *hq,
+                                               float *hsc, int32_t *hds) {
+  store_h_digits_rt(v, pos, row, I, k, hq, hsc, hds, QT == 2);
 }
 
 // One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
@@ -1560,6 +1567,7 @@ struct DownParams {
   int lanes, mpairs;  // as in the gate/up kernel
   int rows;           // output rows per block: rows * n * lanes <= 256
   int lanes_log2;
+  int64_t down_off;   // K-quant down: bytes from a payload's start to its W_down
 };
 
 // One unit = (output row j, expert i), `lanes` lanes, lane l handling pairs
@@ -1651,6 +1659,349 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
     // the weighted rows first, then the residual / earlier sum in one addition,
     // so that a small MoE output on a large residual is rounded once
     float v = 0.f;
+    for (int ii = 0; ii < n; ++ii) v = fmaf(wL[ii], res[threadIdx.x * n + ii], v);
+    a.y[jt] = base_t + v;
+  }
+}
+
+// ------------------------------------------------------ K-quant decode FFN ---
+//
+// Q4_K and Q6_K store weights in super-blocks of 256.  A lane's unit of work
+// (an "item") is half a super-block: 128 consecutive weights of a row, which
+// meet the input digit images of pairs 2 it and 2 it + 1.
+//   Q4_K (144-byte super-blocks, 16-byte aligned): the item loads the
+//   super-block's 16-byte header (d, dmin, the 12 bytes of 6-bit scales and
+//   mins) and its 64 bytes of 4-bit q (chunks 2h and 2h+1: sub-blocks 4h ..
+//   4h+3, low nibbles the even sub-block of a chunk, high nibbles the odd).
+//   Weight d sc q - dmin m: the min term meets the inputs' digit sums.
+//   Q6_K (210-byte super-blocks, so only 2-byte aligned): ql[64h .. +64),
+//   qh[32h .. +32), the 8 scales of the half and d, loaded from the 4-byte
+//   aligned address below (never outside the payload: a payload starts and
+//   ends 16-byte aligned, so its first super-block has offset 0 and its last
+//   one ends on a dword) and realigned with alignbyte.  Each q - 32 is formed
+//   as a signed byte, so no digit sums are needed.
+template <int QT>
+struct KFmt;
+// kDw: dwords an item holds; flights: items per lane loading at once
+template <>
+struct KFmt<12> {
+  static constexpr int kSB = 144, kDw = 20, kGateUpFlight = 2, kDownFlight = 2;
+};
+template <>
+struct KFmt<14> {
+  static constexpr int kSB = 210, kDw = 30, kGateUpFlight = 1, kDownFlight = 2;
+};
+
+// Item it of a row into w; returns the byte shift that realigns a Q6_K item (0 or 2).
+template <int QT>
+__device__ __forceinline__ int load_item(const uint8_t *row, int it, uint32_t (&w)[KFmt<QT>::kDw]) {
+  const int sb = it >> 1, h = it & 1;
+  if constexpr (QT == 12) {
+    const uint8_t *b = row + (int64_t)sb * 144;
+    const u32x4 hd = *(g_u32x4_a4 *)b;
+    w[0] = hd.x;
+    w[1] = hd.y;
+    w[2] = hd.z;
+    w[3] = hd.w;
+    g_u32x4_a4 *q = (g_u32x4_a4 *)(b + 16 + 64 * h);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u32x4 v = q[i];
+      w[4 + 4 * i] = v.x;
+      w[5 + 4 * i] = v.y;
+      w[6 + 4 * i] = v.z;
+      w[7 + 4 * i] = v.w;
+    }
+    return 0;
+  } else {
+    const uint8_t *b = row + (int64_t)sb * 210;
+    const int sh = (int)((uintptr_t)b & 3);
+    const uint8_t *a = b - sh;
+    const uint8_t *ql = a + 64 * h, *qh = a + 128 + 32 * h;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u32x4 v = ((g_u32x4_a4 *)ql)[i];
+      w[4 * i] = v.x;
+      w[4 * i + 1] = v.y;
+      w[4 * i + 2] = v.z;
+      w[4 * i + 3] = v.w;
+    }
+    w[16] = ((g_u32 *)ql)[16];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const u32x4 v = ((g_u32x4_a4 *)qh)[i];
+      w[17 + 4 * i] = v.x;
+      w[18 + 4 * i] = v.y;
+      w[19 + 4 * i] = v.z;
+      w[20 + 4 * i] = v.w;
+    }
+    w[25] = ((g_u32 *)qh)[8];
+    const g_u32 *sc = (g_u32 *)(a + 192 + 8 * h);
+    w[26] = sc[0];
+    w[27] = sc[1];
+    w[28] = sc[2];
+    w[29] = ((g_u32 *)(a + 208))[0];
+    return sh;
+  }
+}
+
+// Partial dot of a Q4_K item with 128 inputs given as digit images (pairs 2it,
+// 2it+1 of qL).  B16 false: the inputs' 32-wide blocks (scales scL[b], digit
+// sums dsL[b + c dstride]); true: 16-wide blocks (scL[q], dsL[q + c dstride]).
+template <bool B16>
+__device__ __forceinline__ float q4k_item_dot(const uint32_t (&w)[20], const uint8_t *qL, int pb, int it,
+                                              const float *scL, const int *dsL, int dstride) {
+  const int h = it & 1;
+  const float d = half_bits_to_float(w[0] & 0xffffu), dmin = half_bits_to_float(w[0] >> 16);
+  const uint32_t B0 = w[1], B1 = w[2], B2 = w[3];  // the 12 scale bytes
+  // byte j of SC / MN: scale / min of sub-block 4h + j
+  const uint32_t SC = h ? ((B2 & 0x0f0f0f0fu) | ((B0 >> 2) & 0x30303030u)) : (B0 & 0x3f3f3f3fu);
+  const uint32_t MN = h ? (((B2 >> 4) & 0x0f0f0f0fu) | ((B1 >> 2) & 0x30303030u)) : (B1 & 0x3f3f3f3fu);
+  float acc = 0.f;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int p = 2 * it + t;
+    uint32_t D[48];
+    load_digits(qL, pb, p, D);
+    int A[4][3] = {};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t q = w[4 + 8 * t + i];
+      const uint32_t lo = q & 0x0f0f0f0fu, hi = (q >> 4) & 0x0f0f0f0fu;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        const int ql = B16 ? (i >> 2) : 0, qh = B16 ? 2 + (i >> 2) : 1;
+        A[ql][c] = sdot4(lo, D[16 * c + i], A[ql][c]);
+        A[qh][c] = sdot4(hi, D[16 * c + 8 + i], A[qh][c]);
+      }
+    }
+    const float sc_lo = (float)((SC >> (16 * t)) & 0xffu), sc_hi = (float)((SC >> (16 * t + 8)) & 0xffu);
+    const float m_lo = (float)((MN >> (16 * t)) & 0xffu), m_hi = (float)((MN >> (16 * t + 8)) & 0xffu);
+    if constexpr (B16) {
+      const float *s = scL + 4 * p;
+      const int *ds = dsL + 4 * p;
+      float x[4], nsum[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        x[q] = s[q] * recombine(A[q][0], A[q][1], A[q][2]);
+        nsum[q] = s[q] * recombine(ds[q], ds[q + dstride], ds[q + 2 * dstride]);
+      }
+      acc += fmaf(d, fmaf(sc_lo, x[0] + x[1], sc_hi * (x[2] + x[3])),
+                  -dmin * fmaf(m_lo, nsum[0] + nsum[1], m_hi * (nsum[2] + nsum[3])));
+    } else {
+      const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
+      const int *ds = dsL + 2 * p;
+      const float n0 = s0 * recombine(ds[0], ds[dstride], ds[2 * dstride]);
+      const float n1 = s1 * recombine(ds[1], ds[1 + dstride], ds[1 + 2 * dstride]);
+      const float x0 = s0 * recombine(A[0][0], A[0][1], A[0][2]);
+      const float x1 = s1 * recombine(A[1][0], A[1][1], A[1][2]);
+      acc += fmaf(d, fmaf(sc_lo, x0, sc_hi * x1), -dmin * fmaf(m_lo, n0, m_hi * n1));
+    }
+  }
+  return acc;
+}
+
+// Partial dot of a Q6_K item (realigned by sh bytes) with 128 inputs as digit
+// images.  B16 false: 32-wide input blocks (scales scL[b]); true: 16-wide (scL[q]).
+template <bool B16>
+__device__ __forceinline__ float q6k_item_dot(const uint32_t (&w)[30], int sh, const uint8_t *qL, int pb,
+                                              int it, const float *scL) {
+  uint32_t QL[16], QH[8];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) QL[i] = __builtin_amdgcn_alignbyte(w[i + 1], w[i], sh);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) QH[i] = __builtin_amdgcn_alignbyte(w[18 + i], w[17 + i], sh);
+  const uint32_t S[2] = {__builtin_amdgcn_alignbyte(w[27], w[26], sh),
+                         __builtin_amdgcn_alignbyte(w[28], w[27], sh)};
+  const float d = half_bits_to_float((w[29] >> (8 * sh)) & 0xffffu);
+  float acc = 0.f;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    uint32_t D[48];
+    load_digits(qL, pb, 2 * it + pp, D);
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      const int g = 2 * pp + gg;  // weights 32g .. 32g+31 of the item
+      int A[2][3] = {};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t lo4 = (QL[8 * (g & 1) + i] >> (4 * (g >> 1))) & 0x0f0f0f0fu;
+        const uint32_t hi2 = (QH[i] >> (2 * g)) & 0x03030303u;
+        // q - 32 as signed bytes: flip bit 5, then copy it into bits 6 and 7
+        const uint32_t v = (lo4 | (hi2 << 4)) ^ 0x20202020u, sg = v & 0x20202020u;
+        const uint32_t q = v | (sg << 1) | (sg << 2);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) A[i >> 2][c] = sdot4(q, D[16 * c + 8 * gg + i], A[i >> 2][c]);
+      }
+      const float s_a = (float)(int8_t)((S[g >> 1] >> (16 * (g & 1))) & 0xffu);
+      const float s_b = (float)(int8_t)((S[g >> 1] >> (16 * (g & 1) + 8)) & 0xffu);
+      const float ra = recombine(A[0][0], A[0][1], A[0][2]), rb = recombine(A[1][0], A[1][1], A[1][2]);
+      if constexpr (B16) {
+        const int q0 = 8 * it + 2 * g;
+        acc += d * fmaf(s_a * scL[q0], ra, s_b * scL[q0 + 1] * rb);
+      } else {
+        acc += d * scL[4 * it + g] * fmaf(s_a, ra, s_b * rb);
+      }
+    }
+  }
+  return acc;
+}
+
+template <int QT, bool B16>
+__device__ __forceinline__ float item_dot(const uint32_t (&w)[KFmt<QT>::kDw], int sh, const uint8_t *qL,
+                                          int pb, int it, const float *scL, const int *dsL, int dstride) {
+  if constexpr (QT == 12)
+    return q4k_item_dot<B16>(w, qL, pb, it, scL, dsL, dstride);
+  else
+    return q6k_item_dot<B16>(w, sh, qL, pb, it, scL);
+}
+
+// gateup_body for the K-quant formats: one unit = row r of W_gate and of W_up,
+// lane l of the unit's lanes handles items l, l+lanes, ... (F of each in flight).
+template <int QT>
+__device__ __forceinline__ void kgateup_body(const GateUpParams &a, const ExpertList &L,
+                                             const int32_t *hit, int blk, uint8_t *smem8) {
+  constexpr int DW = KFmt<QT>::kDw, F = KFmt<QT>::kGateUpFlight, SB = KFmt<QT>::kSB;
+  const int H = a.H, nb = H / 32, ni = H / 128, pb = plane_bytes(H);
+  uint8_t *qL = smem8;
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * pb);
+  int *dsL = reinterpret_cast<int *>(scL + nb);
+  float *hL = reinterpret_cast<float *>(dsL + 3 * nb);
+  const int upb = kThreads / a.lanes;
+  const int bpe = (a.I + upb - 1) / upb;
+  const int ei = blk / bpe;
+  const int n = L.n, pos = L.pos[ei], use = hit ? hit[ei] : 1;
+  const uint8_t *const payload = L.payload[ei];
+  if (ei >= n || !use || payload == nullptr) return;  // uniform over the block
+  const int r0 = (blk - ei * bpe) * upb;
+  const int r = r0 + (threadIdx.x >> a.lanes_log2);
+  const int l = threadIdx.x & (a.lanes - 1);
+  const bool active = r < a.I;
+  const int64_t rowb = (int64_t)(H / 256) * SB, mat = (int64_t)a.I * rowb;
+  const uint8_t *gate = payload + (int64_t)min(r, a.I - 1) * rowb, *up = gate + mat;
+  __shared__ __align__(16) uint8_t dummyL[16];
+  TokStage ts;
+  stage_token_load(a.xq, a.xsc, H, ts);
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t wg[F][DW], wu[F][DW];
+  int shg[F], shu[F];
+#pragma unroll
+  for (int m = 0; m < F; ++m) {  // unconditional: an idle slot reloads item 0 of its (clamped) row
+    const int it = l + m * a.lanes;
+    const int itc = (active && m < a.mpairs && it < ni) ? it : 0;
+    shg[m] = load_item<QT>(gate, itc, wg[m]);
+    shu[m] = load_item<QT>(up, itc, wu[m]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  stage_token_store(ts, H, qL, scL, dummyL);
+  __syncthreads();
+  if constexpr (QT == 12) {
+    digit_sums(qL, H, dsL);
+    __syncthreads();
+  }
+  float g = 0.f, u = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < F; ++m) {
+        const int it = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && it < ni) {
+          shg[m] = load_item<QT>(gate, it, wg[m]);
+          shu[m] = load_item<QT>(up, it, wu[m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < F; ++m) {
+      const int it = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && it < ni) {
+        g += item_dot<QT, false>(wg[m], shg[m], qL, pb, it, scL, dsL, nb);
+        u += item_dot<QT, false>(wu[m], shu[m], qL, pb, it, scL, dsL, nb);
+      }
+    }
+  }
+  g = group_sum(g, a.lanes);
+  u = group_sum(u, a.lanes);
+  if (l == 0) hL[threadIdx.x >> a.lanes_log2] = active ? silu(g) * u : 0.f;
+  __syncthreads();
+  if ((int)threadIdx.x < upb)
+    store_h_digits_rt(hL[threadIdx.x], pos, r0 + threadIdx.x, a.I, a.k, a.hq, a.hsc, a.hds, a.h_sums != 0);
+}
+
+template <int QT, bool DEV>
+__global__ __launch_bounds__(kThreads) void kgateup_kernel(GateUpParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  kgateup_body<QT>(a, DEV ? *a.Ld : a.L, nullptr, blockIdx.x, smem8);
+}
+
+// down_kernel for the K-quant formats: one unit = (output row j, expert i),
+// lanes l handling items l, l+lanes, ... (F in flight); W_down at a.down_off.
+template <int QT, bool DEV>
+__global__ __launch_bounds__(kThreads, 1) void kdown_kernel(DownParams a) {
+  extern __shared__ __align__(16) uint8_t smem8[];
+  __shared__ int posL[kMaxRouted];
+  __shared__ float wL[kMaxRouted];
+  __shared__ __align__(16) uint8_t dummyL[16];
+  constexpr int DW = KFmt<QT>::kDw, F = KFmt<QT>::kDownFlight, SB = KFmt<QT>::kSB;
+  const ExpertList &L = DEV ? *a.Ld : a.L;
+  const int I = a.I, ni = I / 128, n = a.L.n, pb = plane_bytes(I);
+  uint8_t *qL = smem8;
+  float *scL = reinterpret_cast<float *>(smem8 + 3 * n * pb);
+  int *dsL = reinterpret_cast<int *>(scL + n * (I / 16));
+  float *res = reinterpret_cast<float *>(dsL + 3 * n * (I / 16));
+  const int j0 = blockIdx.x * a.rows;
+  const int unit = threadIdx.x >> a.lanes_log2, l = threadIdx.x & (a.lanes - 1);
+  const int i = unit / a.rows, rr = unit - i * a.rows, j = j0 + rr, ic = min(i, n - 1);
+  const bool active = i < n && j < a.H;
+  const int64_t rowb = (int64_t)(I / 256) * SB;
+  const int ndev = L.n;
+  const uint8_t *const payload = L.payload[ic];
+  const int pos_t = (int)threadIdx.x < n ? L.pos[threadIdx.x] : 0;
+  if (ndev != n) return;  // a device list emptied by a routing error (uniform)
+  if ((int)threadIdx.x < n) posL[threadIdx.x] = pos_t;
+  __syncthreads();
+  const uint8_t *row = payload + a.down_off + (int64_t)min(j, a.H - 1) * rowb;
+  HStage st;
+  stage_h_load(a.hq, a.hsc, a.hds, posL, n, I, a.k, QT == 12, st);
+  __builtin_amdgcn_sched_barrier(0);
+  const float w_t = a.w[posL[min((int)threadIdx.x, n - 1)]];
+  const int jt = j0 + (int)threadIdx.x;
+  const bool out_t = (int)threadIdx.x < a.rows && jt < a.H;
+  const float base_ld = (a.mode == 1 ? a.x : a.y)[min(jt, a.H - 1)];
+  const float base_t = a.mode == 0 ? 0.f : base_ld;
+  uint32_t wd[F][DW];
+  int sh[F];
+#pragma unroll
+  for (int m = 0; m < F; ++m) {
+    const int it = l + m * a.lanes;
+    sh[m] = load_item<QT>(row, (active && m < a.mpairs && it < ni) ? it : 0, wd[m]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  stage_h_store(st, n, I, QT == 12, qL, scL, dsL, dummyL);
+  __syncthreads();
+  float acc = 0.f;
+  for (int m0 = 0; m0 < a.mpairs; m0 += F) {
+    if (m0 > 0) {
+#pragma unroll
+      for (int m = 0; m < F; ++m) {
+        const int it = l + (m0 + m) * a.lanes;
+        if (active && m0 + m < a.mpairs && it < ni) sh[m] = load_item<QT>(row, it, wd[m]);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < F; ++m) {
+      const int it = l + (m0 + m) * a.lanes;
+      if (active && m0 + m < a.mpairs && it < ni)
+        acc += item_dot<QT, true>(wd[m], sh[m], qL + 3 * i * pb, pb, it, scL + i * (I / 16),
+                                  dsL + 3 * i * (I / 16), I / 16);
+    }
+  }
+  acc = group_sum(acc, a.lanes);
+  if (active && l == 0) res[rr * n + i] = acc;
+  if ((int)threadIdx.x < n) wL[threadIdx.x] = w_t;
+  __syncthreads();
+  if (out_t) {
+    float v = 0.f;  // rows first, then the residual / earlier sum (as down_kernel)
     for (int ii = 0; ii < n; ++ii) v = fmaf(wL[ii], res[threadIdx.x * n + ii], v);
     a.y[jt] = base_t + v;
   }
@@ -2666,8 +3017,29 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
 
 hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
                          const ExpertList *Ld, hipStream_t s, const Timing &t) {
+  const int gu = fmt_gate_up(qtype), dn = fmt_down(qtype);
+  if (gu == 12 || gu == 14) {
+    if (H % 256 || L.n > kMaxRouted) return hipErrorInvalidValue;
+    GateUpParams a{L, Ld, S.xq, S.xsc, S.hq, S.hsc, S.hds, H, I, k, 0, 0, 0, fmt_needs_sums(dn) ? 1 : 0};
+    pick_lanes(H / 128, gu == 12 ? KFmt<12>::kGateUpFlight : KFmt<14>::kGateUpFlight, kGateUpMaxLanes,
+               a.lanes, a.mpairs);
+    while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
+    const int upb = kThreads / a.lanes;
+    const size_t lds = 3 * (size_t)(H / 64) * kPairPitch + 4 * (size_t)(H / 32) * 4 + 4 * (size_t)upb;
+    dim3 grid(L.n * ((I + upb - 1) / upb));
+    if (gu == 12 && Ld)
+      hipExtLaunchKernelGGL(kgateup_kernel<12, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else if (gu == 12)
+      hipExtLaunchKernelGGL(kgateup_kernel<12, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else if (Ld)
+      hipExtLaunchKernelGGL(kgateup_kernel<14, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else
+      hipExtLaunchKernelGGL(kgateup_kernel<14, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    return hipGetLastError();
+  }
+  if (dn != gu) return hipErrorInvalidValue;  // Q8_0 / Q4_0 models use one format throughout
   const int np = H / 64;
-  GateUpParams a{L, Ld, S.xq, S.xsc, S.hq, S.hsc, S.hds, H, I, k, 0, 0, 0};
+  GateUpParams a{L, Ld, S.xq, S.xsc, S.hq, S.hsc, S.hds, H, I, k, 0, 0, 0, 0};
   pick_lanes(np, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes,
              a.lanes, a.mpairs);
   while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
@@ -2689,9 +3061,33 @@ hipError_t launch_gateup(int qtype, const DecodeScratch &S, int H, int I, int k,
 hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, const ExpertList &L,
                        const ExpertList *Ld, const float *w, const float *x, float *y, int mode,
                        hipStream_t s, const Timing &t) {
-  const int np = I / 64;
   if (3 * L.n * I / 16 > kMaxDig16 * kThreads) return hipErrorInvalidValue;
-  DownParams a{L, Ld, S.hq, S.hsc, S.hds, w, x, y, H, I, k, mode, 0, 0, 0, 0};
+  const int dn = fmt_down(qtype);
+  if (dn == 12 || dn == 14) {
+    if (I % 256 || L.n > kMaxRouted) return hipErrorInvalidValue;
+    DownParams a{L, Ld, S.hq, S.hsc, S.hds, w, x, y, H, I, k, mode, 0, 0, 0, 0,
+                 2 * fmt_matrix_bytes(fmt_gate_up(qtype), I, H)};
+    pick_lanes(I / 128, dn == 12 ? KFmt<12>::kDownFlight : KFmt<14>::kDownFlight, kDownMaxLanes, a.lanes,
+               a.mpairs);
+    while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
+    a.rows = kThreads / (a.lanes * L.n);
+    if (a.rows < 1) return hipErrorInvalidValue;
+    const size_t lds = 3 * (size_t)L.n * (I / 64) * kPairPitch + 4 * (size_t)L.n * (I / 16) * 4 +
+                       4 * (size_t)a.rows * L.n;
+    dim3 grid((H + a.rows - 1) / a.rows);
+    if (dn == 12 && Ld)
+      hipExtLaunchKernelGGL(kdown_kernel<12, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else if (dn == 12)
+      hipExtLaunchKernelGGL(kdown_kernel<12, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else if (Ld)
+      hipExtLaunchKernelGGL(kdown_kernel<14, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    else
+      hipExtLaunchKernelGGL(kdown_kernel<14, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+    return hipGetLastError();
+  }
+  if (dn != fmt_gate_up(qtype)) return hipErrorInvalidValue;
+  const int np = I / 64;
+  DownParams a{L, Ld, S.hq, S.hsc, S.hds, w, x, y, H, I, k, mode, 0, 0, 0, 0, 0};
   pick_lanes(np, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
              a.mpairs);
   while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
@@ -2718,15 +3114,15 @@ size_t mt_gateup_lds(int H, int T) {
 }
 static size_t mt_down_lds(int I, int T) { return (size_t)T * (3 * (size_t)(I / 64) * kPairPitch + I); }
 
-bool mt_ffn_fits(int H, int I, int T) {
-  return T >= 1 && T <= kMtTokens && 3 * T * I / 16 <= kMaxDig16 * kThreads &&
+bool mt_ffn_fits(int qtype, int H, int I, int T) {
+  return (qtype == 8 || qtype == 2) && T >= 1 && T <= kMtTokens && 3 * T * I / 16 <= kMaxDig16 * kThreads &&
          mt_gateup_lds(H, T) <= 64 * 1024 && mt_down_lds(I, T) <= 64 * 1024;
 }
 
 hipError_t launch_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const float *xsc, int8_t *hq,
                             float *hsc, int32_t *hds, int H, int I, int k, int T, int umax,
                             hipStream_t s, const Timing &t) {
-  if (!mt_ffn_fits(H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
+  if (!mt_ffn_fits(qtype, H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
   GateUpMtParams a{W, xq, xsc, hq, hsc, hds, H, I, k, T, 0, 0, 0};
   pick_lanes(H / 64, qtype == 8 ? Fmt<8>::kGateUpFlight : Fmt<2>::kGateUpFlight, kGateUpMaxLanes, a.lanes,
              a.mpairs);
@@ -2744,7 +3140,7 @@ hipError_t launch_gateup_mt(int qtype, const MtWork *W, const int8_t *xq, const 
 hipError_t launch_down_mt(int qtype, const MtWork *W, const int8_t *hq, const float *hsc,
                           const int32_t *hds, float *R, int H, int I, int k, int T, int umax,
                           hipStream_t s, const Timing &t) {
-  if (!mt_ffn_fits(H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
+  if (!mt_ffn_fits(qtype, H, I, T) || umax < 1 || umax > kMtMaxCopy) return hipErrorInvalidValue;
   DownMtParams a{W, hq, hsc, hds, R, H, I, k, T, 0, 0, 0, 0};
   pick_lanes(I / 64, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
              a.mpairs);
@@ -2767,6 +3163,7 @@ hipError_t launch_combine_mt(const float *R, const float *w, const float *x, flo
 }
 
 bool fusable_copy_gateup(int qtype, int H, int I) {
+  if (qtype != 8 && qtype != 2) return false;  // Q8_0 / Q4_0 models (one format, 32-weight blocks)
   const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
   return 2 * 4 * rowb <= (int64_t)kChunkSlots * kThreads * 16 && I % 32 == 0;
 }
@@ -2804,7 +3201,7 @@ constexpr size_t kMtCopyLds = 160 * 1024;  // LDS one workgroup may take on gfx9
 // whose chunk fits the copy slots and whose LDS (T images, hL, the chunk)
 // fits a workgroup; 0 if none does.
 static int mt_copy_rows(int qtype, int H, int I, int T, size_t *lds) {
-  if (!mt_ffn_fits(H, I, T) || I % 32 != 0) return 0;
+  if (!mt_ffn_fits(qtype, H, I, T) || I % 32 != 0) return 0;
   const int64_t rowb = (int64_t)(H / 32) * (qtype == 8 ? 34 : 18);
   const size_t images = (size_t)T * (3 * (size_t)(H / 64) * kPairPitch + 16 * (size_t)(H / 32));
   for (int R = 8; R >= 2; R /= 2) {

@@ -72,8 +72,9 @@ struct TimedSpan {
 struct moe_cache {
   moe_model_desc d{};
   int32_t C = 0;
-  int bb = 0;           // block bytes
-  int64_t M = 0, P = 0; // matrix bytes, payload bytes
+  int64_t M = 0;   // bytes of one W_gate (or W_up) matrix
+  int64_t Md = 0;  // bytes of one W_down matrix (the same as M unless the formats differ)
+  int64_t P = 0;   // payload bytes: 2 M + Md
   hipStream_t main = nullptr, side = nullptr;
   int device = 0;
   bool poisoned = false;
@@ -253,7 +254,15 @@ int check_desc(const moe_model_desc *d, int32_t budget) {
     return fail(MOE_EINVAL, "hidden and inter must be multiples of 64 in [64, 8192]");
   if ((int64_t)d->top_k * d->inter > 12288)
     return fail(MOE_EINVAL, "top_k * inter must be <= 12288 (decode activations are staged in LDS)");
-  if (d->qtype != MOE_Q8_0 && d->qtype != MOE_Q4_0) return fail(MOE_EINVAL, "qtype must be MOE_Q8_0 or MOE_Q4_0");
+  {
+    const int gu = fmt_gate_up(d->qtype), dn = fmt_down(d->qtype);
+    if (d->qtype < 0 || d->qtype > 0xffff || !fmt_known(gu) || !fmt_known(dn) ||
+        (gu != dn && !(fmt_kquant(gu) && fmt_kquant(dn))))
+      return fail(MOE_EINVAL, "qtype must be MOE_Q8_0, MOE_Q4_0, MOE_Q4_K, MOE_Q6_K or a mix of the two "
+                  "K-quant formats (MOE_QTYPE_MIX)");
+    if ((fmt_kquant(gu) && d->hidden % 256) || (fmt_kquant(dn) && d->inter % 256))
+      return fail(MOE_EINVAL, "K-quant formats need hidden (gate/up) and inter (down) multiples of 256");
+  }
   if (budget < d->top_k || budget > d->n_experts)
     return fail(MOE_EINVAL, "budget_slots %d outside [top_k=%d, n_experts=%d]", budget, d->top_k,
                 d->n_experts);
@@ -637,7 +646,7 @@ int forward_decode_dev(moe_cache *c, const float *x, const float *wr, int32_t la
     sp.end();
   }
   {
-    Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * d.hidden * d.inter);
+    Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->Md, 2ull * k * d.hidden * d.inter);
     HIP_TRY(c, launch_down(d.qtype, b.s, d.hidden, d.inter, k, shape, &b.work->list,
                            b.w, x, y, (d.flags & MOE_F_RESIDUAL) ? 1 : 0, c->main, sp.timing()));
     sp.end();
@@ -725,7 +734,7 @@ int forward_decode(moe_cache *c, const float *x, const float *wr, int32_t layer,
     L.pos[L.n++] = all.pos[all.n++] = i;
   }
   const bool resid = d.flags & MOE_F_RESIDUAL;
-  const uint64_t gu_bytes = 2ull * c->M, dn_bytes = (uint64_t)c->M;
+  const uint64_t gu_bytes = 2ull * c->M, dn_bytes = (uint64_t)c->Md;
   const uint64_t gu_flops = 4ull * d.hidden * d.inter, dn_flops = 2ull * d.hidden * d.inter;
   auto gateup = [&](const ExpertList &L) -> int {
     Span sp(c, c->main, MOE_KIND_GATEUP, 1, L.n * gu_bytes, L.n * gu_flops);
@@ -848,7 +857,7 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   // take, the decode GEMVs once per token.  By default the union's gate/up
   // runs inside the copy launch (misses from the rows being copied, hits
   // alongside), as in decode.
-  const bool union_ffn = mt_ffn_fits(H, I, T);
+  const bool union_ffn = mt_ffn_fits(d.qtype, H, I, T);
   const bool fused = union_ffn && !(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup_mt(d.qtype, H, I, T);
   const int umax = std::min(T * k, (int)c->C);
   uint64_t *acc = c->timing_now ? c->dl_copy_acc : nullptr;
@@ -885,7 +894,7 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
         sp.end();
       }
       {
-        Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * H * I);
+        Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->Md, 2ull * k * H * I);
         HIP_TRY(c, launch_down(d.qtype, St, H, I, k, shape, &c->mt_work->list[tk],
                                c->topk_w + (int64_t)tk * k, x + (int64_t)tk * H, y + (int64_t)tk * H, mode,
                                c->main, sp.timing()));
@@ -904,7 +913,7 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   const int32_t verdict = flag[0];
   if (union_ffn && verdict == 0) {
     gu.sp.bytes = (uint64_t)flag[1] * 2 * c->M;
-    dn.sp.bytes = (uint64_t)flag[1] * c->M;
+    dn.sp.bytes = (uint64_t)flag[1] * c->Md;
     if (fused)
       gu.discard();  // timed with the copies
     else
@@ -973,9 +982,9 @@ int moe_cache_create(const moe_model_desc *desc, int32_t budget_slots, moe_cache
   if (!c) return fail(MOE_ENOMEM, "out of host memory");
   c->d = *desc;
   c->C = budget_slots;
-  c->bb = desc->qtype == MOE_Q8_0 ? 34 : 18;
-  c->M = (int64_t)desc->inter * (desc->hidden / 32) * c->bb;
-  c->P = 3 * c->M;
+  c->M = fmt_matrix_bytes(fmt_gate_up(desc->qtype), desc->inter, desc->hidden);
+  c->Md = fmt_matrix_bytes(fmt_down(desc->qtype), desc->hidden, desc->inter);
+  c->P = 2 * c->M + c->Md;
   c->store = static_cast<const uint8_t *>(desc->host_store);
   c->main = static_cast<hipStream_t>(desc->hip_stream);
   const uint64_t want = (uint64_t)desc->n_layers * desc->n_experts * c->P;
@@ -1066,6 +1075,8 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
     return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
+  if (fmt_kquant(fmt_gate_up(c->d.qtype)) || fmt_kquant(fmt_down(c->d.qtype)))
+    return fail(MOE_EINVAL, "K-quant models take one token per layer call here");
   // a small call tries the device path unless the layer's last small call did
   // not fit the slots (then the device step would only report that again); the
   // two paths step the table by the same rule
@@ -1433,7 +1444,7 @@ int small_call_ffn(moe_cache *c, const float *x, int32_t T, int32_t layer, float
       sp.end();
     }
     {
-      Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->M, 2ull * k * H * I);
+      Span sp(c, c->main, MOE_KIND_DOWN, 1, (uint64_t)k * c->Md, 2ull * k * H * I);
       HIP_TRY(c, launch_down(d.qtype, St, H, I, k, L, nullptr, c->topk_w + (int64_t)tk * k,
                              x + (int64_t)tk * H, y + (int64_t)tk * H, mode, c->main, sp.timing()));
       sp.end();
@@ -1569,7 +1580,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
   // decode path, instead of the bf16 GEMMs sized for many tokens: one work
   // list per chunk (its experts, their slots and the (token, rank) positions
   // routed to each), all uploaded at once, and the token digits once
-  const bool mt = T <= kSmallTokens && mt_ffn_fits(H, I, T);
+  const bool mt = T <= kSmallTokens && mt_ffn_fits(d.qtype, H, I, T);
   int mt_positions = 0;
   if (mt) {
     if ((rc = ensure_mt_chunks(c, (int)chunks.size()))) return rc;
@@ -1599,7 +1610,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
     HIP_TRY(c, launch_token_digits(x, T, H, prenorm, c->st_xq, c->st_xsc, c->side));
   }
   const int copy_cap = max_copy();
-  const uint64_t M = (uint64_t)c->M;
+  const uint64_t M = (uint64_t)c->M, Md = (uint64_t)c->Md;
   int waited = -1;
   for (size_t ci = 0; ci < chunks.size(); ++ci) {
     const Chunk &ch = chunks[ci];
@@ -1646,7 +1657,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
         sp.end();
       }
       {
-        Span sp(c, c->side, MOE_KIND_DOWN, 1, umax * M, pos * 2ull * H * I);
+        Span sp(c, c->side, MOE_KIND_DOWN, 1, umax * Md, pos * 2ull * H * I);
         HIP_TRY(c, launch_down_mt(d.qtype, c->pf_mt_dev + ci, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H,
                                   I, k, T, umax, c->side, sp.timing()));
         sp.end();
@@ -1671,7 +1682,7 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
       sp.end();
     }
     {
-      Span sp(c, c->side, MOE_KIND_DOWN, 1, W.count * M, rows * 2ull * H * I);
+      Span sp(c, c->side, MOE_KIND_DOWN, 1, W.count * Md, rows * 2ull * H * I);
       HIP_TRY(c, launch_pf_down(d.qtype, W, c->pf_perm, c->pf_ab, c->topk_w, c->pf_P, T * k, H, I,
                                 c->side, sp.timing()));
       sp.end();

@@ -22,7 +22,10 @@ MOE_F_SIDE_COPY, MOE_F_SDMA_COPY, MOE_F_SPLIT_COPY, MOE_F_SCORE_EVICT = 16, 32, 
 COPY_MODES = {"kernel": 0, "split": MOE_F_SPLIT_COPY, "side": MOE_F_SIDE_COPY, "sdma": MOE_F_SDMA_COPY}
 KIND_ROUTER, KIND_GATEUP, KIND_DOWN, KIND_COPY = 0, 1, 2, 3
 KIND_NAMES = {KIND_ROUTER: "router", KIND_GATEUP: "gateup", KIND_DOWN: "down", KIND_COPY: "copy"}
-QTYPES = {"q8_0": MOE_Q8_0, "q4_0": MOE_Q4_0}
+MOE_Q4_K, MOE_Q6_K = 12, 14
+# model type: the gate/up format's code, the down format's in the next byte when it differs
+QTYPES = {"q8_0": MOE_Q8_0, "q4_0": MOE_Q4_0, "q4_k": MOE_Q4_K, "q6_k": MOE_Q6_K,
+          "q4_k_m": MOE_Q4_K | (MOE_Q6_K << 8)}
 
 
 class MoeError(RuntimeError):

@@ -125,3 +125,28 @@ def edge_tokens(X, zero_row=1, wide_row=3, seed=0):
         mag[1::32] = 1e-6
         X[wide_row] = (mag * np.where(rng.integers(0, 2, size=H) == 1, 1.0, -1.0)).astype(np.float32)
     return X
+
+
+def kquant_golden_blocks(kind):
+    """Raw bytes of the hand-worked K-quant super-blocks of one format ("q4_k" or "q6_k")."""
+    from test_oracle_quant import _kquant_golden
+    return [raw for k, raw, _ in _kquant_golden() if k == kind]
+
+
+def kquant_golden_store(arr, wl, seed=0):
+    """Rewrite a K-quant store: every super-block of every matrix replaced by a hand-worked
+    super-block of that matrix's format (seeded choice), scales, mins and signs included."""
+    rng = np.random.default_rng(500 + seed)
+    gu, dn = wl.formats
+    P, M = wl.payload_bytes, wl.matrix_bytes
+    n_payloads = arr.size // P
+    pay = arr.reshape(n_payloads, P)
+    for fmt, lo, hi in ((gu, 0, 2 * M), (dn, 2 * M, P)):
+        gold = kquant_golden_blocks(fmt)
+        sb = len(gold[0])
+        view = pay[:, lo:hi].reshape(n_payloads, (hi - lo) // sb, sb)
+        pick = rng.integers(0, len(gold), size=view.shape[:2])
+        for g, raw in enumerate(gold):
+            view[pick == g] = raw
+        pay[:, lo:hi] = view.reshape(n_payloads, hi - lo)
+    return arr
