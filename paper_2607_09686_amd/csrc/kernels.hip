@@ -2704,6 +2704,32 @@ typedef __attribute__((address_space(1))) const bf16x8 g_bf16x8;
     DEQ(B[((S) + 1) % 3], ((S) + 1) % 3);                               \
     __syncthreads();                                                    \
   } while (0)
+// GM_K_LOOP: as PF_K_LOOP for the 256-row tiles, whose dequantiser also takes
+// the K step (the K-quant formats locate a step's scales from it).
+#define GM_STEP(S, KT, kt, GLOAD, MMA, DEQ)                             \
+  do {                                                                  \
+    GLOAD(min((kt) + 2, (KT) - 1), A[((S) + 2) % 3], B[((S) + 2) % 3]); \
+    __builtin_amdgcn_sched_barrier(0);                                  \
+    MMA(A[(S)], (S));                                                   \
+    __builtin_amdgcn_sched_barrier(0);                                  \
+    DEQ(B[((S) + 1) % 3], ((S) + 1) % 3, min((kt) + 1, (KT) - 1));      \
+    __syncthreads();                                                    \
+  } while (0)
+#define GM_K_LOOP(KT, GLOAD, MMA, DEQ)                                  \
+  do {                                                                  \
+    GLOAD(0, A[0], B[0]);                                               \
+    GLOAD(min(1, (KT) - 1), A[1], B[1]);                                \
+    DEQ(B[0], 0, 0);                                                    \
+    __syncthreads();                                                    \
+    int kt_ = 0;                                                        \
+    for (; kt_ + 3 <= (KT); kt_ += 3) {                                 \
+      GM_STEP(0, KT, kt_, GLOAD, MMA, DEQ);                             \
+      GM_STEP(1, KT, kt_ + 1, GLOAD, MMA, DEQ);                         \
+      GM_STEP(2, KT, kt_ + 2, GLOAD, MMA, DEQ);                         \
+    }                                                                   \
+    if (kt_ < (KT)) GM_STEP(0, KT, kt_, GLOAD, MMA, DEQ);               \
+    if (kt_ + 1 < (KT)) GM_STEP(1, KT, kt_ + 1, GLOAD, MMA, DEQ);       \
+  } while (0)
 #define PF_K_LOOP(KT, GLOAD, MMA, DEQ)                                  \
   do {                                                                  \
     GLOAD(0, A[0], B[0]);                                               \
@@ -2897,8 +2923,344 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
       }
     }
 }
+// ------------------------------------------- grouped GEMMs, K-quant formats ---
+//
+// The same tiling as pf_gateup_kernel / pf_down_kernel (128-row M-tiles, four
+// waves of 32 rows, K steps of 64 with PF_K_LOOP's two steps of prefetch) with
+// a dequantiser for any of the four formats: thread t takes weight row t % 128
+// of the tile and, per K step, the quarters (t / 128) and (t / 128) + 2 of its
+// 64 weights (16 each).  Used for Q4_K / Q6_K; the 32-weight block formats run
+// the kernels above, whose one-block-per-thread dequantiser measured faster for
+// them (a 256-row, eight-wave variant of this kernel, dequantising each tile
+// once per 256 rows, ran no faster: the loop is bound by latency, not by the
+// dequantisation).
+constexpr int kGmThreads = 256;
+constexpr int kGmBM = 128;
+constexpr int kGmQ = 512 / kGmThreads;  // dequantised quarters per thread and step
+
+// (expert, M-tile) of a flat M-tile index with kGmBM-row tiles.
+__device__ __forceinline__ bool gm_tile(const PfExperts &X, int mt, int &j, int &m0) {
+  for (j = 0; j < X.count; ++j) {
+    const int tiles = (X.n[j] + kGmBM - 1) / kGmBM;
+    if (mt < tiles) {
+      m0 = mt * kGmBM;
+      return true;
+    }
+    mt -= tiles;
+  }
+  return false;
+}
+
+// The raw bytes thread quarter bq (0..3) needs for K step kt of a weight row:
+//   Q8_0 (pair of blocks at 68 kt): the 9 dwords of block bq / 2 (load_half);
+//   Q4_0 (pair at 36 kt): the 5 dwords of block bq / 2 (load_half);
+//   Q4_K (chunk kt % 4 of super-block kt / 4): the 16-byte header and the 16
+//     bytes of q holding weights 16 (bq % 2) .. +15 of the chunk's two sub-blocks;
+//   Q6_K (weights 64 (kt % 4) .. +63 of super-block kt / 4): 20 bytes around the
+//     16 ql bytes and 20 around the 16 qh bytes of the quarter, the dword holding
+//     its scale and the one holding d (addresses rounded down to a dword).
+template <int FMT>
+__device__ __forceinline__ void gm_load_raw(const uint8_t *row, int kt, int bq, uint32_t (&v)[12]) {
+  if constexpr (FMT == 8) {
+    // dwords of the 68-byte pair: v[0] = the one holding block b's d (dword 8b), v[1..5] =
+    // dwords 8b + 4 part .. +4, which hold the 16 q bytes of the quarter (block b = bq / 2,
+    // q bytes 2 + 16 part .. of the block)
+    const g_u32 *pw = (const g_u32 *)(row + (int64_t)kt * 68);
+    const int b = bq >> 1, w0 = 8 * b + 4 * (bq & 1);
+    v[0] = pw[8 * b];
+#pragma unroll
+    for (int i = 0; i < 5; ++i) v[1 + i] = pw[w0 + i];
+  } else if constexpr (FMT == 2) {
+    uint32_t t[9];
+    load_half<FMT>(row + (int64_t)kt * 36, bq >> 1, t);
+#pragma unroll
+    for (int i = 0; i < 5; ++i) v[i] = t[i];
+  } else if constexpr (FMT == 12) {
+    const uint8_t *b = row + (int64_t)(kt >> 2) * 144;
+    const u32x4 hd = *(g_u32x4_a4 *)b;
+    const u32x4 q = *(g_u32x4_a4 *)(b + 16 + 32 * (kt & 3) + 16 * (bq & 1));
+    v[0] = hd.x;
+    v[1] = hd.y;
+    v[2] = hd.z;
+    v[3] = hd.w;
+    v[4] = q.x;
+    v[5] = q.y;
+    v[6] = q.z;
+    v[7] = q.w;
+  } else {
+    const uint8_t *b = row + (int64_t)(kt >> 2) * 210;
+    const int sh = (int)((uintptr_t)b & 3), h = (kt & 3) >> 1, g = 2 * (kt & 1) + (bq >> 1);
+    const int l0 = 16 * (bq & 1);
+    const uint8_t *a = b - sh;
+    const g_u32 *ql = (const g_u32 *)(a + 64 * h + 32 * (g & 1) + l0);
+    const g_u32 *qh = (const g_u32 *)(a + 128 + 32 * h + l0);
+#pragma unroll
+    for (int i = 0; i < 5; ++i) {
+      v[i] = ql[i];
+      v[5 + i] = qh[i];
+    }
+    const uintptr_t sa = (uintptr_t)(b + 192 + 8 * h + 2 * g + (bq & 1));
+    v[10] = *(const g_u32 *)(sa & ~(uintptr_t)3);
+    v[11] = *(const g_u32 *)(a + 208);
+  }
+}
+
+// The 16 weights of the quarter as bf16 (nearest, ties to even, from the fp32
+// value) into dst (16-byte aligned).
+template <int FMT>
+__device__ __forceinline__ void gm_dequant(const uint32_t (&v)[12], const uint8_t *row, int kt, int bq,
+                                           __bf16 *dst) {
+  __bf16 o[16];
+  const int part = bq & 1;
+  if constexpr (FMT == 8) {
+    // block 0: d = bytes 0-1, its q from byte 2 (2 bytes into the window); block 1: d =
+    // bytes 34-35, its q from byte 36 (one dword into the window)
+    const int half = bq >> 1;
+    const float d = half_bits_to_float(half == 0 ? (v[0] & 0xffffu) : (v[0] >> 16));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w = half == 0 ? __builtin_amdgcn_alignbyte(v[2 + j], v[1 + j], 2) : v[2 + j];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o[4 * j + b] = (__bf16)(d * (float)(int8_t)((w >> (8 * b)) & 0xffu));
+    }
+  } else if constexpr (FMT == 2) {
+    // block 0: bytes 0..19 (d = 0-1, nibbles 2..17); block 1: bytes 16..35 (d = 18-19, 20..35);
+    // part 0: the low nibbles (weights 0..15 of the block), part 1: the high ones
+    const int half = bq >> 1;
+    const float d = half_bits_to_float(half == 0 ? (v[0] & 0xffffu) : (v[0] >> 16));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w = half == 0 ? __builtin_amdgcn_alignbyte(v[j + 1], v[j], 2) : v[j + 1];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const uint32_t byte = (w >> (8 * b)) & 0xffu;
+        o[4 * j + b] = (__bf16)(d * (float)((int)(part ? byte >> 4 : byte & 0xfu) - 8));
+      }
+    }
+  } else if constexpr (FMT == 12) {
+    // sub-block 2c + (bq >> 1): low nibbles for bq < 2, high for bq >= 2
+    const int j = 2 * (kt & 3) + (bq >> 1), jj = j & 3;
+    const uint32_t B0 = v[1], B1 = v[2], B2 = v[3];
+    const uint32_t SC = j >= 4 ? ((B2 & 0x0f0f0f0fu) | ((B0 >> 2) & 0x30303030u)) : (B0 & 0x3f3f3f3fu);
+    const uint32_t MN = j >= 4 ? (((B2 >> 4) & 0x0f0f0f0fu) | ((B1 >> 2) & 0x30303030u)) : (B1 & 0x3f3f3f3fu);
+    const float d = half_bits_to_float(v[0] & 0xffffu), dmin = half_bits_to_float(v[0] >> 16);
+    const float ds = d * (float)((SC >> (8 * jj)) & 0xffu), dm = dmin * (float)((MN >> (8 * jj)) & 0xffu);
+    const int nib = 4 * (bq >> 1);
+#pragma unroll
+    for (int j4 = 0; j4 < 4; ++j4)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const float q = (float)((v[4 + j4] >> (8 * b + nib)) & 0xfu);
+        o[4 * j4 + b] = (__bf16)fmaf(ds, q, -dm);
+      }
+  } else {
+    const uint8_t *bb = row + (int64_t)(kt >> 2) * 210;
+    const int sh = (int)((uintptr_t)bb & 3), g = 2 * (kt & 1) + (bq >> 1);
+    const uintptr_t sa = (uintptr_t)(bb + 192 + 8 * ((kt & 3) >> 1) + 2 * g + (bq & 1));
+    const float d = half_bits_to_float((v[11] >> (8 * sh)) & 0xffffu);
+    const float ds = d * (float)(int8_t)((v[10] >> (8 * (sa & 3))) & 0xffu);
+#pragma unroll
+    for (int j4 = 0; j4 < 4; ++j4) {
+      const uint32_t lq = __builtin_amdgcn_alignbyte(v[j4 + 1], v[j4], sh);
+      const uint32_t hq = __builtin_amdgcn_alignbyte(v[6 + j4], v[5 + j4], sh);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int q = (int)(((lq >> (8 * b + 4 * (g >> 1))) & 0xfu) | (((hq >> (8 * b + 2 * g)) & 3u) << 4));
+        o[4 * j4 + b] = (__bf16)(ds * (float)(q - 32));
+      }
+    }
+  }
+  *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(o);
+  *reinterpret_cast<uint4 *>(dst + 8) = *reinterpret_cast<const uint4 *>(o + 8);
+}
+
+struct GmParams {
+  PfExperts X;
+  const int32_t *perm;
+  const __bf16 *A;  // gate/up: xb [2][T][H]; down: ab [2][pairs][I] (hi then lo planes)
+  __bf16 *ab;       // gate/up output [2][pairs][I]
+  const float *w;   // down: routing weights [pairs]
+  float *P;         // down output [pairs][H]
+  int T, pairs, H, I, k;
+  int64_t mat, down_off;  // bytes of W_gate; offset of W_down in a payload
+  int64_t rowb;           // bytes of a weight row of the format (gate/up: H inputs; down: I)
+};
+
+// grid: (M-tiles of the wave's experts, I / 64).  B rows 0..63: W_gate rows
+// n0 .. n0+63, rows 64..127: the same rows of W_up; h = silu(g) u written as
+// bf16 hi and lo terms at the pair's grouped row.
+template <int FMT>
+__global__ __launch_bounds__(kGmThreads, 512 / kGmThreads) void gm_gateup_kernel(GmParams a) {
+  __shared__ __align__(16) __bf16 Bs[3][128][kPfLd];
+  int j, m0;
+  if (!gm_tile(a.X, blockIdx.x, j, m0)) return;
+  const int n0 = blockIdx.y * 64;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const bool live = m0 + 32 * wv < n;  // uniform over the wave
+  const int br = tid & 127, bq = tid >> 7;  // consecutive lanes: consecutive LDS rows; quarters bq + 2 qi
+  const uint8_t *brow = a.X.payload[j] + (br >= 64 ? a.mat : 0) + (int64_t)(n0 + (br & 63)) * a.rowb;
+  g_bf16x8 *xb = (g_bf16x8 *)a.A;
+  const uint32_t lo16 = (uint32_t)((int64_t)a.T * a.H / 8);
+  uint32_t arow[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
+    arow[i] = (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)(a.H / 8) + (lane >> 4);
+  }
+  bf16x8 A[3][2][2][2];  // [set][plane][i][ks]
+  uint32_t B[3][kGmQ][12];
+  f32x4 accg[2][4], accu[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      accg[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      accu[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  auto gload = [&](int kt, bf16x8 (&Ar)[2][2][2], uint32_t (&Bv)[kGmQ][12]) {
+#pragma unroll
+    for (int qi = 0; qi < kGmQ; ++qi) gm_load_raw<FMT>(brow, kt, bq + 2 * qi, Bv[qi]);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          Ar[pl][i][ks] = xb[arow[i] + pl * lo16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+  };
+  auto mma = [&](const bf16x8 (&Ar)[2][2][2], int buf) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = 32 * ks + 8 * (lane >> 4);
+        const bf16x8 bg = *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][c]);
+        const bf16x8 bu = *reinterpret_cast<const bf16x8 *>(&Bs[buf][64 + 16 * q + (lane & 15)][c]);
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bg, accg[i][q], 0, 0, 0);
+            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bu, accu[i][q], 0, 0, 0);
+          }
+      }
+  };
+  auto deq = [&](const uint32_t (&Bv)[kGmQ][12], int buf, int kt) {
+#pragma unroll
+    for (int qi = 0; qi < kGmQ; ++qi)
+      gm_dequant<FMT>(Bv[qi], brow, kt, bq + 2 * qi, &Bs[buf][br][16 * (bq + 2 * qi)]);
+  };
+  GM_K_LOOP(a.H / kPfBK, gload, mma, deq);
+  if (!live) return;
+  const int64_t plane = (int64_t)a.pairs * a.I;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+        if (m < n) {
+          const float v = silu(accg[i][q][r]) * accu[i][q][r];
+          const __bf16 hi = (__bf16)v;
+          const int64_t o = (int64_t)(row0 + m) * a.I + n0 + 16 * q + (lane & 15);
+          a.ab[o] = hi;
+          a.ab[plane + o] = (__bf16)(v - (float)hi);
+        }
+      }
+}
+
+// grid: (M-tiles, ceil(H / 128)).  B rows: W_down rows n0 .. n0+127 (a last
+// tile of 64 columns, H an odd multiple of 64, reads row H-1 for the missing
+// rows and stores only its first 64 columns); K over I.  P[pair] = w * row.
+template <int FMT>
+__global__ __launch_bounds__(kGmThreads, 512 / kGmThreads) void gm_down_kernel(GmParams a) {
+  __shared__ __align__(16) __bf16 Bs[3][128][kPfLd];
+  int j, m0;
+  if (!gm_tile(a.X, blockIdx.x, j, m0)) return;
+  const int n0 = blockIdx.y * 128;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const bool live = m0 + 32 * wv < n;
+  const int br = tid & 127, bq = tid >> 7;
+  const uint8_t *brow = a.X.payload[j] + a.down_off + (int64_t)min(n0 + br, a.H - 1) * a.rowb;
+  g_bf16x8 *ab = (g_bf16x8 *)a.A;
+  const uint32_t pl16 = (uint32_t)((int64_t)a.pairs * a.I / 8);
+  uint32_t arow[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = min(m0 + 32 * wv + 16 * i + (lane & 15), n - 1);
+    arow[i] = (uint32_t)(row0 + m) * (uint32_t)(a.I / 8) + (lane >> 4);
+  }
+  bf16x8 A[3][2][2][2];
+  uint32_t B[3][kGmQ][12];
+  f32x4 acc[2][8];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto gload = [&](int kt, bf16x8 (&Ar)[2][2][2], uint32_t (&Bv)[kGmQ][12]) {
+#pragma unroll
+    for (int qi = 0; qi < kGmQ; ++qi) gm_load_raw<FMT>(brow, kt, bq + 2 * qi, Bv[qi]);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          Ar[pl][i][ks] = ab[arow[i] + pl * pl16 + (uint32_t)(kt * kPfBK / 8 + 4 * ks)];
+  };
+  auto mma = [&](const bf16x8 (&Ar)[2][2][2], int buf) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const bf16x8 bf =
+            *reinterpret_cast<const bf16x8 *>(&Bs[buf][16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i][ks], bf, acc[i][q], 0, 0, 0);
+      }
+  };
+  auto deq = [&](const uint32_t (&Bv)[kGmQ][12], int buf, int kt) {
+#pragma unroll
+    for (int qi = 0; qi < kGmQ; ++qi)
+      gm_dequant<FMT>(Bv[qi], brow, kt, bq + 2 * qi, &Bs[buf][br][16 * (bq + 2 * qi)]);
+  };
+  GM_K_LOOP(a.I / kPfBK, gload, mma, deq);
+  if (!live) return;
+  int pair[2][4];
+  float wt[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      pair[i][r] = a.perm[row0 + min(m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r, n - 1)];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wt[i][r] = a.w[pair[i][r]];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+      if (m < n) {
+        float *dst = a.P + (int64_t)pair[i][r] * a.H + n0 + (lane & 15);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (n0 + 16 * q < a.H) dst[16 * q] = wt[i][r] * acc[i][q][r];
+      }
+    }
+}
+
 #undef PF_K_LOOP
 #undef PF_STEP
+#undef GM_K_LOOP
+#undef GM_STEP
 
 // y[t] = (x[t] if residual) + (sum_j P[t*k + j], j = 0..k-1 in rank order).
 // One block per token, four values per thread and step (H % 4 == 0), the k
@@ -3293,63 +3655,124 @@ hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, 
   return hipGetLastError();
 }
 
-hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
-                            __bf16 *ab, int T, int H, int I, int k, hipStream_t s, const Timing &t) {
-  PfGateUpParams a{};
-  a.X.count = W.count;
+// The wave's experts and the M-tile count of 256-row tiles.
+static int gm_experts(const PfWave &W, PfExperts &X) {
+  X.count = W.count;
   int tiles = 0;
   for (int i = 0; i < W.count; ++i) {
-    a.X.payload[i] = W.payload[i];
-    a.X.row0[i] = W.row0[i];
-    a.X.n[i] = W.n[i];
-    tiles += (W.n[i] + kPfBM - 1) / kPfBM;
+    X.payload[i] = W.payload[i];
+    X.row0[i] = W.row0[i];
+    X.n[i] = W.n[i];
+    tiles += (W.n[i] + kGmBM - 1) / kGmBM;
   }
+  return tiles;
+}
+
+template <template <int> class K>
+static hipError_t gm_launch(int fmt, dim3 grid, const GmParams &a, hipStream_t s, const Timing &t) {
+  switch (fmt) {
+    case 8:
+      hipExtLaunchKernelGGL(K<8>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      break;
+    case 2:
+      hipExtLaunchKernelGGL(K<2>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      break;
+    case 12:
+      hipExtLaunchKernelGGL(K<12>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      break;
+    case 14:
+      hipExtLaunchKernelGGL(K<14>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template <int F>
+struct GmGateUp {
+  static auto fn() { return gm_gateup_kernel<F>; }
+};
+template <int F>
+struct GmDown {
+  static auto fn() { return gm_down_kernel<F>; }
+};
+
+hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
+                            __bf16 *ab, int T, int H, int I, int k, hipStream_t s, const Timing &t) {
+  GmParams a{};
+  const int tiles = gm_experts(W, a.X);
+  const int fmt = fmt_gate_up(qtype);
   a.perm = perm;
-  a.xb = xb;
+  a.A = xb;
   a.ab = ab;
   a.T = T;
   a.pairs = T * k;
   a.H = H;
   a.I = I;
   a.k = k;
+  a.rowb = fmt_matrix_bytes(fmt, 1, H);
+  a.mat = (int64_t)I * a.rowb;
   if (tiles == 0) return hipSuccess;
   // the kernel indexes the activation planes in 16-byte units with 32 bits
-  if (2 * (int64_t)T * H / 8 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
-  dim3 grid(tiles, I / 64);
-  if (qtype == 8)
-    hipExtLaunchKernelGGL(pf_gateup_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
-  else
-    hipExtLaunchKernelGGL(pf_gateup_kernel<2>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
-  return hipGetLastError();
+  if (2 * (int64_t)T * H / 8 > (int64_t)UINT32_MAX || I % 64 || H % 64) return hipErrorInvalidValue;
+  if (fmt == 8 || fmt == 2) {  // the 32-weight block formats: pf_gateup_kernel (measured faster)
+    PfGateUpParams b{};
+    b.X = a.X;
+    int tl = 0;
+    for (int i = 0; i < W.count; ++i) tl += (W.n[i] + kPfBM - 1) / kPfBM;
+    b.perm = perm;
+    b.xb = xb;
+    b.ab = ab;
+    b.T = T;
+    b.pairs = T * k;
+    b.H = H;
+    b.I = I;
+    b.k = k;
+    if (fmt == 8)
+      hipExtLaunchKernelGGL(pf_gateup_kernel<8>, dim3(tl, I / 64), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
+    else
+      hipExtLaunchKernelGGL(pf_gateup_kernel<2>, dim3(tl, I / 64), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
+    return hipGetLastError();
+  }
+  return gm_launch<GmGateUp>(fmt, dim3(tiles, I / 64), a, s, t);
 }
 
 hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *ab,
                           const float *w, float *P, int pairs, int H, int I, hipStream_t s,
                           const Timing &t) {
-  PfDownParams a{};
-  a.X.count = W.count;
-  int tiles = 0;
-  for (int i = 0; i < W.count; ++i) {
-    a.X.payload[i] = W.payload[i];
-    a.X.row0[i] = W.row0[i];
-    a.X.n[i] = W.n[i];
-    tiles += (W.n[i] + kPfBM - 1) / kPfBM;
-  }
+  GmParams a{};
+  const int tiles = gm_experts(W, a.X);
+  const int fmt = fmt_down(qtype);
   a.perm = perm;
-  a.ab = ab;
+  a.A = ab;
   a.w = w;
   a.P = P;
   a.pairs = pairs;
   a.H = H;
   a.I = I;
+  a.rowb = fmt_matrix_bytes(fmt, 1, I);
+  a.down_off = 2 * fmt_matrix_bytes(fmt_gate_up(qtype), I, H);
   if (tiles == 0) return hipSuccess;
-  if (2 * (int64_t)pairs * I / 8 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
-  dim3 grid(tiles, (H + 127) / 128);
-  if (qtype == 8)
-    hipExtLaunchKernelGGL(pf_down_kernel<8>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
-  else
-    hipExtLaunchKernelGGL(pf_down_kernel<2>, grid, dim3(kThreads), 0, s, t.start, t.stop, 0, a);
-  return hipGetLastError();
+  if (2 * (int64_t)pairs * I / 8 > (int64_t)UINT32_MAX || I % 64 || H % 64) return hipErrorInvalidValue;
+  if (fmt == 8 || fmt == 2) {
+    PfDownParams b{};
+    b.X = a.X;
+    int tl = 0;
+    for (int i = 0; i < W.count; ++i) tl += (W.n[i] + kPfBM - 1) / kPfBM;
+    b.perm = perm;
+    b.ab = ab;
+    b.w = w;
+    b.P = P;
+    b.pairs = pairs;
+    b.H = H;
+    b.I = I;
+    if (fmt == 8)
+      hipExtLaunchKernelGGL(pf_down_kernel<8>, dim3(tl, (H + 127) / 128), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
+    else
+      hipExtLaunchKernelGGL(pf_down_kernel<2>, dim3(tl, (H + 127) / 128), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
+    return hipGetLastError();
+  }
+  return gm_launch<GmDown>(fmt, dim3(tiles, (H + 127) / 128), a, s, t);
 }
 
 hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, int H, int k,

@@ -1075,8 +1075,6 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
     return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
-  if (fmt_kquant(fmt_gate_up(c->d.qtype)) || fmt_kquant(fmt_down(c->d.qtype)))
-    return fail(MOE_EINVAL, "K-quant models take one token per layer call here");
   // a small call tries the device path unless the layer's last small call did
   // not fit the slots (then the device step would only report that again); the
   // two paths step the table by the same rule
@@ -1552,14 +1550,30 @@ int forward_prefill_impl(moe_cache *c, const float *x, int32_t T, const float *w
       chunk_of[c->recs[i].expert] = (int)chunks.size() - 1;
     }
   if (!chunks.back().recs.empty()) chunks.emplace_back();
+  // miss chunks of per_chunk, the last one split so that a short chunk ends the
+  // call: its GEMMs are the only ones no later copy hides
+  std::vector<int> caps;
+  {
+    int left = 0;
+    for (const auto &r : c->recs) left += r.hit ? 0 : 1;
+    for (; left > 0; left -= std::min(left, per_chunk)) caps.push_back(std::min(left, per_chunk));
+    const int tail = std::max(1, per_chunk / 4);
+    if (!caps.empty() && caps.back() > tail) {
+      caps.back() -= tail;
+      caps.push_back(tail);
+    }
+  }
+  size_t cap_i = 0;
   int misses_in_cur = 0;
   for (size_t i = 0; i < c->recs.size(); ++i) {
     const moe_step_rec &r = c->recs[i];
     if (r.hit) continue;
     const int dep = r.evicted >= 0 ? chunk_of[r.evicted] : -1;  // -1: not routed in this call
-    if ((dep >= 0 && dep == (int)chunks.size() - 1) || misses_in_cur == per_chunk) {
+    const int cap = cap_i < caps.size() ? caps[cap_i] : per_chunk;
+    if ((dep >= 0 && dep == (int)chunks.size() - 1) || misses_in_cur == cap) {
       chunks.emplace_back();
       misses_in_cur = 0;
+      ++cap_i;
     }
     Chunk &ch = chunks.back();
     ch.recs.push_back((int)i);

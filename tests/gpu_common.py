@@ -122,11 +122,13 @@ def union_gemv_fits(H, I, T):
     return 1 <= T <= 8 and 3 * T * I // 16 <= 9 * 256 and gateup_lds <= 65536 and down_lds <= 65536
 
 
-def small_call_exact(T, H, I, n_union, budget):
+def small_call_exact(T, H, I, n_union, budget, qtype="q8_0"):
     """Whether a multi-token call runs the fp32-accurate GEMVs (exact oracle) rather than the
     bf16 MFMA GEMMs: at most 8 tokens, and either the routed experts fit the slots (decode or
-    union GEMVs) or the union GEMVs take the shape (run per chunk of the host-table path)."""
-    return T <= 8 and (n_union <= budget or union_gemv_fits(H, I, T))
+    union GEMVs) or the union GEMVs take the shape (run per chunk of the host-table path; the
+    union GEMVs read Q8_0 / Q4_0 only)."""
+    union = qtype in ("q8_0", "q4_0") and union_gemv_fits(H, I, T)
+    return T <= 8 and (n_union <= budget or union)
 
 
 def oracle_layer_y(x, wr, store, wl, layer, idx_or, w_or, z, idx_gpu, flipped, bf16=False,

@@ -10,6 +10,7 @@ from edge_blocks import edge_tokens, kquant_golden_store
 from gpu_common import store_buffer
 from test_gpu_decode import run_decode
 from test_gpu_full import verify_chain
+from test_gpu_prefill import run_prefill
 
 pytestmark = pytest.mark.gpu
 
@@ -63,3 +64,28 @@ def test_q4km_decode_full_size():
         verify_chain(wl, wl.budget_slots, wl.rho, st, 16, 6)
     finally:
         st[0].free()
+
+
+@pytest.mark.parametrize("qtype", ["q4_k_m", "q4_k", "q6_k"])
+def test_kquant_prefill_and_small_calls(qtype):
+    """Multi-token calls: 300 tokens with 6 slots (the MFMA grouped GEMMs on bf16 tiles
+    dequantised from the super-blocks, slots reused inside the call), 5 tokens whose experts
+    fit (the decode GEMVs per token) and 8 tokens with 5 slots (the host-table path, MFMA)."""
+    wl = kq_workload(qtype, hidden=1024, inter=512)
+    store = store_buffer(wl)
+    run_prefill(wl, 6, 300, calls=2, prenorm=True, residual=True, store=store)
+    run_prefill(wl, 16, 5, calls=2, prenorm=True, residual=True, store=store)
+    run_prefill(wl, 5, 8, calls=2, prenorm=True, residual=True, store=store)
+    store[0].free()
+
+
+@pytest.mark.parametrize("qtype", ["q4_k_m", "q6_k"])
+def test_kquant_prefill_rows_past_first_tile(qtype):
+    """2048 tokens, 16 experts, top-2: about 256 rows per expert, a full 256-row tile and a
+    partial second one for many experts; every token's y compared, hand-worked super-blocks."""
+    wl = kq_workload(qtype, n_layers=1, hidden=1024, inter=512, top_k=2)
+    keep, ptr, arr = store_buffer(wl)
+    kquant_golden_store(arr, wl, seed=3)
+    xs = [synth.hidden(wl.with_(hidden_seed=91), rho=-1.0, n_tokens=2048)]
+    run_prefill(wl, 6, 2048, calls=1, prenorm=True, residual=False, store=(keep, ptr, arr), xs=xs)
+    keep.free()

@@ -21,10 +21,10 @@ def oracle_routes(x, wr, k, prenorm):
     return z, idx, w, gap
 
 
-def gemv_call(T, idx, budget, H, I):
+def gemv_call(T, idx, budget, H, I, qtype="q8_0"):
     """Whether a multi-token call takes the GEMVs (fp32-accurate) instead of the bf16 MFMA
     GEMMs."""
-    return small_call_exact(T, H, I, len(np.unique(idx)), budget)
+    return small_call_exact(T, H, I, len(np.unique(idx)), budget, qtype)
 
 
 def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens=None, budget=None):
@@ -40,7 +40,7 @@ def check_call(x, wr, arr, wl, layer, idx_g, w_g, y_g, prenorm, residual, tokens
             w_use[t] = softmax_of(z[t], idx_g[t])
             flips += 1
     toks = list(range(x.shape[0])) if tokens is None else list(tokens)
-    exact = budget is not None and gemv_call(x.shape[0], idx_g, budget, wl.hidden, wl.inter)
+    exact = budget is not None and gemv_call(x.shape[0], idx_g, budget, wl.hidden, wl.inter, wl.qtype)
     fn = moe_layer if exact else moe_layer_bf16
     yo = fn(x, wr, arr, Shape.of(wl), layer, routes=(idx_use, w_use), tokens=toks,
             prenorm=prenorm)["y"][toks]
