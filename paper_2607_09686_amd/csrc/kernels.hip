@@ -152,10 +152,15 @@ constexpr int kMaxX4 = 8;  // H <= 8192
 // on a multi-XCD GPU a device-scope fence costs more than a second launch).
 // Every block also forms s = 1/sqrt(mean(x^2) + 1e-6) (or 1) from the whole x,
 // in the same order, so all blocks hold the same s; block b writes the digits
-// of its 32-wide block of x * s, and block 0 writes s at partial[nb * E].
-// MULTI: blocks of rpb rows (a multiple of 32) for multi-token calls; else 32 rows
-// (decode: all of the block's loads issued before the first use).
-template <bool MULTI>
+// of its 32-wide blocks of x * s, and block 0 writes s at partial[nb * E].
+// Thread (c, ph) takes column c and rows r0 + ph + phases j in order.  MULTI:
+// blocks of rpb rows (a multiple of 32) for multi-token calls, 32 rows per
+// thread per round trip; else 32 rows per block, J of them per thread (J =
+// 32 for E > 128, else 16 >= ceil(32 / phases)).  Every load is issued
+// unconditionally at a clamped, valid address and the values outside the
+// block's rows are zeroed afterwards (a guarded load becomes a branch), so
+// the sums are those of the rows in order.
+template <bool MULTI, int J>
 __global__ __launch_bounds__(kThreads) void router_partial_kernel(
     const float *__restrict__ x, const float *__restrict__ wr, int H, int E, int prenorm, int rpb,
     float *__restrict__ partial, int8_t *__restrict__ xq, float *__restrict__ xsc) {
@@ -177,48 +182,51 @@ __global__ __launch_bounds__(kThreads) void router_partial_kernel(
   const int H4 = H / 4;
   const float4 *x4 = reinterpret_cast<const float4 *>(x);
   float acc = 0.f;
-  float xv[kRouterRowsPerBlock], wv[kRouterRowsPerBlock];
+  float xv[J], wv[J];
+  auto load_rows = [&](int j0) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int r = r0 + ph + phases * (j0 + j);
+      const int rc = min(r, r1 - 1);
+      xv[j] = x[rc];
+      wv[j] = wr[(int64_t)rc * E + c];
+    }
+  };
+  auto add_rows = [&](int j0) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const uint32_t keep = ph < phases && r0 + ph + phases * (j0 + j) < r1 ? ~0u : 0u;
+      acc = fmaf(__uint_as_float(__float_as_uint(xv[j]) & keep), __uint_as_float(__float_as_uint(wv[j]) & keep),
+                 acc);
+    }
+  };
   if constexpr (MULTI) {
-    // the block's rows r0 + ph + phases * j, 32 of them per round trip
-    for (int j0 = 0; j0 * phases < rows; j0 += kRouterRowsPerBlock) {
-#pragma unroll
-      for (int j = 0; j < kRouterRowsPerBlock; ++j) {
-        const int r = r0 + ph + phases * (j0 + j);
-        const bool ok = ph < phases && r < r1;
-        xv[j] = ok ? x[r] : 0.f;
-        wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
+    for (int j0 = 0; j0 * phases < rows; j0 += J) {
+      load_rows(j0);
+      add_rows(j0);
     }
   } else {
-#pragma unroll
-    for (int j = 0; j < kRouterRowsPerBlock; ++j) {  // all loads first
-      const int r = r0 + ph + phases * j;
-      const bool ok = ph < phases && r < r1;
-      xv[j] = ok ? x[r] : 0.f;
-      wv[j] = ok ? wr[(int64_t)r * E + c] : 0.f;
-    }
+    load_rows(0);  // all loads first
   }
-  float4 xa[kMaxX4];
+  float4 xa[kMaxX4];  // (zeroed where unused only at the use: overwriting a load's
+                      // destination register would wait for the load)
 #pragma unroll
-  for (int m = 0; m < kMaxX4; ++m) {
-    const int i = tid + m * kThreads;
-    xa[m] = prenorm && i < H4 ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
+  for (int m = 0; m < kMaxX4; ++m) xa[m] = x4[min(tid + m * kThreads, H4 - 1)];
   const int oct = MULTI ? (r1 - r0) / 32 : 1;  // the block's 32-wide blocks of x, an octet of lanes each
-  const float4 mine = tid < 8 * oct ? x4[r0 / 4 + tid] : make_float4(0.f, 0.f, 0.f, 0.f);
-  if constexpr (!MULTI) {
-#pragma unroll
-    for (int j = 0; j < kRouterRowsPerBlock; ++j) acc = fmaf(xv[j], wv[j], acc);
-  }
+  const float4 mine = x4[min(r0 / 4 + tid, H4 - 1)];
+  if constexpr (!MULTI) add_rows(0);
   float ss = 0.f;
 #pragma unroll
   for (int m = 0; m < kMaxX4; ++m) {
-    ss = fmaf(xa[m].x, xa[m].x, ss);
-    ss = fmaf(xa[m].y, xa[m].y, ss);
-    ss = fmaf(xa[m].z, xa[m].z, ss);
-    ss = fmaf(xa[m].w, xa[m].w, ss);
+    const uint32_t keep = prenorm && tid + m * kThreads < H4 ? ~0u : 0u;  // a mask, not a branch
+    const float4 v = make_float4(__uint_as_float(__float_as_uint(xa[m].x) & keep),
+                                 __uint_as_float(__float_as_uint(xa[m].y) & keep),
+                                 __uint_as_float(__float_as_uint(xa[m].z) & keep),
+                                 __uint_as_float(__float_as_uint(xa[m].w) & keep));
+    ss = fmaf(v.x, v.x, ss);
+    ss = fmaf(v.y, v.y, ss);
+    ss = fmaf(v.z, v.z, ss);
+    ss = fmaf(v.w, v.w, ss);
   }
 #pragma unroll
   for (int off = kWave / 2; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
@@ -291,115 +299,92 @@ __global__ __launch_bounds__(kThreads) void token_digits_kernel(const float *__r
   }
 }
 
-// Order-preserving 64-bit rank key of expert e with logit z: the bit image of
-// z (NaN taken as -inf, -0 as +0) above 255 - e, so that a larger key means a
-// larger logit, then a lower id.
-__device__ __forceinline__ uint64_t rank_key(float z, int e) {
+// Order-preserving bits of a routing logit: a larger value means a larger
+// logit (NaN taken as -inf, -0 as +0).  Never 0: the bits of -inf are
+// 0x007fffff, the smallest.
+__device__ __forceinline__ uint32_t logit_bits(float z) {
   z = z != z ? -INFINITY : z + 0.f;
-  uint32_t u = __float_as_uint(z);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return ((uint64_t)u << 8) | (uint64_t)(255 - e);
+  const uint32_t u = __float_as_uint(z);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// One token's routing inside a one-block finishing kernel (all threads; the
-// token's logits z = s * (sum of the partials in block order) with s at
-// partial[nb * E]).  Top-k by rank: expert e is chosen iff fewer than k
-// experts have a larger rank key, and its rank is its position.  Writes the
-// chosen ids and the softmax over their logits to idx / w [k] (and the
-// optional mirrors), the chosen ids to sel [k], keyZ [E] and zlast [E]
-// (nullable); returns the rank of expert tid (E for tid >= E) and sets *bad
-// when a chosen logit is not finite.
-struct RouteLds {
-  float red[kThreads];
-  float zs[256];
-  uint64_t keyZ[256];
-  float zsel[kMaxRouted];
-};
-__device__ __forceinline__ int route_sum(float sacc, float inv, int E, int k, int32_t *idx, float *w,
-                                         int32_t *host_idx, float *host_w, float *zlast, int32_t *sel,
-                                         int32_t *bad, RouteLds &sh) {
-  const int tid = threadIdx.x;
-  const int phases = kThreads / E;
-  const int c = tid % E, ph = tid / E;
-  sh.red[tid] = sacc;
-  __syncthreads();
-  if (tid < E) {
-    float z = 0.f;
-    for (int p = 0; p < phases; ++p) z += sh.red[p * E + tid];
-    z *= inv;
-    sh.zs[tid] = z;
-    sh.keyZ[tid] = rank_key(z, tid);
-    if (zlast) zlast[tid] = z;
-  }
-  __syncthreads();
-  // rank of expert c over the experts [ph E / phases, (ph+1) E / phases)
-  {
-    int r = 0;
-    if (ph < phases) {
-      const uint64_t kc = sh.keyZ[c];
-      const int f0 = ph * E / phases, f1 = (ph + 1) * E / phases;
-      int f = f0;
-      for (; f + 8 <= f1; f += 8) {  // eight independent LDS reads per step
-        uint64_t v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = sh.keyZ[f + j];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) r += v[j] > kc ? 1 : 0;
-      }
-      for (; f < f1; ++f) r += sh.keyZ[f] > kc ? 1 : 0;
-    }
-    __syncthreads();
-    sh.red[tid] = __int_as_float(r);
-  }
-  __syncthreads();
-  int rank = E;
-  if (tid < E) {
-    rank = 0;
-    for (int p = 0; p < phases; ++p) rank += __float_as_int(sh.red[p * E + tid]);
-    if (rank < k) {
-      sel[rank] = tid;
-      sh.zsel[rank] = sh.zs[tid];
-    }
-  }
-  __syncthreads();
-  if (tid < kWave) {  // softmax over the chosen logits (the first is the largest)
-    const bool ok = __ballot(tid < k && !isfinite(sh.zsel[tid < k ? tid : 0])) == 0;
-    const float ex = tid < k && ok ? expf(sh.zsel[tid] - sh.zsel[0]) : 0.f;
-    float sum = ex;
-#pragma unroll
-    for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
-    if (tid < k) {
-      const int32_t id = ok ? sel[tid] : 0x7fffffff;
-      const float wi = ok ? ex / sum : 0.f;
-      idx[tid] = id;
-      w[tid] = wi;
-      if (host_idx) host_idx[tid] = id;
-      if (host_w) host_w[tid] = wi;
-    }
-    if (tid == 0 && !ok) *bad = 1;
-  }
-  return rank;
+// 64-bit rank key of expert e with logit z: its logit bits above 255 - e, so
+// that a larger key means a larger logit, then a lower id.
+__device__ __forceinline__ uint64_t rank_key(float z, int e) {
+  return ((uint64_t)logit_bits(z) << 8) | (uint64_t)(255 - e);
 }
-__device__ __forceinline__ int route_token(const float *__restrict__ partial, int nb, int E, int k,
-                                           int32_t *idx, float *w, int32_t *host_idx, float *host_w,
-                                           float *zlast, int32_t *sel, int32_t *bad, RouteLds &sh) {
-  const int tid = threadIdx.x;
-  const int phases = kThreads / E;
-  const int c = tid % E, ph = tid / E;
-  const float inv = partial[(int64_t)nb * E];
-  const int per = (nb + phases - 1) / phases;
-  float sacc = 0.f;
-  if (ph < phases) {
-    const int b0 = ph * per, b1 = min(nb, b0 + per);
-    for (int b = b0; b < b1; b += 48) {  // one round trip up to 48 partials per lane
-      float v[48];
+
+// Largest x over a full wave (all 64 lanes active): DPP lane swaps xor 1 and
+// xor 2, then the mirrors inside each 8 and each 16 lanes, which leave every
+// row of 16 lanes holding its maximum; the four row maxima are read out.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xb1, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4e, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x141, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xf, 0xf, false));
+  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+  return max(max(a, b), max(c, d));
+}
+
+// Top-k of one token by one full wave over its logits z[0..E) and their bits
+// zb = logit_bits(z) (E <= 256, 1 <= k <= 16, k <= E): k rounds of a wave
+// maximum of the bits, the lowest expert id among equal bits (so the order of
+// rank_key: larger logit first, lower id on a tie), then the softmax over the
+// chosen logits (the first is the largest; the sum in butterfly order).  Lane
+// r < k returns the expert of rank r in sel and its id and weight in id / wt
+// (id 0x7fffffff and weight 0 in every lane if a chosen logit is not finite,
+// which *bad records).
+__device__ __forceinline__ void wave_topk_bits(const uint32_t *zb, const float *z, int E, int k, int32_t &sel,
+                                               int32_t &id, float &wt, int32_t *bad) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t h[4];
 #pragma unroll
-      for (int j = 0; j < 48; ++j) v[j] = b + j < b1 ? partial[(b + j) * E + c] : 0.f;
+  for (int j = 0; j < 4; ++j) h[j] = lane + kWave * j < E ? zb[lane + kWave * j] : 0u;
+  int mine = 0, first = 0;
+  for (int r = 0; r < k; ++r) {
+    const uint32_t m = wave_max_u32(max(max(h[0], h[1]), max(h[2], h[3])));
+    int e = 0;
 #pragma unroll
-      for (int j = 0; j < 48; ++j) sacc += v[j];
+    for (int j = 3; j >= 0; --j) {  // the lowest id holding m
+      const uint64_t b = __ballot(h[j] == m);
+      if (b) e = kWave * j + __builtin_ctzll(b);
     }
+    if (lane == r) mine = e;
+    if (r == 0) first = e;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) h[j] = e == kWave * j + lane ? 0u : h[j];  // taken
   }
-  return route_sum(sacc, inv, E, k, idx, w, host_idx, host_w, zlast, sel, bad, sh);
+  const float z0 = z[first], zl = lane < k ? z[mine] : 0.f;
+  const bool ok = __ballot(lane < k && !isfinite(zl)) == 0;
+  const float ex = lane < k && ok ? expf(zl - z0) : 0.f;
+  float sum = ex;
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+  sel = mine;
+  id = ok ? mine : 0x7fffffff;
+  wt = ok ? ex / sum : 0.f;
+  if (lane == 0 && !ok) *bad = 1;
+}
+
+// The slot table's words that a step reads and rewrites: clock, step, slots
+// in use, trace records written, and the four counters.  Lane i < 8 of a
+// finishing block loads word i (a vector load at a valid address for every
+// lane, so that nothing waits for it before the call's other loads are out);
+// table_word_keep() drops the word of lanes that hold none, at the use.
+__device__ __forceinline__ int64_t table_word_load(const LruDev &lru) {
+  const int i = threadIdx.x;
+  const int64_t *p = i < 3 ? lru.meta + i
+                     : i == 3 ? (lru.trace ? reinterpret_cast<const int64_t *>(lru.trace_n) : lru.meta)
+                     : i < 8 ? reinterpret_cast<const int64_t *>(lru.cnt) + (i - 4)
+                             : lru.meta;
+  return *p;
+}
+__device__ __forceinline__ void table_word_keep(const LruDev &lru, int64_t v, int64_t *words) {
+  const int i = threadIdx.x;
+  if (i < 8) words[i] = i == 3 && !lru.trace ? 0 : v;
 }
 
 // Slot-table step of one layer call inside a one-block kernel (all threads;
@@ -413,7 +398,9 @@ __device__ __forceinline__ int route_token(const float *__restrict__ partial, in
 // outside S in key order, for the misses beyond the free slots in expert
 // order.  Writes the table, the counters, the clock and the trace records;
 // returns this expert's miss flag, final slot, rank among the misses and the
-// number of misses.  |S| <= C.
+// number of misses.  |S| <= C.  In two parts: step_publish (every thread,
+// before a block barrier: the per-wave counts of S and of the misses, and
+// the eviction keys cleared), then table_step after that barrier.
 struct StepLds {
   int32_t cnt[2][kThreads / kWave];
   uint64_t key[256];  // eviction key of each slot's resident (candidates only)
@@ -423,19 +410,23 @@ struct StepResult {
   bool miss;
   int fs, rS, rM, nM;
 };
-__device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool inS, int so, int64_t st,
-                                                 uint64_t zkey, int64_t clock0, int64_t step,
-                                                 int64_t used, uint64_t tn, StepLds &sh) {
+__device__ __forceinline__ void step_publish(const LruDev &lru, bool inS, int so, StepLds &sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const bool miss = inS && so < 0;
-  const bool cand = tid < E && so >= 0 && !inS;
-  const uint64_t bS = __ballot(inS), bM = __ballot(miss), lt = (1ull << lane) - 1ull;
+  const uint64_t bS = __ballot(inS), bM = __ballot(inS && so < 0);
   if (lane == 0) {
     sh.cnt[0][wv] = __popcll(bS);
     sh.cnt[1][wv] = __popcll(bM);
   }
   for (int sl = tid; sl < lru.C; sl += kThreads) sh.key[sl] = UINT64_MAX;
-  __syncthreads();
+}
+__device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool inS, int so, int64_t st,
+                                                 uint64_t zkey, const int64_t *words, StepLds &sh) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int64_t clock0 = words[0], step = words[1], used = words[2];
+  const uint64_t tn = (uint64_t)words[3];
+  const bool miss = inS && so < 0;
+  const bool cand = tid < E && so >= 0 && !inS;
+  const uint64_t bS = __ballot(inS), bM = __ballot(miss), lt = (1ull << lane) - 1ull;
   int rS = __popcll(bS & lt), rM = __popcll(bM & lt), nM = 0, nS = 0;
 #pragma unroll
   for (int v = 0; v < kThreads / kWave; ++v) {
@@ -454,7 +445,15 @@ __device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool 
   bool evicted = false;
   if (cand && nev > 0) {
     int cr = 0;  // residents outside S evicted before this one
-    for (int sl = 0; sl < lru.C; ++sl) cr += sh.key[sl] < vkey ? 1 : 0;
+    int sl = 0;
+    for (; sl + 8 <= lru.C; sl += 8) {  // eight independent LDS reads per step
+      uint64_t v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = sh.key[sl + j];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) cr += v[j] < vkey ? 1 : 0;
+    }
+    for (; sl < lru.C; ++sl) cr += sh.key[sl] < vkey ? 1 : 0;
     if (cr < nev) {
       evicted = true;
       sh.vic[cr] = tid;
@@ -488,11 +487,11 @@ __device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool 
       r[5] = fev;
     }
   }
-  if (tid == 0) {
-    lru.cnt[0] += (uint64_t)(nS - nM);
-    lru.cnt[1] += (uint64_t)nM;
-    lru.cnt[2] += (uint64_t)nev;
-    lru.cnt[3] += (uint64_t)nM * (uint64_t)lru.P;
+  if (tid == 0) {  // (the counters as read at the kernel's start: no load here, at the end)
+    lru.cnt[0] = (uint64_t)words[4] + (uint64_t)(nS - nM);
+    lru.cnt[1] = (uint64_t)words[5] + (uint64_t)nM;
+    lru.cnt[2] = (uint64_t)words[6] + (uint64_t)nev;
+    lru.cnt[3] = (uint64_t)words[7] + (uint64_t)nM * (uint64_t)lru.P;
     lru.meta[0] = clock0 + nS;
     lru.meta[1] = step + 1;
     lru.meta[2] = used + min(nM, nfree);
@@ -501,100 +500,144 @@ __device__ __forceinline__ StepResult table_step(const LruDev &lru, int E, bool 
   return StepResult{miss, fs, rS, rM, nM};
 }
 
-// Decode router, second kernel (one block): the token's routing (route_token)
-// and, with lru.slot_of set, the layer's slot-table step and the work list.
-// Every global load is issued up front (the table state included).  A
-// non-finite chosen logit is a routing failure: the error word is set and the
-// work list left empty.
+// Decode router, second kernel (one block): the token's logits z = s * (the
+// partial sums in block order; s at partial[nb * E]), its top-k by rank (an
+// expert's rank is the number of experts with a larger rank key, counted by
+// all threads at once) and the softmax over the chosen logits, and with
+// lru.slot_of set the layer's slot-table step and the work list.  Every
+// global load is issued first, unconditionally at valid addresses (a guarded
+// load becomes a branch with its own wait), the table's words as vector
+// loads (a scalar load would be waited for before the partials' loads go
+// out); the softmax and every global store but the step's come after the
+// step.  A non-finite chosen logit is a routing failure: the error word is
+// set and the work list left empty.
 __global__ __launch_bounds__(kThreads) void router_finish_kernel(
     const float *__restrict__ partial, int nb, int E, int k, int32_t *idx, float *w,
     int32_t *host_idx, float *host_w, LruDev lru) {
-  __shared__ RouteLds rl;
-  __shared__ StepLds sl;
+  __shared__ float redL[kThreads];
+  __shared__ int32_t cntL[kThreads];
+  __shared__ float zL[256];
+  __shared__ uint64_t keyL[256];
   __shared__ int32_t selL[kMaxRouted];
+  __shared__ int64_t wordsL[8];
+  __shared__ StepLds sl;
   __shared__ int32_t badL;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const bool dev = lru.slot_of != nullptr;
-  // the table state first: its latency hides behind the routing work
-  int so = -1;
-  int64_t st = 0, clock0 = 0, step = 0, used = 0;
-  uint64_t tn = 0;
-  if (dev) {
-    if (tid < E) {
-      so = lru.slot_of[tid];
-      st = lru.stamp[tid];
-    }
-    clock0 = lru.meta[0];
-    step = lru.meta[1];
-    used = lru.meta[2];
-    if (lru.trace) tn = *lru.trace_n;
+  // (without a table the state loads read the partials and are dropped)
+  const int ce = min(tid, E - 1);
+  const int64_t *p64 = reinterpret_cast<const int64_t *>(partial);
+  int so = *(dev ? lru.slot_of + ce : reinterpret_cast<const int32_t *>(partial));
+  int64_t st = *(dev ? lru.stamp + ce : p64);
+  const int64_t word = dev ? table_word_load(lru) : *p64;
+  const float inv = partial[(int64_t)nb * E];
+  // thread (c, ph) adds blocks [ph * per, ph * per + per) of expert c in block order
+  const int phases = kThreads / E;
+  const int c = tid % E, ph = tid / E;
+  const int per = (nb + phases - 1) / phases;
+  const int b0 = ph * per, b1 = ph < phases ? min(nb, b0 + per) : b0;
+  float sacc = 0.f;
+  for (int b = b0; b < b1; b += 48) {  // one round trip for up to 48 partials per lane
+    float v[48];
+#pragma unroll
+    for (int j = 0; j < 48; ++j) v[j] = partial[(int64_t)min(b + j, nb - 1) * E + c];
+#pragma unroll
+    for (int j = 0; j < 48; ++j) sacc += b + j < b1 ? v[j] : 0.f;
   }
-  if (tid == 0) badL = 0;  // ordered before route_token's write by its barriers
-  const int rank = route_token(partial, nb, E, k, idx, w, host_idx, host_w, lru.zlast, selL, &badL, rl);
-  if (!dev) return;  // uniform
+  if (!dev || tid >= E) {
+    so = -1;
+    st = 0;
+  }
+  if (dev) table_word_keep(lru, word, wordsL);
+  redL[tid] = sacc;
+  if (tid == 0) badL = 0;
   __syncthreads();
-  if (badL) {  // no work for this call; reported at the next synchronisation
-    if (tid == 0) {
+  float z = 0.f;
+  if (tid < E) {
+    for (int p = 0; p < phases; ++p) z += redL[p * E + tid];
+    z *= inv;
+    zL[tid] = z;
+    keyL[tid] = rank_key(z, tid);
+  }
+  __syncthreads();
+  {  // thread (c, ph): experts in [ph E / phases, (ph + 1) E / phases) with a larger key than c's
+    int r = 0;
+    if (ph < phases) {
+      const uint64_t kc = keyL[c];
+      const int f0 = ph * E / phases, f1 = (ph + 1) * E / phases;
+      int f = f0;
+      for (; f + 16 <= f1; f += 16) {  // sixteen independent LDS reads per step
+        uint64_t v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = keyL[f + j];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) r += v[j] > kc ? 1 : 0;
+      }
+      for (; f < f1; ++f) r += keyL[f] > kc ? 1 : 0;
+    }
+    cntL[tid] = r;
+  }
+  __syncthreads();
+  int rank = E;
+  if (tid < E) {
+    rank = 0;
+    for (int p = 0; p < phases; ++p) rank += cntL[p * E + tid];
+  }
+  const bool inS = rank < k;
+  if (inS) {
+    selL[rank] = tid;
+    if (!isfinite(z)) badL = 1;
+  }
+  if (dev) step_publish(lru, inS, so, sl);
+  __syncthreads();
+  const bool bad = badL != 0;
+  StepResult o{false, -1, 0, 0, 0};
+  if (dev && !bad) {  // uniform
+    o = table_step(lru, E, inS, so, st, tid < E ? keyL[tid] : 0ull, wordsL, sl);
+    if (inS) {
+      lru.work->hit[rank] = o.miss ? 0 : 1;
+      if (o.miss) {
+        lru.work->src[o.rM] = lru.store + (int64_t)tid * lru.P;
+        lru.work->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
+        lru.work->miss_pos[o.rM] = rank;
+      }
+      lru.work->list.payload[rank] = lru.slots + (int64_t)o.fs * lru.P;
+      lru.work->list.pos[rank] = rank;
+    }
+  }
+  if (tid < kWave) {
+    // the softmax over the chosen logits (the first is the largest), the sum
+    // in the order of a butterfly over lanes xor 32, 16, 8, 4, 2, 1 where
+    // lanes >= k add zeros: with k <= 16 the steps 32 and 16 add +0, and the
+    // rotations by 8, 4, 2, 1 inside each row of 16 lanes pair every lane
+    // with one holding the same value as its xor partner
+    const int e = lane < k ? selL[lane] : 0;
+    const float ex = lane < k && !bad ? expf(zL[e] - zL[selL[0]]) : 0.f;
+    float sum = ex;
+    sum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sum), 0x128, 0xf, 0xf, false));
+    sum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sum), 0x124, 0xf, 0xf, false));
+    sum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sum), 0x122, 0xf, 0xf, false));
+    sum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sum), 0x121, 0xf, 0xf, false));
+    if (lane < k) {
+      const int32_t id = bad ? 0x7fffffff : e;
+      const float wt = bad ? 0.f : ex / sum;
+      idx[lane] = id;
+      w[lane] = wt;
+      if (host_idx) host_idx[lane] = id;
+      if (host_w) host_w[lane] = wt;
+    }
+  }
+  if (lru.zlast && tid < E) lru.zlast[tid] = z;
+  if (dev && tid == 0) {
+    if (bad) {  // no work for this call; reported at the next synchronisation
       *lru.err = 1;
       lru.work->n_copy = 0;
       lru.work->list.n = 0;
+    } else {
+      lru.work->list.n = k;
+      lru.work->n_copy = o.nM;
     }
-    return;
   }
-  const bool inS = rank < k;
-  const StepResult o =
-      table_step(lru, E, inS, so, st, tid < E ? rl.keyZ[tid] : 0ull, clock0, step, used, tn, sl);
-  if (inS) {
-    lru.work->hit[rank] = o.miss ? 0 : 1;
-    if (o.miss) {
-      lru.work->src[o.rM] = lru.store + (int64_t)tid * lru.P;
-      lru.work->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
-      lru.work->miss_pos[o.rM] = rank;
-    }
-    lru.work->list.payload[rank] = lru.slots + (int64_t)o.fs * lru.P;
-    lru.work->list.pos[rank] = rank;
-  }
-  if (tid == 0) {
-    lru.work->list.n = k;
-    lru.work->n_copy = o.nM;
-  }
-}
-
-// Top-k of one token by one wave over the rank keys kz[0..E) (E <= 256, k <=
-// 16): k rounds of a wave-wide maximum (a key names its expert), then the
-// softmax over the chosen logits z as in route_sum.  Lanes < k return their
-// chosen id and weight (id 0x7fffffff and weight 0 if a chosen logit is not
-// finite, which *bad records).
-__device__ __forceinline__ void wave_topk_keys(const uint64_t *kz, const float *z, int E, int k,
-                                               int32_t &id, float &wt, int32_t *bad) {
-  const int lane = threadIdx.x & (kWave - 1);
-  uint64_t kv[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) kv[j] = lane + kWave * j < E ? kz[lane + kWave * j] : 0ull;
-  int my_id = 0, first = 0;
-  for (int r = 0; r < k; ++r) {
-    uint64_t best = kv[0];
-#pragma unroll
-    for (int j = 1; j < 4; ++j) best = kv[j] > best ? kv[j] : best;
-#pragma unroll
-    for (int off = kWave / 2; off >= 1; off >>= 1) {
-      const uint64_t o = __shfl_xor(best, off, kWave);
-      best = o > best ? o : best;
-    }
-    const int e = 255 - (int)(best & 0xffu);
-    if (lane == (e & (kWave - 1))) kv[e / kWave] = 0ull;  // taken
-    if (lane == r) my_id = e;
-    if (r == 0) first = e;
-  }
-  const float z0 = z[first], zl = lane < k ? z[my_id] : 0.f;
-  const bool ok = __ballot(lane < k && !isfinite(zl)) == 0;
-  const float ex = lane < k && ok ? expf(zl - z0) : 0.f;
-  float sum = ex;
-#pragma unroll
-  for (int off = kWave / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, kWave);
-  id = ok ? my_id : 0x7fffffff;
-  wt = ok ? ex / sum : 0.f;
-  if (lane == 0 && !ok) *bad = 1;
 }
 
 // Router of a small multi-token call (T <= kMtTokens), second kernel (one
@@ -611,21 +654,20 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     MtWork *mw, int32_t *flag) {
   __shared__ float redL[kThreads * kMtTokens];  // [phase][token][expert] partial sums (phases * E <= 256)
   __shared__ float zL[kMtTokens][256];
-  __shared__ uint64_t keyL[kMtTokens][256];
+  __shared__ uint32_t zbL[kMtTokens][256];
   __shared__ StepLds sl;
   __shared__ int32_t selL[kMtTokens][kMaxRouted];
   __shared__ uint32_t tokL[256];   // bit t: token t routes the expert
   __shared__ int32_t slotL[256], uL[256];
+  __shared__ int64_t wordsL[8];
   __shared__ int32_t badL;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  int so = -1;
-  int64_t st = 0;
-  if (tid < E) {
-    so = lru.slot_of[tid];
-    st = lru.stamp[tid];
-  }
-  const int64_t clock0 = lru.meta[0], step = lru.meta[1], used = lru.meta[2];
-  const uint64_t tn = lru.trace ? *lru.trace_n : 0;
+  // the table state and words first (vector loads at clamped addresses,
+  // as in router_finish_kernel)
+  const int ce = min(tid, E - 1);
+  int so = lru.slot_of[ce];
+  int64_t st = lru.stamp[ce];
+  const int64_t word = table_word_load(lru);
   if (tid == 0) badL = 0;
   tokL[tid] = 0u;
   // every token's partials in one round trip (nb <= kMtParts): thread (c, ph)
@@ -651,6 +693,11 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     for (int j = 0; j < kMtParts; ++j) a += t < T && ph < phases && b0 + j < b1 ? v[t][j] : 0.f;
     if (t < T && ph < phases) redL[(ph * kMtTokens + t) * E + c] = a;
   }
+  if (tid >= E) {
+    so = -1;
+    st = 0;
+  }
+  table_word_keep(lru, word, wordsL);
   __syncthreads();
   // z = s * (sum over the phases in order), as the decode router forms it
   if (tid < E) {
@@ -661,15 +708,15 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
         for (int p = 0; p < phases; ++p) z += redL[(p * kMtTokens + t) * E + tid];
         z *= iv[t];
         zL[t][tid] = z;
-        keyL[t][tid] = rank_key(z, tid);
+        zbL[t][tid] = logit_bits(z);
       }
     }
   }
   __syncthreads();
   for (int t = wv; t < T; t += kThreads / kWave) {
-    int32_t id;
+    int32_t sel, id;
     float wt;
-    wave_topk_keys(keyL[t], zL[t], E, k, id, wt, &badL);
+    wave_topk_bits(zbL[t], zL[t], E, k, sel, id, wt, &badL);
     if (lane < k) {
       idx[t * k + lane] = id;
       w[t * k + lane] = wt;
@@ -679,6 +726,7 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   }
   __syncthreads();
   const bool inS = tid < E && tokL[tid] != 0u;
+  step_publish(lru, inS, so, sl);
   const int nS = __syncthreads_count(inS);
   if (badL || nS > lru.C) {  // uniform
     if (tid < T) mw->list[tid].n = 0;
@@ -692,7 +740,8 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     }
     return;
   }
-  const StepResult o = table_step(lru, E, inS, so, st, 0ull, clock0, step, used, tn, sl);
+  const StepResult o =
+      table_step(lru, E, inS, so, st, 0ull, wordsL, sl);
   if (inS) {
     slotL[tid] = o.fs;
     uL[tid] = o.rS;
@@ -3335,8 +3384,12 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
                                 const Timing &t) {
   const LruDev none{};
   const int nb = router_decode_grid(H);
-  hipExtLaunchKernelGGL(router_partial_kernel<false>, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0, x,
-                        wr, H, E, (int)prenorm, kRouterRowsPerBlock, partial, xq, xsc);
+  if (E > 128)
+    hipExtLaunchKernelGGL(router_partial_kernel<false, 32>, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0,
+                          x, wr, H, E, (int)prenorm, kRouterRowsPerBlock, partial, xq, xsc);
+  else
+    hipExtLaunchKernelGGL(router_partial_kernel<false, 16>, dim3(nb), dim3(kThreads), 0, s, t.start, nullptr, 0,
+                          x, wr, H, E, (int)prenorm, kRouterRowsPerBlock, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(router_finish_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0, partial,
@@ -3354,7 +3407,7 @@ hipError_t launch_router_small(const float *x, const float *wr, int T, int H, in
   const int pieces = (H + kRouterRowsPerBlock - 1) / kRouterRowsPerBlock;
   const int rpb = kRouterRowsPerBlock * ((pieces + kMtParts - 1) / kMtParts);
   const int nb = (H + rpb - 1) / rpb;
-  hipExtLaunchKernelGGL(router_partial_kernel<true>, dim3(nb, T), dim3(kThreads), 0, s, t.start, nullptr, 0,
+  hipExtLaunchKernelGGL(router_partial_kernel<true, 32>, dim3(nb, T), dim3(kThreads), 0, s, t.start, nullptr, 0,
                         x, wr, H, E, (int)prenorm, rpb, partial, xq, xsc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
