@@ -19,8 +19,9 @@ inline bool fmt_known(int f) { return f == 8 || f == 2 || f == 12 || f == 14; }
 inline bool fmt_kquant(int f) { return f == 12 || f == 14; }
 inline int fmt_block_bytes(int f) { return f == 8 ? 34 : f == 2 ? 18 : f == 12 ? 144 : f == 14 ? 210 : 0; }
 inline int fmt_block_weights(int f) { return fmt_kquant(f) ? 256 : 32; }
-// the activations' digit sums are needed by down formats with an offset (Q4_0) or a min (Q4_K)
-inline bool fmt_needs_sums(int f) { return f == 2 || f == 12; }
+// the activations' digit sums are needed by a down format with a min term (Q4_K); Q4_0's offset
+// is taken into its weights as signed nibbles
+inline bool fmt_needs_sums(int f) { return f == 12; }
 // bytes of a rows x cols matrix (rows of cols inputs) in format f
 inline int64_t fmt_matrix_bytes(int f, int64_t rows, int64_t cols) {
   return rows * (cols / fmt_block_weights(f)) * fmt_block_bytes(f);
@@ -182,7 +183,7 @@ struct DecodeScratch {
   float *xsc;   // [H/32]
   int8_t *hq;   // [3][k*I] digits of the SwiGLU activations, written by gate/up
   float *hsc;   // [k*I/16] their 16-wide block scales
-  int32_t *hds; // [3][k*I/16] digit sums of those blocks (Q4_0 offset)
+  int32_t *hds; // [3][k*I/16] digit sums of those blocks (down format Q4_K)
 };
 
 // Decode FFN.  Gate/up writes the activations of its rows, as digits of

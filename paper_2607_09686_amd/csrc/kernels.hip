@@ -967,12 +967,10 @@ __device__ __forceinline__ float recombine(int i1, int i2, int i3) {
 }
 
 // Partial dot of one pair with the inputs: D[c][j] = digit plane c, dword j of
-// the pair's 64 inputs; sc0/sc1 the two input block scales; dsum[c][0..1]
-// (Q4_0 only) the digit sums of the two blocks, for the offset 8.
+// the pair's 64 inputs; sc0/sc1 the two input block scales.
 template <int QT>
 __device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwords],
-                                          const uint32_t *D, const float sc0, const float sc1,
-                                          const int *ds0, const int *ds1, int dstride) {
+                                          const uint32_t *D, const float sc0, const float sc1) {
   if constexpr (QT == 8) {
     // bytes 0-1 d0 | 2-33 q0 | 34-35 d1 | 36-67 q1
     const float d0 = half_bits_to_float(wd[0] & 0xffffu), d1 = half_bits_to_float(wd[8] >> 16);
@@ -994,43 +992,43 @@ __device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwo
     return fmaf(d0 * sc0, recombine(a1, a2, a3), d1 * sc1 * recombine(b1, b2, b3));
   } else {
     // bytes 0-1 d0 | 2-17 nibbles of block 0 | 18-19 d1 | 20-35 block 1;
-    // nibble byte j: low -> element j, high -> element j+16; weight d*(n-8)
+    // nibble byte j: low -> element j, high -> element j+16; weight d*(n-8).
+    // With bit 3 of every nibble flipped, a nibble is the 4-bit two's
+    // complement of n - 8; moved to the top of its byte (and the other
+    // nibble cleared) the byte is the signed int8 16 (n - 8).  So every dot4
+    // sum is exactly 16 times the offset weights' sum, and so is each step of
+    // the fp32 combination below (scaling by a power of two is exact): the
+    // result, scaled back by 1/16, equals d (sum of (n - 8) D) as combined
+    // from exact integer sums, with no digit sums needed.
     const float d0 = half_bits_to_float(wd[0] & 0xffffu), d1 = half_bits_to_float(wd[4] >> 16);
     int a1 = 0, a2 = 0, a3 = 0, b1 = 0, b2 = 0, b3 = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2);
-      const uint32_t lo = v & 0x0f0f0f0fu, hi = (v >> 4) & 0x0f0f0f0fu;
+      const uint32_t v = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2) ^ 0x88888888u;
+      const uint32_t lo = (v << 4) & 0xf0f0f0f0u, hi = v & 0xf0f0f0f0u;
       a1 = sdot4(hi, D[4 + j], sdot4(lo, D[j], a1));
       a2 = sdot4(hi, D[20 + j], sdot4(lo, D[16 + j], a2));
       a3 = sdot4(hi, D[36 + j], sdot4(lo, D[32 + j], a3));
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v = wd[5 + j];
-      const uint32_t lo = v & 0x0f0f0f0fu, hi = (v >> 4) & 0x0f0f0f0fu;
+      const uint32_t v = wd[5 + j] ^ 0x88888888u;
+      const uint32_t lo = (v << 4) & 0xf0f0f0f0u, hi = v & 0xf0f0f0f0u;
       b1 = sdot4(hi, D[12 + j], sdot4(lo, D[8 + j], b1));
       b2 = sdot4(hi, D[28 + j], sdot4(lo, D[24 + j], b2));
       b3 = sdot4(hi, D[44 + j], sdot4(lo, D[40 + j], b3));
     }
-    a1 -= 8 * ds0[0];
-    a2 -= 8 * ds0[dstride];
-    a3 -= 8 * ds0[2 * dstride];
-    b1 -= 8 * ds1[0];
-    b2 -= 8 * ds1[dstride];
-    b3 -= 8 * ds1[2 * dstride];
-    return fmaf(d0 * sc0, recombine(a1, a2, a3), d1 * sc1 * recombine(b1, b2, b3));
+    return 0.0625f * fmaf(d0 * sc0, recombine(a1, a2, a3), d1 * sc1 * recombine(b1, b2, b3));
   }
 }
 
 // As pair_dot, with inputs in 16-wide digit blocks: sc[0..3] the scales of
-// the pair's four 16-value quarters, ds[c * dstride + q] (Q4_0 only) their
-// digit sums.  A Q4_0 block's low nibbles are its first 16 values and its
-// high nibbles the last 16, so each nibble half meets one input block.
+// the pair's four 16-value quarters.  A Q4_0 block's low nibbles are its
+// first 16 values and its high nibbles the last 16, so each nibble half meets
+// one input block.
 template <int QT>
 __device__ __forceinline__ float pair_dot16(const uint32_t (&wd)[Fmt<QT>::kPairDwords],
-                                            const uint32_t *D, const float *sc, const int *ds,
-                                            int dstride) {
+                                            const uint32_t *D, const float *sc) {
   int A[4][3] = {};  // [quarter][digit plane]
   float d0, d1;
   if constexpr (QT == 8) {
@@ -1049,13 +1047,16 @@ __device__ __forceinline__ float pair_dot16(const uint32_t (&wd)[Fmt<QT>::kPairD
       for (int c = 0; c < 3; ++c) A[2 + (j >> 2)][c] = sdot4(q, D[16 * c + 8 + j], A[2 + (j >> 2)][c]);
     }
   } else {
+    // the nibbles as signed bytes 16 (n - 8), as in pair_dot: sums 16 times the
+    // offset weights' ones, scaled back exactly at the end
     d0 = half_bits_to_float(wd[0] & 0xffffu);
     d1 = half_bits_to_float(wd[4] >> 16);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v0 = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2), v1 = wd[5 + j];
-      const uint32_t lo0 = v0 & 0x0f0f0f0fu, hi0 = (v0 >> 4) & 0x0f0f0f0fu;
-      const uint32_t lo1 = v1 & 0x0f0f0f0fu, hi1 = (v1 >> 4) & 0x0f0f0f0fu;
+      const uint32_t v0 = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2) ^ 0x88888888u;
+      const uint32_t v1 = wd[5 + j] ^ 0x88888888u;
+      const uint32_t lo0 = (v0 << 4) & 0xf0f0f0f0u, hi0 = v0 & 0xf0f0f0f0u;
+      const uint32_t lo1 = (v1 << 4) & 0xf0f0f0f0u, hi1 = v1 & 0xf0f0f0f0u;
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         A[0][c] = sdot4(lo0, D[16 * c + j], A[0][c]);
@@ -1064,16 +1065,13 @@ __device__ __forceinline__ float pair_dot16(const uint32_t (&wd)[Fmt<QT>::kPairD
         A[3][c] = sdot4(hi1, D[16 * c + 12 + j], A[3][c]);
       }
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int c = 0; c < 3; ++c) A[q][c] -= 8 * ds[c * dstride + q];
   }
   const float r0 = fmaf(sc[0], recombine(A[0][0], A[0][1], A[0][2]),
                         sc[1] * recombine(A[1][0], A[1][1], A[1][2]));
   const float r1 = fmaf(sc[2], recombine(A[2][0], A[2][1], A[2][2]),
                         sc[3] * recombine(A[3][0], A[3][1], A[3][2]));
-  return fmaf(d0, r0, d1 * r1);
+  const float r = fmaf(d0, r0, d1 * r1);
+  return QT == 2 ? 0.0625f * r : r;
 }
 
 // The 48 digit dwords of pair p from an LDS digit image (plane stride pb bytes).
@@ -1146,7 +1144,7 @@ __device__ __forceinline__ void stage_token(const int8_t *__restrict__ q,
 }
 
 // Digit sums of every 32-wide block of a staged digit image of n values
-// (Q4_0 offset): dsL[c][b] = sum of the 32 digits of block b in plane c.
+// (the Q4_K min term): dsL[c][b] = sum of the 32 digits of block b in plane c.
 __device__ __forceinline__ void digit_sums(const uint8_t *qL, int n, int *dsL) {
   const int nb = n / 32, pb = plane_bytes(n);
   for (int i = threadIdx.x; i < 3 * nb; i += kThreads) {
@@ -1171,11 +1169,11 @@ struct GateUpParams {
   const float *xsc;  // input block scales [H/32]
   int8_t *hq;        // activation digits [3][k*I]
   float *hsc;        // their 16-wide block scales [k*I/16]
-  int32_t *hds;      // their digit sums [3][k*I/16] (Q4_0)
+  int32_t *hds;      // their digit sums [3][k*I/16] (down format Q4_K)
   int H, I, k;
   int lanes, mpairs;  // lanes per row (power of 2, <= 16), pairs (K-quants: items) per lane
   int lanes_log2;
-  int h_sums;  // K-quant gate/up: also write the activations' digit sums (down format Q4_0 / Q4_K)
+  int h_sums;  // K-quant gate/up: also write the activations' digit sums (down format Q4_K)
 };
 
 // Digits of SwiGLU activations in 16-wide blocks, called by 16 consecutive
@@ -1218,7 +1216,7 @@ __device__ __forceinline__ void store_h_digits_rt(float v, int pos, int row, int
 template <int QT>
 __device__ __forceinline__ void store_h_digits(float v, int pos, int row, int I, int k, int8_t *hq,
                                                float *hsc, int32_t *hds) {
-  store_h_digits_rt(v, pos, row, I, k, hq, hsc, hds, QT == 2);
+  store_h_digits_rt(v, pos, row, I, k, hq, hsc, hds, false);
 }
 
 // One unit = row r of W_gate and row r of W_up; lane l of the unit's `lanes`
@@ -1270,10 +1268,6 @@ __device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertL
   __builtin_amdgcn_sched_barrier(0);
   stage_token_store(ts, H, qL, scL, dummyL);
   __syncthreads();
-  if constexpr (QT == 2) {
-    digit_sums(qL, H, dsL);
-    __syncthreads();
-  }
   float g = 0.f, u = 0.f;
   for (int m0 = 0; m0 < a.mpairs; m0 += F) {
     if (m0 > 0) {
@@ -1293,8 +1287,8 @@ __device__ __forceinline__ void gateup_body(const GateUpParams &a, const ExpertL
         uint32_t D[48];
         load_digits(qL, pb, p, D);
         const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
-        g += pair_dot<QT>(wg[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-        u += pair_dot<QT>(wu[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+        g += pair_dot<QT>(wg[m], D, s0, s1);
+        u += pair_dot<QT>(wu[m], D, s0, s1);
       }
     }
   }
@@ -1397,8 +1391,8 @@ __device__ __forceinline__ void chunk_row_dots(const uint8_t *cL, int ri, int64_
     uint32_t D[48];
     load_digits(qL, pb, p, D);
     const float sc0 = scL[2 * p], sc1 = scL[2 * p + 1];
-    gs += pair_dot<QT>(wg, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-    us += pair_dot<QT>(wu, D, sc0, sc1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+    gs += pair_dot<QT>(wg, D, sc0, sc1);
+    us += pair_dot<QT>(wu, D, sc0, sc1);
   }
 }
 
@@ -1460,10 +1454,6 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
   int miss, g, c = 0;
   bool gu = spans(u, 0, s0, s1, d0, d1, miss, g);
   load_chunk(s0, s1, h16, buf);
-  if constexpr (QT == 2) {
-    __syncthreads();
-    digit_sums(qL, H, dsL);
-  }
   // the gate/up kernel's lanes and pair order, so h is bit-identical to its result
   const int L = a.g.lanes, rr = threadIdx.x >> a.g.lanes_log2, l = threadIdx.x & (L - 1);
   for (;;) {
@@ -1502,7 +1492,7 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_kernel(CopyGateUpParams 
 
 // Stage the activation digits of the listed experts into LDS: digit images
 // qL [n] (three planes of plane_bytes(I) each), scales scL [n][I/16] and
-// (Q4_0) digit sums dsL [n][3][I/16].  Split in two so that the caller can
+// (Q4_K) digit sums dsL [n][3][I/16].  Split in two so that the caller can
 // issue these loads ahead of its weight loads and store them afterwards.
 constexpr int kMaxDig16 = 9;  // 3 * 12288 / 16 / 256
 constexpr int kMaxSc4 = 1;    // 12288 / 16 / 4 / 256
@@ -1609,7 +1599,7 @@ struct DownParams {
   const ExpertList *Ld;  // device list (nullable): read instead of L
   const int8_t *hq;   // activation digits [3][k*I]
   const float *hsc;   // their 16-wide block scales [k*I/16]
-  const int32_t *hds; // their digit sums [3][k*I/16] (Q4_0)
+  const int32_t *hds; // their digit sums [3][k*I/16] (Q4_K)
   const float *w, *x;
   float *y;
   int H, I, k, mode;
@@ -1625,8 +1615,10 @@ struct DownParams {
 // DEV: the list is read from device memory (a.Ld), else from the arguments.
 // Memory round trips: the list; then the activation digits, the routing
 // weights and the weight rows, all in flight together.
-template <int QT, bool DEV>
-__global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
+// NT: threads per block, 256 or 512 (more rows per block, so that the grid
+// fits the compute units once; the first 256 threads stage the activations).
+template <int QT, bool DEV, int NT>
+__global__ __launch_bounds__(NT, 1) void down_kernel(DownParams a) {
   extern __shared__ __align__(16) uint8_t smem8[];
   __shared__ int posL[kMaxRouted];
   __shared__ float wL[kMaxRouted];
@@ -1657,7 +1649,8 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
   const uint8_t *row = payload + 2 * mat + (int64_t)j * rowb;
   const uint8_t *rowv = payload + 2 * mat + (int64_t)min(j, a.H - 1) * rowb;
   HStage st;
-  stage_h_load(a.hq, a.hsc, a.hds, posL, n, I, a.k, QT == 2, st);  // ahead of the weights
+  const bool stager = NT == kThreads || (int)threadIdx.x < kThreads;  // uniform per wave
+  if (stager) stage_h_load(a.hq, a.hsc, a.hds, posL, n, I, a.k, false, st);  // ahead of the weights
   // keeps the staging loads here, ahead of the weight loads (the compiler
   // would otherwise sink each load to its LDS store and wait for it there)
   __builtin_amdgcn_sched_barrier(0);
@@ -1678,7 +1671,7 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
     load_pair<QT>(ok ? row + (int64_t)p * 2 * BB : rowv, wd[m]);
   }
   __builtin_amdgcn_sched_barrier(0);
-  stage_h_store(st, n, I, QT == 2, qL, scL, dsL, dummyL);
+  if (stager) stage_h_store(st, n, I, false, qL, scL, dsL, dummyL);
   __syncthreads();
   float acc = 0.f;
   for (int m0 = 0; m0 < a.mpairs; m0 += F) {
@@ -1695,8 +1688,7 @@ __global__ __launch_bounds__(kThreads, 1) void down_kernel(DownParams a) {
       if (active && m0 + m < a.mpairs && p < np) {
         uint32_t D[48];
         load_digits(qL + 3 * i * pb, pb, p, D);
-        acc += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p,
-                              dsL + 3 * i * (I / 16) + 4 * p, I / 16);
+        acc += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p);
       }
     }
   }
@@ -2075,7 +2067,7 @@ struct GateUpMtParams {
   const float *xsc;  // [T][H/32]
   int8_t *hq;        // [3][T*k*I]
   float *hsc;        // [T*k*I/16]
-  int32_t *hds;      // [3][T*k*I/16] (Q4_0)
+  int32_t *hds;      // [3][T*k*I/16] (unused: no union format needs digit sums)
   int H, I, k, T;
   int lanes, mpairs, lanes_log2;
 };
@@ -2127,13 +2119,6 @@ __device__ __forceinline__ void gateup_mt_body(const GateUpMtParams &a, bool hit
                 reinterpret_cast<float *>(im + 3 * pb), dummyL);
   }
   __syncthreads();
-  if constexpr (QT == 2) {
-    for (int i = 0; i < nt; ++i) {
-      uint8_t *im = smem8 + i * img;
-      digit_sums(im, H, reinterpret_cast<int *>(im + 3 * pb + 4 * nb));
-    }
-    __syncthreads();
-  }
   float g[kMtTokens], v[kMtTokens];
 #pragma unroll
   for (int i = 0; i < kMtTokens; ++i) g[i] = v[i] = 0.f;
@@ -2161,8 +2146,8 @@ __device__ __forceinline__ void gateup_mt_body(const GateUpMtParams &a, bool hit
             uint32_t D[48];
             load_digits(im, pb, p, D);
             const float s0 = scL[2 * p], s1 = scL[2 * p + 1];
-            g[i] += pair_dot<QT>(wg[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
-            v[i] += pair_dot<QT>(wu[m], D, s0, s1, dsL + 2 * p, dsL + 2 * p + 1, nb);
+            g[i] += pair_dot<QT>(wg[m], D, s0, s1);
+            v[i] += pair_dot<QT>(wu[m], D, s0, s1);
           }
         }
       }
@@ -2263,13 +2248,6 @@ __global__ __launch_bounds__(kThreads) void copy_gateup_mt_kernel(CopyGateUpMtPa
   int g, nt, q, c = 0;
   bool gu = spans(u, 0, s0, s1, d0, d1, g, nt, q);
   load_chunk(s0, s1, h16, buf);
-  if constexpr (QT == 2) {
-    __syncthreads();
-    for (int t = 0; t < T; ++t) {
-      uint8_t *im = smem8 + t * img;
-      digit_sums(im, H, reinterpret_cast<int *>(im + 3 * pb + 4 * nb));
-    }
-  }
   const int L = a.g.lanes, rr = threadIdx.x >> a.g.lanes_log2, l = threadIdx.x & (L - 1);
   const int tpp = (kThreads / L) / R;  // tokens per pass: row slot rr -> token rr / R, row rr % R
   const int ri = rr % R;
@@ -2353,7 +2331,7 @@ __global__ __launch_bounds__(kThreads) void down_mt_kernel(DownMtParams a) {
   const uint8_t *row = payload + 2 * mat + (int64_t)j * rowb;
   const uint8_t *rowv = payload + 2 * mat + (int64_t)min(j, a.H - 1) * rowb;
   HStage st;
-  stage_h_load(a.hq, a.hsc, a.hds, posL, nt, I, a.T * a.k, QT == 2, st);  // ahead of the weights
+  stage_h_load(a.hq, a.hsc, a.hds, posL, nt, I, a.T * a.k, false, st);  // ahead of the weights
   __builtin_amdgcn_sched_barrier(0);
   uint32_t wd[F][PD];
 #pragma unroll
@@ -2363,7 +2341,7 @@ __global__ __launch_bounds__(kThreads) void down_mt_kernel(DownMtParams a) {
     load_pair<QT>(ok ? row + (int64_t)p * 2 * BB : rowv, wd[m]);
   }
   __builtin_amdgcn_sched_barrier(0);
-  stage_h_store(st, nt, I, QT == 2, qL, scL, dsL, dummyL);
+  stage_h_store(st, nt, I, false, qL, scL, dsL, dummyL);
   __syncthreads();
   float acc[kMtTokens];
 #pragma unroll
@@ -2385,8 +2363,7 @@ __global__ __launch_bounds__(kThreads) void down_mt_kernel(DownMtParams a) {
           if (i < nt) {
             uint32_t D[48];
             load_digits(qL + 3 * i * pb, pb, p, D);
-            acc[i] += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p, dsL + 3 * i * (I / 16) + 4 * p,
-                                     I / 16);
+            acc[i] += pair_dot16<QT>(wd[m], D, scL + i * (I / 16) + 4 * p);
           }
         }
       }
@@ -3358,6 +3335,19 @@ __global__ __launch_bounds__(kThreads) void pf_combine_kernel(const float *__res
 #endif
 constexpr int kGateUpMaxLanes = MOE_GATEUP_MAX_LANES, kDownMaxLanes = MOE_DOWN_MAX_LANES;
 
+// Compute units of the current device (cached per device; 0 if unknown).
+int device_compute_units() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 void pick_lanes(int np, int in_flight, int max_lanes, int &lanes, int &mpairs) {
   double best = -1e9;
   lanes = max_lanes;
@@ -3506,20 +3496,39 @@ hipError_t launch_down(int qtype, const DecodeScratch &S, int H, int I, int k, c
   pick_lanes(np, qtype == 8 ? Fmt<8>::kDownFlight : Fmt<2>::kDownFlight, kDownMaxLanes, a.lanes,
              a.mpairs);
   while ((1 << a.lanes_log2) < a.lanes) ++a.lanes_log2;
-  a.rows = kThreads / (a.lanes * L.n);
+  if (L.n < 1 || L.n > kMaxRouted) return hipErrorInvalidValue;
+  // rows per block: 256 threads' worth, or, where that would need more blocks
+  // than there are compute units, up to 512 threads' worth so that one round
+  // of blocks covers H (each block stages all experts' activations once)
+  const int per_row = a.lanes * L.n;
+  int nt = kThreads;
+  a.rows = kThreads / per_row;
+  const int cus = device_compute_units();
+  if (a.rows >= 1 && cus > 0 && (H + a.rows - 1) / a.rows > cus) {
+    const int want = (H + cus - 1) / cus;
+    if (want * per_row <= 2 * kThreads) {
+      nt = 2 * kThreads;
+      a.rows = want;
+    }
+  }
   if (a.rows < 1) return hipErrorInvalidValue;
   const size_t lds = 3 * (size_t)L.n * np * kPairPitch + 4 * (size_t)L.n * (I / 16) * 4 +
                      4 * (size_t)a.rows * L.n;
   dim3 grid((H + a.rows - 1) / a.rows);
-  if (L.n > kMaxRouted) return hipErrorInvalidValue;
-  if (qtype == 8 && Ld)
-    hipExtLaunchKernelGGL(down_kernel<8, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
-  else if (qtype == 8)
-    hipExtLaunchKernelGGL(down_kernel<8, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
-  else if (Ld)
-    hipExtLaunchKernelGGL(down_kernel<2, true>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
-  else
-    hipExtLaunchKernelGGL(down_kernel<2, false>, grid, dim3(kThreads), lds, s, t.start, t.stop, 0, a);
+#define MOE_DOWN_LAUNCH(Q, D, N) \
+  hipExtLaunchKernelGGL(down_kernel<Q, D, N>, grid, dim3(N), lds, s, t.start, t.stop, 0, a)
+  if (nt == kThreads) {
+    if (qtype == 8 && Ld) MOE_DOWN_LAUNCH(8, true, kThreads);
+    else if (qtype == 8) MOE_DOWN_LAUNCH(8, false, kThreads);
+    else if (Ld) MOE_DOWN_LAUNCH(2, true, kThreads);
+    else MOE_DOWN_LAUNCH(2, false, kThreads);
+  } else {
+    if (qtype == 8 && Ld) MOE_DOWN_LAUNCH(8, true, 2 * kThreads);
+    else if (qtype == 8) MOE_DOWN_LAUNCH(8, false, 2 * kThreads);
+    else if (Ld) MOE_DOWN_LAUNCH(2, true, 2 * kThreads);
+    else MOE_DOWN_LAUNCH(2, false, 2 * kThreads);
+  }
+#undef MOE_DOWN_LAUNCH
   return hipGetLastError();
 }
 
