@@ -57,6 +57,7 @@ struct WorkList {
 constexpr int kMtTokens = 8;
 constexpr int kMtMaxCopy = kMtTokens * kMaxRouted;
 constexpr int kMtParts = 16;  // router partial blocks per token of such a call
+constexpr int kMtMaxChunks = 8;  // chunks of a small call whose union exceeds the slots
 struct MtWork {
   int32_t n_copy, n_union;
   const uint8_t *src[kMtMaxCopy];
@@ -112,9 +113,11 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
 // that union exceeds the slots.  flag[0] (host memory) becomes 0 (done), 1
 // (union too large: table untouched, mw empty) or 2 (routing failure);
 // flag[1] the union's size.
+// mw: max_chunks work lists (1 <= max_chunks <= kMtMaxChunks); flag: host
+// memory [3] (verdict, union size, chunks).
 hipError_t launch_router_small(const float *x, const float *wr, int T, int H, int E, int k, float *partial,
                                int32_t *idx, float *w, int8_t *xq, float *xsc, bool prenorm,
-                               const LruDev &lru, MtWork *mw, int32_t *flag, hipStream_t s,
+                               const LruDev &lru, MtWork *mw, int32_t *flag, int max_chunks, hipStream_t s,
                                const Timing &t = {});
 
 // The FFN of a small multi-token call from its work list, each union expert's

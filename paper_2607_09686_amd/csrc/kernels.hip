@@ -643,22 +643,38 @@ __global__ __launch_bounds__(kThreads) void router_finish_kernel(
 // Router of a small multi-token call (T <= kMtTokens), second kernel (one
 // block): every token's logits (the decode router's sums), top-k and softmax
 // by one wave per token, then one slot-table step for the union S of the
-// tokens' routed experts, and a work list: the misses' copies, per token its
-// k experts' slots in rank order, and per union expert its tokens.  If |S|
-// exceeds the slots (slots would be reused inside the call) the table is
-// left untouched and the work list empty; flag[0] (host memory) gets 0
-// (done), 1 (|S| > C) or 2 (routing failure, also in the error word) and
-// flag[1] the union's size.
+// tokens' routed experts (the rule of slot_lru.h) and the work lists.
+//
+// When |S| exceeds the slots, misses beyond the free slots and the slots of
+// the residents outside S take, in ascending order, the slot of the resident
+// member of S with the smallest stamp, i.e. the lowest id among the members
+// holding a slot at that point (stamps follow the ids): slots are reused
+// inside the call.  The experts are then computed in chunks, each chunk's
+// copies, gate/up and down after the previous chunk's: a miss goes into the
+// chunk after the one of the expert whose slot it takes (and not before the
+// previous miss), every other expert into chunk 0.  mw[c] holds chunk c's
+// copies and union experts.  With more than max_chunks chunks the table is
+// left untouched and mw[0] empty.  flag (host memory) gets [0] 0 (done), 1
+// (left to the caller: too many chunks) or 2 (routing failure, also in the
+// error word), [1] the union's size and [2] the number of chunks.
 __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
     const float *__restrict__ partial, int nb, int T, int E, int k, int32_t *idx, float *w, LruDev lru,
-    MtWork *mw, int32_t *flag) {
+    MtWork *mw, int32_t *flag, int max_chunks) {
   __shared__ float redL[kThreads * kMtTokens];  // [phase][token][expert] partial sums (phases * E <= 256)
   __shared__ float zL[kMtTokens][256];
   __shared__ uint32_t zbL[kMtTokens][256];
   __shared__ StepLds sl;
   __shared__ int32_t selL[kMtTokens][kMaxRouted];
   __shared__ uint32_t tokL[256];   // bit t: token t routes the expert
-  __shared__ int32_t slotL[256], uL[256];
+  __shared__ int32_t slotL[256], uL[256];  // per expert: slot at placement, index in its chunk's union
+  __shared__ int32_t chunkL[256];           // per expert: chunk
+  __shared__ uint8_t goneL[256];            // member of S whose slot a later miss takes
+  __shared__ int32_t missL[kMtMaxCopy], mslotL[kMtMaxCopy], mevL[kMtMaxCopy];  // per miss, in order
+  __shared__ uint64_t resL[kThreads / kWave];  // members of S holding a slot once the free and
+                                              // outside residents' slots are taken
+  __shared__ int32_t ccntL[kThreads / kWave][kMtMaxChunks];  // per wave and chunk: experts
+  __shared__ int32_t rfirstL[kMtMaxChunks + 1];              // first miss of each chunk
+  __shared__ int32_t nchunkL;
   __shared__ int64_t wordsL[8];
   __shared__ int32_t badL;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
@@ -670,6 +686,8 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   const int64_t word = table_word_load(lru);
   if (tid == 0) badL = 0;
   tokL[tid] = 0u;
+  goneL[tid] = 0;
+  chunkL[tid] = 0;
   // every token's partials in one round trip (nb <= kMtParts): thread (c, ph)
   // adds, per token, blocks [ph * per, ph * per + per) of expert c in block
   // order (unconditional loads at clamped, valid addresses, selected
@@ -728,46 +746,198 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
   const bool inS = tid < E && tokL[tid] != 0u;
   step_publish(lru, inS, so, sl);
   const int nS = __syncthreads_count(inS);
-  if (badL || nS > lru.C) {  // uniform
+  if (badL) {  // uniform
     if (tid < T) mw->list[tid].n = 0;
     if (tid == 0) {
       mw->n_copy = 0;
       mw->n_union = 0;
-      if (badL) *lru.err = 1;
+      *lru.err = 1;
       flag[1] = nS;
+      flag[2] = 0;
       __threadfence_system();
-      flag[0] = badL ? 2 : 1;
+      flag[0] = 2;
     }
     return;
   }
-  const StepResult o =
-      table_step(lru, E, inS, so, st, 0ull, wordsL, sl);
-  if (inS) {
-    slotL[tid] = o.fs;
-    uL[tid] = o.rS;
-    if (o.miss) {
-      mw->src[o.rM] = lru.store + (int64_t)tid * lru.P;
-      mw->dst[o.rM] = lru.slots + (int64_t)o.fs * lru.P;
-      mw->mu[o.rM] = (uint8_t)o.rS;
+  // the step's counts (as table_step): rank in S, rank among the misses
+  const int64_t clock0 = wordsL[0], step = wordsL[1], used = wordsL[2];
+  const uint64_t tn = (uint64_t)wordsL[3];
+  const int C = lru.C;
+  const bool miss = inS && so < 0;
+  const bool res = tid < E && so >= 0 && !inS;  // residents outside S
+  const uint64_t lt = (1ull << lane) - 1ull;
+  int rS = __popcll(__ballot(inS) & lt), rM = __popcll(__ballot(miss) & lt), nM = 0;
+#pragma unroll
+  for (int v = 0; v < kThreads / kWave; ++v) {
+    if (v < wv) {
+      rS += sl.cnt[0][v];
+      rM += sl.cnt[1][v];
     }
-    mw->upay[o.rS] = lru.slots + (int64_t)o.fs * lru.P;
-    mw->unt[o.rS] = (uint8_t)__popc(tokL[tid]);
-    mw->uhit[o.rS] = (uint8_t)!o.miss;
+    nM += sl.cnt[1][v];
+  }
+  const int nfree = C - (int)used;
+  const int q = C - (nS - nM);                  // misses placed without taking a slot of S
+  const int nev = max(0, min(nM, q) - nfree);   // residents outside S evicted
+  const uint64_t vkey = res ? (uint64_t)st : 0ull;
+  if (res) sl.key[so] = vkey;
+  __syncthreads();
+  bool evicted = false;
+  if (res && nev > 0) {
+    int cr = 0;
+    int i = 0;
+    for (; i + 8 <= C; i += 8) {
+      uint64_t v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = sl.key[i + j];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) cr += v[j] < vkey ? 1 : 0;
+    }
+    for (; i < C; ++i) cr += sl.key[i] < vkey ? 1 : 0;
+    if (cr < nev) {
+      evicted = true;
+      sl.vic[cr] = tid;
+      sl.vsl[cr] = so;
+    }
   }
   __syncthreads();
-  // (token t, rank j): its expert's slot, and its place among the expert's tokens
+  // placements that take a free slot or an outside resident's; the members of
+  // S holding a slot after them
+  if (inS) slotL[tid] = so;
+  if (miss) {
+    missL[rM] = tid;
+    if (rM < q) {
+      const int fs = rM < nfree ? (int)used + rM : sl.vsl[rM - nfree];
+      slotL[tid] = fs;
+      mslotL[rM] = fs;
+      mevL[rM] = rM < nfree ? -1 : sl.vic[rM - nfree];
+    }
+  }
+  {
+    const uint64_t m = __ballot(inS && (!miss || rM < q));
+    if (lane == 0) resL[wv] = m;
+  }
+  if (tid == 0) {
+    rfirstL[0] = 0;
+    nchunkL = 1;
+  }
+  __syncthreads();
+  if (nM > q && wv == 0) {  // uniform: the misses that take a slot of S, in order (one wave)
+    uint64_t r[kThreads / kWave];
+#pragma unroll
+    for (int j = 0; j < kThreads / kWave; ++j) r[j] = resL[j];
+    int cur = 0;
+    for (int i = q; i < nM; ++i) {
+      int v = 0;
+#pragma unroll
+      for (int j = kThreads / kWave - 1; j >= 0; --j)  // the lowest id holding a slot
+        if (r[j]) v = kWave * j + __builtin_ctzll(r[j]);
+      const int sv = slotL[v], cv = chunkL[v], mi = missL[i];
+      const int cm = max(cur, cv + 1);
+      if (cm != cur && lane == 0 && cm <= kMtMaxChunks) rfirstL[cm] = i;
+      cur = cm;
+      r[v / kWave] &= ~(1ull << (v % kWave));
+      r[mi / kWave] |= 1ull << (mi % kWave);
+      if (lane == 0) {
+        slotL[mi] = sv;
+        chunkL[mi] = cm;
+        mslotL[i] = sv;
+        mevL[i] = v;
+        goneL[v] = 1;
+      }
+    }
+    if (lane == 0) nchunkL = cur + 1;
+  }
+  __syncthreads();
+  const int nchunk = nchunkL;
+  if (nchunk > max_chunks) {  // uniform: left to the caller, the table untouched
+    if (tid < T) mw->list[tid].n = 0;
+    if (tid == 0) {
+      mw->n_copy = 0;
+      mw->n_union = 0;
+      flag[1] = nS;
+      flag[2] = nchunk;
+      __threadfence_system();
+      flag[0] = 1;
+    }
+    return;
+  }
+  if (tid == 0) rfirstL[nchunk] = nM;
+  // each expert's index in its chunk's union (ascending id)
+  const int ch = chunkL[tid];
+  int uidx = 0;
+  for (int c2 = 0; c2 < nchunk; ++c2) {
+    const uint64_t m = __ballot(inS && ch == c2);
+    if (ch == c2) uidx = __popcll(m & lt);
+    if (lane == 0) ccntL[wv][c2] = __popcll(m);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < kThreads / kWave; ++v)
+    if (v < wv) uidx += ccntL[v][ch];
+  // the table: stamps, final slots and occupants, evictions, trace
+  if (evicted) lru.slot_of[tid] = -1;
+  if (inS) {
+    const int fs = slotL[tid];
+    const bool gone = goneL[tid] != 0;
+    lru.stamp[tid] = clock0 + rS + 1;
+    if (gone) lru.slot_of[tid] = -1;
+    else if (miss) lru.slot_of[tid] = fs;
+    if (!gone) lru.expert_in[fs] = tid;
+    if (lru.trace) {
+      int32_t *r = lru.trace + 6 * (int64_t)(tn + rS);
+      r[0] = lru.layer;
+      r[1] = (int32_t)step;
+      r[2] = tid;
+      r[3] = miss ? 0 : 1;
+      r[4] = miss ? mslotL[rM] : so;
+      r[5] = miss ? mevL[rM] : -1;
+    }
+    // chunk ch's work: this expert in its union; a miss in its copies
+    MtWork &W = mw[ch];
+    if (miss) {
+      const int mi = rM - rfirstL[ch];
+      W.src[mi] = lru.store + (int64_t)tid * lru.P;
+      W.dst[mi] = lru.slots + (int64_t)fs * lru.P;
+      W.mu[mi] = (uint8_t)uidx;
+    }
+    W.upay[uidx] = lru.slots + (int64_t)fs * lru.P;
+    W.unt[uidx] = (uint8_t)__popc(tokL[tid]);
+    W.uhit[uidx] = (uint8_t)!miss;
+    uL[tid] = uidx;
+  }
+  if (tid == 0) {
+    lru.cnt[0] = (uint64_t)wordsL[4] + (uint64_t)(nS - nM);
+    lru.cnt[1] = (uint64_t)wordsL[5] + (uint64_t)nM;
+    lru.cnt[2] = (uint64_t)wordsL[6] + (uint64_t)max(0, nM - nfree);
+    lru.cnt[3] = (uint64_t)wordsL[7] + (uint64_t)nM * (uint64_t)lru.P;
+    lru.meta[0] = clock0 + nS;
+    lru.meta[1] = step + 1;
+    lru.meta[2] = used + min(nM, nfree);
+    if (lru.trace) *lru.trace_n = tn + (uint64_t)nS;
+  }
+  __syncthreads();
+  // (token t, rank j): its expert's place among the expert's tokens; with one
+  // chunk also its slot in the token's list (read by the per-token GEMVs)
   for (int i = tid; i < T * k; i += kThreads) {
     const int t = i / k, j = i - t * k;
     const int e = selL[t][j];
-    mw->list[t].payload[j] = lru.slots + (int64_t)slotL[e] * lru.P;
-    mw->list[t].pos[j] = j;
-    mw->uq[uL[e]][__popc(tokL[e] & ((1u << t) - 1u))] = (uint8_t)i;
+    mw[chunkL[e]].uq[uL[e]][__popc(tokL[e] & ((1u << t) - 1u))] = (uint8_t)i;
+    if (nchunk == 1) {
+      mw->list[t].payload[j] = lru.slots + (int64_t)slotL[e] * lru.P;
+      mw->list[t].pos[j] = j;
+    }
   }
-  if (tid < T) mw->list[tid].n = k;
+  if (tid < T) mw->list[tid].n = nchunk == 1 ? k : 0;
+  if (tid < nchunk) {
+    mw[tid].n_copy = rfirstL[tid + 1] - rfirstL[tid];
+    int nu = 0;
+#pragma unroll
+    for (int v = 0; v < kThreads / kWave; ++v) nu += ccntL[v][tid];
+    mw[tid].n_union = nu;
+  }
   if (tid == 0) {
-    mw->n_copy = o.nM;
-    mw->n_union = nS;
     flag[1] = nS;
+    flag[2] = nchunk;
     __threadfence_system();
     flag[0] = 0;
   }
@@ -3389,9 +3559,10 @@ hipError_t launch_router_decode(const float *x, const float *wr, int H, int E, i
 
 hipError_t launch_router_small(const float *x, const float *wr, int T, int H, int E, int k, float *partial,
                                int32_t *idx, float *w, int8_t *xq, float *xsc, bool prenorm,
-                               const LruDev &lru, MtWork *mw, int32_t *flag, hipStream_t s,
+                               const LruDev &lru, MtWork *mw, int32_t *flag, int max_chunks, hipStream_t s,
                                const Timing &t) {
-  if (T < 1 || T > kMtTokens || !lru.slot_of) return hipErrorInvalidValue;
+  if (T < 1 || T > kMtTokens || !lru.slot_of || max_chunks < 1 || max_chunks > kMtMaxChunks)
+    return hipErrorInvalidValue;
   // at most kMtParts blocks per token, so the finishing block loads every
   // token's partials in one round trip
   const int pieces = (H + kRouterRowsPerBlock - 1) / kRouterRowsPerBlock;
@@ -3402,7 +3573,7 @@ hipError_t launch_router_small(const float *x, const float *wr, int T, int H, in
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(router_finish_mt_kernel, dim3(1), dim3(kThreads), 0, s, nullptr, t.stop, 0,
-                        partial, nb, T, E, k, idx, w, lru, mw, flag);
+                        partial, nb, T, E, k, idx, w, lru, mw, flag, max_chunks);
   return hipGetLastError();
 }
 

@@ -121,9 +121,9 @@ struct moe_cache {
   WorkList *dl_work = nullptr;
   // small multi-token calls stepped on the device
   float *mt_partial = nullptr;  // [kMtTokens][router grid * E + 1]
-  MtWork *mt_work = nullptr;
-  int32_t *mt_flag = nullptr;   // pinned [2]: verdict (0 done, 1 union exceeds the slots, 2
-                                //   routing failure), union size
+  MtWork *mt_work = nullptr;    // [kMtMaxChunks] work lists, one per chunk of a call
+  int32_t *mt_flag = nullptr;   // pinned [3]: verdict (0 done, 1 left to the host table, 2
+                                //   routing failure), union size, chunks
   int8_t *mt_hq = nullptr;      // [3][kMtTokens * k * I] activation digits by (token, rank)
   float *mt_hsc = nullptr;      // [kMtTokens * k * I / 16]
   int32_t *mt_hds = nullptr;    // [3][kMtTokens * k * I / 16]
@@ -383,8 +383,8 @@ int alloc_dev_tables(moe_cache *c) {
       hipMalloc(&c->dl_work, sizeof(WorkList)) != hipSuccess ||
       hipMalloc(&c->mt_partial, ((size_t)router_decode_grid(c->d.hidden) * E + 1) * kMtTokens *
                                     sizeof(float)) != hipSuccess ||
-      hipMalloc(&c->mt_work, sizeof(MtWork)) != hipSuccess ||
-      hipHostMalloc(&c->mt_flag, 2 * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
+      hipMalloc(&c->mt_work, kMtMaxChunks * sizeof(MtWork)) != hipSuccess ||
+      hipHostMalloc(&c->mt_flag, 3 * sizeof(int32_t), hipHostMallocCoherent) != hipSuccess ||
       hipHostMalloc(&c->dl_stage, table_stage_bytes((int)E, (int)C), hipHostMallocDefault) !=
           hipSuccess) {
     (void)hipGetLastError();
@@ -413,7 +413,7 @@ int clear_dev_tables(moe_cache *c) {
   HIP_TRY(c, hipMemsetAsync(c->dl_zlast, 0, E * 4, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_copy_acc, 0, 16, c->main));
   HIP_TRY(c, hipMemsetAsync(c->dl_work, 0, sizeof(WorkList), c->main));
-  HIP_TRY(c, hipMemsetAsync(c->mt_work, 0, sizeof(MtWork), c->main));
+  HIP_TRY(c, hipMemsetAsync(c->mt_work, 0, kMtMaxChunks * sizeof(MtWork), c->main));
   c->dl_trace_pending = 0;
   return MOE_OK;
 }
@@ -818,13 +818,15 @@ int forward_prefill(moe_cache *c, const float *x, int32_t T, const float *wr, in
 // A multi-token call of at most kMtTokens tokens with the layer's table on
 // the device: per token the decode router's partials and digits, then one
 // block routes every token, steps the table over the union of their experts
-// and writes the work list (two launches); the misses' copies from that list
-// and per token the decode GEMVs over its own experts follow, all queued on
-// the caller's stream.  The host then waits for the table step only to learn
-// whether the union fit the slots: if not, the table was left untouched, the
-// queued copies and GEMVs find an empty list, and the call is run by the
-// multi-token path with the table on the host (which reuses slots inside the
-// call).
+// and writes the work lists (two launches); the misses' copies and the
+// union's GEMVs of the first chunk follow, all queued on the caller's stream.
+// The host then waits for the table step to learn the number of chunks (more
+// than one when the union exceeds the slots and slots are reused inside the
+// call), queues the other chunks' copies and GEMVs behind the first one's and
+// the combination.  With more chunks than kMtMaxChunks, or for shapes the
+// union GEMVs do not take when the union exceeds the slots, the table is left
+// untouched, the queued kernels find an empty list and the call is run by
+// the multi-token path with the table on the host.
 int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, int32_t layer, float *y,
                       moe_counters *delta, int32_t *dbg_idx, float *dbg_w) {
   const moe_model_desc &d = c->d;
@@ -840,6 +842,13 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
   if (c->dl_trace && c->dl_trace_pending + (int64_t)T * k > c->dl_trace_cap && (rc = drain_dev_trace(c)))
     return rc;
   const LruDev L = dev_table(c, layer);
+  // the union's GEMVs (each expert's weights read once; their byte counts are
+  // set once the union's size is known) or, for shapes those kernels do not
+  // take, the decode GEMVs once per token (then one chunk only).  By default
+  // the union's gate/up runs inside the copy launch (misses from the rows
+  // being copied, hits alongside), as in decode.
+  const bool union_ffn = mt_ffn_fits(d.qtype, H, I, T);
+  const bool fused = union_ffn && !(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup_mt(d.qtype, H, I, T);
   volatile int32_t *flag = c->mt_flag;
   flag[0] = -1;
   {
@@ -847,41 +856,38 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
             2ull * T * H * E);
     HIP_TRY(c, launch_router_small(x, wr, T, H, E, k, c->mt_partial, c->topk_idx, c->topk_w, c->st_xq,
                                    c->st_xsc, (d.flags & MOE_F_PRENORM) != 0, L, c->mt_work, c->mt_flag,
-                                   c->main, sp.timing()));
+                                   union_ffn ? kMtMaxChunks : 1, c->main, sp.timing()));
     sp.end();
   }
   HIP_TRY(c, hipEventRecord(c->ev_route, c->main));
   if (c->dl_trace) c->dl_trace_pending += (int64_t)T * k;
-  // the union's GEMVs (each expert's weights read once; their byte counts are
-  // set once the union's size is known) or, for shapes those kernels do not
-  // take, the decode GEMVs once per token.  By default the union's gate/up
-  // runs inside the copy launch (misses from the rows being copied, hits
-  // alongside), as in decode.
-  const bool union_ffn = mt_ffn_fits(d.qtype, H, I, T);
-  const bool fused = union_ffn && !(d.flags & MOE_F_SPLIT_COPY) && fusable_copy_gateup_mt(d.qtype, H, I, T);
   const int umax = std::min(T * k, (int)c->C);
   uint64_t *acc = c->timing_now ? c->dl_copy_acc : nullptr;
-  {
-    Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
-    if (fused)
-      HIP_TRY(c, launch_copy_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc,
-                                       c->mt_hds, H, I, k, T, umax, c->P, kCopyGrid, acc, c->main,
-                                       sp.timing()));
-    else
-      HIP_TRY(c, launch_materialize_list(c->mt_work, c->P, kCopyGrid, acc, c->main, sp.timing()));
-    sp.end();
-  }
+  // one chunk's copies and union GEMVs (gu / dn: the spans of its GEMVs)
+  auto chunk_ffn = [&](const MtWork *W, Span &gu, Span &dn) -> int {
+    {
+      Span sp(c, c->main, MOE_KIND_COPY, 0, 0, 0);  // copies and bytes come from the device
+      if (fused)
+        HIP_TRY(c, launch_copy_gateup_mt(d.qtype, W, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc, c->mt_hds, H,
+                                         I, k, T, umax, c->P, kCopyGrid, acc, c->main, sp.timing()));
+      else
+        HIP_TRY(c, launch_materialize_list(W, c->P, kCopyGrid, acc, c->main, sp.timing()));
+      sp.end();
+    }
+    if (union_ffn) {
+      if (!fused)
+        HIP_TRY(c, launch_gateup_mt(d.qtype, W, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc, c->mt_hds, H, I,
+                                    k, T, umax, c->main, gu.timing()));
+      HIP_TRY(c, launch_down_mt(d.qtype, W, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H, I, k, T, umax,
+                                c->main, dn.timing()));
+    }
+    return MOE_OK;
+  };
   const int mode = (d.flags & MOE_F_RESIDUAL) ? 1 : 0;
   Span gu(c, c->main, MOE_KIND_GATEUP, 1, 0, 4ull * T * k * H * I);
   Span dn(c, c->main, MOE_KIND_DOWN, 1, 0, 2ull * T * k * H * I);
-  if (union_ffn) {
-    if (!fused)
-      HIP_TRY(c, launch_gateup_mt(d.qtype, c->mt_work, c->st_xq, c->st_xsc, c->mt_hq, c->mt_hsc,
-                                  c->mt_hds, H, I, k, T, umax, c->main, gu.timing()));
-    HIP_TRY(c, launch_down_mt(d.qtype, c->mt_work, c->mt_hq, c->mt_hsc, c->mt_hds, c->mt_R, H, I, k, T,
-                              umax, c->main, dn.timing()));
-    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->mt_work, c->main));
-  } else {
+  if ((rc = chunk_ffn(c->mt_work, gu, dn))) return rc;
+  if (!union_ffn) {
     ExpertList shape{};
     shape.n = k;
     for (int32_t tk = 0; tk < T; ++tk) {
@@ -911,7 +917,12 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
     }
   }
   const int32_t verdict = flag[0];
+  const int32_t n_chunks = flag[2];
   if (union_ffn && verdict == 0) {
+    if (n_chunks < 1 || n_chunks > kMtMaxChunks) {
+      c->poisoned = true;
+      return fail(MOE_EHIP, "multi-token table step reported %d chunks", n_chunks);
+    }
     gu.sp.bytes = (uint64_t)flag[1] * 2 * c->M;
     dn.sp.bytes = (uint64_t)flag[1] * c->Md;
     if (fused)
@@ -919,6 +930,19 @@ int forward_small_dev(moe_cache *c, const float *x, int32_t T, const float *wr, 
     else
       gu.end();
     dn.end();
+    // the other chunks, each after the previous one (their copies overwrite
+    // slots of experts computed in an earlier chunk), then the combination
+    for (int ch = 1; ch < n_chunks; ++ch) {
+      Span gu2(c, c->main, MOE_KIND_GATEUP, 1, 0, 0);
+      Span dn2(c, c->main, MOE_KIND_DOWN, 1, 0, 0);
+      if ((rc = chunk_ffn(c->mt_work + ch, gu2, dn2))) return rc;
+      if (fused)
+        gu2.discard();
+      else
+        gu2.end();
+      dn2.end();
+    }
+    HIP_TRY(c, launch_combine_mt(c->mt_R, c->topk_w, x, y, H, k, T, mode, c->mt_work, c->main));
   } else {
     gu.discard();
     dn.discard();
@@ -1075,10 +1099,13 @@ int moe_layer_forward_dbg(moe_cache *c, const float *x, int32_t n_tokens, const 
     return fail(MOE_EINVAL, "n_tokens * max(hidden, top_k * inter) must be <= 2^34");
   if (c->d.flags & MOE_F_SCORE_EVICT)
     return fail(MOE_EINVAL, "MOE_F_SCORE_EVICT takes one token per layer call");
-  // a small call tries the device path unless the layer's last small call did
-  // not fit the slots (then the device step would only report that again); the
-  // two paths step the table by the same rule
-  if (c->dev_lru && n_tokens <= kSmallTokens && !c->small_overflow[layer])
+  // a small call tries the device path, which also takes unions larger than
+  // the slots (in chunks) where the union GEMVs take the shape; for other
+  // shapes unless the layer's last small call did not fit the slots (then the
+  // device step would only report that again).  The two paths step the table
+  // by the same rule.
+  if (c->dev_lru && n_tokens <= kSmallTokens &&
+      (!c->small_overflow[layer] || mt_ffn_fits(c->d.qtype, c->d.hidden, c->d.inter, n_tokens)))
     return forward_small_dev(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
   return forward_prefill(c, x, n_tokens, router_w, layer, y, delta, topk_idx, topk_w);
 }

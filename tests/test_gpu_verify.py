@@ -101,12 +101,15 @@ def test_verify_small(qtype, budget, q):
 
 
 def test_a3b_verify_full_size():
+    """The A3B windows at their budget and at 19 slots (15 %), where most windows' unions
+    exceed the slots and the device steps them in chunks."""
     wl = synth.WORKLOADS["a3b_verify"]
     st = store_buffer(wl)
     try:
-        c, steps = verify_chain(wl, wl.budget_slots, st, 16, 5)
-        assert sum(g for _, _, g in steps) == wl.n_tokens
-        assert c.materialized_bytes == c.misses * wl.payload_bytes
+        for budget, seed in ((wl.budget_slots, 5), (19, 6)):
+            c, steps = verify_chain(wl, budget, st, 16, seed)
+            assert sum(g for _, _, g in steps) == wl.n_tokens
+            assert c.materialized_bytes == c.misses * wl.payload_bytes
     finally:
         st[0].free()
 
