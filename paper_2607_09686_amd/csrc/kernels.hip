@@ -2793,21 +2793,35 @@ __global__ __launch_bounds__(kThreads) void group_scatter_kernel(const int32_t *
   (void)tail;
 }
 
-// One wave's experts for the grouped GEMMs (kernel argument).
-constexpr int kPfMaxExperts = 96;
+// One wave's experts for the grouped GEMMs (kernel argument, about 3 KB).
+constexpr int kPfMaxExperts = 128;
+constexpr int kPfMaxTiles = 512;
 struct PfExperts {
   const uint8_t *payload[kPfMaxExperts];
   int32_t row0[kPfMaxExperts];  // first row of the expert's pairs in perm / Ab
   int32_t n[kPfMaxExperts];     // pairs (tokens) routed to it
   int32_t count;
+  // flat M-tile t (128 rows): expert in the low byte, the expert's M-tile in the
+  // high byte; ntiles == 0 when the launch's tiles do not fit (then a scan)
+  int32_t ntiles;
+  uint16_t tile[kPfMaxTiles];
 };
 
 constexpr int kPfBM = 128;  // tokens per tile
 constexpr int kPfBK = 64;   // one pair of weight blocks per row
 constexpr int kPfLd = kPfBK + 8;  // LDS row stride in bf16 (padding against bank conflicts)
 
-// (expert, M-tile) of a flat M-tile index; returns false past the end.
+// (expert, M-tile) of a flat M-tile index; returns false past the end.  One
+// lookup in the launch's tile table (a scan over the experts, one dependent
+// scalar load each, took microseconds for the last tiles of a launch).
 __device__ __forceinline__ bool pf_tile(const PfExperts &X, int mt, int &j, int &m0) {
+  if (X.ntiles > 0) {
+    if (mt >= X.ntiles) return false;
+    const uint32_t v = X.tile[mt];
+    j = (int)(v & 0xffu);
+    m0 = (int)(v >> 8) * kPfBM;
+    return true;
+  }
   for (j = 0; j < X.count; ++j) {
     const int tiles = (X.n[j] + kPfBM - 1) / kPfBM;
     if (mt < tiles) {
@@ -3473,6 +3487,14 @@ constexpr int kGmQ = 512 / kGmThreads;  // dequantised quarters per thread and s
 
 // (expert, M-tile) of a flat M-tile index with kGmBM-row tiles.
 __device__ __forceinline__ bool gm_tile(const PfExperts &X, int mt, int &j, int &m0) {
+  static_assert(kGmBM == kPfBM, "the tile table is built for 128-row tiles");
+  if (X.ntiles > 0) {
+    if (mt >= X.ntiles) return false;
+    const uint32_t v = X.tile[mt];
+    j = (int)(v & 0xffu);
+    m0 = (int)(v >> 8) * kGmBM;
+    return true;
+  }
   for (j = 0; j < X.count; ++j) {
     const int tiles = (X.n[j] + kGmBM - 1) / kGmBM;
     if (mt < tiles) {
@@ -3618,6 +3640,9 @@ struct GmParams {
   int64_t mat, down_off;  // bytes of W_gate; offset of W_down in a payload
   int64_t rowb;           // bytes of a weight row of the format (gate/up: H inputs; down: I)
 };
+// kernel arguments stay within 4 KB
+static_assert(sizeof(GmParams) <= 4096 && sizeof(PfGateUpParams) <= 4096 && sizeof(PfDownParams) <= 4096,
+              "grouped-GEMM kernel arguments exceed 4 KB");
 
 // grid: (M-tiles of the wave's experts, I / 64).  B rows 0..63: W_gate rows
 // n0 .. n0+63, rows 64..127: the same rows of W_up; h = silu(g) u written as
@@ -4229,12 +4254,17 @@ hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, 
 static int gm_experts(const PfWave &W, PfExperts &X) {
   X.count = W.count;
   int tiles = 0;
+  bool table = true;
   for (int i = 0; i < W.count; ++i) {
     X.payload[i] = W.payload[i];
     X.row0[i] = W.row0[i];
     X.n[i] = W.n[i];
-    tiles += (W.n[i] + kGmBM - 1) / kGmBM;
+    const int ti = (W.n[i] + kGmBM - 1) / kGmBM;
+    if (ti > 256 || tiles + ti > kPfMaxTiles) table = false;
+    for (int m = 0; table && m < ti; ++m) X.tile[tiles + m] = (uint16_t)(i | (m << 8));
+    tiles += ti;
   }
+  X.ntiles = table ? tiles : 0;
   return tiles;
 }
 
@@ -4269,6 +4299,7 @@ struct GmDown {
 
 hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
                             __bf16 *ab, int T, int H, int I, int k, hipStream_t s, const Timing &t) {
+  if (W.count < 0 || W.count > kPfMaxExperts) return hipErrorInvalidValue;
   GmParams a{};
   const int tiles = gm_experts(W, a.X);
   const int fmt = fmt_gate_up(qtype);
@@ -4319,6 +4350,7 @@ hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, con
 hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *ab,
                           const float *w, float *P, int pairs, int H, int I, hipStream_t s,
                           const Timing &t) {
+  if (W.count < 0 || W.count > kPfMaxExperts) return hipErrorInvalidValue;
   GmParams a{};
   const int tiles = gm_experts(W, a.X);
   const int fmt = fmt_down(qtype);
