@@ -190,6 +190,17 @@ def test_prefill_other_shapes(shape):
         run_prefill(wl, C, T)
 
 
+def test_prefill_tiles_past_the_table():
+    """A warm call whose 65 536 (token, expert) pairs make more 128-row tiles than the
+    grouped GEMMs' per-launch tile table holds (512): the kernels find their tile by the
+    scan over the experts instead.  The first call copies every expert in; the second
+    runs all 16 as hits in one launch.  Routes, trace, counters and every token's
+    output against the bf16-weight oracle."""
+    for qt in ("q8_0", "q4_0"):
+        wl = synth.WORKLOADS["tiny"].with_(n_experts=16, top_k=8, qtype=qt, name=f"pftiles_{qt}")
+        run_prefill(wl, 16, 8192, calls=2)
+
+
 def test_a3b_prefill_full_size():
     """4096 tokens through all 48 layers of the A3B stack, 45 slots, cold cache,
     pre-norm residual chain on the GPU; every route and the whole trace checked,
