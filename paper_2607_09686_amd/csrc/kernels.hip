@@ -3056,172 +3056,7 @@ __device__ __forceinline__ void dma16(const void *g, void *dst) {
   __builtin_amdgcn_global_load_lds((g_void *)g, (lds_void *)dst, 16, 0, 0);
 }
 
-// Wide-tile gate/up GEMM (I a multiple of 128): one block per (M-tile of 128
-// rows, 128 gate + 128 up columns), 512 threads.  Waves 0-3 multiply (wave c:
-// tile rows 32c..32c+31 against all 256 weight columns, the same MFMA sequence
-// per accumulator as pf_gateup_kernel); waves 4-7 stage the next K step: the
-// activation tile (both planes) by direct global -> LDS loads, each 8 lanes one
-// full 128-byte row segment with its 16-byte chunks XOR-swizzled by row (so the
-// MFMA fragment reads hit distinct banks), and the weight tile dequantised from
-// one pair of blocks per thread.  Each stage has its own LDS array, so that the
-// compiler sees the reads of one stage not alias the loads into the other.  The
-// 1-D grid runs the six (or I/128) column tiles of an M-tile, and an expert's
-// M-tiles, one after the other on the same XCD (block L runs on XCD L % 8), so
-// that their shared activation rows and weights are reused from that XCD's L2.
 constexpr int kPfWideThreads = 512;
-template <int QT>
-__global__ __launch_bounds__(kPfWideThreads, 1) void pf_gateup_wide_kernel(PfGateUpParams a) {
-  __shared__ __align__(16) __bf16 As0[2][128][64], As1[2][128][64];  // [plane][row][k], swizzled
-  __shared__ __align__(16) __bf16 Bs0[256][kPfLd], Bs1[256][kPfLd];   // rows 0..127 gate, 128..255 up
-  constexpr int BB = Fmt<QT>::kBlockBytes;
-  constexpr int PW = QT == 8 ? 17 : 9;  // dwords of one pair of blocks
-  const int NT = a.I / 128, total = gridDim.x;
-  int mt, nt;
-  {
-    const int L = blockIdx.x, x = L % 8, idx = L / 8, per = total / 8, rem = total % 8;
-    const int w = x * per + min(x, rem) + idx;
-    mt = w / NT;
-    nt = w % NT;
-  }
-  int j, m0;
-  if (!pf_tile(a.X, mt, j, m0)) return;
-  const int n0 = nt * 128;
-  const int n = a.X.n[j], row0 = a.X.row0[j];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int KT = a.H / kPfBK;
-  if (wv >= 4) {
-    // producer: thread pt owns weight row pt of the tile (gate rows, then up rows)
-    const int pw = wv - 4, pt = tid - 256;
-    const int64_t rowb = (int64_t)(a.H / 32) * BB, mat = (int64_t)a.I * rowb;
-    const uint32_t *bptr = reinterpret_cast<const uint32_t *>(a.X.payload[j] + (pt >= 128 ? mat : 0) +
-                                                             (int64_t)(n0 + (pt & 127)) * rowb);
-    // activation loads: wave pw issues g = 8 pw + u (u < 8): plane g / 16, tile
-    // rows 8 (g % 16) .. +7; element offsets into xb (32 bits, checked at launch)
-    uint32_t asrc[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
-      const int m = min(m0 + r, n - 1);
-      const int c = (lane & 7) ^ (lane >> 3);
-      asrc[u] = (uint32_t)p * (uint32_t)(a.T * a.H) + (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)a.H + 8 * c;
-    }
-    auto aload = [&](int kt, __bf16 (*As)[128][64]) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int g = 8 * pw + u;
-        dma16(a.xb + (asrc[u] + (uint32_t)(kt * kPfBK)), &As[g >> 4][8 * (g & 15)][0]);
-      }
-    };
-    auto bload = [&](int kt, uint32_t (&v)[PW]) {
-      const uint32_t *q = bptr + (int64_t)kt * (2 * BB / 4);
-#pragma unroll
-      for (int i = 0; i < PW; ++i) v[i] = q[i];
-    };
-    auto deq = [&](const uint32_t (&v)[PW], __bf16 *dst) {
-      uint32_t h0[9], h1[9];
-      constexpr int o1 = QT == 8 ? 8 : 4;
-#pragma unroll
-      for (int i = 0; i < 9; ++i) {
-        h0[i] = i < PW ? v[i] : 0u;
-        h1[i] = i + o1 < PW ? v[i + o1] : 0u;
-      }
-      dequant_half<QT>(h0, 0, dst);
-      dequant_half<QT>(h1, 1, dst + 32);
-    };
-    uint32_t B0[PW], B1[PW];
-    aload(0, As0);
-    bload(0, B0);
-    bload(min(1, KT - 1), B1);
-    deq(B0, &Bs0[pt][0]);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // step kt: stage kt + 1 into the other LDS arrays; the raw weights of kt + 1
-    // are in BO, BS takes those of kt + 2
-#define PFW_PROD(BS, BO, AN, BN, kt)                           \
-  do {                                                         \
-    if ((kt) + 1 < KT) {                                       \
-      aload((kt) + 1, AN);                                     \
-      bload(min((kt) + 2, KT - 1), BS);                        \
-      deq(BO, &BN[pt][0]);                                     \
-    }                                                          \
-    __builtin_amdgcn_s_waitcnt(0);                             \
-    __syncthreads();                                           \
-  } while (0)
-    int kt = 0;
-    for (; kt + 2 <= KT; kt += 2) {
-      PFW_PROD(B0, B1, As1, Bs1, kt);
-      PFW_PROD(B1, B0, As0, Bs0, kt + 1);
-    }
-    if (kt < KT) PFW_PROD(B0, B1, As1, Bs1, kt);
-#undef PFW_PROD
-    return;
-  }
-  // consumer wave wv: rows 32 wv .. +31 of the tile, 8 + 8 column subtiles
-  f32x4 accg[2][8], accu[2][8];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      accg[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-      accu[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  const int gr = lane & 15;
-  auto mma = [&](__bf16 (*As)[128][64], __bf16 (*Bs)[kPfLd]) {
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 Ar[2][2];
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int r = 32 * wv + 16 * i + (lane & 15);
-          const int c = (4 * ks + (lane >> 4)) ^ (r & 7);
-          Ar[pl][i] = *reinterpret_cast<const bf16x8 *>(&As[pl][r][8 * c]);
-        }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int c = 32 * ks + 8 * (lane >> 4);
-        const bf16x8 bg = *reinterpret_cast<const bf16x8 *>(&Bs[gr + 16 * q][c]);
-        const bf16x8 bu = *reinterpret_cast<const bf16x8 *>(&Bs[128 + gr + 16 * q][c]);
-#pragma unroll
-        for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            accg[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i], bg, accg[i][q], 0, 0, 0);
-            accu[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i], bu, accu[i][q], 0, 0, 0);
-          }
-      }
-    }
-  };
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 2 <= KT; kt += 2) {
-    mma(As0, Bs0);
-    __syncthreads();
-    mma(As1, Bs1);
-    __syncthreads();
-  }
-  if (kt < KT) {
-    mma(As0, Bs0);
-    __syncthreads();
-  }
-  const int64_t plane = (int64_t)a.pairs * a.I;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
-        if (m < n) {
-          const float v = silu_fast(accg[i][q][r]) * accu[i][q][r];
-          const __bf16 hi = (__bf16)v;
-          const int64_t o = (int64_t)(row0 + m) * a.I + n0 + 16 * q + (lane & 15);
-          a.ab[o] = hi;
-          a.ab[plane + o] = (__bf16)(v - (float)hi);
-        }
-      }
-}
 
 struct PfDownParams {
   PfExperts X;
@@ -3312,161 +3147,6 @@ __global__ __launch_bounds__(kThreads, 2) void pf_down_kernel(PfDownParams a) {
 #pragma unroll
         for (int q = 0; q < 8; ++q)
           if (n0 + 16 * q < a.H) dst[16 * q] = wt[i][r] * acc[i][q][r];
-      }
-    }
-}
-// Wide-tile down GEMM (H a multiple of 256): one block per (M-tile of 128 rows,
-// 256 output columns), 512 threads, the structure of pf_gateup_wide_kernel:
-// waves 0-3 multiply (wave c: rows 32c..32c+31, all 256 columns, the MFMA
-// sequence per accumulator of pf_down_kernel), waves 4-7 stage the next K step
-// (the activation rows, contiguous in perm order, by direct global -> LDS
-// loads; one weight row of W_down per thread, dequantised).  1-D grid with the
-// column tiles of an M-tile consecutive on one XCD.
-template <int QT>
-__global__ __launch_bounds__(kPfWideThreads, 1) void pf_down_wide_kernel(PfDownParams a) {
-  __shared__ __align__(16) __bf16 As0[2][128][64], As1[2][128][64];  // [plane][row][k], swizzled
-  __shared__ __align__(16) __bf16 Bs0[256][kPfLd], Bs1[256][kPfLd];   // output columns n0..n0+255
-  constexpr int BB = Fmt<QT>::kBlockBytes;
-  constexpr int PW = QT == 8 ? 17 : 9;
-  const int NT = a.H / 256, total = gridDim.x;
-  int mt, nt;
-  {
-    const int L = blockIdx.x, x = L % 8, idx = L / 8, per = total / 8, rem = total % 8;
-    const int w = x * per + min(x, rem) + idx;
-    mt = w / NT;
-    nt = w % NT;
-  }
-  int j, m0;
-  if (!pf_tile(a.X, mt, j, m0)) return;
-  const int n0 = nt * 256;
-  const int n = a.X.n[j], row0 = a.X.row0[j];
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
-  const int KT = a.I / kPfBK;
-  if (wv >= 4) {
-    const int pw = wv - 4, pt = tid - 256;
-    const int64_t rowb = (int64_t)(a.I / 32) * BB;
-    const int64_t mat = (int64_t)a.I * ((int64_t)(a.H / 32) * BB);
-    const uint32_t *bptr =
-        reinterpret_cast<const uint32_t *>(a.X.payload[j] + 2 * mat + (int64_t)(n0 + pt) * rowb);
-    uint32_t asrc[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
-      const int m = min(m0 + r, n - 1);
-      const int c = (lane & 7) ^ (lane >> 3);
-      asrc[u] = (uint32_t)p * (uint32_t)(a.pairs * a.I) + (uint32_t)(row0 + m) * (uint32_t)a.I + 8 * c;
-    }
-    auto aload = [&](int kt, __bf16 (*As)[128][64]) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int g = 8 * pw + u;
-        dma16(a.ab + (asrc[u] + (uint32_t)(kt * kPfBK)), &As[g >> 4][8 * (g & 15)][0]);
-      }
-    };
-    auto bload = [&](int kt, uint32_t (&v)[PW]) {
-      const uint32_t *q = bptr + (int64_t)kt * (2 * BB / 4);
-#pragma unroll
-      for (int i = 0; i < PW; ++i) v[i] = q[i];
-    };
-    auto deq = [&](const uint32_t (&v)[PW], __bf16 *dst) {
-      uint32_t h0[9], h1[9];
-      constexpr int o1 = QT == 8 ? 8 : 4;
-#pragma unroll
-      for (int i = 0; i < 9; ++i) {
-        h0[i] = i < PW ? v[i] : 0u;
-        h1[i] = i + o1 < PW ? v[i + o1] : 0u;
-      }
-      dequant_half<QT>(h0, 0, dst);
-      dequant_half<QT>(h1, 1, dst + 32);
-    };
-    uint32_t B0[PW], B1[PW];
-    aload(0, As0);
-    bload(0, B0);
-    bload(min(1, KT - 1), B1);
-    deq(B0, &Bs0[pt][0]);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-#define PFW_PROD(BS, BO, AN, BN, kt)                           \
-  do {                                                         \
-    if ((kt) + 1 < KT) {                                       \
-      aload((kt) + 1, AN);                                     \
-      bload(min((kt) + 2, KT - 1), BS);                        \
-      deq(BO, &BN[pt][0]);                                     \
-    }                                                          \
-    __builtin_amdgcn_s_waitcnt(0);                             \
-    __syncthreads();                                           \
-  } while (0)
-    int kt = 0;
-    for (; kt + 2 <= KT; kt += 2) {
-      PFW_PROD(B0, B1, As1, Bs1, kt);
-      PFW_PROD(B1, B0, As0, Bs0, kt + 1);
-    }
-    if (kt < KT) PFW_PROD(B0, B1, As1, Bs1, kt);
-#undef PFW_PROD
-    return;
-  }
-  f32x4 acc[2][16];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int q = 0; q < 16; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto mma = [&](__bf16 (*As)[128][64], __bf16 (*Bs)[kPfLd]) {
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 Ar[2][2];
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int r = 32 * wv + 16 * i + (lane & 15);
-          const int c = (4 * ks + (lane >> 4)) ^ (r & 7);
-          Ar[pl][i] = *reinterpret_cast<const bf16x8 *>(&As[pl][r][8 * c]);
-        }
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const bf16x8 bf =
-            *reinterpret_cast<const bf16x8 *>(&Bs[16 * q + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
-#pragma unroll
-        for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-            acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i], bf, acc[i][q], 0, 0, 0);
-      }
-    }
-  };
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 2 <= KT; kt += 2) {
-    mma(As0, Bs0);
-    __syncthreads();
-    mma(As1, Bs1);
-    __syncthreads();
-  }
-  if (kt < KT) {
-    mma(As0, Bs0);
-    __syncthreads();
-  }
-  // the lane's 8 output rows: pair ids, then their weights
-  int pair[2][4];
-  float wt[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      pair[i][r] = a.perm[row0 + min(m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r, n - 1)];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) wt[i][r] = a.w[pair[i][r]];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
-      if (m < n) {
-        float *dst = a.P + (int64_t)pair[i][r] * a.H + n0 + (lane & 15);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) dst[16 * q] = wt[i][r] * acc[i][q][r];
       }
     }
 }
@@ -4251,6 +3931,291 @@ hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, 
 }
 
 // The wave's experts and the M-tile count of 256-row tiles.
+// ------------------------------------------------ wide-tile grouped GEMMs ---
+//
+// One block per (M-tile of 128 rows, 256 columns), 512 threads: waves 0-3
+// multiply (wave c: tile rows 32c..32c+31 against all 256 weight columns, the
+// MFMA sequence per accumulator of pf_gateup_kernel / pf_down_kernel), waves
+// 4-7 stage the next K step of 64: the activation tile (both planes) by direct
+// global -> LDS loads, each 8 lanes one full 128-byte row segment with its
+// 16-byte chunks XOR-swizzled by row (so the MFMA operand reads hit distinct
+// banks), and the weight tile dequantised from the raw bytes of one weight row
+// per thread, loaded a step ahead.  Each LDS stage is its own array, so that
+// the compiler sees the reads of one stage not alias the loads into the other.
+// The 1-D grid runs the column tiles of an M-tile, then an expert's M-tiles, one
+// after the other on the same XCD (block L runs on XCD L % 8), so that their
+// shared activation rows and weights come from that XCD's L2.
+//
+// A producer thread's raw bytes of one K step (64 weights of its row):
+//   Q8_0 / Q4_0: the pair of blocks (17 / 9 dwords);
+//   Q4_K / Q6_K: the four 16-weight quarters as gm_load_raw takes them.
+template <int FMT>
+struct WideRaw {
+  static constexpr int kDw = FMT == 8 ? 17 : FMT == 2 ? 9 : 48;
+};
+template <int FMT>
+__device__ __forceinline__ void wide_load(const uint8_t *row, int kt, uint32_t (&v)[WideRaw<FMT>::kDw]) {
+  if constexpr (FMT == 8 || FMT == 2) {
+    const uint32_t *q = reinterpret_cast<const uint32_t *>(row + (int64_t)kt * 2 * Fmt<FMT>::kBlockBytes);
+#pragma unroll
+    for (int i = 0; i < WideRaw<FMT>::kDw; ++i) v[i] = q[i];
+  } else {
+#pragma unroll
+    for (int bq = 0; bq < 4; ++bq) {
+      uint32_t t[12];
+      gm_load_raw<FMT>(row, kt, bq, t);
+#pragma unroll
+      for (int i = 0; i < 12; ++i) v[12 * bq + i] = t[i];
+    }
+  }
+}
+// The row's 64 weights of step kt as bf16 into dst (16-byte aligned).
+template <int FMT>
+__device__ __forceinline__ void wide_dequant(const uint32_t (&v)[WideRaw<FMT>::kDw], const uint8_t *row,
+                                             int kt, __bf16 *dst) {
+  if constexpr (FMT == 8 || FMT == 2) {
+    constexpr int PW = WideRaw<FMT>::kDw, o1 = FMT == 8 ? 8 : 4;
+    uint32_t h0[9], h1[9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+      h0[i] = i < PW ? v[i] : 0u;
+      h1[i] = i + o1 < PW ? v[i + o1] : 0u;
+    }
+    dequant_half<FMT>(h0, 0, dst);
+    dequant_half<FMT>(h1, 1, dst + 32);
+  } else {
+#pragma unroll
+    for (int bq = 0; bq < 4; ++bq) {
+      uint32_t t[12];
+#pragma unroll
+      for (int i = 0; i < 12; ++i) t[i] = v[12 * bq + i];
+      gm_dequant<FMT>(t, row, kt, bq, dst + 16 * bq);
+    }
+  }
+}
+
+// The (M-tile, column tile) of this block in the XCD-grouped order.
+__device__ __forceinline__ void wide_tile(int NT, int &mt, int &nt) {
+  const int total = gridDim.x, L = blockIdx.x, x = L % 8, idx = L / 8, per = total / 8, rem = total % 8;
+  const int w = x * per + min(x, rem) + idx;
+  mt = w / NT;
+  nt = w % NT;
+}
+
+// Producer waves' K loop: stage kt + 1 while the consumers multiply kt.
+// arow(u): element offset (into the activation planes) of DMA instruction u of
+// this lane; row: the thread's weight row.
+template <int FMT, int KROWS>
+__device__ __forceinline__ void wide_produce(const __bf16 *Abase, const uint32_t (&asrc)[8], const uint8_t *row,
+                                            int KT, int pw, int pt, __bf16 (*As0)[128][64],
+                                            __bf16 (*As1)[128][64], __bf16 (*Bs0)[kPfLd],
+                                            __bf16 (*Bs1)[kPfLd]) {
+  auto aload = [&](int kt, __bf16 (*As)[128][64]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int g = 8 * pw + u;
+      dma16(Abase + (asrc[u] + (uint32_t)(kt * kPfBK)), &As[g >> 4][8 * (g & 15)][0]);
+    }
+  };
+  uint32_t B0[WideRaw<FMT>::kDw], B1[WideRaw<FMT>::kDw];
+  aload(0, As0);
+  wide_load<FMT>(row, 0, B0);
+  wide_load<FMT>(row, min(1, KT - 1), B1);
+  wide_dequant<FMT>(B0, row, 0, &Bs0[pt][0]);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // step kt: stage kt + 1 into the other arrays; the raw weights of kt + 1 are
+  // in BO, BS takes those of kt + 2
+#define WIDE_PROD(BS, BO, AN, BN, kt)                          \
+  do {                                                         \
+    if ((kt) + 1 < KT) {                                       \
+      aload((kt) + 1, AN);                                     \
+      wide_load<FMT>(row, min((kt) + 2, KT - 1), BS);          \
+      wide_dequant<FMT>(BO, row, (kt) + 1, &BN[pt][0]);        \
+    }                                                          \
+    __builtin_amdgcn_s_waitcnt(0);                             \
+    __syncthreads();                                           \
+  } while (0)
+  int kt = 0;
+  for (; kt + 2 <= KT; kt += 2) {
+    WIDE_PROD(B0, B1, As1, Bs1, kt);
+    WIDE_PROD(B1, B0, As0, Bs0, kt + 1);
+  }
+  if (kt < KT) WIDE_PROD(B0, B1, As1, Bs1, kt);
+#undef WIDE_PROD
+  (void)KROWS;
+}
+
+// Consumer MFMAs of one K step: wave wv's 32 rows against NQ 16-column subtiles
+// of each of the NB weight groups (gate/up: NB 2 groups of 8; down: 1 of 16).
+template <int NB, int NQ>
+__device__ __forceinline__ void wide_mma(f32x4 (&acc)[NB][2][NQ], __bf16 (*As)[128][64], __bf16 (*Bs)[kPfLd],
+                                         int wv, int lane) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    bf16x8 Ar[2][2];
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int r = 32 * wv + 16 * i + (lane & 15);
+        const int c = (4 * ks + (lane >> 4)) ^ (r & 7);
+        Ar[pl][i] = *reinterpret_cast<const bf16x8 *>(&As[pl][r][8 * c]);
+      }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int c = 32 * ks + 8 * (lane >> 4);
+      bf16x8 bf[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        bf[b] = *reinterpret_cast<const bf16x8 *>(&Bs[128 * b + 16 * q + (lane & 15)][c]);
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[b][i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ar[pl][i], bf[b], acc[b][i][q], 0, 0, 0);
+    }
+  }
+}
+
+// Gate/up (I a multiple of 128): weight rows 0..127 of the tile are W_gate rows
+// n0 .. n0+127, rows 128..255 the same rows of W_up; h = silu(g) u written as bf16
+// hi and lo terms at the pair's grouped row.
+template <int FMT>
+__global__ __launch_bounds__(kPfWideThreads, 1) void pf_gateup_wide_kernel(GmParams a) {
+  __shared__ __align__(16) __bf16 As0[2][128][64], As1[2][128][64];  // [plane][row][k], swizzled
+  __shared__ __align__(16) __bf16 Bs0[256][kPfLd], Bs1[256][kPfLd];
+  int mt, nt, j, m0;
+  wide_tile(a.I / 128, mt, nt);
+  if (!gm_tile(a.X, mt, j, m0)) return;
+  const int n0 = nt * 128;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int KT = a.H / kPfBK;
+  if (wv >= 4) {
+    const int pw = wv - 4, pt = tid - 256;
+    const uint8_t *row = a.X.payload[j] + (pt >= 128 ? a.mat : 0) + (int64_t)(n0 + (pt & 127)) * a.rowb;
+    // DMA instruction g = 8 pw + u: plane g / 16, tile rows 8 (g % 16) .. +7;
+    // element offsets into xb (32 bits, checked at launch)
+    uint32_t asrc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
+      const int m = min(m0 + r, n - 1);
+      const int c = (lane & 7) ^ (lane >> 3);
+      asrc[u] = (uint32_t)p * (uint32_t)(a.T * a.H) + (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)a.H + 8 * c;
+    }
+    wide_produce<FMT, 256>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
+    return;
+  }
+  f32x4 acc[2][2][8];  // [gate, up][i][q]
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[b][i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 <= KT; kt += 2) {
+    wide_mma<2, 8>(acc, As0, Bs0, wv, lane);
+    __syncthreads();
+    wide_mma<2, 8>(acc, As1, Bs1, wv, lane);
+    __syncthreads();
+  }
+  if (kt < KT) {
+    wide_mma<2, 8>(acc, As0, Bs0, wv, lane);
+    __syncthreads();
+  }
+  const int64_t plane = (int64_t)a.pairs * a.I;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+        if (m < n) {
+          const float v = silu_fast(acc[0][i][q][r]) * acc[1][i][q][r];
+          const __bf16 hi = (__bf16)v;
+          const int64_t o = (int64_t)(row0 + m) * a.I + n0 + 16 * q + (lane & 15);
+          a.ab[o] = hi;
+          a.ab[plane + o] = (__bf16)(v - (float)hi);
+        }
+      }
+}
+
+// Down (H a multiple of 256): weight rows are W_down rows n0 .. n0+255; the
+// activation rows are the expert's, contiguous in perm order; P[pair] = w * row.
+template <int FMT>
+__global__ __launch_bounds__(kPfWideThreads, 1) void pf_down_wide_kernel(GmParams a) {
+  __shared__ __align__(16) __bf16 As0[2][128][64], As1[2][128][64];
+  __shared__ __align__(16) __bf16 Bs0[256][kPfLd], Bs1[256][kPfLd];
+  int mt, nt, j, m0;
+  wide_tile(a.H / 256, mt, nt);
+  if (!gm_tile(a.X, mt, j, m0)) return;
+  const int n0 = nt * 256;
+  const int n = a.X.n[j], row0 = a.X.row0[j];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+  const int KT = a.I / kPfBK;
+  if (wv >= 4) {
+    const int pw = wv - 4, pt = tid - 256;
+    const uint8_t *row = a.X.payload[j] + a.down_off + (int64_t)(n0 + pt) * a.rowb;
+    uint32_t asrc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
+      const int m = min(m0 + r, n - 1);
+      const int c = (lane & 7) ^ (lane >> 3);
+      asrc[u] = (uint32_t)p * (uint32_t)(a.pairs * a.I) + (uint32_t)(row0 + m) * (uint32_t)a.I + 8 * c;
+    }
+    wide_produce<FMT, 256>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
+    return;
+  }
+  f32x4 acc[1][2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[0][i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 <= KT; kt += 2) {
+    wide_mma<1, 16>(acc, As0, Bs0, wv, lane);
+    __syncthreads();
+    wide_mma<1, 16>(acc, As1, Bs1, wv, lane);
+    __syncthreads();
+  }
+  if (kt < KT) {
+    wide_mma<1, 16>(acc, As0, Bs0, wv, lane);
+    __syncthreads();
+  }
+  // the lane's 8 output rows: pair ids, then their weights
+  int pair[2][4];
+  float wt[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      pair[i][r] = a.perm[row0 + min(m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r, n - 1)];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wt[i][r] = a.w[pair[i][r]];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + 32 * wv + 16 * i + 4 * (lane >> 4) + r;
+      if (m < n) {
+        float *dst = a.P + (int64_t)pair[i][r] * a.H + n0 + (lane & 15);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) dst[16 * q] = wt[i][r] * acc[0][i][q][r];
+      }
+    }
+}
+
 static int gm_experts(const PfWave &W, PfExperts &X) {
   X.count = W.count;
   int tiles = 0;
@@ -4269,19 +4234,20 @@ static int gm_experts(const PfWave &W, PfExperts &X) {
 }
 
 template <template <int> class K>
-static hipError_t gm_launch(int fmt, dim3 grid, const GmParams &a, hipStream_t s, const Timing &t) {
+static hipError_t gm_launch(int fmt, dim3 grid, const GmParams &a, hipStream_t s, const Timing &t,
+                            int threads = kGmThreads) {
   switch (fmt) {
     case 8:
-      hipExtLaunchKernelGGL(K<8>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      hipExtLaunchKernelGGL(K<8>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     case 2:
-      hipExtLaunchKernelGGL(K<2>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      hipExtLaunchKernelGGL(K<2>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     case 12:
-      hipExtLaunchKernelGGL(K<12>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      hipExtLaunchKernelGGL(K<12>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     case 14:
-      hipExtLaunchKernelGGL(K<14>::fn(), grid, dim3(kGmThreads), 0, s, t.start, t.stop, 0, a);
+      hipExtLaunchKernelGGL(K<14>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     default:
       return hipErrorInvalidValue;
@@ -4295,6 +4261,14 @@ struct GmGateUp {
 template <int F>
 struct GmDown {
   static auto fn() { return gm_down_kernel<F>; }
+};
+template <int F>
+struct WideGateUp {
+  static auto fn() { return pf_gateup_wide_kernel<F>; }
+};
+template <int F>
+struct WideDown {
+  static auto fn() { return pf_down_wide_kernel<F>; }
 };
 
 hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *xb,
@@ -4316,6 +4290,11 @@ hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, con
   if (tiles == 0) return hipSuccess;
   // the kernel indexes the activation planes in 16-byte units with 32 bits
   if (2 * (int64_t)T * H / 8 > (int64_t)UINT32_MAX || I % 64 || H % 64) return hipErrorInvalidValue;
+  if (I % 128 == 0 && 2 * (int64_t)T * H <= (int64_t)UINT32_MAX) {
+    // wide tiles, every format; element offsets into both activation planes fit 32 bits
+    const dim3 g((unsigned)tiles * (unsigned)(I / 128));
+    return gm_launch<WideGateUp>(fmt, g, a, s, t, kPfWideThreads);
+  }
   if (fmt == 8 || fmt == 2) {  // the 32-weight block formats: pf_gateup_kernel (measured faster)
     PfGateUpParams b{};
     b.X = a.X;
@@ -4329,15 +4308,6 @@ hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, con
     b.H = H;
     b.I = I;
     b.k = k;
-    if (I % 128 == 0 && 2 * (int64_t)T * H <= (int64_t)UINT32_MAX) {
-      // wide tiles; element offsets into both activation planes fit 32 bits
-      const dim3 g((unsigned)tl * (unsigned)(I / 128));
-      if (fmt == 8)
-        hipExtLaunchKernelGGL(pf_gateup_wide_kernel<8>, g, dim3(kPfWideThreads), 0, s, t.start, t.stop, 0, b);
-      else
-        hipExtLaunchKernelGGL(pf_gateup_wide_kernel<2>, g, dim3(kPfWideThreads), 0, s, t.start, t.stop, 0, b);
-      return hipGetLastError();
-    }
     if (fmt == 8)
       hipExtLaunchKernelGGL(pf_gateup_kernel<8>, dim3(tl, I / 64), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
     else
@@ -4365,6 +4335,11 @@ hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const
   a.down_off = 2 * fmt_matrix_bytes(fmt_gate_up(qtype), I, H);
   if (tiles == 0) return hipSuccess;
   if (2 * (int64_t)pairs * I / 8 > (int64_t)UINT32_MAX || I % 64 || H % 64) return hipErrorInvalidValue;
+  if (H % 256 == 0 && 2 * (int64_t)pairs * I <= (int64_t)UINT32_MAX) {
+    // wide tiles, every format; element offsets into both activation planes fit 32 bits
+    const dim3 g((unsigned)tiles * (unsigned)(H / 256));
+    return gm_launch<WideDown>(fmt, g, a, s, t, kPfWideThreads);
+  }
   if (fmt == 8 || fmt == 2) {
     PfDownParams b{};
     b.X = a.X;
@@ -4377,15 +4352,6 @@ hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const
     b.pairs = pairs;
     b.H = H;
     b.I = I;
-    if (H % 256 == 0 && 2 * (int64_t)pairs * I <= (int64_t)UINT32_MAX) {
-      // wide tiles; element offsets into both activation planes fit 32 bits
-      const dim3 g((unsigned)tl * (unsigned)(H / 256));
-      if (fmt == 8)
-        hipExtLaunchKernelGGL(pf_down_wide_kernel<8>, g, dim3(kPfWideThreads), 0, s, t.start, t.stop, 0, b);
-      else
-        hipExtLaunchKernelGGL(pf_down_wide_kernel<2>, g, dim3(kPfWideThreads), 0, s, t.start, t.stop, 0, b);
-      return hipGetLastError();
-    }
     if (fmt == 8)
       hipExtLaunchKernelGGL(pf_down_kernel<8>, dim3(tl, (H + 127) / 128), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
     else

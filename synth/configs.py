@@ -106,6 +106,9 @@ A3B_PREFILL = A3B_DECODE.with_(name="a3b_prefill", n_tokens=4096, rho=-1.0, budg
                                cache_percent=35,
                                hidden_seed=5, mode="prefill")
 
+# Prefill of the Q4_K_M A3B stack (Q4_K gate/up, Q6_K down): the K-quant grouped GEMMs.
+A3B_Q4KM_PREFILL = A3B_PREFILL.with_(name="q4km_prefill", qtype="q4_k_m", model_seed=6)
+
 # Speculative verification windows through the A3B stack: 1 + 4 tokens per layer call, each
 # draft accepted with probability 0.75 until the first rejection; 25 % cache (32 slots), the
 # paper's setting for its speculative comparison.  Same weights and hidden-state stream as
@@ -114,4 +117,4 @@ A3B_VERIFY = A3B_DECODE.with_(name="a3b_verify", budget_slots=32, cache_percent=
                               accept_q=0.75, mode="verify")
 
 WORKLOADS = {w.name: w for w in (TINY, A3B_DECODE, A3B_SWEEP, Q4_DECODE, A3B_Q4KM_DECODE, A3B_PREFILL,
-                                 A3B_VERIFY)}
+                                 A3B_Q4KM_PREFILL, A3B_VERIFY)}

@@ -93,7 +93,7 @@ def test_workload_sizes(name):
     wl = synth.WORKLOADS[name]
     expect_p = {"tiny": 104448, "a3b_decode": 5013504, "a3b_sweep": 5013504,
                 "q4_decode": 6690816, "a3b_prefill": 5013504, "a3b_verify": 5013504,
-                "q4km_decode": 3059712}[name]
+                "q4km_decode": 3059712, "q4km_prefill": 3059712}[name]
     assert wl.payload_bytes == expect_p
     assert wl.payload_bytes % 16 == 0
 
