@@ -3949,9 +3949,11 @@ hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, 
 // A producer thread's raw bytes of one K step (64 weights of its row):
 //   Q8_0 / Q4_0: the pair of blocks (17 / 9 dwords);
 //   Q4_K / Q6_K: the four 16-weight quarters as gm_load_raw takes them.
+//   Q6_K: the 64 bytes of ql, 32 of qh, the 4 scales and d that the step's 64
+//     weights use, as aligned dwords around them (see wide_dequant).
 template <int FMT>
 struct WideRaw {
-  static constexpr int kDw = FMT == 8 ? 17 : FMT == 2 ? 9 : 48;
+  static constexpr int kDw = FMT == 8 ? 17 : FMT == 2 ? 9 : FMT == 14 ? 29 : 48;
 };
 template <int FMT>
 __device__ __forceinline__ void wide_load(const uint8_t *row, int kt, uint32_t (&v)[WideRaw<FMT>::kDw]) {
@@ -3959,6 +3961,26 @@ __device__ __forceinline__ void wide_load(const uint8_t *row, int kt, uint32_t (
     const uint32_t *q = reinterpret_cast<const uint32_t *>(row + (int64_t)kt * 2 * Fmt<FMT>::kBlockBytes);
 #pragma unroll
     for (int i = 0; i < WideRaw<FMT>::kDw; ++i) v[i] = q[i];
+  } else if constexpr (FMT == 14) {
+    // step kt: quarter kt % 4 of super-block kt / 4 (210 bytes, 2-byte aligned;
+    // a: its address rounded down to a dword).  Half h = quarter / 2 holds
+    // ql[64 h, +64), qh[32 h, +32), scales[8 h, +8); the quarter's half of them
+    // is sub = quarter % 2.  Loaded: 17 dwords from a + 64 h, 9 from a + 128 + 32 h,
+    // 2 from a + 192 + 8 h + 4 sub, the one at a + 208 (d).  The furthest byte is
+    // a + 211, inside the payload: a payload ends 16-byte aligned, so its last
+    // super-block starts at an address 2 mod 4 and ends at a + 212.
+    const uint8_t *b = row + (int64_t)(kt >> 2) * 210;
+    const uint8_t *a = b - ((uintptr_t)b & 3);
+    const int h = (kt & 3) >> 1, sub = kt & 1;
+    const g_u32 *ql = (const g_u32 *)(a + 64 * h), *qh = (const g_u32 *)(a + 128 + 32 * h);
+#pragma unroll
+    for (int i = 0; i < 17; ++i) v[i] = ql[i];
+#pragma unroll
+    for (int i = 0; i < 9; ++i) v[17 + i] = qh[i];
+    const g_u32 *sc = (const g_u32 *)(a + 192 + 8 * h + 4 * sub);
+    v[26] = sc[0];
+    v[27] = sc[1];
+    v[28] = *(const g_u32 *)(a + 208);
   } else {
 #pragma unroll
     for (int bq = 0; bq < 4; ++bq) {
@@ -3983,6 +4005,36 @@ __device__ __forceinline__ void wide_dequant(const uint32_t (&v)[WideRaw<FMT>::k
     }
     dequant_half<FMT>(h0, 0, dst);
     dequant_half<FMT>(h1, 1, dst + 32);
+  } else if constexpr (FMT == 14) {
+    // Q6_K weight l (< 32) of the half's first group: ql[l] nibble 4 sub, qh[l]
+    // bits 4 sub .. +1, scale 2 sub + l / 16; of the second group (l + 32):
+    // ql[l + 32] nibble 4 sub, qh[l] bits 4 sub + 2 .. +3, scale 2 sub + 2 + l / 16.
+    // Four 6-bit q are assembled per dword (one per byte); each weight is
+    // ds (q - 32) = fma(ds, q, -32 ds) rounded once (32 ds is exact), as the
+    // quarter dequantiser forms it.
+    const int sh = 8 * (int)((uintptr_t)(row + (int64_t)(kt >> 2) * 210) & 3), sub = kt & 1;
+    const uint32_t sc4 = __builtin_amdgcn_alignbyte(v[27], v[26], sh / 8);
+    const float d = half_bits_to_float((v[28] >> sh) & 0xffffu);
+    float ds[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) ds[g] = d * (float)(int8_t)((sc4 >> (8 * g)) & 0xffu);
+    __bf16 o[64];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t hq = __builtin_amdgcn_alignbyte(v[18 + j], v[17 + j], sh / 8);
+#pragma unroll
+      for (int grp = 0; grp < 2; ++grp) {
+        const uint32_t lq = __builtin_amdgcn_alignbyte(v[8 * grp + j + 1], v[8 * grp + j], sh / 8);
+        const uint32_t q4 = ((lq >> (4 * sub)) & 0x0f0f0f0fu) | (((hq >> (4 * sub + 2 * grp)) & 0x03030303u) << 4);
+        const float dsg = ds[2 * grp + (j >> 2)];
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          o[32 * grp + 4 * j + b] = (__bf16)fmaf(dsg, (float)((q4 >> (8 * b)) & 0xffu), -32.f * dsg);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      *reinterpret_cast<uint4 *>(dst + 8 * i) = *reinterpret_cast<const uint4 *>(o + 8 * i);
   } else {
 #pragma unroll
     for (int bq = 0; bq < 4; ++bq) {
@@ -4003,9 +4055,9 @@ __device__ __forceinline__ void wide_tile(int NT, int &mt, int &nt) {
 }
 
 // Producer waves' K loop: stage kt + 1 while the consumers multiply kt.
-// arow(u): element offset (into the activation planes) of DMA instruction u of
-// this lane; row: the thread's weight row.
-template <int FMT, int KROWS>
+// asrc[u]: element offset (into the activation planes) of this lane's 16 bytes
+// in DMA instruction u; row: the thread's weight row.
+template <int FMT>
 __device__ __forceinline__ void wide_produce(const __bf16 *Abase, const uint32_t (&asrc)[8], const uint8_t *row,
                                             int KT, int pw, int pt, __bf16 (*As0)[128][64],
                                             __bf16 (*As1)[128][64], __bf16 (*Bs0)[kPfLd],
@@ -4043,7 +4095,6 @@ __device__ __forceinline__ void wide_produce(const __bf16 *Abase, const uint32_t
   }
   if (kt < KT) WIDE_PROD(B0, B1, As1, Bs1, kt);
 #undef WIDE_PROD
-  (void)KROWS;
 }
 
 // Consumer MFMAs of one K step: wave wv's 32 rows against NQ 16-column subtiles
@@ -4107,7 +4158,7 @@ __global__ __launch_bounds__(kPfWideThreads, 1) void pf_gateup_wide_kernel(GmPar
       const int c = (lane & 7) ^ (lane >> 3);
       asrc[u] = (uint32_t)p * (uint32_t)(a.T * a.H) + (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)a.H + 8 * c;
     }
-    wide_produce<FMT, 256>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
+    wide_produce<FMT>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
     return;
   }
   f32x4 acc[2][2][8];  // [gate, up][i][q]
@@ -4171,7 +4222,7 @@ __global__ __launch_bounds__(kPfWideThreads, 1) void pf_down_wide_kernel(GmParam
       const int c = (lane & 7) ^ (lane >> 3);
       asrc[u] = (uint32_t)p * (uint32_t)(a.pairs * a.I) + (uint32_t)(row0 + m) * (uint32_t)a.I + 8 * c;
     }
-    wide_produce<FMT, 256>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
+    wide_produce<FMT>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
     return;
   }
   f32x4 acc[1][2][16];
