@@ -105,7 +105,8 @@ def test_q4_0_tiny():
 
 @pytest.mark.parametrize("shape", [(64, 64, 1, 1, 1), (320, 192, 5, 3, 3), (1024, 384, 40, 6, 9),
                                    (768, 1408, 256, 8, 40), (2816, 704, 64, 16, 17),
-                                   (8192, 64, 3, 2, 2), (128, 8192, 4, 1, 1)])
+                                   (8192, 64, 3, 2, 2), (128, 8192, 4, 1, 1),
+                                   (1024, 768, 256, 16, 20)])  # E, top_k, top_k * inter at the limits
 def test_other_shapes(shape):
     H, I, E, k, C = shape
     for qt in ("q8_0", "q4_0"):

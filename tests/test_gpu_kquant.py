@@ -35,7 +35,7 @@ def test_kquant_decode_copy_modes(qtype):
 
 @pytest.mark.parametrize("shape", [(256, 256, 8, 2, 2), (2048, 768, 32, 8, 9), (1024, 512, 64, 6, 7),
                                    (768, 1280, 16, 8, 8), (4096, 256, 16, 16, 16),
-                                   (256, 3072, 4, 4, 4)])
+                                   (256, 3072, 4, 4, 4), (1024, 768, 256, 16, 20)])
 @pytest.mark.parametrize("qtype", ["q4_k_m", "q4_k", "q6_k"])
 def test_kquant_decode_shapes(qtype, shape):
     H, I, E, k, C = shape
