@@ -137,7 +137,13 @@ __device__ __forceinline__ float octet_digits(float4 v, uint32_t (&dw)[3]) {
   return s;
 }
 
+// Dot product of four signed byte pairs plus c.  Where c is a known zero (the
+// first term of a chain) the saturating form is used: it takes the zero as an
+// inline constant, while the accumulating form the compiler picks otherwise
+// needs the zero moved into its destination register first.  Four products
+// of bytes stay far inside int32, so the saturation never acts.
 __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  if (__builtin_constant_p(c) && c == 0) return __builtin_amdgcn_sdot4((int)a, (int)b, 0, true);
   return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
@@ -1136,6 +1142,14 @@ __device__ __forceinline__ float recombine(int i1, int i2, int i3) {
   return fmaf((float)i3, 1.f / 64516.f, fmaf((float)i2, 1.f / 254.f, (float)i1));
 }
 
+// Four Q4_0 nibbles of a dword as signed bytes 16 (n - 8): bit 3 of the nibble
+// flipped makes it the 4-bit two's complement of n - 8, and at the top of its
+// byte (the other nibble cleared) the byte is 16 (n - 8).  q4_lo takes the low
+// nibble of each byte, q4_hi the high one; the flip of bit 7 after the shift
+// is the flip of bit 3 before it.
+__device__ __forceinline__ uint32_t q4_lo(uint32_t w) { return ((w << 4) & 0xf0f0f0f0u) ^ 0x80808080u; }
+__device__ __forceinline__ uint32_t q4_hi(uint32_t w) { return (w & 0xf0f0f0f0u) ^ 0x80808080u; }
+
 // Partial dot of one pair with the inputs: D[c][j] = digit plane c, dword j of
 // the pair's 64 inputs; sc0/sc1 the two input block scales.
 template <int QT>
@@ -1174,16 +1188,16 @@ __device__ __forceinline__ float pair_dot(const uint32_t (&wd)[Fmt<QT>::kPairDwo
     int a1 = 0, a2 = 0, a3 = 0, b1 = 0, b2 = 0, b3 = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2) ^ 0x88888888u;
-      const uint32_t lo = (v << 4) & 0xf0f0f0f0u, hi = v & 0xf0f0f0f0u;
+      const uint32_t v = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2);
+      const uint32_t lo = q4_lo(v), hi = q4_hi(v);
       a1 = sdot4(hi, D[4 + j], sdot4(lo, D[j], a1));
       a2 = sdot4(hi, D[20 + j], sdot4(lo, D[16 + j], a2));
       a3 = sdot4(hi, D[36 + j], sdot4(lo, D[32 + j], a3));
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v = wd[5 + j] ^ 0x88888888u;
-      const uint32_t lo = (v << 4) & 0xf0f0f0f0u, hi = v & 0xf0f0f0f0u;
+      const uint32_t v = wd[5 + j];
+      const uint32_t lo = q4_lo(v), hi = q4_hi(v);
       b1 = sdot4(hi, D[12 + j], sdot4(lo, D[8 + j], b1));
       b2 = sdot4(hi, D[28 + j], sdot4(lo, D[24 + j], b2));
       b3 = sdot4(hi, D[44 + j], sdot4(lo, D[40 + j], b3));
@@ -1223,10 +1237,8 @@ __device__ __forceinline__ float pair_dot16(const uint32_t (&wd)[Fmt<QT>::kPairD
     d1 = half_bits_to_float(wd[4] >> 16);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t v0 = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2) ^ 0x88888888u;
-      const uint32_t v1 = wd[5 + j] ^ 0x88888888u;
-      const uint32_t lo0 = (v0 << 4) & 0xf0f0f0f0u, hi0 = v0 & 0xf0f0f0f0u;
-      const uint32_t lo1 = (v1 << 4) & 0xf0f0f0f0u, hi1 = v1 & 0xf0f0f0f0u;
+      const uint32_t v0 = __builtin_amdgcn_alignbyte(wd[j + 1], wd[j], 2), v1 = wd[5 + j];
+      const uint32_t lo0 = q4_lo(v0), hi0 = q4_hi(v0), lo1 = q4_lo(v1), hi1 = q4_hi(v1);
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         A[0][c] = sdot4(lo0, D[16 * c + j], A[0][c]);
@@ -4284,15 +4296,19 @@ static int gm_experts(const PfWave &W, PfExperts &X) {
   return tiles;
 }
 
-template <template <int> class K>
+// kAll: a kernel for every format; otherwise for the K-quant formats only (the
+// 32-weight formats' 256-thread grouped GEMMs are pf_gateup_kernel / pf_down_kernel).
+template <template <int> class K, bool kAll = true>
 static hipError_t gm_launch(int fmt, dim3 grid, const GmParams &a, hipStream_t s, const Timing &t,
                             int threads = kGmThreads) {
   switch (fmt) {
     case 8:
-      hipExtLaunchKernelGGL(K<8>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
+      if constexpr (!kAll) return hipErrorInvalidValue;
+      else hipExtLaunchKernelGGL(K<8>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     case 2:
-      hipExtLaunchKernelGGL(K<2>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
+      if constexpr (!kAll) return hipErrorInvalidValue;
+      else hipExtLaunchKernelGGL(K<2>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
       break;
     case 12:
       hipExtLaunchKernelGGL(K<12>::fn(), grid, dim3(threads), 0, s, t.start, t.stop, 0, a);
@@ -4365,7 +4381,7 @@ hipError_t launch_pf_gateup(int qtype, const PfWave &W, const int32_t *perm, con
       hipExtLaunchKernelGGL(pf_gateup_kernel<2>, dim3(tl, I / 64), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
     return hipGetLastError();
   }
-  return gm_launch<GmGateUp>(fmt, dim3(tiles, I / 64), a, s, t);
+  return gm_launch<GmGateUp, false>(fmt, dim3(tiles, I / 64), a, s, t);
 }
 
 hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const __bf16 *ab,
@@ -4409,7 +4425,7 @@ hipError_t launch_pf_down(int qtype, const PfWave &W, const int32_t *perm, const
       hipExtLaunchKernelGGL(pf_down_kernel<2>, dim3(tl, (H + 127) / 128), dim3(kThreads), 0, s, t.start, t.stop, 0, b);
     return hipGetLastError();
   }
-  return gm_launch<GmDown>(fmt, dim3(tiles, (H + 127) / 128), a, s, t);
+  return gm_launch<GmDown, false>(fmt, dim3(tiles, (H + 127) / 128), a, s, t);
 }
 
 hipError_t launch_pf_combine(const float *P, const float *x, float *y, int T, int H, int k,
