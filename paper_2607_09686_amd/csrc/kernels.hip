@@ -3965,8 +3965,30 @@ hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, 
 //     weights use, as aligned dwords around them (see wide_dequant).
 template <int FMT>
 struct WideRaw {
-  static constexpr int kDw = FMT == 8 ? 17 : FMT == 2 ? 9 : FMT == 14 ? 29 : 48;
+  static constexpr int kDw = FMT == 8 ? 17 : FMT == 2 ? 9 : FMT == 14 ? 19 : 48;
 };
+
+// K order of the wide kernels' steps.  A step multiplies 64 inputs; the sum
+// over K does not depend on the order in which they are visited, so a format
+// may visit them in the order its bytes hold them, as long as the activation
+// tile and the weight tile use the same one.  Step kt, 16-byte chunk c of the
+// step (eight inputs) covers K indices wide_kbase(kt) + wide_kchunk(c) + 0..7.
+// Q6_K: a step is one quarter (n, j) of a super-block, n = the half (128
+// weights), j = which 16 of each of its four 32-weight groups: the weights
+// 128 n + 32 g + 16 j + l (g < 4, l < 16), whose low bits sit in 16 bytes of
+// ql for g = 0, 2 (low and high nibbles), 16 bytes for g = 1, 3, and whose high
+// bits sit in 16 bytes of qh (two bits per group).  So every loaded byte is
+// used, once.  Tile position 16 g + l holds weight 128 n + 32 g + 16 j + l.
+template <int FMT>
+__device__ __forceinline__ uint32_t wide_kbase(int kt) {
+  if constexpr (FMT == 14) return 256u * (uint32_t)(kt >> 2) + 128u * (uint32_t)((kt >> 1) & 1) + 16u * (uint32_t)(kt & 1);
+  return (uint32_t)(kt * kPfBK);
+}
+template <int FMT>
+__device__ __forceinline__ uint32_t wide_kchunk(int c) {
+  if constexpr (FMT == 14) return 32u * (uint32_t)(c >> 1) + 8u * (uint32_t)(c & 1);
+  return 8u * (uint32_t)c;
+}
 template <int FMT>
 __device__ __forceinline__ void wide_load(const uint8_t *row, int kt, uint32_t (&v)[WideRaw<FMT>::kDw]) {
   if constexpr (FMT == 8 || FMT == 2) {
@@ -3974,25 +3996,33 @@ __device__ __forceinline__ void wide_load(const uint8_t *row, int kt, uint32_t (
 #pragma unroll
     for (int i = 0; i < WideRaw<FMT>::kDw; ++i) v[i] = q[i];
   } else if constexpr (FMT == 14) {
-    // step kt: quarter kt % 4 of super-block kt / 4 (210 bytes, 2-byte aligned;
-    // a: its address rounded down to a dword).  Half h = quarter / 2 holds
-    // ql[64 h, +64), qh[32 h, +32), scales[8 h, +8); the quarter's half of them
-    // is sub = quarter % 2.  Loaded: 17 dwords from a + 64 h, 9 from a + 128 + 32 h,
-    // 2 from a + 192 + 8 h + 4 sub, the one at a + 208 (d).  The furthest byte is
-    // a + 211, inside the payload: a payload ends 16-byte aligned, so its last
-    // super-block starts at an address 2 mod 4 and ends at a + 212.
+    // step kt: quarter (n, j) = ((kt / 2) % 2, kt % 2) of super-block kt / 4
+    // (210 bytes, 2-byte aligned; a: its address rounded down to a dword).  Its
+    // bytes: ql[64 n + 16 j, +16), ql[64 n + 32 + 16 j, +16), qh[32 n + 16 j, +16),
+    // scales 8 n + j + 2 g, d.  Loaded: five dwords from each of a + 64 n + 16 j,
+    // a + 64 n + 32 + 16 j and a + 128 + 32 n + 16 j (16 bytes plus the 2 of a
+    // misaligned start), three from a + 192 + 8 n, the one at a + 208 (d).  The
+    // furthest byte is a + 211, inside the payload: a payload ends 16-byte
+    // aligned, so its last super-block starts at an address 2 mod 4 and ends at
+    // a + 212.
     const uint8_t *b = row + (int64_t)(kt >> 2) * 210;
     const uint8_t *a = b - ((uintptr_t)b & 3);
-    const int h = (kt & 3) >> 1, sub = kt & 1;
-    const g_u32 *ql = (const g_u32 *)(a + 64 * h), *qh = (const g_u32 *)(a + 128 + 32 * h);
+    const int n = (kt >> 1) & 1, j = kt & 1;
+    const uint8_t *run[3] = {a + 64 * n + 16 * j, a + 64 * n + 32 + 16 * j, a + 128 + 32 * n + 16 * j};
 #pragma unroll
-    for (int i = 0; i < 17; ++i) v[i] = ql[i];
-#pragma unroll
-    for (int i = 0; i < 9; ++i) v[17 + i] = qh[i];
-    const g_u32 *sc = (const g_u32 *)(a + 192 + 8 * h + 4 * sub);
-    v[26] = sc[0];
-    v[27] = sc[1];
-    v[28] = *(const g_u32 *)(a + 208);
+    for (int r = 0; r < 3; ++r) {
+      const u32x4 q = *(g_u32x4_a4 *)run[r];
+      v[5 * r] = q.x;
+      v[5 * r + 1] = q.y;
+      v[5 * r + 2] = q.z;
+      v[5 * r + 3] = q.w;
+      v[5 * r + 4] = ((const g_u32 *)run[r])[4];
+    }
+    const g_u32 *sc = (const g_u32 *)(a + 192 + 8 * n);
+    v[15] = sc[0];
+    v[16] = sc[1];
+    v[17] = sc[2];
+    v[18] = *(const g_u32 *)(a + 208);
   } else {
 #pragma unroll
     for (int bq = 0; bq < 4; ++bq) {
@@ -4018,31 +4048,34 @@ __device__ __forceinline__ void wide_dequant(const uint32_t (&v)[WideRaw<FMT>::k
     dequant_half<FMT>(h0, 0, dst);
     dequant_half<FMT>(h1, 1, dst + 32);
   } else if constexpr (FMT == 14) {
-    // Q6_K weight l (< 32) of the half's first group: ql[l] nibble 4 sub, qh[l]
-    // bits 4 sub .. +1, scale 2 sub + l / 16; of the second group (l + 32):
-    // ql[l + 32] nibble 4 sub, qh[l] bits 4 sub + 2 .. +3, scale 2 sub + 2 + l / 16.
+    // Q6_K weight 128 n + 32 g + 16 j + l of the step (tile position 16 g + l):
+    // low four bits from ql run g % 2 (low nibbles for g < 2, high for g >= 2),
+    // high two bits from bits 2 g, 2 g + 1 of qh byte l, scale 8 n + 2 g + j.
     // Four 6-bit q are assembled per dword (one per byte); each weight is
     // ds (q - 32) = fma(ds, q, -32 ds) rounded once (32 ds is exact), as the
     // quarter dequantiser forms it.
-    const int sh = 8 * (int)((uintptr_t)(row + (int64_t)(kt >> 2) * 210) & 3), sub = kt & 1;
-    const uint32_t sc4 = __builtin_amdgcn_alignbyte(v[27], v[26], sh / 8);
-    const float d = half_bits_to_float((v[28] >> sh) & 0xffffu);
+    const int sh = (int)((uintptr_t)(row + (int64_t)(kt >> 2) * 210) & 3), j = kt & 1;
+    const uint64_t sc8 = (uint64_t)__builtin_amdgcn_alignbyte(v[17], v[16], sh) << 32 |
+                         __builtin_amdgcn_alignbyte(v[16], v[15], sh);
+    const float d = half_bits_to_float((v[18] >> (8 * sh)) & 0xffffu);
     float ds[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) ds[g] = d * (float)(int8_t)((sc4 >> (8 * g)) & 0xffu);
+    for (int g = 0; g < 4; ++g) ds[g] = d * (float)(int8_t)((sc8 >> (8 * (2 * g + j))) & 0xffu);
     __bf16 o[64];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t hq = __builtin_amdgcn_alignbyte(v[18 + j], v[17 + j], sh / 8);
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t lA = __builtin_amdgcn_alignbyte(v[i + 1], v[i], sh);
+      const uint32_t lB = __builtin_amdgcn_alignbyte(v[6 + i], v[5 + i], sh);
+      const uint32_t hq = __builtin_amdgcn_alignbyte(v[11 + i], v[10 + i], sh);
+      const uint32_t q[4] = {(lA & 0x0f0f0f0fu) | ((hq << 4) & 0x30303030u),
+                             (lB & 0x0f0f0f0fu) | ((hq << 2) & 0x30303030u),
+                             ((lA >> 4) & 0x0f0f0f0fu) | (hq & 0x30303030u),
+                             ((lB >> 4) & 0x0f0f0f0fu) | ((hq >> 2) & 0x30303030u)};
 #pragma unroll
-      for (int grp = 0; grp < 2; ++grp) {
-        const uint32_t lq = __builtin_amdgcn_alignbyte(v[8 * grp + j + 1], v[8 * grp + j], sh / 8);
-        const uint32_t q4 = ((lq >> (4 * sub)) & 0x0f0f0f0fu) | (((hq >> (4 * sub + 2 * grp)) & 0x03030303u) << 4);
-        const float dsg = ds[2 * grp + (j >> 2)];
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
-          o[32 * grp + 4 * j + b] = (__bf16)fmaf(dsg, (float)((q4 >> (8 * b)) & 0xffu), -32.f * dsg);
-      }
+          o[16 * g + 4 * i + b] = (__bf16)fmaf(ds[g], (float)((q[g] >> (8 * b)) & 0xffu), -32.f * ds[g]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -4078,7 +4111,7 @@ __device__ __forceinline__ void wide_produce(const __bf16 *Abase, const uint32_t
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int g = 8 * pw + u;
-      dma16(Abase + (asrc[u] + (uint32_t)(kt * kPfBK)), &As[g >> 4][8 * (g & 15)][0]);
+      dma16(Abase + (asrc[u] + wide_kbase<FMT>(kt)), &As[g >> 4][8 * (g & 15)][0]);
     }
   };
   uint32_t B0[WideRaw<FMT>::kDw], B1[WideRaw<FMT>::kDw];
@@ -4168,7 +4201,8 @@ __global__ __launch_bounds__(kPfWideThreads, 1) void pf_gateup_wide_kernel(GmPar
       const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
       const int m = min(m0 + r, n - 1);
       const int c = (lane & 7) ^ (lane >> 3);
-      asrc[u] = (uint32_t)p * (uint32_t)(a.T * a.H) + (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)a.H + 8 * c;
+      asrc[u] = (uint32_t)p * (uint32_t)(a.T * a.H) + (uint32_t)(a.perm[row0 + m] / a.k) * (uint32_t)a.H +
+                wide_kchunk<FMT>(c);
     }
     wide_produce<FMT>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
     return;
@@ -4232,7 +4266,8 @@ __global__ __launch_bounds__(kPfWideThreads, 1) void pf_down_wide_kernel(GmParam
       const int g = 8 * pw + u, p = g >> 4, r = 8 * (g & 15) + (lane >> 3);
       const int m = min(m0 + r, n - 1);
       const int c = (lane & 7) ^ (lane >> 3);
-      asrc[u] = (uint32_t)p * (uint32_t)(a.pairs * a.I) + (uint32_t)(row0 + m) * (uint32_t)a.I + 8 * c;
+      asrc[u] = (uint32_t)p * (uint32_t)(a.pairs * a.I) + (uint32_t)(row0 + m) * (uint32_t)a.I +
+                wide_kchunk<FMT>(c);
     }
     wide_produce<FMT>(a.A, asrc, row, KT, pw, pt, As0, As1, Bs0, Bs1);
     return;
