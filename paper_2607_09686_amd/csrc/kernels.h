@@ -158,8 +158,9 @@ hipError_t launch_token_digits(const float *x, int T, int H, bool prenorm, int8_
 // Prefill.  inv[t] = 1/rms (or 1) and xb [2][T][H] = x * inv as bf16 hi and lo terms.
 hipError_t launch_prefill_prep(const float *x, int T, int H, bool prenorm, float *inv, __bf16 *xb,
                                hipStream_t s);
-// Stable grouping of the T*k (token, expert) pairs by expert: counts [E],
-// offsets [E+1], perm [T*k] (pair ids t*k + j).
+// Stable grouping of the T*k (token, expert) pairs by expert: counts (scratch of
+// group_counts_ints(E) ints), offsets [E+1], perm [T*k] (pair ids t*k + j).
+int group_counts_ints(int E);
 hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, int32_t *offsets,
                         int32_t *perm, hipStream_t s);
 // The experts of one wave (count <= pf_max_experts()).

@@ -2680,41 +2680,28 @@ __global__ __launch_bounds__(kThreads) void prefill_prep_kernel(const float *__r
   }
 }
 
-// Grouping of the (token, rank) pairs by expert (a stable counting sort).
-// The pair ids are read as 16-byte groups of four; npairs % 4 trailing pairs
-// are read one by one.  Loads are unconditional at clamped, valid addresses
-// and selected afterwards (a guarded load becomes a branch with its own wait).
-constexpr int kGroupBatch = 32;  // 16-byte loads in flight per thread
+// Grouping of the (token, rank) pairs by expert (a stable counting sort) in two
+// launches over chunks of the pair list: group_hist_kernel counts each chunk's
+// pairs per expert, group_place_kernel gives every pair its place.  The pairs
+// of expert e are perm[offsets[e] .. offsets[e+1]) in pair order: those of
+// earlier chunks first, and inside a chunk by rank (earlier rounds of 256
+// pairs, earlier waves of the round, earlier lanes of the wave).
+constexpr int kGroupChunks = 512;  // most chunks per call (rows of the count table)
 
-// counts[e] = number of pairs routed to e; block e scans every pair, its
-// threads taking the 16-byte groups tid, tid + 256, ...
-__global__ __launch_bounds__(kThreads) void group_count_kernel(const int32_t *__restrict__ idx,
-                                                               int npairs,
-                                                               int32_t *__restrict__ counts) {
-  __shared__ int wsum[kThreads / kWave];
-  const int e = blockIdx.x, tid = threadIdx.x;
-  const int n4 = npairs / 4;
-  const int4 *v4 = reinterpret_cast<const int4 *>(idx);
-  int c = 0;
-  for (int base = 0; base < n4; base += kThreads * kGroupBatch) {
-    int4 q[kGroupBatch];
-#pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(base + tid + m * kThreads, n4 - 1)];
-#pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m)
-      if (base + tid + m * kThreads < n4)
-        c += (q[m].x == e) + (q[m].y == e) + (q[m].z == e) + (q[m].w == e);
-  }
-  if (tid < npairs - 4 * n4) c += idx[4 * n4 + tid] == e;
-#pragma unroll
-  for (int off = kWave / 2; off >= 1; off >>= 1) c += __shfl_xor(c, off, kWave);
-  if ((tid & (kWave - 1)) == 0) wsum[tid / kWave] = c;
+// counts[c][e] = pairs of chunk c (pairs c*chunk .. +chunk) routed to e.
+__global__ __launch_bounds__(kThreads) void group_hist_kernel(const int32_t *__restrict__ idx, int npairs,
+                                                              int E, int chunk, int32_t *__restrict__ counts) {
+  __shared__ int h[kThreads];  // E <= 256
+  if ((int)threadIdx.x < E) h[threadIdx.x] = 0;
   __syncthreads();
-  if (tid == 0) {
-    int tot = 0;
-    for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
-    counts[e] = tot;
-  }
+  const int p0 = blockIdx.x * chunk, p1 = min(npairs, p0 + chunk);
+#pragma unroll 4
+  for (int p = p0 + (int)threadIdx.x; p < p1; p += kThreads) {
+    const int e = idx[p];
+    if ((unsigned)e < (unsigned)E) atomicAdd(&h[e], 1);  // an invalid id is left out (the host
+  }                                                       // then sees offsets[E] != npairs)
+  __syncthreads();
+  if ((int)threadIdx.x < E) counts[(int64_t)blockIdx.x * E + threadIdx.x] = h[threadIdx.x];
 }
 
 // Exclusive prefix sum of v over the block's threads (all threads call it).
@@ -2738,71 +2725,77 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *wsum, int &total
   return before + inc - v;
 }
 
-// perm[offsets[e] + r] = the r-th pair (in pair order) routed to e;
-// offsets[e] = sum of counts below e, offsets[E] = npairs (block E-1 writes
-// it).  Thread tid takes a contiguous run of 16-byte groups (the trailing
-// pairs go to the last thread), so one block-wide scan of the threads' hit
-// counts orders the pairs: a first pass counts, a second writes.
-__global__ __launch_bounds__(kThreads) void group_scatter_kernel(const int32_t *__restrict__ idx,
-                                                                 int npairs, int E,
-                                                                 const int32_t *__restrict__ counts,
-                                                                 int32_t *__restrict__ offsets,
-                                                                 int32_t *__restrict__ perm) {
-  __shared__ int wsum[kThreads / kWave];
-  __shared__ int wsum2[kThreads / kWave];
-  const int e = blockIdx.x, tid = threadIdx.x;
-  // offset of e: the counts of the experts below it (E <= 256)
-  int total = 0;
-  const int below = block_exclusive_scan(tid < E ? counts[tid] : 0, wsum, total);
-  __shared__ int off_s;
-  if (tid == e) off_s = below;
-  __syncthreads();
-  const int off = off_s;
-  if (tid == 0) {
-    offsets[e] = off;
-    if (e == E - 1) offsets[E] = total;
-  }
-  const int n4 = npairs / 4, tail = npairs - 4 * n4;
-  const int seg = (n4 + kThreads - 1) / kThreads;  // 16-byte groups per thread
-  const int g0 = min(n4, tid * seg), g1 = min(n4, g0 + seg);
-  const int4 *v4 = reinterpret_cast<const int4 *>(idx);
-  auto hits4 = [&](const int4 &q) {
-    return (q.x == e) + (q.y == e) + (q.z == e) + (q.w == e);
-  };
-  int c = 0;
-  for (int g = g0; g < g1; g += kGroupBatch) {
-    int4 q[kGroupBatch];
+// Block c: the first place of its pairs of each expert (offsets[e] plus the
+// pairs of e in earlier chunks), then its pairs round by round: a pair's rank
+// among the round's pairs of its expert is the count in earlier waves plus the
+// lanes before it in its wave with the same expert (eight ballots on the id's
+// bits).  Block 0 also writes offsets [E + 1].
+__global__ __launch_bounds__(kThreads) void group_place_kernel(const int32_t *__restrict__ idx, int npairs,
+                                                               int E, int chunk, int nchunks,
+                                                               const int32_t *__restrict__ counts,
+                                                               int32_t *__restrict__ offsets,
+                                                               int32_t *__restrict__ perm) {
+  constexpr int NW = kThreads / kWave;
+  __shared__ int base[kThreads];
+  __shared__ int wc[NW][kThreads];  // pairs of each expert in each wave of the round
+  __shared__ int wsum[NW];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave, c = blockIdx.x;
+  int tot = 0, before = 0;
+  if (tid < E)
+    for (int q0 = 0; q0 < nchunks; q0 += 16) {  // 16 loads in flight
+      int v[16];
 #pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(g + m, max(n4 - 1, 0))];
+      for (int u = 0; u < 16; ++u) v[u] = counts[(int64_t)min(q0 + u, nchunks - 1) * E + tid];
 #pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m)
-      if (g + m < g1) c += hits4(q[m]);
-  }
-  const bool last = tid == kThreads - 1;
-  if (last)
-    for (int i = 4 * n4; i < npairs; ++i) c += idx[i] == e;
-  int dummy = 0;
-  int pos = off + block_exclusive_scan(c, wsum2, dummy);
-  if (c == 0) return;  // (no barrier follows)
-  for (int g = g0; g < g1; g += kGroupBatch) {
-    int4 q[kGroupBatch];
-#pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m) q[m] = v4[min(g + m, max(n4 - 1, 0))];
-#pragma unroll
-    for (int m = 0; m < kGroupBatch; ++m) {
-      if (g + m < g1) {
-        const int i = 4 * (g + m);
-        if (q[m].x == e) perm[pos++] = i;
-        if (q[m].y == e) perm[pos++] = i + 1;
-        if (q[m].z == e) perm[pos++] = i + 2;
-        if (q[m].w == e) perm[pos++] = i + 3;
+      for (int u = 0; u < 16; ++u) {
+        const int q = q0 + u;
+        tot += q < nchunks ? v[u] : 0;
+        before += q < c ? v[u] : 0;
       }
     }
+  int total = 0;
+  const int first = block_exclusive_scan(tid < E ? tot : 0, wsum, total);
+  if (tid < E) {
+    base[tid] = first + before;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) wc[w][tid] = 0;
+    if (c == 0) offsets[tid] = first;
   }
-  if (last)
-    for (int i = 4 * n4; i < npairs; ++i)
-      if (idx[i] == e) perm[pos++] = i;
-  (void)tail;
+  if (c == 0 && tid == 0) offsets[E] = total;
+  __syncthreads();
+  const int p0 = c * chunk, p1 = min(npairs, p0 + chunk);
+  for (int r0 = p0; r0 < p1; r0 += kThreads) {  // uniform
+    const int p = r0 + tid;
+    const int ep = idx[min(p, p1 - 1)];
+    const bool ok = p < p1 && (unsigned)ep < (unsigned)E;
+    const int e = ok ? ep : 0;
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (e >> b) & 1;
+      const uint64_t m = __ballot(ok && bit);
+      peers &= bit ? m : ~m;
+    }
+    const uint64_t below = peers & ((1ull << lane) - 1ull);
+    if (ok && below == 0) wc[wv][e] = __popcll(peers);
+    __syncthreads();
+    if (ok) {
+      int pos = base[e] + __popcll(below);
+      for (int w = 0; w < wv; ++w) pos += wc[w][e];
+      perm[pos] = p;
+    }
+    __syncthreads();
+    if (tid < E) {
+      int add = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        add += wc[w][tid];
+        wc[w][tid] = 0;
+      }
+      base[tid] += add;
+    }
+    __syncthreads();
+  }
 }
 
 // One wave's experts for the grouped GEMMs (kernel argument, about 3 KB).
@@ -3932,13 +3925,20 @@ hipError_t launch_prefill_prep(const float *x, int T, int H, bool prenorm, float
   return hipGetLastError();
 }
 
+int group_counts_ints(int E) { return kGroupChunks * E; }
+
 hipError_t launch_group(const int32_t *idx, int npairs, int E, int32_t *counts, int32_t *offsets,
                         int32_t *perm, hipStream_t s) {
-  hipLaunchKernelGGL(group_count_kernel, dim3(E), dim3(kThreads), 0, s, idx, npairs, counts);
+  if (npairs < 1 || E < 1 || E > kThreads) return hipErrorInvalidValue;
+  // chunks of a multiple of 256 pairs, at least 1024 and at most kGroupChunks of them
+  const int per = std::max(1024, (npairs + kGroupChunks - 1) / kGroupChunks);
+  const int chunk = (per + kThreads - 1) / kThreads * kThreads;
+  const int nchunks = (npairs + chunk - 1) / chunk;
+  hipLaunchKernelGGL(group_hist_kernel, dim3(nchunks), dim3(kThreads), 0, s, idx, npairs, E, chunk, counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_scatter_kernel, dim3(E), dim3(kThreads), 0, s, idx, npairs, E, counts,
-                     offsets, perm);
+  hipLaunchKernelGGL(group_place_kernel, dim3(nchunks), dim3(kThreads), 0, s, idx, npairs, E, chunk, nchunks,
+                     counts, offsets, perm);
   return hipGetLastError();
 }
 

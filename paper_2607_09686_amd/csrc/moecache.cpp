@@ -92,7 +92,7 @@ struct moe_cache {
   int64_t pf_cap = 0;
   float *pf_inv = nullptr;      // [T]
   __bf16 *pf_xb = nullptr;      // [2][T][H] (hi, lo)
-  int32_t *pf_counts = nullptr; // [E]
+  int32_t *pf_counts = nullptr; // grouping scratch, group_counts_ints(E)
   int32_t *pf_off = nullptr;    // [E+1]
   int32_t *pf_perm = nullptr;   // [T*k]
   __bf16 *pf_ab = nullptr;      // [2][T*k][I] (hi, lo)
@@ -1374,7 +1374,7 @@ int ensure_prefill(moe_cache *c, int64_t T) {
   const int64_t H = c->d.hidden, I = c->d.inter, E = c->d.n_experts, k = c->d.top_k;
   if (hipMalloc(&c->pf_inv, T * sizeof(float)) != hipSuccess ||
       hipMalloc(&c->pf_xb, 2 * T * H * sizeof(__bf16)) != hipSuccess ||
-      hipMalloc(&c->pf_counts, E * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&c->pf_counts, group_counts_ints((int)E) * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->pf_off, (E + 1) * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->pf_perm, T * k * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&c->pf_ab, 2 * T * k * I * sizeof(__bf16)) != hipSuccess ||
