@@ -952,19 +952,20 @@ __global__ __launch_bounds__(kThreads) void router_finish_mt_kernel(
 // Partial logits zp[s][T][E] = x[T][rows of slice s] W_r[rows of slice s][E]
 // on the fp32 matrix cores (v_mfma_f32_16x16x4_f32, fp32 products and sums):
 // a block owns 64 tokens, 128 expert columns (blockIdx.y) and one of `slices`
-// slices of H (blockIdx.z); wave w owns tokens 32 (w & 1) .. +31 (two 16-row
-// subtiles) and experts 64 (w >> 1) .. +63 (four 16-column subtiles).  K runs
+// slices of H (blockIdx.z); its eight waves (two per SIMD, to cover each
+// other's waits) each own tokens 32 (w & 1) .. +31 (two 16-row subtiles) and
+// experts 32 (w >> 1) .. +31 (two 16-column subtiles).  K runs
 // over the slice in 32-row chunks staged through LDS (x as float4, W_r as
 // coalesced scalars: E need not be a multiple of 4), the next chunk loaded
 // into registers while the current one is multiplied.  The top-k kernel adds
 // the slices in order.  Few tokens get many slices (a 5-token call would
 // otherwise read all of W_r with 4 blocks).
 constexpr int kPfTok = 32;  // token granularity of router_slices
-constexpr int kRtTok = 64, kRtCols = 128, kRtK = 32;
+constexpr int kRtTok = 64, kRtCols = 128, kRtK = 32, kRtThreads = 512;
 constexpr int kRtXPitch = 34;   // floats: 16 rows x 2 k of one read on distinct banks
 constexpr int kRtWPitch = 144;  // floats: consecutive k rows 16 banks apart
 
-__global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__restrict__ x,
+__global__ __launch_bounds__(kRtThreads) void router_logits_kernel(const float *__restrict__ x,
                                                                  const float *__restrict__ wr,
                                                                  int T, int H, int E, int slices,
                                                                  float *__restrict__ zp) {
@@ -974,44 +975,44 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
   const int t0 = blockIdx.x * kRtTok, c0 = blockIdx.y * kRtCols;
   const int per = ((H + slices - 1) / slices + kRtK - 1) / kRtK * kRtK;
   const int rbeg = blockIdx.z * per, rend = min(H, rbeg + per);  // multiples of 32
-  // loads of one chunk: x rows as float4 (i = tid + 256 m: row i / 8, k 4 (i % 8)),
-  // W_r elements (i = tid + 256 m: k i / 128, column i % 128); clamped, selected on store
-  float4 xv[2];
-  float wvv[16];
+  // loads of one chunk: x rows as float4 (thread i: row i / 8, k 4 (i % 8)),
+  // W_r elements (i = tid + 512 m: k i / 128, column i % 128); clamped, selected on store
+  float4 xv[1];
+  float wvv[8];
   auto gload = [&](int r0) {
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
-      const int i = tid + m * kThreads, row = i >> 3, k4 = (i & 7) * 4;
+    for (int m = 0; m < 1; ++m) {
+      const int i = tid + m * kRtThreads, row = i >> 3, k4 = (i & 7) * 4;
       const int t = min(t0 + row, T - 1);
       xv[m] = *reinterpret_cast<const float4 *>(x + (int64_t)t * H + r0 + k4);
     }
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int i = tid + m * kThreads, kk = i >> 7, col = i & (kRtCols - 1);
+    for (int m = 0; m < 8; ++m) {
+      const int i = tid + m * kRtThreads, kk = i >> 7, col = i & (kRtCols - 1);
       wvv[m] = wr[(int64_t)(r0 + kk) * E + min(c0 + col, E - 1)];
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
-      const int i = tid + m * kThreads, row = i >> 3, k4 = (i & 7) * 4;
+    for (int m = 0; m < 1; ++m) {
+      const int i = tid + m * kRtThreads, row = i >> 3, k4 = (i & 7) * 4;
       const bool ok = t0 + row < T;
       float2 *d = reinterpret_cast<float2 *>(&xs[buf][row][k4]);
       d[0] = ok ? make_float2(xv[m].x, xv[m].y) : make_float2(0.f, 0.f);
       d[1] = ok ? make_float2(xv[m].z, xv[m].w) : make_float2(0.f, 0.f);
     }
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int i = tid + m * kThreads, kk = i >> 7, col = i & (kRtCols - 1);
+    for (int m = 0; m < 8; ++m) {
+      const int i = tid + m * kRtThreads, kk = i >> 7, col = i & (kRtCols - 1);
       ws[buf][kk][col] = c0 + col < E ? wvv[m] : 0.f;
     }
   };
-  f32x4 acc[2][4];
+  f32x4 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int wrow = 32 * (wv & 1), wcol = 64 * (wv >> 1);
+    for (int q = 0; q < 2; ++q) acc[i][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int wrow = 32 * (wv & 1), wcol = 32 * (wv >> 1);
   int buf = 0;
   if (rbeg < rend) {
     gload(rbeg);
@@ -1024,15 +1025,15 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
 #pragma unroll
     for (int s4 = 0; s4 < kRtK / 4; ++s4) {
       const int kk = 4 * s4 + (lane >> 4);
-      float av[2], bv[4];
+      float av[2], bv[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) av[i] = xs[buf][wrow + 16 * i + (lane & 15)][kk];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) bv[q] = ws[buf][kk][wcol + 16 * q + (lane & 15)];
+      for (int q = 0; q < 2; ++q) bv[q] = ws[buf][kk][wcol + 16 * q + (lane & 15)];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int q = 0; q < 2; ++q)
           acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[q], acc[i][q], 0, 0, 0);
     }
     if (more) lstore(buf ^ 1);
@@ -1048,7 +1049,7 @@ __global__ __launch_bounds__(kThreads) void router_logits_kernel(const float *__
       const int t = t0 + wrow + 16 * i + 4 * (lane >> 4) + r;
       if (t >= T) continue;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < 2; ++q) {
         const int col = c0 + wcol + 16 * q + (lane & 15);
         if (col < E) z[(int64_t)t * E + col] = acc[i][q][r];
       }
@@ -2672,11 +2673,20 @@ __global__ __launch_bounds__(kThreads) void prefill_prep_kernel(const float *__r
   for (int i = 0; i < kThreads / kWave; ++i) tot += wsum[i];
   const float s = prenorm ? 1.f / sqrtf(tot / (float)H + 1e-6f) : 1.f;
   if (threadIdx.x == 0) inv[t] = s;
-  for (int i = threadIdx.x; i < H; i += kThreads) {
-    const float v = xt[i] * s;
-    const __bf16 hi = (__bf16)v;
-    xb[(int64_t)t * H + i] = hi;
-    xb[(int64_t)T * H + (int64_t)t * H + i] = (__bf16)(v - (float)hi);
+  // eight consecutive values per thread (H % 64 == 0): two 16-byte loads, one
+  // 16-byte store to each plane
+  __bf16 *hi8 = xb + (int64_t)t * H, *lo8 = xb + (int64_t)T * H + (int64_t)t * H;
+  for (int i = 8 * threadIdx.x; i < H; i += 8 * kThreads) {
+    const float4 a = *reinterpret_cast<const float4 *>(xt + i), b = *reinterpret_cast<const float4 *>(xt + i + 4);
+    const float v[8] = {a.x * s, a.y * s, a.z * s, a.w * s, b.x * s, b.y * s, b.z * s, b.w * s};
+    __bf16 h[8], l[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      h[j] = (__bf16)v[j];
+      l[j] = (__bf16)(v[j] - (float)h[j]);
+    }
+    *reinterpret_cast<uint4 *>(hi8 + i) = *reinterpret_cast<const uint4 *>(h);
+    *reinterpret_cast<uint4 *>(lo8 + i) = *reinterpret_cast<const uint4 *>(l);
   }
 }
 
@@ -3629,7 +3639,7 @@ hipError_t launch_router_prefill(const float *x, const float *wr, int T, int H, 
   const int slices = router_slices(T);
   hipLaunchKernelGGL(router_logits_kernel,
                      dim3((T + kRtTok - 1) / kRtTok, (E + kRtCols - 1) / kRtCols, slices),
-                     dim3(kThreads), 0, s, x, wr, T, H, E, slices, z);
+                     dim3(kRtThreads), 0, s, x, wr, T, H, E, slices, z);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int wpb = kThreads / kWave;
