@@ -201,12 +201,14 @@ def test_prefill_tiles_past_the_table():
         run_prefill(wl, 16, 8192, calls=2)
 
 
-def test_a3b_prefill_full_size():
-    """4096 tokens through all 48 layers of the A3B stack, 45 slots, cold cache,
-    pre-norm residual chain on the GPU; every route and the whole trace checked,
-    outputs of sampled tokens in sampled layers against the bf16 oracle."""
+@pytest.mark.parametrize("name", ["a3b_prefill", "q4km_prefill"])
+def test_a3b_prefill_full_size(name):
+    """4096 tokens through all 48 layers of the A3B stack (Q8_0, and the Q4_K_M mix:
+    Q4_K gate/up, Q6_K down), 45 slots, cold cache, pre-norm residual chain on the GPU;
+    every route and the whole trace checked, outputs of sampled tokens in sampled
+    layers against the bf16 oracle."""
     torch = torch_cuda()
-    wl = synth.WORKLOADS["a3b_prefill"]
+    wl = synth.WORKLOADS[name]
     keep, ptr, arr = store_buffer(wl)
     R = synth.router(wl)
     X = synth.hidden(wl)
@@ -216,7 +218,7 @@ def test_a3b_prefill_full_size():
     inputs, outputs, routes = {}, {}, []
     h = torch.from_numpy(X).cuda()
     y = torch.empty_like(h)
-    log(f"a3b prefill: {T} tokens x {L} layers, C={wl.budget_slots}")
+    log(f"{name}: {T} tokens x {L} layers, C={wl.budget_slots}")
     for l in range(L):
         xin = h.cpu().numpy()
         delta, idx, w = cache.layer_forward(h, torch.from_numpy(R[l]).cuda(), l, y, n_tokens=T,
