@@ -201,47 +201,51 @@ def test_prefill_tiles_past_the_table():
         run_prefill(wl, 16, 8192, calls=2)
 
 
-@pytest.mark.parametrize("name", ["a3b_prefill", "q4km_prefill"])
-def test_a3b_prefill_full_size(name):
+@pytest.mark.parametrize("name,budget,calls", [("a3b_prefill", None, 1), ("q4km_prefill", None, 1),
+                                                ("a3b_prefill", 128, 2)])
+def test_a3b_prefill_full_size(name, budget, calls):
     """4096 tokens through all 48 layers of the A3B stack (Q8_0, and the Q4_K_M mix:
-    Q4_K gate/up, Q6_K down), 45 slots, cold cache, pre-norm residual chain on the GPU;
-    every route and the whole trace checked, outputs of sampled tokens in sampled
-    layers against the bf16 oracle."""
+    Q4_K gate/up, Q6_K down), pre-norm residual chain on the GPU: 45 slots from a cold
+    cache, or every expert resident (128 slots, the second call all hits: each layer's
+    128 experts in one launch of each grouped GEMM).  Every route and the whole trace
+    checked, outputs of sampled tokens in sampled layers of the last call against the
+    bf16 oracle."""
     torch = torch_cuda()
     wl = synth.WORKLOADS[name]
+    C = wl.budget_slots if budget is None else budget
     keep, ptr, arr = store_buffer(wl)
     R = synth.router(wl)
     X = synth.hidden(wl)
-    cache = make_cache(wl, ptr, wl.budget_slots, trace=True, residual=True, prenorm=True)
+    cache = make_cache(wl, ptr, C, trace=True, residual=True, prenorm=True)
     T, L = X.shape[0], wl.n_layers
     check_layers = {0, L // 2, L - 1}
-    inputs, outputs, routes = {}, {}, []
-    h = torch.from_numpy(X).cuda()
-    y = torch.empty_like(h)
-    log(f"{name}: {T} tokens x {L} layers, C={wl.budget_slots}")
-    for l in range(L):
-        xin = h.cpu().numpy()
-        delta, idx, w = cache.layer_forward(h, torch.from_numpy(R[l]).cuda(), l, y, n_tokens=T,
-                                            routes=True)
-        routes.append((xin, idx, w))
-        if l in check_layers:
-            inputs[l] = xin
-            outputs[l] = y.cpu().numpy()
-        assert delta.misses == len(np.unique(idx))   # every layer starts cold
-        h, y = y, h
-    assert np.all(np.isfinite(h.cpu().numpy()))
-    log("  routes")
-    flips = 0
-    for l, (xin, idx, w) in enumerate(routes):
-        z, io, wo, gap = oracle_routes(xin, R[l], wl.top_k, True)
-        for t in np.nonzero(np.any(np.sort(io, 1) != np.sort(idx, 1), axis=1))[0]:
-            assert gap[t] < TIE_GAP, f"layer {l} token {t}: gap {gap[t]}"
-            flips += 1
-    log(f"  near-tie flips: {flips}; trace")
+    log(f"{name}: {T} tokens x {L} layers, C={C}, {calls} call(s)")
+    lrus = [LayerLRU(wl.n_experts, C, wl.payload_bytes, l) for l in range(L)]
     want = []
-    for l, (xin, idx, w) in enumerate(routes):
-        lru = LayerLRU(wl.n_experts, wl.budget_slots, wl.payload_bytes, l)
-        want.extend(lru.step(np.unique(idx)))
+    flips = 0
+    for c in range(calls):
+        inputs, outputs, routes = {}, {}, []
+        h = torch.from_numpy(X).cuda()
+        y = torch.empty_like(h)
+        for l in range(L):
+            xin = h.cpu().numpy()
+            delta, idx, w = cache.layer_forward(h, torch.from_numpy(R[l]).cuda(), l, y, n_tokens=T,
+                                                routes=True)
+            routes.append((xin, idx, w))
+            if l in check_layers:
+                inputs[l] = xin
+                outputs[l] = y.cpu().numpy()
+            step = lrus[l].step(np.unique(idx))
+            want.extend(step)
+            assert delta.misses == sum(1 for r in step if not r[3])
+            h, y = y, h
+        assert np.all(np.isfinite(h.cpu().numpy()))
+        for l, (xin, idx, w) in enumerate(routes):
+            z, io, wo, gap = oracle_routes(xin, R[l], wl.top_k, True)
+            for t in np.nonzero(np.any(np.sort(io, 1) != np.sort(idx, 1), axis=1))[0]:
+                assert gap[t] < TIE_GAP, f"call {c} layer {l} token {t}: gap {gap[t]}"
+                flips += 1
+    log(f"  near-tie flips: {flips}; trace")
     assert cache.read_trace() == want
     rng = np.random.default_rng(5)
     worst = 0.0
@@ -249,7 +253,7 @@ def test_a3b_prefill_full_size(name):
         toks = sorted(rng.choice(T, size=6, replace=False).tolist())
         xin, idx, w = routes[l]
         _, err = check_call(xin, R[l], arr, wl, l, idx, w, outputs[l], True, True, tokens=toks,
-                            budget=wl.budget_slots)
+                            budget=C)
         worst = max(worst, err)
     log(f"  ok: worst err/rms {worst:.2e}; counters {cache.counters()}")
     cache.close()
